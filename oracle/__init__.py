@@ -1,0 +1,20 @@
+"""Float64 CPU oracle for the mixed-adapter LoRA layer.
+
+TEST INFRASTRUCTURE ONLY: imported by tests/, by the smoke check and by the
+benchmark's CPU-baseline leg, never by the product path.  It shares no code
+with the HIP library (no kernels, headers, helpers or constants).
+
+Parity pins (tests/test_oracle_pins.py): hand-derived worked examples in
+tests/golden/, scalar brute force on tiny inputs, exact linearity of the
+masked loss in A and in B (pins the backward), closed forms for permutation /
+diagonal / rank-1 adapters, integer-valued exactness, and planted-mistake
+checks that each pin rejects.  No function here is "parity unpinned".
+"""
+from .lora_oracle import (effective_ids, canonical_plan, plan_bruteforce,
+                          segments_to_ids, shrink, expand, apply, delta_rows,
+                          apply_bruteforce, grad, grad_bruteforce, masked_loss,
+                          rel_fro, max_abs)
+
+__all__ = ["effective_ids", "canonical_plan", "plan_bruteforce", "segments_to_ids",
+           "shrink", "expand", "apply", "delta_rows", "apply_bruteforce", "grad",
+           "grad_bruteforce", "masked_loss", "rel_fro", "max_abs"]

@@ -1,0 +1,357 @@
+"""Float64 CPU oracle for the mixed-adapter LoRA layer.
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path imports, links or runs
+this module; only the tests, the smoke check and the benchmark's CPU-baseline
+leg do.  It shares no code with the HIP library.
+
+What it computes (all arithmetic in float64 on the exact stored input values;
+widening bfloat16 or binary32 to float64 is exact):
+
+* ``canonical_plan``  -- grouping of token rows by adapter identity, the
+  gather step of the paper's gather-group-compute-scatter structure
+  (Section 3.4, the rollout kernel paragraph and Figure 2) and the routing of
+  trainable rows by adapter identity (Section 3.5, "Batch routing").
+* ``apply`` / ``shrink`` / ``expand`` -- the adapter residual of the LoRA layer
+  equation in Section 3.4, y = x W^T + s_a (x A_a^T) B_a^T, evaluated per adapter
+  group as Delta_a = s_a (X_a A_a^T) B_a^T and added back to the original rows.
+* ``grad`` -- the adapter-local gradients dA_a, dB_a of the loss through that
+  residual, restricted to rows whose explicit loss mask is nonzero (Section 3.3
+  for the mask, Section 3.5 for adapter-local gradients).  The paper does not
+  write the backward; it is the chain rule on the LoRA equation:
+  with H = X_m A_a^T and G = dY_m B_a,  dB_a = s_a dY_m^T H  and
+  dA_a = s_a G^T X_m.
+* ``*_bruteforce`` -- scalar Python loops over the same definitions, used only
+  as an independent pin on tiny inputs.
+
+Conventions: ``A[a]`` is ``[r_a, d_in]``, ``B[a]`` is ``[d_out, r_a]`` (the paper's
+shapes), ``None`` for an empty slot.  Ids are in ``[-1, S)``; -1 means no
+adapter.  An id outside that range, or naming an empty slot, is a data error:
+the row is treated as -1 and the plan's error flag is set.
+"""
+import numpy as np
+
+
+# ----------------------------------------------------------------------------
+# grouping (the gather / routing step)
+# ----------------------------------------------------------------------------
+
+def effective_ids(idx, num_slots, ranks=None):
+    """Ids after validation: invalid ids and ids naming an empty slot become -1.
+
+    Returns ``(eff_ids int64[n], error bool)``.
+    """
+    idx = np.asarray(idx, dtype=np.int64)
+    bad = (idx < -1) | (idx >= num_slots)
+    eff = np.where(bad, -1, idx)
+    if ranks is not None:
+        ranks = np.asarray(ranks)
+        live = eff >= 0
+        empty = np.zeros_like(live)
+        empty[live] = ranks[eff[live]] <= 0
+        bad = bad | empty
+        eff = np.where(empty, -1, eff)
+    return eff, bool(bad.any())
+
+
+def _group(eff, num_slots):
+    """counts, exclusive offsets and the stable per-adapter row order."""
+    live = eff >= 0
+    counts = np.bincount(eff[live], minlength=num_slots).astype(np.int64)
+    offsets = np.zeros(num_slots + 1, dtype=np.int64)
+    np.cumsum(counts, out=offsets[1:])
+    key = np.where(live, eff, num_slots)          # rows with no adapter sort last
+    order = np.argsort(key, kind="stable")
+    perm = order[: offsets[-1]]
+    return counts, offsets, perm
+
+
+def _runs(eff):
+    """Maximal runs [start, start+len) of one adapter id >= 0, ascending start."""
+    n = eff.size
+    if n == 0:
+        z = np.zeros(0, np.int64)
+        return z, z, z
+    live = eff >= 0
+    prev = np.concatenate([[-2], eff[:-1]])
+    starts = np.nonzero(live & (eff != prev))[0]
+    nxt = np.concatenate([eff[1:], [-2]])
+    ends = np.nonzero(live & (eff != nxt))[0]
+    return starts, ends - starts + 1, eff[starts]
+
+
+def canonical_plan(idx, num_slots, mask=None, ranks=None):
+    """The canonical grouping arrays (all int64 numpy arrays).
+
+    counts[a]   number of rows with id a
+    offsets     exclusive prefix sum of counts, length S+1
+    perm        row indices grouped by adapter, ascending row order inside a group
+    run_start, run_len, run_adapter   maximal runs of one adapter id
+    m_counts, m_offsets, m_perm       the same grouping over rows with mask != 0
+    error       True if any id was invalid or named an empty slot
+    """
+    eff, error = effective_ids(idx, num_slots, ranks)
+    counts, offsets, perm = _group(eff, num_slots)
+    rs, rl, ra = _runs(eff)
+    if mask is None:
+        eff_m = eff
+    else:
+        eff_m = np.where(np.asarray(mask) != 0, eff, -1)
+    m_counts, m_offsets, m_perm = _group(eff_m, num_slots)
+    return dict(counts=counts, offsets=offsets, perm=perm, n_runs=rs.size,
+                run_start=rs, run_len=rl, run_adapter=ra, m_counts=m_counts,
+                m_offsets=m_offsets, m_perm=m_perm, error=error, eff=eff)
+
+
+def plan_bruteforce(idx, num_slots, mask=None, ranks=None):
+    """Scalar enumeration of the same arrays (independent pin for the plan)."""
+    n = len(idx)
+    eff, error = [], False
+    for t in range(n):
+        a = int(idx[t])
+        ok = -1 <= a < num_slots and (a < 0 or ranks is None or ranks[a] > 0)
+        if not ok:
+            error = True
+            a = -1
+        eff.append(a)
+    counts = [0] * num_slots
+    perm_lists = [[] for _ in range(num_slots)]
+    m_lists = [[] for _ in range(num_slots)]
+    for t in range(n):
+        if eff[t] >= 0:
+            counts[eff[t]] += 1
+            perm_lists[eff[t]].append(t)
+            if mask is None or mask[t] != 0:
+                m_lists[eff[t]].append(t)
+    offsets = [0]
+    for a in range(num_slots):
+        offsets.append(offsets[-1] + counts[a])
+    m_offsets = [0]
+    for a in range(num_slots):
+        m_offsets.append(m_offsets[-1] + len(m_lists[a]))
+    rs, rl, ra = [], [], []
+    t = 0
+    while t < n:
+        if eff[t] < 0:
+            t += 1
+            continue
+        u = t
+        while u + 1 < n and eff[u + 1] == eff[t]:
+            u += 1
+        rs.append(t)
+        rl.append(u - t + 1)
+        ra.append(eff[t])
+        t = u + 1
+    return dict(counts=counts, offsets=offsets,
+                perm=[t for a in range(num_slots) for t in perm_lists[a]],
+                n_runs=len(rs), run_start=rs, run_len=rl, run_adapter=ra,
+                m_counts=[len(m) for m in m_lists], m_offsets=m_offsets,
+                m_perm=[t for a in range(num_slots) for t in m_lists[a]], error=error)
+
+
+def segments_to_ids(seg_offsets, seg_adapter, n):
+    """Per-row ids from contiguous segments [seg_offsets[s], seg_offsets[s+1]).
+    Rows outside every segment get -1."""
+    idx = np.full(n, -1, dtype=np.int64)
+    for s in range(len(seg_adapter)):
+        idx[int(seg_offsets[s]):int(seg_offsets[s + 1])] = int(seg_adapter[s])
+    return idx
+
+
+# ----------------------------------------------------------------------------
+# forward: shrink, expand, apply (Section 3.4, LoRA equation and Delta_a)
+# ----------------------------------------------------------------------------
+
+def shrink(eff, X, A, H=None):
+    """H[t, :r_a] = X[t] A_a^T for every row t with adapter a (unscaled).
+
+    ``H`` (float64 [n, >= r_max]) is updated in place if given; rows with no
+    adapter and columns >= r_a are left as they were.
+    """
+    n = X.shape[0]
+    r_max = max([a.shape[0] for a in A if a is not None] + [0])
+    if H is None:
+        H = np.zeros((n, r_max))
+    for a, Aa in enumerate(A):
+        rows = np.nonzero(eff == a)[0]
+        if rows.size == 0 or Aa is None:
+            continue
+        H[rows, : Aa.shape[0]] = X[rows] @ Aa.T
+    return H
+
+
+def expand(eff, H, Y, B, scale):
+    """Y[t] += s_a H[t, :r_a] B_a^T for every row t with adapter a; returns a new
+    float64 array, rows with no adapter copied unchanged."""
+    out = np.array(Y, dtype=np.float64, copy=True)
+    for a, Ba in enumerate(B):
+        rows = np.nonzero(eff == a)[0]
+        if rows.size == 0 or Ba is None:
+            continue
+        r = Ba.shape[1]
+        out[rows] += float(scale[a]) * (H[rows, :r] @ Ba.T)
+    return out
+
+
+def apply(eff, X, Y, A, B, scale):
+    """Y_out = Y + Delta with Delta_a = s_a (X_a A_a^T) B_a^T scattered back to
+    the rows of group a.  Rows with no adapter are copied bit for bit."""
+    out = np.array(Y, dtype=np.float64, copy=True)
+    for a in range(len(A)):
+        if A[a] is None:
+            continue
+        rows = np.nonzero(eff == a)[0]
+        if rows.size == 0:
+            continue
+        Ha = X[rows] @ A[a].T
+        out[rows] += float(scale[a]) * (Ha @ B[a].T)
+    return out
+
+
+def delta_rows(eff, X, A, B, scale, rows):
+    """The residual Delta[t] for the listed rows only (zero for rows with no
+    adapter); used to check large cases on sampled rows."""
+    rows = np.asarray(rows, dtype=np.int64)
+    d_out = next(b.shape[0] for b in B if b is not None)
+    out = np.zeros((rows.size, d_out))
+    for i, t in enumerate(rows):
+        a = int(eff[t])
+        if a < 0:
+            continue
+        h = A[a] @ X[t]
+        out[i] = float(scale[a]) * (B[a] @ h)
+    return out
+
+
+def apply_bruteforce(eff, X, Y, A, B, scale):
+    """Scalar loops over the LoRA equation, row by row (tiny inputs only)."""
+    n, d_in = X.shape
+    d_out = Y.shape[1]
+    out = [[float(Y[t][o]) for o in range(d_out)] for t in range(n)]
+    for t in range(n):
+        a = int(eff[t])
+        if a < 0:
+            continue
+        r = A[a].shape[0]
+        h = []
+        for j in range(r):
+            acc = 0.0
+            for k in range(d_in):
+                acc += float(X[t][k]) * float(A[a][j][k])
+            h.append(acc)
+        for o in range(d_out):
+            acc = 0.0
+            for j in range(r):
+                acc += h[j] * float(B[a][o][j])
+            out[t][o] += float(scale[a]) * acc
+    return np.array(out)
+
+
+# ----------------------------------------------------------------------------
+# backward: masked, adapter-local gradients (Sections 3.3 and 3.5)
+# ----------------------------------------------------------------------------
+
+def grad(eff, mask, X, dY, A, B, scale, H_saved=None):
+    """dA_a, dB_a over rows T_a^m = {t : eff[t] = a and mask[t] != 0}.
+
+    dB_a = s_a dY_m^T (X_m A_a^T)     [d_out, r_a]
+    dA_a = s_a (dY_m B_a)^T X_m       [r_a, d_in]
+
+    Rows outside T_a^m are never read.  A slot with no such row gets exact
+    zeros.  ``H_saved`` (float64 [n, >= r_a]) replaces X_m A_a^T when given.
+    Returns two lists indexed by slot (None for empty slots).
+    """
+    dA, dB = [], []
+    for a in range(len(A)):
+        if A[a] is None:
+            dA.append(None)
+            dB.append(None)
+            continue
+        r = A[a].shape[0]
+        sel = eff == a
+        if mask is not None:
+            sel = sel & (np.asarray(mask) != 0)
+        rows = np.nonzero(sel)[0]
+        if rows.size == 0:
+            dA.append(np.zeros_like(A[a], dtype=np.float64))
+            dB.append(np.zeros_like(B[a], dtype=np.float64))
+            continue
+        Xm = X[rows]
+        dYm = dY[rows]
+        Ha = H_saved[rows, :r] if H_saved is not None else Xm @ A[a].T
+        Ga = dYm @ B[a]
+        s = float(scale[a])
+        dB.append(s * (dYm.T @ Ha))
+        dA.append(s * (Ga.T @ Xm))
+    return dA, dB
+
+
+def grad_bruteforce(eff, mask, X, dY, A, B, scale):
+    """Scalar loops for dA, dB (tiny inputs only)."""
+    n, d_in = X.shape
+    d_out = dY.shape[1]
+    dA, dB = [], []
+    for a in range(len(A)):
+        if A[a] is None:
+            dA.append(None)
+            dB.append(None)
+            continue
+        r = A[a].shape[0]
+        s = float(scale[a])
+        gA = [[0.0] * d_in for _ in range(r)]
+        gB = [[0.0] * r for _ in range(d_out)]
+        for t in range(n):
+            if int(eff[t]) != a or (mask is not None and mask[t] == 0):
+                continue
+            h = [sum(float(X[t][k]) * float(A[a][j][k]) for k in range(d_in)) for j in range(r)]
+            g = [sum(float(dY[t][o]) * float(B[a][o][j]) for o in range(d_out)) for j in range(r)]
+            for o in range(d_out):
+                for j in range(r):
+                    gB[o][j] += s * float(dY[t][o]) * h[j]
+            for j in range(r):
+                for k in range(d_in):
+                    gA[j][k] += s * g[j] * float(X[t][k])
+        dA.append(np.array(gA))
+        dB.append(np.array(gB))
+    return dA, dB
+
+
+def masked_loss(eff, mask, X, dY, A, B, scale):
+    """L = sum over masked rows t with an adapter of <dY_t, Delta_t>.
+
+    L is linear in each A_a (B fixed) and in each B_a (A fixed), and its partial
+    derivatives are exactly dA_a and dB_a; the tests use this to pin ``grad``.
+    """
+    total = 0.0
+    for a in range(len(A)):
+        if A[a] is None:
+            continue
+        sel = eff == a
+        if mask is not None:
+            sel = sel & (np.asarray(mask) != 0)
+        rows = np.nonzero(sel)[0]
+        if rows.size == 0:
+            continue
+        D = float(scale[a]) * ((X[rows] @ A[a].T) @ B[a].T)
+        total += float(np.sum(dY[rows] * D))
+    return total
+
+
+# ----------------------------------------------------------------------------
+# comparison metrics
+# ----------------------------------------------------------------------------
+
+def rel_fro(out, ref):
+    """||out - ref||_F / ||ref||_F (0 when both are zero)."""
+    out = np.asarray(out, np.float64)
+    ref = np.asarray(ref, np.float64)
+    den = np.linalg.norm(ref)
+    num = np.linalg.norm(out - ref)
+    if den == 0.0:
+        return 0.0 if num == 0.0 else float("inf")
+    return float(num / den)
+
+
+def max_abs(out, ref):
+    out = np.asarray(out, np.float64)
+    ref = np.asarray(ref, np.float64)
+    return float(np.max(np.abs(out - ref))) if out.size else 0.0

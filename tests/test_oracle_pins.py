@@ -1,0 +1,454 @@
+"""Pins of the float64 oracle against things other than itself (CPU only).
+
+* hand-derived worked examples (tests/golden/*.txt),
+* scalar brute force on tiny inputs (a different evaluation order and no
+  grouping / gather / scatter),
+* exact linearity of the masked loss in A and in B, which ties the backward to
+  the forward without restating the gradient formula,
+* closed forms (permutation x diagonal adapters, rank-1 adapters),
+* integer-valued inputs checked with exact Python integer arithmetic,
+* invariants (id -1 rows bit-identical, zero B, permutation, mask exactness),
+* planted mistakes: each plausible bug in the oracle must make a pin fail.
+"""
+import fractions
+import types
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from helpers import f64_case, load_golden
+
+pytestmark = pytest.mark.filterwarnings("ignore::RuntimeWarning")
+
+
+# ----------------------------------------------------------------------------
+# pin checks, parameterised by the implementation so planted mistakes can be run
+# ----------------------------------------------------------------------------
+
+def check_plan_golden(impl):
+    g = load_golden("plan_worked_example.txt")
+    p = impl.canonical_plan(g["idx"].astype(np.int64), int(g["num_slots"][0]),
+                            mask=g["mask"].astype(np.uint8))
+    for k in ("counts", "offsets", "perm", "run_start", "run_len", "run_adapter",
+              "m_counts", "m_offsets", "m_perm"):
+        if not np.array_equal(np.asarray(p[k]), g[k].astype(np.int64)):
+            return False
+    return p["n_runs"] == int(g["n_runs"][0]) and p["error"] == bool(g["error"][0])
+
+
+def _plan_fuzz_cases():
+    rng = np.random.default_rng(1234)
+    cases = [
+        (np.full(37, -1), 5, None),
+        (np.zeros(50, np.int64), 1, None),
+        (np.arange(40) % 7, 7, rng.integers(0, 2, 40)),
+        (np.zeros(0, np.int64), 3, None),
+        (np.array([3, 3, 3, -1, 3, 9, -7, 0]), 4, np.array([1, 0, 1, 1, 1, 1, 1, 0])),
+    ]
+    for s in range(30):
+        n = int(rng.integers(1, 300))
+        S = int(rng.integers(1, 40))
+        idx = rng.integers(-2, S + 1, n)
+        seg = rng.random() < 0.5
+        if seg:
+            idx = np.repeat(rng.integers(-1, S, n // 9 + 1), 9)[:n]
+        mask = rng.integers(0, 2, n) if rng.random() < 0.6 else None
+        cases.append((idx, S, mask))
+    return cases
+
+
+def check_plan_bruteforce(impl):
+    for idx, S, mask in _plan_fuzz_cases():
+        ranks = np.ones(S, np.int64)
+        p = impl.canonical_plan(idx, S, mask=mask, ranks=ranks)
+        b = oracle.plan_bruteforce(list(idx), S, mask=None if mask is None else list(mask),
+                                   ranks=list(ranks))
+        for k in ("counts", "offsets", "perm", "run_start", "run_len", "run_adapter",
+                  "m_counts", "m_offsets", "m_perm"):
+            if not np.array_equal(np.asarray(p[k], np.int64), np.asarray(b[k], np.int64)):
+                return False
+        if p["n_runs"] != b["n_runs"] or p["error"] != b["error"]:
+            return False
+    return True
+
+
+def _golden_forward():
+    g = load_golden("forward_worked_example.txt")
+    d_in, d_out = int(g["d_in"][0]), int(g["d_out"][0])
+    r = g["rank"].astype(int)
+    A = [g["A0"].reshape(r[0], d_in), g["A1"].reshape(r[1], d_in)]
+    B = [g["B0"].reshape(d_out, r[0]), g["B1"].reshape(d_out, r[1])]
+    X = g["X"].reshape(-1, d_in)
+    Y = g["Y"].reshape(-1, d_out)
+    return g, A, B, X, Y, g["idx"].astype(np.int64), g["scale"]
+
+
+def check_forward_golden(impl):
+    g, A, B, X, Y, idx, s = _golden_forward()
+    out = impl.apply(idx, X, Y, A, B, s)
+    return np.array_equal(out, g["Y_out"].reshape(Y.shape))
+
+
+def _tiny_case(seed, n=13, d_in=7, d_out=5, S=3, mask_p=None, frac_none=0.2):
+    c = workloads.random_case(seed, n, d_in, d_out, S, rank_choices=(1, 2, 3, 4),
+                              frac_none=frac_none, x_dtype="f32", w_dtype="f32",
+                              y_dtype="f32", mask_p=mask_p, want_dy=mask_p is not None)
+    X, A, B, Y, dY = f64_case(c)
+    eff, _ = oracle.effective_ids(c.idx, S, c.ranks)
+    return c, eff, X, A, B, Y, dY
+
+
+def check_forward_bruteforce(impl):
+    for seed in range(6):
+        c, eff, X, A, B, Y, _ = _tiny_case(seed)
+        ref = oracle.apply_bruteforce(eff, X, Y, A, B, c.scales)
+        out = impl.apply(eff, X, Y, A, B, c.scales)
+        if not np.allclose(out, ref, rtol=1e-12, atol=1e-12):
+            return False
+    return True
+
+
+def check_forward_closed_form(impl):
+    """A = permutation matrix, B = diagonal: Delta[t, o] = s * d_o * X[t, pi(o)]."""
+    rng = np.random.default_rng(7)
+    n, d = 9, 6
+    pi = rng.permutation(d)
+    P = np.zeros((d, d))
+    P[np.arange(d), pi] = 1.0                    # (X P^T)[t, j] = X[t, pi(j)]
+    diag = rng.integers(1, 9, d).astype(np.float64)
+    X = rng.integers(-5, 6, (n, d)).astype(np.float64)
+    Y = rng.integers(-5, 6, (n, d)).astype(np.float64)
+    idx = np.zeros(n, np.int64)
+    out = impl.apply(idx, X, Y, [P], [np.diag(diag)], np.array([0.5]))
+    expect = Y + 0.5 * diag[None, :] * X[:, pi]
+    if not np.array_equal(out, expect):
+        return False
+    # rank-1: A = u^T, B = v  ->  Delta[t] = s (X[t] . u) v
+    u = rng.integers(-3, 4, d).astype(np.float64)
+    v = rng.integers(-3, 4, d + 2).astype(np.float64)
+    Y2 = np.zeros((n, d + 2))
+    out = impl.apply(idx, X, Y2, [u[None, :]], [v[:, None]], np.array([2.0]))
+    expect = np.array([[2.0 * sum(X[t, k] * u[k] for k in range(d)) * v[o]
+                        for o in range(d + 2)] for t in range(n)])
+    return np.array_equal(out, expect)
+
+
+def check_forward_integer_exact(impl):
+    """Integer inputs, power-of-two scales: compare with exact rational arithmetic."""
+    c = workloads.random_case(21, 40, 24, 20, 4, rank_choices=(1, 3, 8), frac_none=0.25,
+                              x_dtype="f32", w_dtype="f32", y_dtype="f32", int_values=True)
+    X, A, B, Y, _ = f64_case(c)
+    eff, _ = oracle.effective_ids(c.idx, c.num_slots, c.ranks)
+    out = impl.apply(eff, X, Y, A, B, c.scales)
+    for t in range(c.n):
+        a = int(eff[t])
+        for o in range(c.d_out):
+            exp = fractions.Fraction(int(Y[t, o]))
+            if a >= 0:
+                h = [sum(int(X[t, k]) * int(A[a][j, k]) for k in range(c.d_in))
+                     for j in range(A[a].shape[0])]
+                exp += fractions.Fraction(float(c.scales[a])) * sum(
+                    h[j] * int(B[a][o, j]) for j in range(len(h)))
+            if fractions.Fraction(out[t, o]) != exp:
+                return False
+    return True
+
+
+def check_grad_golden(impl):
+    g, A, B, X, _, idx, s = _golden_forward()
+    gg = load_golden("grad_worked_example.txt")
+    dY = gg["dY"].reshape(X.shape[0], -1)
+    for tag in ("a", "b"):
+        mask = gg["mask_" + tag].astype(np.uint8)
+        dA, dB = impl.grad(idx, mask, X, dY, A, B, s)
+        for a in range(2):
+            if not np.array_equal(dA[a].ravel(), gg[f"dA{a}_{tag}"]):
+                return False
+            if not np.array_equal(dB[a].ravel(), gg[f"dB{a}_{tag}"]):
+                return False
+        if impl.masked_loss(idx, mask, X, dY, A, B, s) != gg["loss_" + tag][0]:
+            return False
+    return True
+
+
+def check_grad_linearity(impl):
+    """L(A + eps E) - L(A) = eps <dA, E> and the same for B, exactly up to f64
+    rounding, because the masked loss is linear in A (B fixed) and in B (A fixed).
+    The loss uses the forward oracle, so this ties the backward to the forward."""
+    for seed in range(4):
+        c, eff, X, A, B, Y, dY = _tiny_case(100 + seed, n=17, mask_p=0.6)
+        dA, dB = impl.grad(eff, c.mask, X, dY, A, B, c.scales)
+        L0 = oracle.masked_loss(eff, c.mask, X, dY, A, B, c.scales)
+        rng = np.random.default_rng(seed)
+        for a in range(c.num_slots):
+            if A[a] is None:
+                continue
+            for which in ("A", "B"):
+                W = A if which == "A" else B
+                E = rng.standard_normal(W[a].shape)
+                eps = 0.37
+                W2 = [w.copy() if w is not None else None for w in W]
+                W2[a] = W[a] + eps * E
+                L1 = oracle.masked_loss(eff, c.mask, X, dY, W2 if which == "A" else A,
+                                        B if which == "A" else W2, c.scales)
+                g = dA[a] if which == "A" else dB[a]
+                pred = eps * float(np.sum(g * E))
+                if abs((L1 - L0) - pred) > 1e-10 * max(1.0, abs(pred), abs(L0)):
+                    return False
+    return True
+
+
+def check_grad_bruteforce(impl):
+    for seed in range(3):
+        c, eff, X, A, B, Y, dY = _tiny_case(200 + seed, n=11, d_in=5, d_out=4, mask_p=0.5)
+        dA, dB = impl.grad(eff, c.mask, X, dY, A, B, c.scales)
+        rA, rB = oracle.grad_bruteforce(eff, c.mask, X, dY, A, B, c.scales)
+        for a in range(c.num_slots):
+            if A[a] is None:
+                continue
+            if not (np.allclose(dA[a], rA[a], rtol=1e-12, atol=1e-12)
+                    and np.allclose(dB[a], rB[a], rtol=1e-12, atol=1e-12)):
+                return False
+    return True
+
+
+def check_grad_mask_exact(impl):
+    """Masked-out rows hold NaN / Inf / 1e30 in X and dY: dA, dB are byte-identical
+    to the run where those rows are zero."""
+    c, eff, X, A, B, Y, dY = _tiny_case(300, n=19, mask_p=0.5)
+    out = c.mask == 0
+    X0, dY0 = X.copy(), dY.copy()
+    X0[out] = 0.0
+    dY0[out] = 0.0
+    X1, dY1 = X.copy(), dY.copy()
+    junk = np.array([np.nan, np.inf, -np.inf, 1e30])
+    X1[out] = junk[np.arange(X1[out].size) % 4].reshape(X1[out].shape)
+    dY1[out] = junk[np.arange(dY1[out].size) % 4].reshape(dY1[out].shape)
+    a0, b0 = impl.grad(eff, c.mask, X0, dY0, A, B, c.scales)
+    a1, b1 = impl.grad(eff, c.mask, X1, dY1, A, B, c.scales)
+    for a in range(c.num_slots):
+        if A[a] is None:
+            continue
+        if a0[a].tobytes() != a1[a].tobytes() or b0[a].tobytes() != b1[a].tobytes():
+            return False
+    return True
+
+
+ALL_CHECKS = [check_plan_golden, check_plan_bruteforce, check_forward_golden,
+              check_forward_bruteforce, check_forward_closed_form,
+              check_forward_integer_exact, check_grad_golden, check_grad_linearity,
+              check_grad_bruteforce, check_grad_mask_exact]
+
+
+# ----------------------------------------------------------------------------
+# the oracle passes every pin
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("check", ALL_CHECKS, ids=lambda f: f.__name__)
+def test_oracle_pin(check):
+    assert check(oracle)
+
+
+def test_none_rows_bit_identical():
+    """Rows with id -1 are copied bit for bit, including -0.0 and NaN payloads."""
+    c, eff, X, A, B, Y, _ = _tiny_case(5)
+    Y = Y.copy()
+    none = np.nonzero(eff < 0)[0]
+    Y[none[0], 0] = -0.0
+    Y[none[-1], 1] = np.nan
+    out = oracle.apply(eff, X, Y, A, B, c.scales)
+    assert out[none].tobytes() == Y[none].tobytes()
+
+
+def test_zero_B_or_A_leaves_Y():
+    c, eff, X, A, B, Y, _ = _tiny_case(6)
+    zB = [np.zeros_like(b) if b is not None else None for b in B]
+    zA = [np.zeros_like(a) if a is not None else None for a in A]
+    assert np.array_equal(oracle.apply(eff, X, Y, A, zB, c.scales), Y)
+    assert np.array_equal(oracle.apply(eff, X, Y, zA, B, c.scales), Y)
+
+
+def test_permutation_invariance():
+    """Permuting rows permutes the output; gradients do not change."""
+    c, eff, X, A, B, Y, dY = _tiny_case(8, n=31, mask_p=0.5)
+    p = np.random.default_rng(3).permutation(c.n)
+    out = oracle.apply(eff, X, Y, A, B, c.scales)
+    outp = oracle.apply(eff[p], X[p], Y[p], A, B, c.scales)
+    assert np.allclose(outp, out[p], rtol=1e-13, atol=1e-13)
+    dA, dB = oracle.grad(eff, c.mask, X, dY, A, B, c.scales)
+    dAp, dBp = oracle.grad(eff[p], c.mask[p], X[p], dY[p], A, B, c.scales)
+    for a in range(c.num_slots):
+        if A[a] is not None:
+            assert np.allclose(dAp[a], dA[a], rtol=1e-12, atol=1e-12)
+            assert np.allclose(dBp[a], dB[a], rtol=1e-12, atol=1e-12)
+
+
+def test_shrink_then_expand_is_apply():
+    c, eff, X, A, B, Y, _ = _tiny_case(9)
+    H = oracle.shrink(eff, X, A)
+    assert np.allclose(oracle.expand(eff, H, Y, B, c.scales),
+                       oracle.apply(eff, X, Y, A, B, c.scales), rtol=1e-13, atol=1e-13)
+
+
+def test_delta_rows_matches_apply():
+    c, eff, X, A, B, Y, _ = _tiny_case(10)
+    rows = np.arange(c.n)
+    assert np.allclose(oracle.delta_rows(eff, X, A, B, c.scales, rows),
+                       oracle.apply(eff, X, Y, A, B, c.scales) - Y, rtol=1e-12, atol=1e-12)
+
+
+def test_segments_equal_ids():
+    seg_offsets = np.array([0, 3, 3, 7, 12])
+    seg_adapter = np.array([2, 0, 2, 1])
+    ids = oracle.segments_to_ids(seg_offsets, seg_adapter, 14)
+    assert ids.tolist() == [2, 2, 2, 2, 2, 2, 2, 1, 1, 1, 1, 1, -1, -1]
+    p = oracle.canonical_plan(ids, 3)
+    assert p["n_runs"] == 2                       # adjacent same-adapter segments merge
+
+
+def test_h_saved_equals_recompute():
+    c, eff, X, A, B, Y, dY = _tiny_case(11, mask_p=0.7)
+    H = oracle.shrink(eff, X, A)
+    dA0, dB0 = oracle.grad(eff, c.mask, X, dY, A, B, c.scales)
+    dA1, dB1 = oracle.grad(eff, c.mask, X, dY, A, B, c.scales, H_saved=H)
+    for a in range(c.num_slots):
+        if A[a] is not None:
+            assert np.allclose(dA0[a], dA1[a], rtol=1e-13, atol=1e-13)
+            assert np.allclose(dB0[a], dB1[a], rtol=1e-13, atol=1e-13)
+
+
+def test_explicit_mask_not_inferred_from_zero_dy():
+    """A trainable row whose dY is zero is still counted as trainable (Section 3.3:
+    the span comes from the mask, not from a nonzero learning signal)."""
+    idx = np.array([0, 0, 1])
+    mask = np.array([1, 0, 1])
+    p = oracle.canonical_plan(idx, 2, mask=mask)
+    assert p["m_counts"].tolist() == [1, 1]
+
+
+# ----------------------------------------------------------------------------
+# planted mistakes: each must be rejected by at least one pin
+# ----------------------------------------------------------------------------
+
+def _mutant(**overrides):
+    ns = types.SimpleNamespace(canonical_plan=oracle.canonical_plan, apply=oracle.apply,
+                               grad=oracle.grad, masked_loss=oracle.masked_loss)
+    for k, v in overrides.items():
+        setattr(ns, k, v)
+    return ns
+
+
+def _apply_transposed_B(eff, X, Y, A, B, scale):
+    out = np.array(Y, dtype=np.float64, copy=True)
+    for a in range(len(A)):
+        rows = np.nonzero(eff == a)[0]
+        if rows.size == 0 or A[a] is None:
+            continue
+        Bt = B[a].T if B[a].shape[0] == B[a].shape[1] else B[a][::-1]
+        out[rows] += float(scale[a]) * ((X[rows] @ A[a].T) @ Bt.T)
+    return out
+
+
+def _apply_no_scale(eff, X, Y, A, B, scale):
+    return oracle.apply(eff, X, Y, A, B, np.ones_like(scale))
+
+
+def _apply_wrong_rows(eff, X, Y, A, B, scale):
+    return oracle.apply(np.roll(eff, 1), X, Y, A, B, scale)
+
+
+def _apply_touches_none_rows(eff, X, Y, A, B, scale):
+    return oracle.apply(np.where(eff < 0, 0, eff), X, Y, A, B, scale)
+
+
+def _grad_mask_ignored(eff, mask, X, dY, A, B, scale, H_saved=None):
+    return oracle.grad(eff, None, X, dY, A, B, scale)
+
+
+def _grad_swapped(eff, mask, X, dY, A, B, scale, H_saved=None):
+    dA, dB = oracle.grad(eff, mask, X, dY, A, B, scale)
+    # dA computed from H instead of G (a wrong chain-rule term)
+    out = []
+    for a in range(len(A)):
+        if A[a] is None:
+            out.append(None)
+            continue
+        sel = (eff == a) & (np.asarray(mask) != 0)
+        rows = np.nonzero(sel)[0]
+        H = X[rows] @ A[a].T
+        out.append(float(scale[a]) * (H.T @ X[rows]))
+    return out, dB
+
+
+def _grad_sign(eff, mask, X, dY, A, B, scale, H_saved=None):
+    dA, dB = oracle.grad(eff, mask, X, dY, A, B, scale)
+    return dA, [(-b if b is not None else None) for b in dB]
+
+
+def _grad_no_scale(eff, mask, X, dY, A, B, scale, H_saved=None):
+    return oracle.grad(eff, mask, X, dY, A, B, np.ones_like(scale))
+
+
+def _grad_mask_multiplied(eff, mask, X, dY, A, B, scale, H_saved=None):
+    m = np.asarray(mask, np.float64)[:, None]
+    return oracle.grad(eff, None, X * m, dY * m, A, B, scale)
+
+
+def _plan_unstable(idx, num_slots, mask=None, ranks=None):
+    p = oracle.canonical_plan(idx, num_slots, mask=mask, ranks=ranks)
+    p = dict(p)
+    perm = np.array(p["perm"])
+    off = p["offsets"]
+    for a in range(num_slots):
+        perm[off[a]:off[a + 1]] = perm[off[a]:off[a + 1]][::-1]
+    p["perm"] = perm
+    return p
+
+
+def _plan_inclusive_offsets(idx, num_slots, mask=None, ranks=None):
+    p = dict(oracle.canonical_plan(idx, num_slots, mask=mask, ranks=ranks))
+    p["offsets"] = np.concatenate([p["offsets"][1:], p["offsets"][-1:]])
+    return p
+
+
+def _plan_mask_ignored(idx, num_slots, mask=None, ranks=None):
+    return oracle.canonical_plan(idx, num_slots, mask=None, ranks=ranks)
+
+
+def _plan_no_validation(idx, num_slots, mask=None, ranks=None):
+    p = dict(oracle.canonical_plan(np.clip(idx, -1, num_slots - 1), num_slots, mask=mask,
+                                   ranks=ranks))
+    return p
+
+
+MUTANTS = {
+    "apply_transposed_B": _mutant(apply=_apply_transposed_B),
+    "apply_no_scale": _mutant(apply=_apply_no_scale),
+    "apply_wrong_rows": _mutant(apply=_apply_wrong_rows),
+    "apply_touches_none_rows": _mutant(apply=_apply_touches_none_rows),
+    "grad_mask_ignored": _mutant(grad=_grad_mask_ignored),
+    "grad_wrong_chain_term": _mutant(grad=_grad_swapped),
+    "grad_sign": _mutant(grad=_grad_sign),
+    "grad_no_scale": _mutant(grad=_grad_no_scale),
+    "grad_mask_multiplied": _mutant(grad=_grad_mask_multiplied),
+    "plan_unstable": _mutant(canonical_plan=_plan_unstable),
+    "plan_inclusive_offsets": _mutant(canonical_plan=_plan_inclusive_offsets),
+    "plan_mask_ignored": _mutant(canonical_plan=_plan_mask_ignored),
+    "plan_no_validation": _mutant(canonical_plan=_plan_no_validation),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_planted_mistake_is_caught(name):
+    impl = MUTANTS[name]
+    failed = []
+    for check in ALL_CHECKS:
+        try:
+            ok = check(impl)
+        except Exception:
+            ok = False
+        if not ok:
+            failed.append(check.__name__)
+    assert failed, f"planted mistake {name} passed every pin"
