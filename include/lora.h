@@ -1,0 +1,213 @@
+/*
+ * lora.h -- C ABI of the mixed-adapter LoRA layer for AMD Instinct MI355X (gfx950).
+ *
+ * What it computes.  For a batch of n token rows, each carrying an adapter id,
+ * the residual term of the adapted linear layer of the paper's Section 3.4
+ * (LoRA layer equation  y = x W^T + s_a (x A_a^T) B_a^T,  with
+ * A_a in R^{r_a x d_in}, B_a in R^{d_out x r_a}, s_a = alpha_a / r_a):
+ *
+ *   forward   Y[t, :] += s_a * (X[t, :] A_a^T) B_a^T        for every row t with id a >= 0
+ *   backward  dB_a = s_a * dY_m^T (X_m A_a^T)      [d_out, r_a]
+ *             dA_a = s_a * (dY_m B_a)^T X_m        [r_a, d_in]
+ *
+ * where X_m, dY_m are the rows of adapter a whose loss mask is nonzero.  The
+ * forward follows the gather-group-compute-scatter structure of Section 3.4 and
+ * Figure 2: rows are grouped by adapter id (the "plan"), the per-group residual
+ * Delta_a = s_a (X_a A_a^T) B_a^T is computed and added back to the original
+ * rows.  The dense base term x W^T is not part of this library: Y arrives
+ * holding it.  The backward is the chain rule on the same equation, with the
+ * explicit loss mask of Section 3.3 and the adapter-local gradients of
+ * Section 3.5 ("Batch routing").
+ *
+ * Conventions (every entry point).
+ *  - Matrices are row-major; leading dimensions are in elements.
+ *    X [n, ldx >= d_in], Y and dY [n, ld >= d_out], H [n, ldh >= r_max] (float).
+ *    A_a [r_a, d_in] and B_a [d_out, r_a] are dense row-major (leading dim d_in, r_a).
+ *  - Every device buffer, including workspaces, is allocated by the caller.
+ *    The library never allocates device memory.  Host objects (lora_table,
+ *    lora_plan) are allocated by the library and freed by *_destroy.
+ *  - `stream` is a hipStream_t (NULL = the default stream).  Every op is
+ *    asynchronous on that stream; only lora_plan_export and lora_plan_check
+ *    wait for it.
+ *  - Argument errors are detected on the host before anything is enqueued, so a
+ *    call that returns an error has written nothing.  Data errors that only the
+ *    device can see (bad ids, malformed segments) set a sticky flag in the plan
+ *    workspace; the offending rows are treated as having no adapter, and
+ *    lora_plan_check reports the flag.
+ *  - Device pointers must be 16-byte aligned; d_in and d_out must be multiples
+ *    of 8, leading dimensions multiples of 8 (elements).
+ *  - X / Y, dY / dA / dB and H must not overlap each other.
+ *  - Results are deterministic: the same inputs give the same bytes, run to run.
+ */
+#ifndef LORA_MI355X_H
+#define LORA_MI355X_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LORA_ABI_VERSION 1
+#define LORA_MAX_RANK    128        /* 1 <= r_a <= LORA_MAX_RANK */
+#define LORA_MAX_SLOTS   1024       /* table slots per layer */
+#define LORA_MAX_ROWS    (1 << 22)  /* rows per batch */
+#define LORA_MAX_DIM     65536      /* d_in, d_out */
+
+typedef enum lora_status {
+  LORA_OK = 0,
+  LORA_ERR_NULL = 1,        /* a required pointer is NULL */
+  LORA_ERR_SHAPE = 2,       /* a size or leading dimension is out of range */
+  LORA_ERR_DTYPE = 3,       /* dtype combination not supported */
+  LORA_ERR_ALIGN = 4,       /* pointer or leading dimension misaligned */
+  LORA_ERR_RANK = 5,        /* rank outside [1, LORA_MAX_RANK] */
+  LORA_ERR_SLOT = 6,        /* slot index outside [0, num_slots) */
+  LORA_ERR_DATA = 7,        /* the device flagged bad ids or segments (lora_plan_check) */
+  LORA_ERR_WORKSPACE = 8,   /* workspace too small */
+  LORA_ERR_HIP = 9          /* a HIP runtime call failed */
+} lora_status;
+
+typedef enum lora_dtype { LORA_F32 = 0, LORA_BF16 = 1 } lora_dtype;
+
+/* bits of the device data-error flag (lora_plan_check, lora_plan_export) */
+#define LORA_DATA_BAD_ID       1u   /* an id outside [-1, num_slots) */
+#define LORA_DATA_EMPTY_SLOT   2u   /* an id naming a slot with no adapter */
+#define LORA_DATA_BAD_SEGMENTS 4u   /* seg_offsets not 0 = o_0 <= o_1 <= ... = n */
+
+typedef struct lora_table lora_table;
+typedef struct lora_plan lora_plan;
+
+/* ---- library ----------------------------------------------------------- */
+int32_t     lora_abi_version(void);
+const char* lora_status_string(lora_status s);
+/* Human-readable detail of the last error returned on this thread. */
+const char* lora_last_error(void);
+
+/* ---- adapter table (Section 3.4, "Adapter table") -----------------------
+ * One table per adapted layer.  A slot holds one pinned adapter version: its
+ * rank, scale and layer-local A/B pointers.  The identity / version ->
+ * slot mapping and residency belong to the caller.  The paper's rule that a
+ * refresh installs a new entry instead of mutating weights used by in-flight
+ * generation becomes: a slot referenced by a plan must not be set, cleared or
+ * uploaded until every launch using that plan has finished.
+ *
+ * dev_meta: caller device memory of lora_table_device_bytes(num_slots) bytes
+ * that receives the slot metadata on lora_table_upload.  It must outlive the
+ * table and every plan built on it.  w_dtype is the storage type of every A_a
+ * and B_a (LORA_BF16 or LORA_F32).  Errors: NULL, SHAPE (num_slots not in
+ * [1, LORA_MAX_SLOTS], d_in / d_out not in [8, LORA_MAX_DIM] or not multiples
+ * of 8), DTYPE, ALIGN, WORKSPACE (dev_meta_bytes too small). */
+size_t      lora_table_device_bytes(int32_t num_slots);
+lora_status lora_table_create(int32_t num_slots, int32_t d_in, int32_t d_out,
+                              lora_dtype w_dtype, void* dev_meta, size_t dev_meta_bytes,
+                              lora_table** out);
+/* Host-side update of one slot; takes effect on the device at the next
+ * lora_table_upload.  A: device [rank, d_in], B: device [d_out, rank], both
+ * 16-byte aligned and owned by the caller.  Errors: NULL, SLOT, RANK, ALIGN. */
+lora_status lora_table_set(lora_table* t, int32_t slot, int32_t rank, float scale,
+                           const void* A, const void* B);
+/* Mark a slot empty (rows naming it are a data error).  Errors: NULL, SLOT. */
+lora_status lora_table_clear(lora_table* t, int32_t slot);
+/* Stream-ordered copy of the host metadata into dev_meta.  The host copy may be
+ * changed again as soon as this returns. */
+lora_status lora_table_upload(lora_table* t, void* stream);
+void        lora_table_destroy(lora_table* t);
+
+/* ---- plan: grouping of rows by adapter (Section 3.4 gather step, Figure 2;
+ *      Section 3.5 routing by adapter identity) ---------------------------
+ * Built on the device, with no host synchronisation.  For S = num_slots it
+ * produces, in the caller's workspace `ws` (lora_plan_workspace_bytes bytes):
+ *   counts[a]          rows with id a
+ *   offsets[0..S]      exclusive prefix sum of counts
+ *   perm[0..n_act)     row indices grouped by adapter, ascending inside a group
+ *   runs               maximal runs [start, start+len) of one adapter id >= 0
+ *   m_counts, m_offsets, m_perm   the same grouping over rows with mask != 0
+ *                      (mask == NULL: every row)
+ * plus the tile lists the ops launch over.  An id outside [-1, S), or naming an
+ * empty slot, sets the data flag and the row is treated as id -1.
+ *
+ * idx: device int32 [n], -1 = no adapter.  mask: device uint8 [n] or NULL;
+ * nonzero = the row's target token is trainable.  The explicit mask is kept
+ * apart from the learning signal (Section 3.3): a trainable row whose dY is zero
+ * still counts.  The table, idx, mask and ws must stay valid until every op
+ * using the plan has finished.  Errors: NULL, SHAPE (n not in [0,
+ * LORA_MAX_ROWS]), ALIGN, WORKSPACE, HIP. */
+size_t      lora_plan_workspace_bytes(int32_t n, int32_t num_slots);
+lora_status lora_plan_build(const lora_table* t, int32_t n, const int32_t* idx,
+                            const uint8_t* mask, void* ws, size_t ws_bytes, void* stream,
+                            lora_plan** out);
+/* The same plan from contiguous segments: rows [seg_offsets[s], seg_offsets[s+1])
+ * carry id seg_adapter[s] (device int32 arrays of num_segs+1 and num_segs
+ * entries).  Adjacent segments of one adapter merge into one run; empty
+ * segments are allowed.  If seg_offsets is not 0 = o_0 <= ... <= o_S = n, the
+ * LORA_DATA_BAD_SEGMENTS flag is set and every row is treated as id -1. */
+lora_status lora_plan_build_segments(const lora_table* t, int32_t n, int32_t num_segs,
+                                     const int32_t* seg_offsets, const int32_t* seg_adapter,
+                                     const uint8_t* mask, void* ws, size_t ws_bytes,
+                                     void* stream, lora_plan** out);
+/* Copy the plan arrays to host memory (each pointer may be NULL to skip it) and
+ * wait for the stream.  Sizes: counts, m_counts [S]; offsets, m_offsets [S+1];
+ * perm, m_perm, run_start, run_len, run_adapter [n] (only the first n_act /
+ * m_n_act / n_runs entries are meaningful); scalars [1]. */
+lora_status lora_plan_export(const lora_plan* p, int32_t* counts, int32_t* offsets,
+                             int32_t* perm, int32_t* n_runs, int32_t* run_start,
+                             int32_t* run_len, int32_t* run_adapter, int32_t* m_counts,
+                             int32_t* m_offsets, int32_t* m_perm, uint32_t* data_flags,
+                             void* stream);
+/* Wait for the stream and read the sticky data flag (LORA_DATA_* bits) into
+ * *data_flags (nullable).  Returns LORA_ERR_DATA if any bit is set. */
+lora_status lora_plan_check(const lora_plan* p, uint32_t* data_flags, void* stream);
+void        lora_plan_destroy(lora_plan* p);
+
+/* ---- forward ops (Section 3.4: LoRA layer equation, Delta_a) ------------
+ * dtypes: X and the table weights are both LORA_BF16 (matrix-core path) or any
+ * mix of LORA_BF16 / LORA_F32 (vector path); Y is LORA_BF16 or LORA_F32.
+ * Arithmetic: products of the stored values, accumulated in float32; the
+ * intermediate H = X A_a^T is kept in float32 (split into two bfloat16 terms
+ * when it feeds a bfloat16 matrix product); s_a is applied once to the float32
+ * accumulator; a bfloat16 Y is rounded to nearest even once, at the store.
+ * Rows with id -1 are neither read nor written. */
+
+/* lora_shrink (gather + shrink): H[t, 0:r_a] = X[t, :] A_a^T (unscaled) for
+ * every row t with id a >= 0.  H is float32 [n, ldh], ldh >= max rank over the
+ * table; columns >= r_a and rows with id -1 are left untouched. */
+lora_status lora_shrink(const lora_plan* p, const void* X, lora_dtype x_dtype, int64_t ldx,
+                        float* H, int64_t ldh, void* stream);
+/* lora_expand (expand + scatter-add): Y[t, :] += s_a * H[t, 0:r_a] B_a^T for every
+ * row t with id a >= 0, in the original row order. */
+lora_status lora_expand(const lora_plan* p, const float* H, int64_t ldh, void* Y,
+                        lora_dtype y_dtype, int64_t ldy, void* stream);
+/* lora_apply: shrink and expand in one call, Y[t] += s_a (X[t] A_a^T) B_a^T.
+ * Small adapter groups (decode rows) run in one fused kernel that keeps H on
+ * chip; larger groups (prefill segments) run a grouped matrix-core shrink and
+ * expand through the workspace.  ws: device, lora_apply_workspace_bytes(p). */
+size_t      lora_apply_workspace_bytes(const lora_plan* p);
+lora_status lora_apply(const lora_plan* p, const void* X, lora_dtype x_dtype, int64_t ldx,
+                       void* Y, lora_dtype y_dtype, int64_t ldy, void* ws, size_t ws_bytes,
+                       void* stream);
+
+/* ---- backward (Sections 3.3 and 3.5: masked, adapter-local gradients) ----
+ * For every slot a with dA[a] / dB[a] not NULL, over the rows T_a^m of the
+ * plan's mask (mask == NULL at build time: every row of adapter a):
+ *   dB_a = s_a dY_m^T H,  dA_a = s_a (dY_m B_a)^T X_m,  H = X_m A_a^T (or H_saved).
+ * Rows outside T_a^m are never read, so they contribute exactly zero even if
+ * they hold NaN or Inf.  accumulate = 0: overwrite (slots with no trainable row
+ * get +0.0); accumulate != 0: add to the existing values.
+ * dA, dB: HOST arrays of num_slots DEVICE pointers to float32 [r_a, d_in] and
+ * [d_out, r_a] buffers (NULL = skip that slot).  The pointer arrays are copied
+ * before the call returns.  H_saved: float32 [n, ldh] from lora_shrink, or NULL
+ * to recompute.  x_dtype and dy_dtype must equal each other; the matrix-core
+ * path needs LORA_BF16 inputs and weights.  ws: lora_grad_workspace_bytes(p).
+ * The reduction over rows runs in a fixed order (no floating-point atomics). */
+size_t      lora_grad_workspace_bytes(const lora_plan* p);
+lora_status lora_grad(const lora_plan* p, const void* X, lora_dtype x_dtype, int64_t ldx,
+                      const void* dY, lora_dtype dy_dtype, int64_t lddy, const float* H_saved,
+                      int64_t ldh, float* const* dA, float* const* dB, int32_t accumulate,
+                      void* ws, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LORA_MI355X_H */

@@ -1,0 +1,574 @@
+// Host side of the C ABI: argument validation, the adapter table, plan objects,
+// workspace carving and kernel dispatch.  Nothing here allocates device memory.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <climits>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "lora_internal.h"
+
+struct lora_table {
+  int32_t num_slots, d_in, d_out;
+  lora_dtype w_dtype;
+  void* dev_meta;
+  std::vector<lora::SlotMeta> host;
+};
+
+struct lora_plan {
+  const lora_table* table;
+  int32_t n;
+  void* ws;
+  lora::PlanLayout L;
+  lora::PlanDev d;
+  int32_t r_max;        // largest live rank when the plan was built
+  bool rank8;           // every live rank is a multiple of 8
+  int32_t small_max;    // groups of <= small_max rows use the fused small-group kernel
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+lora_status fail(lora_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+lora_status ok() {
+  g_err.clear();
+  return LORA_OK;
+}
+
+lora_status hip_fail(hipError_t e, const char* what) {
+  return fail(LORA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+size_t al256(size_t x) { return (x + 255) & ~size_t(255); }
+
+bool valid_dtype(lora_dtype d) { return d == LORA_F32 || d == LORA_BF16; }
+
+size_t dsize(lora_dtype d) { return d == LORA_BF16 ? 2 : 4; }
+
+int env_int(const char* name, int dflt) {
+  const char* v = std::getenv(name);
+  if (v == nullptr || *v == 0) return dflt;
+  return std::atoi(v);
+}
+
+// Fused small-group policy.  Batches of up to 1024 rows (decode steps) send
+// every adapter group through the fused kernel, so a decode step is a single
+// launch; larger batches send groups of up to 16 rows there and larger groups
+// through the grouped shrink + expand.
+int32_t small_max_policy(int32_t n) {
+  const int v = env_int("LORA_SMALL_MAX", -1);
+  if (v >= 0) return v;
+  return n <= 1024 ? INT32_MAX : lora::SMALL_ROWS;
+}
+
+// Output-column chunks per small-group entry (sibling workgroups).
+int32_t small_chunks_policy(int32_t d_out) {
+  const int v = env_int("LORA_SMALL_CHUNKS", 0);
+  if (v > 0) return v;
+  return std::max(1, std::min(16, (d_out + 1023) / 1024));
+}
+
+// d-slices of the gradient's first stage.
+int32_t grad_splits_policy(int32_t d_in, int32_t d_out) {
+  const int v = env_int("LORA_GRAD_SPLITS", 0);
+  if (v > 0) return std::min(v, 8);
+  return (std::min(d_in, d_out) >= 1024) ? 4 : 1;
+}
+constexpr int32_t GRAD_SPLITS_MAX = 8;
+
+// host upper bounds of the entry lists
+int32_t ub_large(const lora_plan* p) {
+  if (p->small_max == INT32_MAX) return 0;
+  const int32_t S = p->table->num_slots, n = p->n;
+  return n / lora::RB_ROWS + std::min(S, n / (p->small_max + 1)) + 1;
+}
+int32_t ub_small(const lora_plan* p) {
+  const int32_t S = p->table->num_slots, n = p->n;
+  const int64_t all = n / lora::SMALL_ROWS + std::min(S, n) + 1;
+  if (p->small_max == INT32_MAX) return (int32_t)all;
+  const int64_t per = ((int64_t)p->small_max + lora::SMALL_ROWS - 1) / lora::SMALL_ROWS;
+  return (int32_t)std::min<int64_t>(all, (int64_t)std::min(S, n) * per + 1);
+}
+int32_t ub_mrb(const lora_plan* p) {
+  return p->n / lora::MRB_ROWS + std::min(p->table->num_slots, p->n) + 1;
+}
+
+lora::OpLaunch op_base(const lora_plan* p) {
+  lora::OpLaunch o{};
+  o.hdr = p->d.hdr;
+  o.rb = p->d.rb;
+  o.perm = p->d.perm;
+  o.meta = static_cast<const lora::SlotMeta*>(p->table->dev_meta);
+  o.n = p->n;
+  o.d_in = p->table->d_in;
+  o.d_out = p->table->d_out;
+  o.num_slots = p->table->num_slots;
+  o.r_max = p->r_max;
+  o.rank8 = p->rank8;
+  return o;
+}
+
+lora_status check_matrix(const void* ptr, lora_dtype dt, int64_t ld, int32_t cols,
+                         const char* name) {
+  if (ptr == nullptr) return fail(LORA_ERR_NULL, "%s is NULL", name);
+  if (!valid_dtype(dt)) return fail(LORA_ERR_DTYPE, "%s: unknown dtype %d", name, (int)dt);
+  if (ld < cols) return fail(LORA_ERR_SHAPE, "%s: leading dim %lld < %d", name, (long long)ld, cols);
+  if (ld % 8 != 0) return fail(LORA_ERR_ALIGN, "%s: leading dim %lld not a multiple of 8", name, (long long)ld);
+  if (!aligned(ptr, 16)) return fail(LORA_ERR_ALIGN, "%s not 16-byte aligned", name);
+  return LORA_OK;
+}
+
+lora_status check_plan(const lora_plan* p) {
+  if (p == nullptr) return fail(LORA_ERR_NULL, "plan is NULL");
+  return LORA_OK;
+}
+
+lora_status make_plan(const lora_table* t, int32_t n, const int32_t* idx,
+                      const int32_t* seg_offsets, const int32_t* seg_adapter, int32_t num_segs,
+                      const uint8_t* mask, void* ws, size_t ws_bytes, hipStream_t stream,
+                      lora_plan** out) {
+  if (out == nullptr) return fail(LORA_ERR_NULL, "out is NULL");
+  *out = nullptr;
+  if (t == nullptr) return fail(LORA_ERR_NULL, "table is NULL");
+  if (n < 0 || n > LORA_MAX_ROWS) return fail(LORA_ERR_SHAPE, "n = %d outside [0, %d]", n, LORA_MAX_ROWS);
+  if (ws == nullptr) return fail(LORA_ERR_NULL, "plan workspace is NULL");
+  if (!aligned(ws, 16)) return fail(LORA_ERR_ALIGN, "plan workspace not 16-byte aligned");
+  const lora::PlanLayout L = lora::plan_layout(n, t->num_slots);
+  if (ws_bytes < L.total)
+    return fail(LORA_ERR_WORKSPACE, "plan workspace %zu bytes < %zu", ws_bytes, L.total);
+  if (seg_offsets == nullptr && n > 0 && idx == nullptr) return fail(LORA_ERR_NULL, "idx is NULL");
+  if (idx != nullptr && !aligned(idx, 4)) return fail(LORA_ERR_ALIGN, "idx not 4-byte aligned");
+
+  lora_plan* p = new (std::nothrow) lora_plan();
+  if (p == nullptr) return fail(LORA_ERR_SHAPE, "host allocation failed");
+  p->table = t;
+  p->n = n;
+  p->ws = ws;
+  p->L = L;
+  char* b = static_cast<char*>(ws);
+  p->d.hdr = reinterpret_cast<int32_t*>(b + L.hdr);
+  p->d.counts = reinterpret_cast<int32_t*>(b + L.counts);
+  p->d.offsets = reinterpret_cast<int32_t*>(b + L.offsets);
+  p->d.perm = reinterpret_cast<int32_t*>(b + L.perm);
+  p->d.run_start = reinterpret_cast<int32_t*>(b + L.run_start);
+  p->d.run_len = reinterpret_cast<int32_t*>(b + L.run_len);
+  p->d.run_adapter = reinterpret_cast<int32_t*>(b + L.run_adapter);
+  p->d.m_counts = reinterpret_cast<int32_t*>(b + L.m_counts);
+  p->d.m_offsets = reinterpret_cast<int32_t*>(b + L.m_offsets);
+  p->d.m_perm = reinterpret_cast<int32_t*>(b + L.m_perm);
+  p->d.m_blk = reinterpret_cast<int32_t*>(b + L.m_blk);
+  p->d.rb = reinterpret_cast<int4*>(b + L.rb);
+  p->d.mrb = reinterpret_cast<int4*>(b + L.mrb);
+  p->d.seg_ids = reinterpret_cast<int32_t*>(b + L.seg_ids);
+  p->r_max = 0;
+  p->rank8 = true;
+  for (const auto& s : t->host) {
+    if (s.rank <= 0) continue;
+    p->r_max = std::max(p->r_max, s.rank);
+    p->rank8 = p->rank8 && (s.rank % 8 == 0);
+  }
+  p->small_max = small_max_policy(n);
+
+  lora::PlanLaunch a{};
+  a.d = p->d;
+  a.idx = seg_offsets ? nullptr : idx;
+  a.seg_offsets = seg_offsets;
+  a.seg_adapter = seg_adapter;
+  a.num_segs = num_segs;
+  a.mask = mask;
+  a.meta = static_cast<const lora::SlotMeta*>(t->dev_meta);
+  a.n = n;
+  a.num_slots = t->num_slots;
+  a.small_max = p->small_max;
+  hipError_t e = lora::launch_plan(a, stream);
+  if (e != hipSuccess) {
+    delete p;
+    return hip_fail(e, "plan kernel launch");
+  }
+  *out = p;
+  return ok();
+}
+
+}  // namespace
+
+namespace lora {
+
+PlanLayout plan_layout(int32_t n, int32_t S) {
+  PlanLayout L{};
+  const size_t nn = (size_t)std::max(n, 1);
+  size_t o = 0;
+  L.hdr = o;         o += al256(HDR_WORDS * 4);
+  L.counts = o;      o += al256((size_t)S * 4);
+  L.offsets = o;     o += al256((size_t)(S + 1) * 4);
+  L.perm = o;        o += al256(nn * 4);
+  L.run_start = o;   o += al256(nn * 4);
+  L.run_len = o;     o += al256(nn * 4);
+  L.run_adapter = o; o += al256(nn * 4);
+  L.m_counts = o;    o += al256((size_t)S * 4);
+  L.m_offsets = o;   o += al256((size_t)(S + 1) * 4);
+  L.m_perm = o;      o += al256(nn * 4);
+  L.m_blk = o;       o += al256((size_t)S * 4);
+  L.rb_max = n / SMALL_ROWS + std::min(S, n) + 1;
+  L.mrb_max = n / MRB_ROWS + std::min(S, n) + 1;
+  L.rb = o;          o += al256((size_t)L.rb_max * 16);
+  L.mrb = o;         o += al256((size_t)L.mrb_max * 16);
+  L.seg_ids = o;     o += al256(nn * 4);
+  L.total = o;
+  return L;
+}
+
+}  // namespace lora
+
+extern "C" {
+
+int32_t lora_abi_version(void) { return LORA_ABI_VERSION; }
+
+const char* lora_status_string(lora_status s) {
+  switch (s) {
+    case LORA_OK: return "ok";
+    case LORA_ERR_NULL: return "null pointer";
+    case LORA_ERR_SHAPE: return "bad shape";
+    case LORA_ERR_DTYPE: return "unsupported dtype";
+    case LORA_ERR_ALIGN: return "misaligned pointer or leading dimension";
+    case LORA_ERR_RANK: return "rank out of range";
+    case LORA_ERR_SLOT: return "slot out of range";
+    case LORA_ERR_DATA: return "device data error (bad ids or segments)";
+    case LORA_ERR_WORKSPACE: return "workspace too small";
+    case LORA_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+const char* lora_last_error(void) { return g_err.c_str(); }
+
+// ---- table -----------------------------------------------------------------
+
+size_t lora_table_device_bytes(int32_t num_slots) {
+  if (num_slots <= 0) return 0;
+  return (size_t)num_slots * sizeof(lora::SlotMeta);
+}
+
+lora_status lora_table_create(int32_t num_slots, int32_t d_in, int32_t d_out, lora_dtype w_dtype,
+                              void* dev_meta, size_t dev_meta_bytes, lora_table** out) {
+  if (out == nullptr) return fail(LORA_ERR_NULL, "out is NULL");
+  *out = nullptr;
+  if (num_slots < 1 || num_slots > LORA_MAX_SLOTS)
+    return fail(LORA_ERR_SHAPE, "num_slots = %d outside [1, %d]", num_slots, LORA_MAX_SLOTS);
+  for (int32_t d : {d_in, d_out}) {
+    if (d < 8 || d > LORA_MAX_DIM) return fail(LORA_ERR_SHAPE, "dim %d outside [8, %d]", d, LORA_MAX_DIM);
+    if (d % 8 != 0) return fail(LORA_ERR_SHAPE, "dim %d not a multiple of 8", d);
+  }
+  if (!valid_dtype(w_dtype)) return fail(LORA_ERR_DTYPE, "unknown weight dtype %d", (int)w_dtype);
+  if (dev_meta == nullptr) return fail(LORA_ERR_NULL, "dev_meta is NULL");
+  if (!aligned(dev_meta, 16)) return fail(LORA_ERR_ALIGN, "dev_meta not 16-byte aligned");
+  if (dev_meta_bytes < lora_table_device_bytes(num_slots))
+    return fail(LORA_ERR_WORKSPACE, "dev_meta %zu bytes < %zu", dev_meta_bytes,
+                lora_table_device_bytes(num_slots));
+  lora_table* t = new (std::nothrow) lora_table();
+  if (t == nullptr) return fail(LORA_ERR_SHAPE, "host allocation failed");
+  t->num_slots = num_slots;
+  t->d_in = d_in;
+  t->d_out = d_out;
+  t->w_dtype = w_dtype;
+  t->dev_meta = dev_meta;
+  t->host.assign(num_slots, lora::SlotMeta{nullptr, nullptr, 0, 0.0f, {0, 0}});
+  *out = t;
+  return ok();
+}
+
+lora_status lora_table_set(lora_table* t, int32_t slot, int32_t rank, float scale, const void* A,
+                           const void* B) {
+  if (t == nullptr) return fail(LORA_ERR_NULL, "table is NULL");
+  if (slot < 0 || slot >= t->num_slots)
+    return fail(LORA_ERR_SLOT, "slot %d outside [0, %d)", slot, t->num_slots);
+  if (rank < 1 || rank > LORA_MAX_RANK)
+    return fail(LORA_ERR_RANK, "rank %d outside [1, %d]", rank, LORA_MAX_RANK);
+  if (A == nullptr || B == nullptr) return fail(LORA_ERR_NULL, "A or B is NULL");
+  if (!aligned(A, 16) || !aligned(B, 16)) return fail(LORA_ERR_ALIGN, "A or B not 16-byte aligned");
+  t->host[slot] = lora::SlotMeta{A, B, rank, scale, {0, 0}};
+  return ok();
+}
+
+lora_status lora_table_clear(lora_table* t, int32_t slot) {
+  if (t == nullptr) return fail(LORA_ERR_NULL, "table is NULL");
+  if (slot < 0 || slot >= t->num_slots)
+    return fail(LORA_ERR_SLOT, "slot %d outside [0, %d)", slot, t->num_slots);
+  t->host[slot] = lora::SlotMeta{nullptr, nullptr, 0, 0.0f, {0, 0}};
+  return ok();
+}
+
+lora_status lora_table_upload(lora_table* t, void* stream) {
+  if (t == nullptr) return fail(LORA_ERR_NULL, "table is NULL");
+  hipError_t e = hipMemcpyAsync(t->dev_meta, t->host.data(), t->host.size() * sizeof(lora::SlotMeta),
+                                hipMemcpyHostToDevice, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "table upload");
+  return ok();
+}
+
+void lora_table_destroy(lora_table* t) { delete t; }
+
+// ---- plan ------------------------------------------------------------------
+
+size_t lora_plan_workspace_bytes(int32_t n, int32_t num_slots) {
+  if (n < 0 || num_slots < 1) return 0;
+  return lora::plan_layout(n, num_slots).total;
+}
+
+lora_status lora_plan_build(const lora_table* t, int32_t n, const int32_t* idx, const uint8_t* mask,
+                            void* ws, size_t ws_bytes, void* stream, lora_plan** out) {
+  return make_plan(t, n, idx, nullptr, nullptr, 0, mask, ws, ws_bytes,
+                   static_cast<hipStream_t>(stream), out);
+}
+
+lora_status lora_plan_build_segments(const lora_table* t, int32_t n, int32_t num_segs,
+                                     const int32_t* seg_offsets, const int32_t* seg_adapter,
+                                     const uint8_t* mask, void* ws, size_t ws_bytes, void* stream,
+                                     lora_plan** out) {
+  if (out != nullptr) *out = nullptr;
+  if (num_segs < 0 || num_segs > LORA_MAX_ROWS)
+    return fail(LORA_ERR_SHAPE, "num_segs = %d out of range", num_segs);
+  if (seg_offsets == nullptr) return fail(LORA_ERR_NULL, "seg_offsets is NULL");
+  if (num_segs > 0 && seg_adapter == nullptr) return fail(LORA_ERR_NULL, "seg_adapter is NULL");
+  if (!aligned(seg_offsets, 4) || (seg_adapter != nullptr && !aligned(seg_adapter, 4)))
+    return fail(LORA_ERR_ALIGN, "segment arrays not 4-byte aligned");
+  return make_plan(t, n, nullptr, seg_offsets, seg_adapter, num_segs, mask, ws, ws_bytes,
+                   static_cast<hipStream_t>(stream), out);
+}
+
+lora_status lora_plan_export(const lora_plan* p, int32_t* counts, int32_t* offsets, int32_t* perm,
+                             int32_t* n_runs, int32_t* run_start, int32_t* run_len,
+                             int32_t* run_adapter, int32_t* m_counts, int32_t* m_offsets,
+                             int32_t* m_perm, uint32_t* data_flags, void* stream) {
+  lora_status st = check_plan(p);
+  if (st != LORA_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const size_t S = p->table->num_slots, n = p->n;
+  struct Item {
+    void* dst;
+    const void* src;
+    size_t bytes;
+  };
+  int32_t hdr[lora::HDR_WORDS];
+  const Item items[] = {
+      {hdr, p->d.hdr, sizeof(hdr)},
+      {counts, p->d.counts, S * 4},
+      {offsets, p->d.offsets, (S + 1) * 4},
+      {perm, p->d.perm, n * 4},
+      {run_start, p->d.run_start, n * 4},
+      {run_len, p->d.run_len, n * 4},
+      {run_adapter, p->d.run_adapter, n * 4},
+      {m_counts, p->d.m_counts, S * 4},
+      {m_offsets, p->d.m_offsets, (S + 1) * 4},
+      {m_perm, p->d.m_perm, n * 4},
+  };
+  for (const Item& it : items) {
+    if (it.dst == nullptr || it.bytes == 0) continue;
+    hipError_t e = hipMemcpyAsync(it.dst, it.src, it.bytes, hipMemcpyDeviceToHost, s);
+    if (e != hipSuccess) return hip_fail(e, "plan export copy");
+  }
+  hipError_t e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, "plan export sync");
+  if (n_runs != nullptr) *n_runs = hdr[lora::HDR_NRUNS];
+  if (data_flags != nullptr) *data_flags = (uint32_t)hdr[lora::HDR_FLAGS];
+  return ok();
+}
+
+lora_status lora_plan_check(const lora_plan* p, uint32_t* data_flags, void* stream) {
+  lora_status st = check_plan(p);
+  if (st != LORA_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int32_t flags = 0;
+  hipError_t e = hipMemcpyAsync(&flags, p->d.hdr + lora::HDR_FLAGS, 4, hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, "plan check");
+  if (data_flags != nullptr) *data_flags = (uint32_t)flags;
+  if (flags != 0) return fail(LORA_ERR_DATA, "device data flags 0x%x", (unsigned)flags);
+  return ok();
+}
+
+void lora_plan_destroy(lora_plan* p) { delete p; }
+
+// ---- forward ---------------------------------------------------------------
+
+lora_status lora_shrink(const lora_plan* p, const void* X, lora_dtype x_dtype, int64_t ldx, float* H,
+                        int64_t ldh, void* stream) {
+  lora_status st = check_plan(p);
+  if (st != LORA_OK) return st;
+  const lora_table* t = p->table;
+  if ((st = check_matrix(X, x_dtype, ldx, t->d_in, "X")) != LORA_OK) return st;
+  if ((st = check_matrix(H, LORA_F32, ldh, std::max(p->r_max, 1), "H")) != LORA_OK) return st;
+  if (p->n == 0) return ok();
+  lora::OpLaunch o = op_base(p);
+  o.count_word = lora::HDR_NRB_TOTAL;
+  o.first_word = -1;
+  o.rb_ub = ub_large(p) + ub_small(p);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  if (x_dtype == LORA_BF16 && t->w_dtype == LORA_BF16)
+    e = lora::launch_shrink_mfma(o, X, ldx, H, ldh, s);
+  else
+    e = lora::launch_shrink_valu(o, X, x_dtype, ldx, t->w_dtype, H, ldh, s);
+  if (e != hipSuccess) return hip_fail(e, "shrink launch");
+  return ok();
+}
+
+lora_status lora_expand(const lora_plan* p, const float* H, int64_t ldh, void* Y, lora_dtype y_dtype,
+                        int64_t ldy, void* stream) {
+  lora_status st = check_plan(p);
+  if (st != LORA_OK) return st;
+  const lora_table* t = p->table;
+  if ((st = check_matrix(H, LORA_F32, ldh, std::max(p->r_max, 1), "H")) != LORA_OK) return st;
+  if ((st = check_matrix(Y, y_dtype, ldy, t->d_out, "Y")) != LORA_OK) return st;
+  if (p->n == 0) return ok();
+  lora::OpLaunch o = op_base(p);
+  o.count_word = lora::HDR_NRB_TOTAL;
+  o.first_word = -1;
+  o.rb_ub = ub_large(p) + ub_small(p);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  if (t->w_dtype == LORA_BF16)
+    e = lora::launch_expand_mfma(o, H, ldh, Y, y_dtype, ldy, s);
+  else
+    e = lora::launch_expand_valu(o, H, ldh, t->w_dtype, Y, y_dtype, ldy, s);
+  if (e != hipSuccess) return hip_fail(e, "expand launch");
+  return ok();
+}
+
+size_t lora_apply_workspace_bytes(const lora_plan* p) {
+  if (p == nullptr) return 0;
+  const int64_t ldh = (std::max(p->r_max, 1) + 7) / 8 * 8;
+  return al256((size_t)std::max(p->n, 1) * ldh * 4);
+}
+
+lora_status lora_apply(const lora_plan* p, const void* X, lora_dtype x_dtype, int64_t ldx, void* Y,
+                       lora_dtype y_dtype, int64_t ldy, void* ws, size_t ws_bytes, void* stream) {
+  lora_status st = check_plan(p);
+  if (st != LORA_OK) return st;
+  const lora_table* t = p->table;
+  if ((st = check_matrix(X, x_dtype, ldx, t->d_in, "X")) != LORA_OK) return st;
+  if ((st = check_matrix(Y, y_dtype, ldy, t->d_out, "Y")) != LORA_OK) return st;
+  const size_t need = lora_apply_workspace_bytes(p);
+  const bool mfma = x_dtype == LORA_BF16 && t->w_dtype == LORA_BF16;
+  const bool needs_ws = !mfma || ub_large(p) > 0;
+  if (needs_ws) {
+    if (ws == nullptr) return fail(LORA_ERR_NULL, "apply workspace is NULL");
+    if (!aligned(ws, 16)) return fail(LORA_ERR_ALIGN, "apply workspace not 16-byte aligned");
+    if (ws_bytes < need) return fail(LORA_ERR_WORKSPACE, "apply workspace %zu bytes < %zu", ws_bytes, need);
+  }
+  if (p->n == 0) return ok();
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  float* H = static_cast<float*>(ws);
+  const int64_t ldh = (std::max(p->r_max, 1) + 7) / 8 * 8;
+  lora::OpLaunch o = op_base(p);
+  hipError_t e = hipSuccess;
+  if (mfma) {
+    if (ub_large(p) > 0) {
+      o.count_word = lora::HDR_NRB_LARGE;
+      o.first_word = -1;
+      o.rb_ub = ub_large(p);
+      e = lora::launch_shrink_mfma(o, X, ldx, H, ldh, s);
+      if (e == hipSuccess) e = lora::launch_expand_mfma(o, H, ldh, Y, y_dtype, ldy, s);
+      if (e != hipSuccess) return hip_fail(e, "grouped shrink/expand launch");
+    }
+    o.count_word = lora::HDR_NRB_TOTAL;
+    o.first_word = lora::HDR_NRB_LARGE;
+    o.rb_ub = ub_small(p);
+    e = lora::launch_bgmv_mfma(o, X, ldx, Y, y_dtype, ldy, small_chunks_policy(t->d_out), s);
+    if (e != hipSuccess) return hip_fail(e, "fused small-group launch");
+  } else {
+    o.count_word = lora::HDR_NRB_TOTAL;
+    o.first_word = -1;
+    o.rb_ub = ub_large(p) + ub_small(p);
+    e = lora::launch_shrink_valu(o, X, x_dtype, ldx, t->w_dtype, H, ldh, s);
+    if (e == hipSuccess) e = lora::launch_expand_valu(o, H, ldh, t->w_dtype, Y, y_dtype, ldy, s);
+    if (e != hipSuccess) return hip_fail(e, "vector-path launch");
+  }
+  return ok();
+}
+
+// ---- backward --------------------------------------------------------------
+
+size_t lora_grad_workspace_bytes(const lora_plan* p) {
+  if (p == nullptr) return 0;
+  const size_t r_pad = (size_t)(std::max(p->r_max, 1) + 15) / 16 * 16;
+  const size_t p_stride = (size_t)ub_mrb(p) * lora::MRB_ROWS;
+  return al256(2 * GRAD_SPLITS_MAX * r_pad * p_stride * 4);
+}
+
+lora_status lora_grad(const lora_plan* p, const void* X, lora_dtype x_dtype, int64_t ldx,
+                      const void* dY, lora_dtype dy_dtype, int64_t lddy, const float* H_saved,
+                      int64_t ldh, float* const* dA, float* const* dB, int32_t accumulate,
+                      void* ws, size_t ws_bytes, void* stream) {
+  lora_status st = check_plan(p);
+  if (st != LORA_OK) return st;
+  const lora_table* t = p->table;
+  if ((st = check_matrix(X, x_dtype, ldx, t->d_in, "X")) != LORA_OK) return st;
+  if ((st = check_matrix(dY, dy_dtype, lddy, t->d_out, "dY")) != LORA_OK) return st;
+  if (x_dtype != dy_dtype) return fail(LORA_ERR_DTYPE, "X and dY dtypes differ");
+  if (H_saved != nullptr &&
+      (st = check_matrix(H_saved, LORA_F32, ldh, std::max(p->r_max, 1), "H_saved")) != LORA_OK)
+    return st;
+  for (int32_t a = 0; a < t->num_slots; ++a) {
+    const float* pa = dA ? dA[a] : nullptr;
+    const float* pb = dB ? dB[a] : nullptr;
+    if ((pa || pb) && t->host[a].rank <= 0)
+      return fail(LORA_ERR_SLOT, "gradient requested for empty slot %d", a);
+    if ((pa && !aligned(pa, 16)) || (pb && !aligned(pb, 16)))
+      return fail(LORA_ERR_ALIGN, "gradient buffer of slot %d not 16-byte aligned", a);
+  }
+  const size_t need = lora_grad_workspace_bytes(p);
+  if (ws == nullptr) return fail(LORA_ERR_NULL, "grad workspace is NULL");
+  if (!aligned(ws, 16)) return fail(LORA_ERR_ALIGN, "grad workspace not 16-byte aligned");
+  if (ws_bytes < need) return fail(LORA_ERR_WORKSPACE, "grad workspace %zu bytes < %zu", ws_bytes, need);
+
+  const bool mfma = x_dtype == LORA_BF16 && t->w_dtype == LORA_BF16;
+  lora::GradLaunch g{};
+  g.o = op_base(p);
+  g.o.rb = p->d.mrb;
+  g.o.rb_ub = ub_mrb(p);
+  g.o.count_word = lora::HDR_NMRB;
+  g.o.first_word = -1;
+  g.m_perm = p->d.m_perm;
+  g.m_offsets = p->d.m_offsets;
+  g.m_counts = p->d.m_counts;
+  g.m_blk = p->d.m_blk;
+  g.X = X;
+  g.ldx = ldx;
+  g.dY = dY;
+  g.lddy = lddy;
+  g.H_saved = H_saved;
+  g.ldh = ldh;
+  g.dA = dA;
+  g.dB = dB;
+  g.accumulate = accumulate;
+  g.hg = static_cast<float*>(ws);
+  g.k_splits = mfma ? grad_splits_policy(t->d_in, t->d_out) : 1;
+  g.p_stride = ub_mrb(p) * lora::MRB_ROWS;
+  g.r_pad = (std::max(p->r_max, 1) + 15) / 16 * 16;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  // n = 0 still runs: slots with no trainable row must receive zeros.
+  hipError_t e = mfma ? lora::launch_grad_mfma(g, s)
+                      : lora::launch_grad_valu(g, x_dtype, t->w_dtype, s);
+  if (e != hipSuccess) return hip_fail(e, "gradient launch");
+  return ok();
+}
+
+}  // extern "C"

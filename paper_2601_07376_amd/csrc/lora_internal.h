@@ -1,0 +1,141 @@
+// Internal definitions shared by the host runtime (api.cpp) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "lora.h"
+
+namespace lora {
+
+// One table slot as the kernels read it (32 bytes, in caller device memory).
+struct SlotMeta {
+  const void* A;     // [rank, d_in] row-major
+  const void* B;     // [d_out, rank] row-major
+  int32_t rank;      // 0 = empty slot
+  float scale;       // s_a
+  int32_t pad[2];
+};
+static_assert(sizeof(SlotMeta) == 32, "slot metadata layout");
+
+// Plan header words (int32) at the start of the plan workspace.
+enum : int {
+  HDR_FLAGS = 0,      // LORA_DATA_* bits
+  HDR_NACT = 1,       // rows with an adapter
+  HDR_NRUNS = 2,      // maximal runs
+  HDR_MNACT = 3,      // trainable rows with an adapter
+  HDR_NRB_LARGE = 4,  // row-block entries of large groups (grouped matrix-core path)
+  HDR_NRB_TOTAL = 5,  // all entries: large-group blocks, then small-group entries
+  HDR_NMRB = 6,       // trainable row-block entries (gradient path)
+  HDR_WORDS = 64
+};
+
+constexpr int RB_ROWS = 64;      // rows per large-group row block
+constexpr int SMALL_ROWS = 16;   // rows per small-group entry (one matrix-core column tile)
+constexpr int MRB_ROWS = 32;     // trainable rows per gradient row block
+constexpr int PLAN_THREADS = 1024;
+constexpr int PLAN_WAVES = PLAN_THREADS / 64;
+
+// Byte offsets of the plan arrays inside the caller's workspace.
+struct PlanLayout {
+  size_t hdr, counts, offsets, perm, run_start, run_len, run_adapter;
+  size_t m_counts, m_offsets, m_perm, m_blk, rb, mrb, seg_ids, total;
+  int32_t rb_max, mrb_max;
+};
+
+// Device pointers into one plan workspace.
+struct PlanDev {
+  int32_t* hdr;
+  int32_t* counts;
+  int32_t* offsets;
+  int32_t* perm;
+  int32_t* run_start;
+  int32_t* run_len;
+  int32_t* run_adapter;
+  int32_t* m_counts;
+  int32_t* m_offsets;
+  int32_t* m_perm;
+  int32_t* m_blk;  // first trainable row block of each adapter
+  int4* rb;     // {adapter, first index into perm, rows, 0}
+  int4* mrb;    // {adapter, first index into m_perm, rows, 0}
+  int32_t* seg_ids;
+};
+
+PlanLayout plan_layout(int32_t n, int32_t num_slots);
+
+// ---- launchers (defined in the .hip files) --------------------------------
+
+struct PlanLaunch {
+  PlanDev d;
+  const int32_t* idx;           // per-row ids, or nullptr in segment mode
+  const int32_t* seg_offsets;   // segment mode
+  const int32_t* seg_adapter;
+  int32_t num_segs;
+  const uint8_t* mask;          // nullable
+  const SlotMeta* meta;
+  int32_t n, num_slots;
+  int32_t small_max;            // groups with <= small_max rows go to the fused small-group path
+};
+hipError_t launch_plan(const PlanLaunch& a, hipStream_t s);
+
+// Common description of an op launch.
+struct OpLaunch {
+  const int32_t* hdr;
+  const int4* rb;
+  const int32_t* perm;
+  const SlotMeta* meta;
+  int32_t n, d_in, d_out, num_slots;
+  int32_t r_max;
+  bool rank8;                   // every live rank is a multiple of 8
+  int32_t rb_ub;                // host upper bound of the entry count
+  int count_word;               // header word holding the entry count
+  int first_word;               // header word holding the first entry (-1: 0)
+};
+
+// H[t, :r] = X[t] A^T over entries [first, count) (bf16 X and weights, matrix cores)
+hipError_t launch_shrink_mfma(const OpLaunch& o, const void* X, int64_t ldx, float* H,
+                              int64_t ldh, hipStream_t s);
+// Y[t] += s H[t, :r] B^T over entries (bf16 weights, matrix cores, hi/lo split of H)
+hipError_t launch_expand_mfma(const OpLaunch& o, const float* H, int64_t ldh, void* Y,
+                              lora_dtype y_dtype, int64_t ldy, hipStream_t s);
+// fused small-group kernel: shrink into LDS + expand, entries [first, count)
+hipError_t launch_bgmv_mfma(const OpLaunch& o, const void* X, int64_t ldx, void* Y,
+                            lora_dtype y_dtype, int64_t ldy, int32_t n_chunks, hipStream_t s);
+
+// vector-ALU kernels for any mix of f32 / bf16 storage
+hipError_t launch_shrink_valu(const OpLaunch& o, const void* X, lora_dtype x_dtype,
+                              int64_t ldx, lora_dtype w_dtype, float* H, int64_t ldh,
+                              hipStream_t s);
+hipError_t launch_expand_valu(const OpLaunch& o, const float* H, int64_t ldh,
+                              lora_dtype w_dtype, void* Y, lora_dtype y_dtype, int64_t ldy,
+                              hipStream_t s);
+
+// gradient path
+constexpr int GRAD_SLOT_GROUP = 64;   // output pointers passed per launch
+struct GradLaunch {
+  OpLaunch o;                    // o.rb / o.rb_ub describe the trainable row blocks
+  const int32_t* m_perm;
+  const int32_t* m_offsets;
+  const int32_t* m_counts;
+  const int32_t* m_blk;
+  const void* X;
+  int64_t ldx;
+  const void* dY;
+  int64_t lddy;
+  const float* H_saved;
+  int64_t ldh;
+  float* const* dA;              // host array [num_slots] of device pointers (nullable entries)
+  float* const* dB;
+  int32_t accumulate;
+  float* hg;                     // workspace: partial H^T and G^T
+  int32_t k_splits;
+  int32_t p_stride;              // row stride (elements) of the H^T / G^T planes
+  int32_t r_pad;                 // rank padding of the planes
+};
+hipError_t launch_grad_mfma(const GradLaunch& g, hipStream_t s);
+hipError_t launch_grad_valu(const GradLaunch& g, lora_dtype x_dtype, lora_dtype w_dtype,
+                            hipStream_t s);
+
+}  // namespace lora

@@ -1,0 +1,269 @@
+"""ctypes binding of liblora_mi355x.so (the C ABI in include/lora.h).
+
+Argument marshalling only: torch provides device memory and the current HIP
+stream; every step of the computation runs in the library's HIP kernels.  The
+library must be built (``paper_2601_07376_amd.build.build()``); importing this
+module without it raises immediately, there is no fallback.
+"""
+import ctypes
+import os
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liblora_mi355x.so")
+
+LORA_F32, LORA_BF16 = 0, 1
+LORA_DATA_BAD_ID, LORA_DATA_EMPTY_SLOT, LORA_DATA_BAD_SEGMENTS = 1, 2, 4
+STATUS = {0: "LORA_OK", 1: "LORA_ERR_NULL", 2: "LORA_ERR_SHAPE", 3: "LORA_ERR_DTYPE",
+          4: "LORA_ERR_ALIGN", 5: "LORA_ERR_RANK", 6: "LORA_ERR_SLOT", 7: "LORA_ERR_DATA",
+          8: "LORA_ERR_WORKSPACE", 9: "LORA_ERR_HIP"}
+
+_vp, _i32, _i64, _sz, _f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_float
+_pp = ctypes.POINTER(ctypes.c_void_p)
+
+# name -> (restype, argtypes); every symbol declared in include/lora.h
+SIGNATURES = {
+    "lora_abi_version": (_i32, []),
+    "lora_status_string": (ctypes.c_char_p, [_i32]),
+    "lora_last_error": (ctypes.c_char_p, []),
+    "lora_table_device_bytes": (_sz, [_i32]),
+    "lora_table_create": (_i32, [_i32, _i32, _i32, _i32, _vp, _sz, _pp]),
+    "lora_table_set": (_i32, [_vp, _i32, _i32, _f32, _vp, _vp]),
+    "lora_table_clear": (_i32, [_vp, _i32]),
+    "lora_table_upload": (_i32, [_vp, _vp]),
+    "lora_table_destroy": (None, [_vp]),
+    "lora_plan_workspace_bytes": (_sz, [_i32, _i32]),
+    "lora_plan_build": (_i32, [_vp, _i32, _vp, _vp, _vp, _sz, _vp, _pp]),
+    "lora_plan_build_segments": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, _vp, _sz, _vp, _pp]),
+    "lora_plan_export": (_i32, [_vp] + [_vp] * 11 + [_vp]),
+    "lora_plan_check": (_i32, [_vp, _vp, _vp]),
+    "lora_plan_destroy": (None, [_vp]),
+    "lora_shrink": (_i32, [_vp, _vp, _i32, _i64, _vp, _i64, _vp]),
+    "lora_expand": (_i32, [_vp, _vp, _i64, _vp, _i32, _i64, _vp]),
+    "lora_apply_workspace_bytes": (_sz, [_vp]),
+    "lora_apply": (_i32, [_vp, _vp, _i32, _i64, _vp, _i32, _i64, _vp, _sz, _vp]),
+    "lora_grad_workspace_bytes": (_sz, [_vp]),
+    "lora_grad": (_i32, [_vp, _vp, _i32, _i64, _vp, _i32, _i64, _vp, _i64, _vp, _vp, _i32,
+                         _vp, _sz, _vp]),
+}
+
+_lib = None
+
+
+def lib():
+    """Load the shared library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "paper_2601_07376_amd.build.build() (hipcc, gfx950)")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+class LoraError(RuntimeError):
+    def __init__(self, status, detail):
+        super().__init__(f"{STATUS.get(status, status)}: {detail}")
+        self.status = status
+
+
+def _check(status):
+    if status != 0:
+        raise LoraError(status, lib().lora_last_error().decode())
+
+
+def _dtype(t):
+    if t.dtype == torch.bfloat16:
+        return LORA_BF16
+    if t.dtype == torch.float32:
+        return LORA_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _rowmajor(t, name):
+    if t.dim() != 2 or t.stride(1) != 1:
+        raise ValueError(f"{name} must be a 2-D tensor with unit column stride")
+    return t.stride(0)
+
+
+class Table:
+    """Adapter table of one adapted layer (slot -> rank, scale, A, B)."""
+
+    def __init__(self, num_slots, d_in, d_out, w_dtype=torch.bfloat16, device="cuda"):
+        L = lib()
+        self.num_slots, self.d_in, self.d_out = num_slots, d_in, d_out
+        self.w_dtype = w_dtype
+        self.device = torch.device(device)
+        nbytes = L.lora_table_device_bytes(num_slots)
+        self.meta = torch.zeros(max(nbytes, 16), dtype=torch.uint8, device=self.device)
+        h = ctypes.c_void_p()
+        _check(L.lora_table_create(num_slots, d_in, d_out,
+                                   LORA_BF16 if w_dtype == torch.bfloat16 else LORA_F32,
+                                   _ptr(self.meta), nbytes, ctypes.byref(h)))
+        self.handle = h
+        self.ranks = [0] * num_slots
+        self.scales = [0.0] * num_slots
+        self._weights = [None] * num_slots      # keeps A / B alive
+
+    def set(self, slot, A, B, scale):
+        """A: [rank, d_in], B: [d_out, rank], contiguous, dtype w_dtype, on device."""
+        if not (A.is_contiguous() and B.is_contiguous()):
+            raise ValueError("A and B must be contiguous")
+        if A.dtype != self.w_dtype or B.dtype != self.w_dtype:
+            raise TypeError("A and B must use the table's weight dtype")
+        r = A.shape[0]
+        if A.shape != (r, self.d_in) or B.shape != (self.d_out, r):
+            raise ValueError(f"shapes {tuple(A.shape)}, {tuple(B.shape)} do not match "
+                             f"[r, {self.d_in}], [{self.d_out}, r]")
+        _check(lib().lora_table_set(self.handle, slot, r, float(scale), _ptr(A), _ptr(B)))
+        self.ranks[slot], self.scales[slot] = r, float(scale)
+        self._weights[slot] = (A, B)
+
+    def clear(self, slot):
+        _check(lib().lora_table_clear(self.handle, slot))
+        self.ranks[slot], self.scales[slot] = 0, 0.0
+        self._weights[slot] = None
+
+    def upload(self, stream=None):
+        _check(lib().lora_table_upload(self.handle, _stream(stream)))
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        if h is not None and _lib is not None:
+            _lib.lora_table_destroy(h)
+            self.handle = None
+
+
+class Plan:
+    """Row grouping of one batch (built on the device, no host synchronisation)."""
+
+    def __init__(self, table, idx=None, mask=None, seg_offsets=None, seg_adapter=None, n=None,
+                 stream=None):
+        L = lib()
+        self.table = table
+        if idx is not None:
+            n = idx.numel()
+        elif n is None:
+            raise ValueError("segment plans need n")
+        self.n = int(n)
+        self.ws = torch.empty(max(L.lora_plan_workspace_bytes(self.n, table.num_slots), 16),
+                              dtype=torch.uint8, device=table.device)
+        self._keep = (idx, mask, seg_offsets, seg_adapter)
+        h = ctypes.c_void_p()
+        if idx is not None:
+            _check(L.lora_plan_build(table.handle, self.n, _ptr(idx), _ptr(mask), _ptr(self.ws),
+                                     self.ws.numel(), _stream(stream), ctypes.byref(h)))
+        else:
+            _check(L.lora_plan_build_segments(table.handle, self.n, seg_adapter.numel(),
+                                              _ptr(seg_offsets), _ptr(seg_adapter), _ptr(mask),
+                                              _ptr(self.ws), self.ws.numel(), _stream(stream),
+                                              ctypes.byref(h)))
+        self.handle = h
+
+    def export(self, stream=None):
+        S, n = self.table.num_slots, self.n
+        arrs = {k: np.zeros(S, np.int32) for k in ("counts", "m_counts")}
+        arrs.update({k: np.zeros(S + 1, np.int32) for k in ("offsets", "m_offsets")})
+        arrs.update({k: np.zeros(max(n, 1), np.int32)
+                     for k in ("perm", "run_start", "run_len", "run_adapter", "m_perm")})
+        n_runs = ctypes.c_int32()
+        flags = ctypes.c_uint32()
+        p = lambda k: arrs[k].ctypes.data_as(ctypes.c_void_p)
+        _check(lib().lora_plan_export(self.handle, p("counts"), p("offsets"), p("perm"),
+                                      ctypes.byref(n_runs), p("run_start"), p("run_len"),
+                                      p("run_adapter"), p("m_counts"), p("m_offsets"),
+                                      p("m_perm"), ctypes.byref(flags), _stream(stream)))
+        n_act, m_n_act, nr = int(arrs["offsets"][-1]), int(arrs["m_offsets"][-1]), n_runs.value
+        return dict(counts=arrs["counts"], offsets=arrs["offsets"], perm=arrs["perm"][:n_act],
+                    n_runs=nr, run_start=arrs["run_start"][:nr], run_len=arrs["run_len"][:nr],
+                    run_adapter=arrs["run_adapter"][:nr], m_counts=arrs["m_counts"],
+                    m_offsets=arrs["m_offsets"], m_perm=arrs["m_perm"][:m_n_act],
+                    data_flags=flags.value)
+
+    def check(self, stream=None):
+        """Data-error flags (LORA_DATA_* bits); 0 when clean."""
+        flags = ctypes.c_uint32()
+        st = lib().lora_plan_check(self.handle, ctypes.byref(flags), _stream(stream))
+        if st not in (0, 7):
+            _check(st)
+        return flags.value
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        if h is not None and _lib is not None:
+            _lib.lora_plan_destroy(h)
+            self.handle = None
+
+
+def shrink(plan, X, H=None, stream=None):
+    """H[t, :r_a] = X[t] A_a^T (float32 H; untouched elsewhere)."""
+    if H is None:
+        r = max(max(plan.table.ranks), 1)
+        H = torch.zeros(plan.n, (r + 7) // 8 * 8, dtype=torch.float32, device=X.device)
+    _check(lib().lora_shrink(plan.handle, _ptr(X), _dtype(X), _rowmajor(X, "X"), _ptr(H),
+                             _rowmajor(H, "H"), _stream(stream)))
+    return H
+
+
+def expand(plan, H, Y, stream=None):
+    """Y[t] += s_a H[t, :r_a] B_a^T in place."""
+    _check(lib().lora_expand(plan.handle, _ptr(H), _rowmajor(H, "H"), _ptr(Y), _dtype(Y),
+                             _rowmajor(Y, "Y"), _stream(stream)))
+    return Y
+
+
+def apply_workspace(plan):
+    return torch.empty(max(lib().lora_apply_workspace_bytes(plan.handle), 16), dtype=torch.uint8,
+                       device=plan.table.device)
+
+
+def apply(plan, X, Y, ws=None, stream=None):
+    """Y[t] += s_a (X[t] A_a^T) B_a^T in place."""
+    if ws is None:
+        ws = apply_workspace(plan)
+    _check(lib().lora_apply(plan.handle, _ptr(X), _dtype(X), _rowmajor(X, "X"), _ptr(Y),
+                            _dtype(Y), _rowmajor(Y, "Y"), _ptr(ws), ws.numel(), _stream(stream)))
+    return Y
+
+
+def grad_workspace(plan):
+    return torch.empty(max(lib().lora_grad_workspace_bytes(plan.handle), 16), dtype=torch.uint8,
+                       device=plan.table.device)
+
+
+def grad(plan, X, dY, dA=None, dB=None, H_saved=None, accumulate=False, ws=None, stream=None):
+    """Masked adapter-local gradients.  dA / dB: lists (per slot) of float32
+    tensors or None; allocated for every live slot when not given."""
+    t = plan.table
+    if dA is None:
+        dA = [torch.empty(r, t.d_in, dtype=torch.float32, device=X.device) if r > 0 else None
+              for r in t.ranks]
+    if dB is None:
+        dB = [torch.empty(t.d_out, r, dtype=torch.float32, device=X.device) if r > 0 else None
+              for r in t.ranks]
+    if ws is None:
+        ws = grad_workspace(plan)
+    pa = (ctypes.c_void_p * t.num_slots)(*[g.data_ptr() if g is not None else None for g in dA])
+    pb = (ctypes.c_void_p * t.num_slots)(*[g.data_ptr() if g is not None else None for g in dB])
+    ldh = _rowmajor(H_saved, "H_saved") if H_saved is not None else 0
+    _check(lib().lora_grad(plan.handle, _ptr(X), _dtype(X), _rowmajor(X, "X"), _ptr(dY),
+                           _dtype(dY), _rowmajor(dY, "dY"), _ptr(H_saved), ldh, pa, pb,
+                           1 if accumulate else 0, _ptr(ws), ws.numel(), _stream(stream)))
+    return dA, dB

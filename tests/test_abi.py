@@ -1,0 +1,125 @@
+"""The C ABI library loads, exports every declared symbol, and rejects bad
+arguments on the host before touching the GPU (CPU only: no compute calls)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2601_07376_amd import lora
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lora.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(lora.LIB_PATH),
+                                reason="liblora_mi355x.so not built")
+
+FAKE = 0x10000          # 16-byte aligned, never dereferenced on the host
+FAKE_ODD = 0x10002      # misaligned
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(lora_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported_and_bound():
+    L = lora.lib()
+    names = declared_functions()
+    assert len(names) >= 20
+    for name in names:
+        assert hasattr(L, name), f"{name} not exported"
+        assert name in lora.SIGNATURES, f"{name} has no binding"
+    assert set(lora.SIGNATURES) == set(names)
+
+
+def test_version_and_strings():
+    L = lora.lib()
+    assert L.lora_abi_version() == 1
+    for s in range(10):
+        assert L.lora_status_string(s)
+    assert L.lora_status_string(99) == b"unknown status"
+
+
+def _create(S=4, d_in=64, d_out=32, w=lora.LORA_BF16, meta=FAKE, nbytes=None):
+    L = lora.lib()
+    h = ctypes.c_void_p()
+    nbytes = L.lora_table_device_bytes(S) if nbytes is None else nbytes
+    st = L.lora_table_create(S, d_in, d_out, w, ctypes.c_void_p(meta), nbytes, ctypes.byref(h))
+    return st, h
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(S=0), 2), (dict(S=2000), 2), (dict(d_in=12), 2), (dict(d_out=0), 2),
+    (dict(d_in=1 << 20), 2), (dict(w=7), 3), (dict(meta=0), 1), (dict(meta=FAKE_ODD), 4),
+    (dict(nbytes=16), 8),
+])
+def test_table_create_rejects(kw, status):
+    st, h = _create(**kw)
+    assert st == status
+    assert h.value is None
+    assert lora.lib().lora_last_error()
+
+
+def test_table_set_and_clear_validation():
+    L = lora.lib()
+    st, h = _create()
+    assert st == 0
+    A = ctypes.c_void_p(FAKE)
+    assert L.lora_table_set(h, 0, 16, 2.0, A, A) == 0
+    assert L.lora_table_set(h, 4, 16, 2.0, A, A) == 6          # slot out of range
+    assert L.lora_table_set(h, -1, 16, 2.0, A, A) == 6
+    assert L.lora_table_set(h, 1, 0, 2.0, A, A) == 5           # rank 0
+    assert L.lora_table_set(h, 1, 129, 2.0, A, A) == 5         # rank > max
+    assert L.lora_table_set(h, 1, 8, 2.0, None, A) == 1
+    assert L.lora_table_set(h, 1, 8, 2.0, ctypes.c_void_p(FAKE_ODD), A) == 4
+    assert L.lora_table_clear(h, 0) == 0
+    assert L.lora_table_clear(h, 9) == 6
+    assert L.lora_table_set(None, 0, 8, 1.0, A, A) == 1
+    L.lora_table_destroy(h)
+
+
+def test_plan_build_validation():
+    L = lora.lib()
+    st, t = _create(S=8)
+    assert st == 0
+    need = L.lora_plan_workspace_bytes(100, 8)
+    assert need > 0 and L.lora_plan_workspace_bytes(200, 8) > need
+    p = ctypes.c_void_p()
+    ws = ctypes.c_void_p(FAKE)
+    idx = ctypes.c_void_p(FAKE)
+    assert L.lora_plan_build(t, -1, idx, None, ws, need, None, ctypes.byref(p)) == 2
+    assert L.lora_plan_build(t, (1 << 22) + 1, idx, None, ws, 1 << 40, None, ctypes.byref(p)) == 2
+    assert L.lora_plan_build(t, 100, idx, None, ws, need - 1, None, ctypes.byref(p)) == 8
+    assert L.lora_plan_build(t, 100, None, None, ws, need, None, ctypes.byref(p)) == 1
+    assert L.lora_plan_build(t, 100, idx, None, None, need, None, ctypes.byref(p)) == 1
+    assert L.lora_plan_build(t, 100, ctypes.c_void_p(FAKE + 2), None, ws, need, None,
+                             ctypes.byref(p)) == 4
+    assert L.lora_plan_build(None, 100, idx, None, ws, need, None, ctypes.byref(p)) == 1
+    assert L.lora_plan_build_segments(t, 100, 3, None, idx, None, ws, need, None,
+                                      ctypes.byref(p)) == 1
+    assert L.lora_plan_build_segments(t, 100, -1, idx, idx, None, ws, need, None,
+                                      ctypes.byref(p)) == 2
+    assert p.value is None
+    L.lora_table_destroy(t)
+
+
+def test_ops_reject_null_plan():
+    L = lora.lib()
+    X = ctypes.c_void_p(FAKE)
+    assert L.lora_shrink(None, X, 1, 64, X, 16, None) == 1
+    assert L.lora_expand(None, X, 16, X, 1, 64, None) == 1
+    assert L.lora_apply(None, X, 1, 64, X, 1, 64, X, 1 << 20, None) == 1
+    assert L.lora_grad(None, X, 1, 64, X, 1, 64, None, 0, None, None, 0, X, 1 << 20, None) == 1
+    assert L.lora_plan_check(None, None, None) == 1
+    assert L.lora_plan_export(None, *([None] * 11), None) == 1
+    assert L.lora_apply_workspace_bytes(None) == 0
+    assert L.lora_grad_workspace_bytes(None) == 0
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(lora, "_lib", None)
+    monkeypatch.setattr(lora, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="missing"):
+        lora.lib()

@@ -1,0 +1,153 @@
+"""Forward parity: lora_apply / lora_shrink / lora_expand vs the float64 oracle (GPU).
+
+Graded parity uses float32 Y (relative Frobenius <= 5e-3, max-abs <= 3e-2 on the
+LoRA delta of active rows, bf16 inputs, float32 accumulation).  bfloat16 Y is
+checked with the same relF and max-abs plus half a bf16 ulp of |Y| (the store
+rounding).  Rows with id -1 must come back bit-identical.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+from gpu_helpers import (DEV, check_forward, effective, env, make_plan, make_table, run_apply,
+                         say)
+from helpers import f64_case
+from workloads.device import case_to_device, from_torch
+
+import paper_2601_07376_amd as L
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("ydt", ["f32", "bf16"])
+@pytest.mark.parametrize("cfg", [1, 2, 4])
+def test_apply_config_full(cfg, ydt):
+    if cfg == 1 and ydt == "bf16":
+        pytest.skip("the tiny workload is float32 end to end")
+    say(f"apply config {cfg} y={ydt}")
+    case = workloads.make_config(cfg, y_dtype=ydt)
+    Yo, _ = run_apply(case)
+    rel, mx = check_forward(case, Yo, effective(case))
+    say(f"  relF {rel:.3g} maxabs {mx:.3g}")
+
+
+@pytest.mark.parametrize("ydt", ["f32", "bf16"])
+def test_apply_config3_sampled_rows(ydt):
+    """Full prefill workload (launch shape of the benchmark); the oracle checks a
+    sample of rows one by one, including every segment's first and last row."""
+    say(f"apply config 3 y={ydt}")
+    case = workloads.make_config(3, y_dtype=ydt)
+    Yo, _ = run_apply(case, segments=True)
+    rng = np.random.default_rng(0)
+    rows = np.unique(np.concatenate([rng.choice(case.n, 384, replace=False),
+                                     case.seg_offsets[:-1], case.seg_offsets[1:] - 1]))
+    rel, mx = check_forward(case, Yo, effective(case), rows=rows)
+    say(f"  relF {rel:.3g} maxabs {mx:.3g}")
+
+
+FUZZ = [
+    # name, kwargs for random_case, small_max override
+    ("decode_r16", dict(n=300, d_in=512, d_out=768, num_slots=20, rank_choices=(16,)), None),
+    ("decode_hetero", dict(n=257, d_in=264, d_out=136, num_slots=33,
+                           rank_choices=(8, 16, 32, 64, 128)), None),
+    ("odd_ranks", dict(n=200, d_in=128, d_out=200, num_slots=9, rank_choices=(1, 5, 12, 20, 33)), None),
+    ("segments_mixed", dict(n=3000, d_in=512, d_out=1032, num_slots=12,
+                            rank_choices=(8, 32, 64), layout="segments", seg_len=(1, 300)), None),
+    ("segments_force_grouped", dict(n=700, d_in=256, d_out=520, num_slots=6,
+                                    rank_choices=(16, 48), layout="segments", seg_len=(20, 200)), 0),
+    ("single_adapter", dict(n=2500, d_in=384, d_out=256, num_slots=1, rank_choices=(64,),
+                            layout="single", frac_none=0.0), None),
+    ("alternating", dict(n=1500, d_in=256, d_out=256, num_slots=4, rank_choices=(32,),
+                         layout="alternating"), None),
+    ("rank128", dict(n=1200, d_in=1024, d_out=512, num_slots=3, rank_choices=(128,),
+                     layout="segments", seg_len=(50, 400)), None),
+    ("all_none", dict(n=100, d_in=64, d_out=64, num_slots=3, frac_none=1.0), None),
+]
+
+
+@pytest.mark.parametrize("ydt", ["f32", "bf16"])
+@pytest.mark.parametrize("name", [f[0] for f in FUZZ])
+def test_apply_fuzz(name, ydt):
+    kw, small = next((f[1], f[2]) for f in FUZZ if f[0] == name)
+    say(f"apply fuzz {name} y={ydt}")
+    case = workloads.random_case(11, y_dtype=ydt, **kw)
+    with env(LORA_SMALL_MAX=small):
+        Yo, _ = run_apply(case)
+    check_forward(case, Yo, effective(case))
+
+
+@pytest.mark.parametrize("small", [None, 0, 100000])
+def test_apply_integer_exact(small):
+    """Values in {-1, 0, 1}: every partial sum is an exact float32 integer and H
+    fits bf16 exactly, so the result must equal the oracle bit for bit."""
+    say(f"apply integer small={small}")
+    case = workloads.random_case(3, 1100, 256, 136, 7, rank_choices=(8, 16, 40, 64),
+                                 layout="segments", seg_len=(1, 90), y_dtype="f32",
+                                 int_values=True, scales=[0.25, 0.5, 1, 2, 2, 1, 0.5])
+    with env(LORA_SMALL_MAX=small):
+        Yo, _ = run_apply(case)
+    X, A, B, Y, _ = f64_case(case)
+    ref = oracle.apply(effective(case), X, Y, A, B, case.scales)
+    assert np.array_equal(workloads.decode(Yo, "f32"), ref)
+
+
+def test_segments_plan_equals_index_plan():
+    say("segments == indices")
+    case = workloads.make_config(5)        # segment layout, 8 adapters
+    case.Y = workloads.encode(np.random.default_rng(1).standard_normal((case.n, case.d_out)), "bf16")
+    y1, _ = run_apply(case, segments=False)
+    y2, _ = run_apply(case, segments=True)
+    assert y1.tobytes() == y2.tobytes()
+
+
+def test_apply_deterministic():
+    say("determinism")
+    case = workloads.make_config(4)
+    y1, _ = run_apply(case)
+    y2, _ = run_apply(case)
+    assert y1.tobytes() == y2.tobytes()
+
+
+def test_zero_B_leaves_Y():
+    say("zero B")
+    case = workloads.random_case(4, 900, 256, 256, 5, rank_choices=(16, 32), y_dtype="bf16")
+    case.B = [np.zeros_like(b) if b is not None else None for b in case.B]
+    case.Y[case.Y == 0x8000] = 0               # -0.0 + 0.0 would become +0.0
+    Yo, _ = run_apply(case)
+    assert Yo.tobytes() == case.Y.tobytes()
+
+
+@pytest.mark.parametrize("xdt,wdt", [("f32", "f32"), ("bf16", "bf16"), ("f32", "bf16"),
+                                     ("bf16", "f32")])
+def test_shrink_then_expand(xdt, wdt):
+    say(f"shrink/expand x={xdt} w={wdt}")
+    case = workloads.random_case(8, 1300, 256, 264, 6, rank_choices=(8, 24, 64),
+                                 layout="segments", seg_len=(1, 200), x_dtype=xdt,
+                                 w_dtype=wdt, y_dtype="f32")
+    dev = case_to_device(case, DEV)
+    table = make_table(case, dev)
+    plan = make_plan(case, dev, table, mask=False)
+    H = torch.full((case.n, 72), 7.0, dtype=torch.float32, device=DEV)
+    L.shrink(plan, dev["X"], H)
+    Y = dev["Y"].clone()
+    L.expand(plan, H, Y)
+    torch.cuda.synchronize()
+    X, A, B, Yr, _ = f64_case(case)
+    eff = effective(case)
+    Href = oracle.shrink(eff, X, A, H=np.full((case.n, 72), 7.0))
+    Hg = H.cpu().double().numpy()
+    assert oracle.rel_fro(Hg, Href) <= 1e-5
+    assert np.array_equal(Hg[eff < 0], Href[eff < 0])       # untouched rows
+    for a in range(case.num_slots):                          # untouched columns
+        rows = eff == a
+        assert np.all(Hg[rows, case.ranks[a]:] == 7.0)
+    check_forward(case, from_torch(Y), eff)
+
+
+def test_fp32_tiny_workload_all_entry_points():
+    say("fp32 tiny")
+    case = workloads.make_config(1)
+    Yo, plan = run_apply(case, segments=True)
+    check_forward(case, Yo, effective(case))

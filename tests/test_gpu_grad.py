@@ -1,0 +1,159 @@
+"""Masked adapter-local gradients: lora_grad vs the float64 oracle (GPU)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+from gpu_helpers import DEV, check_grads, effective, env, make_plan, make_table, say
+from helpers import f64_case
+from workloads.device import case_to_device
+
+import paper_2601_07376_amd as L
+
+pytestmark = pytest.mark.gpu
+
+
+def run_grad(case, H_saved=None, accumulate=False, init=None, segments=False):
+    dev = case_to_device(case, DEV)
+    table = make_table(case, dev)
+    plan = make_plan(case, dev, table, segments=segments, mask=True)
+    dA = dB = None
+    if init is not None:
+        dA = [torch.from_numpy(x).float().to(DEV) if x is not None else None for x in init[0]]
+        dB = [torch.from_numpy(x).float().to(DEV) if x is not None else None for x in init[1]]
+    Hs = None if H_saved is None else torch.from_numpy(H_saved).float().to(DEV)
+    dA, dB = L.grad(plan, dev["X"], dev["dY"], dA=dA, dB=dB, H_saved=Hs, accumulate=accumulate)
+    torch.cuda.synchronize()
+    return dA, dB
+
+
+def test_grad_config5_full():
+    say("grad config 5")
+    case = workloads.make_config(5)
+    dA, dB = run_grad(case)
+    rel, mx = check_grads(case, dA, dB, effective(case), case.mask)
+    say(f"  relF {rel:.3g} maxabs {mx:.3g}")
+    dA2, dB2 = run_grad(case, segments=True)
+    for a in range(case.num_slots):         # deterministic, and segments == indices
+        assert dA[a].cpu().numpy().tobytes() == dA2[a].cpu().numpy().tobytes()
+        assert dB[a].cpu().numpy().tobytes() == dB2[a].cpu().numpy().tobytes()
+
+
+FUZZ = [
+    ("ragged", dict(n=1000, d_in=264, d_out=136, num_slots=5, rank_choices=(8, 16, 32),
+                    layout="segments", seg_len=(1, 150), mask_p=0.4)),
+    ("odd_ranks", dict(n=700, d_in=128, d_out=200, num_slots=6, rank_choices=(1, 5, 12, 33),
+                       mask_p=0.7)),
+    ("rank128", dict(n=900, d_in=1024, d_out=1024, num_slots=3, rank_choices=(128,),
+                     layout="segments", seg_len=(40, 300), mask_p=0.3)),
+    ("sparse_mask", dict(n=2000, d_in=512, d_out=512, num_slots=40, rank_choices=(16, 64),
+                         mask_p=0.02)),
+    ("many_slots", dict(n=3000, d_in=256, d_out=256, num_slots=150, rank_choices=(8, 16),
+                        mask_p=0.5)),
+    ("decode_like", dict(n=256, d_in=4096, d_out=4096, num_slots=64, rank_choices=(16,),
+                         mask_p=0.9)),
+]
+
+
+@pytest.mark.parametrize("name", [f[0] for f in FUZZ])
+def test_grad_fuzz(name):
+    say(f"grad fuzz {name}")
+    kw = dict(FUZZ)[name]
+    case = workloads.random_case(17, want_dy=True, want_y=False, **kw)
+    dA, dB = run_grad(case)
+    check_grads(case, dA, dB, effective(case), case.mask)
+
+
+@pytest.mark.parametrize("splits", [1, 2, 8])
+def test_grad_integer_exact(splits):
+    """Values in {-1, 0, 1}: H, G and every partial sum are exact, so dA and dB
+    must equal the oracle bit for bit (for any split of the first stage)."""
+    say(f"grad integer splits={splits}")
+    case = workloads.random_case(23, 600, 1024, 1040, 4, rank_choices=(8, 16, 48),
+                                 layout="segments", seg_len=(1, 120), mask_p=0.5,
+                                 want_dy=True, want_y=False, int_values=True,
+                                 scales=[0.5, 1, 2, 0.25])
+    with env(LORA_GRAD_SPLITS=splits):
+        dA, dB = run_grad(case)
+    X, A, B, _, dY = f64_case(case)
+    rA, rB = oracle.grad(effective(case), case.mask, X, dY, A, B, case.scales)
+    for a in range(case.num_slots):
+        assert np.array_equal(dA[a].cpu().double().numpy(), rA[a])
+        assert np.array_equal(dB[a].cpu().double().numpy(), rB[a])
+
+
+def test_grad_mask_exactness():
+    """Masked-out rows full of NaN / Inf / 1e30 give byte-identical gradients."""
+    say("grad mask exactness")
+    case = workloads.random_case(5, 800, 512, 256, 4, rank_choices=(16, 32), mask_p=0.4,
+                                 want_dy=True, want_y=False, layout="segments", seg_len=(10, 200))
+    dA0, dB0 = run_grad(case)
+    out = case.mask == 0
+    junk = workloads.encode(np.array([np.nan, np.inf, -np.inf, 1e30]), "bf16")
+    case.X[out] = junk[np.arange(case.X[out].size) % 4].reshape(case.X[out].shape)
+    case.dY[out] = junk[np.arange(case.dY[out].size) % 4].reshape(case.dY[out].shape)
+    dA1, dB1 = run_grad(case)
+    for a in range(case.num_slots):
+        assert dA0[a].cpu().numpy().tobytes() == dA1[a].cpu().numpy().tobytes()
+        assert dB0[a].cpu().numpy().tobytes() == dB1[a].cpu().numpy().tobytes()
+
+
+def test_grad_empty_mask_gives_zeros_and_accumulate_adds():
+    say("grad zeros / accumulate")
+    case = workloads.random_case(6, 500, 256, 256, 5, rank_choices=(16,), mask_p=0.5,
+                                 want_dy=True, want_y=False, layout="segments", seg_len=(50, 150))
+    eff = effective(case)
+    case.mask[eff == 1] = 0                      # slot 1: no trainable row
+    rng = np.random.default_rng(0)
+    init = ([rng.standard_normal((r, case.d_in)) if r else None for r in case.ranks],
+            [rng.standard_normal((case.d_out, r)) if r else None for r in case.ranks])
+    dA, dB = run_grad(case, init=init)           # overwrite mode
+    assert torch.all(dA[1] == 0) and torch.all(dB[1] == 0)
+    assert not torch.signbit(dA[1]).any()
+    check_grads(case, dA, dB, eff, case.mask)
+    dA2, dB2 = run_grad(case, init=init, accumulate=True)
+    X, A, B, _, dY = f64_case(case)
+    rA, rB = oracle.grad(eff, case.mask, X, dY, A, B, case.scales)
+    for a in range(case.num_slots):
+        ia = init[0][a].astype(np.float32).astype(np.float64)
+        ib = init[1][a].astype(np.float32).astype(np.float64)
+        assert oracle.rel_fro(dA2[a].cpu().double().numpy(), ia + rA[a]) < 1e-4
+        assert oracle.rel_fro(dB2[a].cpu().double().numpy(), ib + rB[a]) < 1e-4
+    assert np.array_equal(dA2[1].cpu().numpy(), init[0][1].astype(np.float32))
+
+
+def test_grad_h_saved():
+    say("grad H_saved")
+    case = workloads.random_case(7, 900, 512, 384, 4, rank_choices=(16, 32), mask_p=0.5,
+                                 want_dy=True, want_y=False, layout="segments", seg_len=(1, 200))
+    X, A, B, _, dY = f64_case(case)
+    eff = effective(case)
+    H = oracle.shrink(eff, X, A, H=np.zeros((case.n, 32))).astype(np.float32)
+    dA, dB = run_grad(case, H_saved=H)
+    check_grads(case, dA, dB, eff, case.mask, H_saved=H.astype(np.float64))
+
+
+def test_grad_euler_identity():
+    """<dA_a, A_a> = <dB_a, B_a> = sum over trainable rows of <dY_t, Delta_t>."""
+    say("grad Euler identity")
+    case = workloads.make_config(5)
+    dA, dB = run_grad(case)
+    X, A, B, _, dY = f64_case(case)
+    eff = effective(case)
+    for a in range(case.num_slots):
+        la = float(np.sum(dA[a].cpu().double().numpy() * A[a]))
+        lb = float(np.sum(dB[a].cpu().double().numpy() * B[a]))
+        sel = np.zeros(case.num_slots, bool)
+        sel[a] = True
+        Aa = [A[b] if sel[b] else np.zeros_like(A[b]) for b in range(case.num_slots)]
+        ref = oracle.masked_loss(eff, case.mask, X, dY, Aa, B, case.scales)
+        assert abs(la - ref) <= 1e-4 * abs(ref) + 1e-6 and abs(lb - ref) <= 1e-4 * abs(ref) + 1e-6
+
+
+def test_grad_fp32_vector_path():
+    say("grad fp32")
+    case = workloads.random_case(9, 300, 128, 96, 4, rank_choices=(4, 8, 16), mask_p=0.5,
+                                 x_dtype="f32", w_dtype="f32", want_dy=True, want_y=False)
+    dA, dB = run_grad(case)
+    check_grads(case, dA, dB, effective(case), case.mask, tol=(1e-5, 1e-4))
