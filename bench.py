@@ -1,0 +1,382 @@
+#!/usr/bin/env python3
+"""Benchmark of the mixed-adapter LoRA layer on one MI355X.
+
+One step = one pass of the whole hot path over one batch: the device-built row
+grouping (plan) followed by the forward residual (lora_apply), or, for the
+masked-backward workload, the plan followed by lora_grad.  The headline line is
+the decode workload (256 single-token rows over 64 rank-16 adapters, hidden
+4096 -> 4096, bf16): tokens/s of whole steps.  The other four workloads are
+measured the same way and reported under "extra".
+
+Measurement protocol
+  * inputs are resident in HBM before timing; each workload keeps R copies of its
+    inputs and weights at distinct addresses and step i uses copy i % R, with
+    R * working set >= 576 MB, so every step reads cold (no Infinity Cache hits
+    left over from the previous step);
+  * the timed region is enqueued behind a GPU-side start gate (a bounded sleep
+    kernel), so the GPU runs the K steps back to back without waiting on the
+    host; HIP events on the compute stream bracket the region and each op;
+  * achieved bandwidth = algorithmic bytes (each tensor counted once at its
+    minimum: touched rows of X and Y, touched adapters' weights, ids) divided by
+    the average op duration; the peak is MI355X's 8 TB/s HBM.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--configs 1,2,3,4,5]
+"""
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0      # dense bf16 matrix cores
+FP32_PEAK_TFLOPS = 157.3       # vector fp32
+ROTATE_BYTES = 576 << 20       # >= 2 x 288 MB of rotating working set
+HEADLINE = 2
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+KERNEL_SOURCES = ["fwd_mfma.hip", "grad.hip", "plan.hip", "fwd_valu.hip"]
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--configs", default="1,2,3,4,5")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="also run a plain 1 GiB device copy (counter calibration)")
+    return ap.parse_args()
+
+
+def source_digest():
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2601_07376_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+# ----------------------------------------------------------------------------
+# algorithmic bytes and flops (each tensor once, at its minimum)
+# ----------------------------------------------------------------------------
+
+def workload_counts(case):
+    idx = case.idx
+    act = idx >= 0
+    touched = np.unique(idx[act])
+    xs = 2 if case.x_dtype == "bf16" else 4
+    ws = 2 if case.w_dtype == "bf16" else 4
+    ys = 2 if case.y_dtype == "bf16" else 4
+    d_in, d_out = case.d_in, case.d_out
+    ranks = case.ranks.astype(np.int64)
+    if case.mask is None:                  # forward
+        n_act = int(act.sum())
+        w_bytes = int(np.sum(ranks[touched]) * (d_in + d_out) * ws)
+        op_bytes = n_act * d_in * xs + 2 * n_act * d_out * ys + w_bytes
+        plan_bytes = case.n * 4
+        flops = int(np.sum(2 * ranks[idx[act]] * (d_in + d_out)))
+        return dict(n=case.n, n_act=n_act, adapters=len(touched), op_bytes=op_bytes,
+                    plan_bytes=plan_bytes, flops=flops)
+    m = act & (case.mask != 0)
+    n_m = int(m.sum())
+    live = np.nonzero(ranks > 0)[0]
+    op_bytes = (n_m * (d_in + d_out) * xs
+                + int(np.sum(ranks[live]) * (d_in + d_out) * (ws + 4)))
+    flops = int(np.sum(4 * ranks[idx[m]] * (d_in + d_out)))
+    return dict(n=case.n, n_act=int(act.sum()), n_masked=n_m, adapters=len(live),
+                op_bytes=op_bytes, plan_bytes=case.n * 5, flops=flops)
+
+
+# ----------------------------------------------------------------------------
+# one workload on the GPU
+# ----------------------------------------------------------------------------
+
+class Rig:
+    """R device copies of one workload, each with its own table and workspaces."""
+
+    def __init__(self, case, copies):
+        import torch
+        import paper_2601_07376_amd as L
+        from workloads.device import case_to_device
+        self.case, self.L, self.torch = case, L, torch
+        base = case_to_device(case, "cuda")
+        wdt = torch.bfloat16 if case.w_dtype == "bf16" else torch.float32
+        self.sets = []
+        for r in range(copies):
+            if r == 0:
+                d = dict(base)
+            else:
+                d = {k: ([t.clone() if t is not None else None for t in v]
+                         if isinstance(v, list) else (v.clone() if v is not None else None))
+                     for k, v in base.items()}
+            table = L.Table(case.num_slots, case.d_in, case.d_out, w_dtype=wdt, device="cuda")
+            for a in range(case.num_slots):
+                if case.ranks[a] > 0:
+                    table.set(a, d["A"][a], d["B"][a], float(case.scales[a]))
+            table.upload()
+            n = case.n
+            d["table"] = table
+            d["plan_ws"] = torch.empty(max(L.lib().lora_plan_workspace_bytes(n, case.num_slots), 16),
+                                       dtype=torch.uint8, device="cuda")
+            # a plan object only to size the op workspaces
+            if "seg_offsets" in d:
+                probe = L.Plan(table, seg_offsets=d["seg_offsets"], seg_adapter=d["seg_adapter"],
+                               n=n, mask=d["mask"])
+            else:
+                probe = L.Plan(table, idx=d["idx"], mask=d["mask"])
+            if case.mask is None:
+                d["op_ws"] = L.apply_workspace(probe)
+            else:
+                d["op_ws"] = L.grad_workspace(probe)
+                d["dA"] = [torch.empty(int(r_), case.d_in, dtype=torch.float32, device="cuda")
+                           if r_ > 0 else None for r_ in case.ranks]
+                d["dB"] = [torch.empty(case.d_out, int(r_), dtype=torch.float32, device="cuda")
+                           if r_ > 0 else None for r_ in case.ranks]
+                S = case.num_slots
+                d["pA"] = (ctypes.c_void_p * S)(*[t.data_ptr() if t is not None else None
+                                                   for t in d["dA"]])
+                d["pB"] = (ctypes.c_void_p * S)(*[t.data_ptr() if t is not None else None
+                                                   for t in d["dB"]])
+            del probe
+            self.sets.append(d)
+        torch.cuda.synchronize()
+
+    def step(self, i, ev=None):
+        """Enqueue one step on the current stream (plan build + op)."""
+        L, case = self.L, self.case
+        lib = L.lib()
+        d = self.sets[i % len(self.sets)]
+        stream = ctypes.c_void_p(self.torch.cuda.current_stream().cuda_stream)
+        h = ctypes.c_void_p()
+        mask = d["mask"].data_ptr() if d["mask"] is not None else None
+        if "seg_offsets" in d:
+            st = lib.lora_plan_build_segments(d["table"].handle, case.n, d["seg_adapter"].numel(),
+                                              d["seg_offsets"].data_ptr(),
+                                              d["seg_adapter"].data_ptr(), mask,
+                                              d["plan_ws"].data_ptr(), d["plan_ws"].numel(),
+                                              stream, ctypes.byref(h))
+        else:
+            st = lib.lora_plan_build(d["table"].handle, case.n, d["idx"].data_ptr(), mask,
+                                     d["plan_ws"].data_ptr(), d["plan_ws"].numel(), stream,
+                                     ctypes.byref(h))
+        assert st == 0, lib.lora_last_error()
+        if ev is not None:
+            ev[0].record()
+        X = d["X"]
+        xdt = 1 if case.x_dtype == "bf16" else 0
+        if case.mask is None:
+            Y = d["Y"]
+            st = lib.lora_apply(h, X.data_ptr(), xdt, X.stride(0), Y.data_ptr(),
+                                1 if case.y_dtype == "bf16" else 0, Y.stride(0),
+                                d["op_ws"].data_ptr(), d["op_ws"].numel(), stream)
+        else:
+            dY = d["dY"]
+            st = lib.lora_grad(h, X.data_ptr(), xdt, X.stride(0), dY.data_ptr(), xdt,
+                               dY.stride(0), None, 0, d["pA"], d["pB"], 0,
+                               d["op_ws"].data_ptr(), d["op_ws"].numel(), stream)
+        assert st == 0, lib.lora_last_error()
+        if ev is not None:
+            ev[1].record()
+        lib.lora_plan_destroy(h)      # host object only; enqueued work keeps its arguments
+
+
+def sleep_rate(torch):
+    """GPU sleep-kernel cycles per millisecond (for the start gate)."""
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    torch.cuda._sleep(2_000_000)
+    e1.record()
+    torch.cuda.synchronize()
+    return 2_000_000 / max(e0.elapsed_time(e1), 1e-3)
+
+
+def run_workload(cfg, steps, warmup, rate):
+    import torch
+    import workloads
+    t0 = time.time()
+    case = workloads.make_config(cfg)
+    counts = workload_counts(case)
+    ws_bytes = counts["op_bytes"] + counts["plan_bytes"]
+    copies = 1 if cfg == 1 else max(1, min(64, -(-ROTATE_BYTES // max(ws_bytes, 1))))
+    rig = Rig(case, copies)
+    log(f"[bench] workload {cfg} {case.name}: n={case.n} copies={copies} "
+        f"(setup {time.time() - t0:.1f}s)")
+
+    # warmup, and the host's enqueue cost per step (sizes the start gate)
+    c0 = time.perf_counter()
+    for i in range(warmup):
+        rig.step(i)
+    host_ms = (time.perf_counter() - c0) * 1e3 / max(warmup, 1)
+    torch.cuda.synchronize()
+
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    es, ee = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    gate_ms = min(500.0, 2.0 + 2.0 * host_ms * steps)
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    torch.cuda._sleep(int(gate_ms * rate))
+    es.record()
+    for i in range(steps):
+        rig.step(i, evs[i])
+    ee.record()
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - w0) * 1e3
+    gpu_ms = es.elapsed_time(ee)
+    op_us = np.array([a.elapsed_time(b) * 1e3 for a, b in evs])
+    ms_step = gpu_ms / steps
+    op_mean = float(op_us.mean())
+    r = dict(workload=case.name, config=cfg, copies=copies, steps=steps,
+             ms_per_step=ms_step, tokens_per_s=case.n / (ms_step * 1e-3),
+             op_us_mean=op_mean, op_us_p10=float(np.percentile(op_us, 10)),
+             op_us_p90=float(np.percentile(op_us, 90)),
+             op=("lora_grad" if case.mask is not None else "lora_apply"),
+             wall_ms_incl_gate=wall_ms, gate_ms=gate_ms, host_enqueue_ms_per_step=host_ms,
+             **counts)
+    r["op_GBps"] = counts["op_bytes"] / (op_mean * 1e-6) / 1e9
+    r["op_hbm_frac"] = r["op_GBps"] / HBM_PEAK_GBS
+    r["op_TFLOPs"] = counts["flops"] / (op_mean * 1e-6) / 1e12
+    peak_f = BF16_PEAK_TFLOPS if case.x_dtype == "bf16" else FP32_PEAK_TFLOPS
+    r["op_mfma_frac"] = r["op_TFLOPs"] / peak_f
+    # the matrix-core fraction an HBM-bound op can reach at this intensity
+    r["mfma_frac_ceiling"] = min(1.0, (counts["flops"] / counts["op_bytes"]) * HBM_PEAK_GBS
+                                 / 1e3 / peak_f)
+    r["step_GBps"] = ws_bytes / (ms_step * 1e-3) / 1e9
+    log(f"[bench]   {r['op']}: {op_mean:.2f} us (p10 {r['op_us_p10']:.2f}, p90 "
+        f"{r['op_us_p90']:.2f}), {r['op_GBps']:.0f} GB/s = {100 * r['op_hbm_frac']:.1f}% HBM, "
+        f"{r['op_TFLOPs']:.1f} TFLOP/s; step {ms_step * 1e3:.2f} us, "
+        f"{r['tokens_per_s']:.3e} tokens/s")
+    del rig
+    torch.cuda.empty_cache()
+    return r, case
+
+
+def calib_copy():
+    """A plain device copy of 1 GiB (read 1 GiB, write 1 GiB) for counter scaling."""
+    import torch
+    a = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    a.fill_(1)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    log(f"[bench] calibration copy 1 GiB: {ms:.3f} ms = {2 * (1 << 30) / ms / 1e6:.0f} GB/s")
+    return dict(bytes_read=1 << 30, bytes_written=1 << 30, ms=ms)
+
+
+def cpu_baseline(case, seconds):
+    """The float64 oracle on the host (plan + residual), on the whole headline batch."""
+    import oracle
+    from threadpoolctl import threadpool_info
+    import workloads
+    X = workloads.decode(case.X, case.x_dtype)
+    Y = workloads.decode(case.Y, case.y_dtype)
+    A = [workloads.decode(a, case.w_dtype) for a in case.A]
+    B = [workloads.decode(b, case.w_dtype) for b in case.B]
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        eff, _ = oracle.effective_ids(case.idx, case.num_slots, case.ranks)
+        oracle.canonical_plan(case.idx, case.num_slots, ranks=case.ranks)
+        oracle.apply(eff, X, Y, A, B, case.scales)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    return dict(value=case.n * reps / el, unit="tokens/s", cores=int(threads), kind="oracle",
+                sample=f"{reps} passes of the full {case.name} batch ({case.n} rows): "
+                       f"plan + float64 residual, {el:.1f} s")
+
+
+def traffic_for(result):
+    """HBM bytes per op from committed rocprofv3 counter runs, if they were taken
+    on the current kernel sources; otherwise None."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    with open(TRAFFIC_FILE) as f:
+        t = json.load(f)
+    if t.get("source_digest") != source_digest():
+        return None
+    w = t.get("workloads", {}).get(result["workload"])
+    return None if w is None else w.get("bytes_per_op")
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    import paper_2601_07376_amd as L
+    L.lib()
+    cfgs = [int(c) for c in args.configs.split(",") if c]
+    if HEADLINE not in cfgs:
+        cfgs = [HEADLINE] + cfgs
+    rate = sleep_rate(torch)
+    results, head_case = {}, None
+    for c in cfgs:
+        r, case = run_workload(c, args.steps, args.warmup, rate)
+        results[c] = r
+        if c == HEADLINE:
+            head_case = case
+    calib = calib_copy() if args.calib_copy else None
+    h = results[HEADLINE]
+    traffic = traffic_for(h)
+    roof = dict(bound="hbm", kernel="fused_small_kernel (lora_apply, decode)",
+                achieved=round(h["op_GBps"], 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                frac=round(h["op_hbm_frac"], 4), traffic=traffic,
+                bytes_per_launch=h["op_bytes"], avg_launch_us=round(h["op_us_mean"], 3))
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(head_case, args.cpu_seconds)
+        log(f"[bench] cpu baseline (oracle): {cpu['value']:.3e} tokens/s on {cpu['cores']} threads")
+    line = {
+        "metric": "mixed-adapter LoRA tokens/s (decode step: plan + fused residual)",
+        "value": round(h["tokens_per_s"], 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(h["ms_per_step"], 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "decode_bgmv", "tokens": h["n"], "active_rows": h["n_act"],
+                   "adapters": 64, "rank": 16, "d_in": 4096, "d_out": 4096,
+                   "y_dtype": "bf16", "parallelism": "none (1 GPU)"},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "extra": {"workloads": [results[c] for c in cfgs], "calibration_copy": calib,
+                  "source_digest": source_digest()},
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -23,8 +23,41 @@ __device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
   return u >> 16;
 }
 
-__device__ __forceinline__ uint4 ldg16(const void* p) {
-  return *reinterpret_cast<const uint4*>(p);
+// Plain accessors for buffers passed as kernel arguments (the compiler knows
+// those are global memory).
+__device__ __forceinline__ uint4 ldg16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
+__device__ __forceinline__ void stg16(void* p, uint4 v) { *reinterpret_cast<uint4*>(p) = v; }
+__device__ __forceinline__ float4 ldg_f4(const float* p) {
+  return *reinterpret_cast<const float4*>(p);
+}
+__device__ __forceinline__ void stg_f4(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
+template <typename T>
+__device__ __forceinline__ T ldg(const T* p) {
+  return *p;
+}
+template <typename T>
+__device__ __forceinline__ void stg(T* p, T v) {
+  *p = v;
+}
+
+// Adapter weights are reached through pointers read from the slot table, which
+// the compiler can only treat as generic (flat) pointers; flat loads also count
+// against the LDS/scalar counter and force extra waits.  They are read with
+// buffer loads instead: a buffer resource (base, size in bytes) plus 32-bit byte
+// offsets.  Offsets at or past the size read as zero.  Word 3 is the gfx9-family
+// resource format.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                           (int)0x00020000);
+}
+__device__ __forceinline__ uint4 bload16(rsrc_t r, uint32_t byte_off) {
+  const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 0);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ uint32_t bload_u16(rsrc_t r, uint32_t byte_off) {
+  return (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, byte_off, 0, 0);
 }
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) {
@@ -62,16 +95,74 @@ __device__ __forceinline__ f32x4 mfma_16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
-// Eight consecutive bf16 weights starting at column j of a row of `len`
-// elements; columns >= len read as zero.  `aligned` promises 16-byte alignment
-// and j + 8 <= len whenever j < len.
-__device__ __forceinline__ bf16x8 load_row8(const uint16_t* row, int j, int len, bool aligned) {
-  if (j >= len) return zero_bf16x8();
-  if (aligned) return as_bf16x8(ldg16(row + j));
+// Eight consecutive bf16 weights of a row that starts at element `row0` of a
+// weight buffer, columns [j, j + 8) of a row of len.  With RANK8 (len a multiple
+// of 8) this is one 16-byte load from a clamped column and the lanes with
+// j >= len hold another column's weights: the caller zeroes them where the
+// operand is consumed (selecting at load time would make the load wait at
+// once).  Without RANK8 the columns >= len are zero.
+template <bool RANK8>
+__device__ __forceinline__ bf16x8 wrow8(rsrc_t w, uint32_t row0, int j, int len) {
+  if (RANK8) {
+    const int jj = j < len ? j : len - 8;
+    return as_bf16x8(bload16(w, (row0 + (uint32_t)jj) * 2u));
+  }
   uint32_t b[8];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) b[i] = (j + i < len) ? (uint32_t)row[j + i] : 0u;
+  for (int i = 0; i < 8; ++i) {
+    const int jj = j + i < len ? j + i : len - 1;
+    const uint32_t v = bload_u16(w, (row0 + (uint32_t)jj) * 2u);
+    b[i] = (j + i < len) ? v : 0u;
+  }
   return pack_bf16x8(b);
+}
+
+// Keep-loads-unconditional helper: the hot loops read from addresses that are
+// always inside the buffer (clamped) and zero the lanes that are padding with a
+// select, so no load sits behind a divergent branch and the compiler can keep
+// many loads in flight (a divergent branch makes it wait for every outstanding
+// load at the join).
+__device__ __forceinline__ bf16x8 sel(bool keep, bf16x8 v) { return keep ? v : zero_bf16x8(); }
+
+
+// Wave-uniform views of per-tile metadata.  Entries and slot records are read
+// with vector loads; readfirstlane tells the compiler the values are the same in
+// every lane, so they live in scalar registers (a buffer resource built from a
+// value the compiler thinks may differ per lane would be looped over lanes).
+__device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+// Index of this wave in the workgroup, known to the compiler to be wave-uniform
+// (so loops and branches that depend on it stay scalar, not exec-masked).
+__device__ __forceinline__ int wave_id() { return uni((int)(threadIdx.x >> 6)); }
+
+__device__ __forceinline__ int4 load_entry(const int4* list, int i) {
+  const int4 e = list[i];
+  return make_int4(uni(e.x), uni(e.y), uni(e.z), uni(e.w));
+}
+
+struct Slot {
+  const void* A;
+  const void* B;
+  int rank;
+  float scale;
+};
+
+__device__ __forceinline__ const void* uni_ptr(const void* p) {
+  const uint64_t v = reinterpret_cast<uint64_t>(p);
+  const uint64_t lo = (uint32_t)uni((int)(uint32_t)v);
+  const uint64_t hi = (uint32_t)uni((int)(uint32_t)(v >> 32));
+  return reinterpret_cast<const void*>(lo | (hi << 32));
+}
+
+template <typename Meta>
+__device__ __forceinline__ Slot load_slot(const Meta* meta, int a) {
+  const Meta m = meta[a];
+  Slot s;
+  s.A = uni_ptr(m.A);
+  s.B = uni_ptr(m.B);
+  s.rank = uni(m.rank);
+  s.scale = __int_as_float(uni(__float_as_int(m.scale)));
+  return s;
 }
 
 // Tile range of the XCD this workgroup runs on.  Workgroups are dispatched to

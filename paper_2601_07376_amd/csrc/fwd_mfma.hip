@@ -11,11 +11,16 @@
 //          columns are split over sibling workgroups that recompute the small
 //          shrink from L2 and are placed on the same XCD.
 //
+// All three are bound by HBM bandwidth, so the loops are written for memory-
+// level parallelism: the shrink streams X and A in double-buffered batches of
+// k-steps, and Y and B loads are issued before the matrix-core work they wait on.
+//
 // Matrix core: v_mfma_f32_16x16x32_bf16.  Lane l holds row (l % 16) of the A
 // operand and column (l % 16) of the B operand, eight consecutive K values at
 // K offset 8 * (l / 16); the accumulator lane l holds rows 4 * (l / 16) + v,
 // v = 0..3, of column l % 16.
 #include <algorithm>
+#include <cstdlib>
 
 #include "device_common.h"
 #include "lora_internal.h"
@@ -45,58 +50,95 @@ __device__ __forceinline__ void entry_range(const FwdArgs& p, int& first, int& c
   count = p.hdr[p.count_word] - first;
 }
 
-// Eight float32 H values H[row][j..j+8) (zero past r), split into hi / lo.
+// Eight float32 H values H[row][j..j+8), split into hi / lo; zero past r or
+// when the row is padding.  hrow must point at a real row (clamped).
 template <bool RANK8>
-__device__ __forceinline__ void load_h_split(const float* hrow, int j, int r, bf16x8& hi,
-                                             bf16x8& lo) {
+__device__ __forceinline__ void load_h_split(const float* hrow, int j, int r, bool valid,
+                                             bf16x8& hi, bf16x8& lo) {
   float h[8];
-  if (RANK8 && j < r) {
-    const float4 a = *reinterpret_cast<const float4*>(hrow + j);
-    const float4 b = *reinterpret_cast<const float4*>(hrow + j + 4);
-    h[0] = a.x; h[1] = a.y; h[2] = a.z; h[3] = a.w;
-    h[4] = b.x; h[5] = b.y; h[6] = b.z; h[7] = b.w;
+  if (RANK8) {
+    const int jj = j < r ? j : r - 8;
+    const float4 a = ldg_f4(hrow + jj);
+    const float4 b = ldg_f4(hrow + jj + 4);
+    const bool k = valid && j < r;
+    h[0] = k ? a.x : 0.f; h[1] = k ? a.y : 0.f; h[2] = k ? a.z : 0.f; h[3] = k ? a.w : 0.f;
+    h[4] = k ? b.x : 0.f; h[5] = k ? b.y : 0.f; h[6] = k ? b.z : 0.f; h[7] = k ? b.w : 0.f;
   } else {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) h[i] = (j + i < r) ? hrow[j + i] : 0.0f;
+    for (int i = 0; i < 8; ++i) h[i] = (valid && j + i < r) ? ldg(hrow + j + i) : 0.0f;
   }
   split_hi_lo(h, hi, lo);
 }
 
-// Y[t, o .. o+16) += s * acc, where acc[q][v] holds output o + 4 q + v.
+// ---------------------------------------------------------------------------
+// Output-column layout of one wave's 64-column slice.  Tile q (0..3) of the
+// expand product, operand row m, covers column
+//     o_w + 32 (q / 2) + 8 (m / 4) + 4 (q % 2) + (m % 4),
+// so lane l (og = l / 16) holds, for one row, the 8 consecutive columns
+// o_w + 32 c + 8 og + [0, 8) of tiles q = 2c, 2c + 1 (c = 0, 1), and one load
+// instruction of the wave covers 64 contiguous bytes of 16 rows.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int out_col(int o_w, int q, int m) {
+  return o_w + 32 * (q >> 1) + 8 * (m >> 2) + 4 * (q & 1) + (m & 3);
+}
+
 template <bool YBF16>
-__device__ __forceinline__ void y_update16(void* Yv, int64_t ldy, int t, int o, int d_out,
-                                           float s, const f32x4 (&acc)[4]) {
-  if (YBF16) {
-    uint16_t* Y = reinterpret_cast<uint16_t*>(Yv) + (int64_t)t * ldy;
+struct YFrag {
+  uint4 v[YBF16 ? 2 : 4];
+};
+
+template <bool YBF16>
+__device__ __forceinline__ void y_load(YFrag<YBF16>& f, const void* Yv, int64_t ldy, int t,
+                                       int o_w, int og, int d_out) {
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      const int oc = o + 8 * c;
-      if (oc >= d_out) continue;
-      uint4 v = *reinterpret_cast<const uint4*>(Y + oc);
-      uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  for (int c = 0; c < 2; ++c) {
+    int o = o_w + 32 * c + 8 * og;
+    o = o < d_out ? o : d_out - 8;          // clamped; such lanes are never stored
+    if (YBF16) {
+      const uint16_t* Y = reinterpret_cast<const uint16_t*>(Yv) + (int64_t)t * ldy;
+      f.v[c] = ldg16(Y + o);
+    } else {
+      const float* Y = reinterpret_cast<const float*>(Yv) + (int64_t)t * ldy;
+      f.v[2 * c] = ldg16(Y + o);
+      f.v[2 * c + 1] = ldg16(Y + o + 4);
+    }
+  }
+}
+
+// y = y + s * acc (float32), rounded once to the storage type, and stored.
+template <bool YBF16>
+__device__ __forceinline__ void y_store(const YFrag<YBF16>& f, void* Yv, int64_t ldy, int t,
+                                        int o_w, int og, int d_out, float s,
+                                        const f32x4 (&acc)[4]) {
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    const int o = o_w + 32 * c + 8 * og;
+    if (o >= d_out) continue;
+    if (YBF16) {
+      uint16_t* Y = reinterpret_cast<uint16_t*>(Yv) + (int64_t)t * ldy;
+      const uint32_t w[4] = {f.v[c].x, f.v[c].y, f.v[c].z, f.v[c].w};
+      uint32_t o4[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int q = 2 * c + (i >> 1), e0 = (2 * i) & 3;
-        const float y0 = bf16_to_f32(w[i] & 0xffffu);
-        const float y1 = bf16_to_f32(w[i] >> 16);
-        const uint32_t r0 = f32_to_bf16_rne(fmaf(s, acc[q][e0], y0));
-        const uint32_t r1 = f32_to_bf16_rne(fmaf(s, acc[q][e0 + 1], y1));
-        w[i] = r0 | (r1 << 16);
+        const uint32_t r0 = f32_to_bf16_rne(fmaf(s, acc[q][e0], bf16_to_f32(w[i] & 0xffffu)));
+        const uint32_t r1 = f32_to_bf16_rne(fmaf(s, acc[q][e0 + 1], bf16_to_f32(w[i] >> 16)));
+        o4[i] = r0 | (r1 << 16);
       }
-      *reinterpret_cast<uint4*>(Y + oc) = make_uint4(w[0], w[1], w[2], w[3]);
-    }
-  } else {
-    float* Y = reinterpret_cast<float*>(Yv) + (int64_t)t * ldy;
+      stg16(Y + o, make_uint4(o4[0], o4[1], o4[2], o4[3]));
+    } else {
+      float* Y = reinterpret_cast<float*>(Yv) + (int64_t)t * ldy;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int oq = o + 4 * q;
-      if (oq >= d_out) continue;
-      float4 v = *reinterpret_cast<const float4*>(Y + oq);
-      v.x = fmaf(s, acc[q][0], v.x);
-      v.y = fmaf(s, acc[q][1], v.y);
-      v.z = fmaf(s, acc[q][2], v.z);
-      v.w = fmaf(s, acc[q][3], v.w);
-      *reinterpret_cast<float4*>(Y + oq) = v;
+      for (int h = 0; h < 2; ++h) {
+        const uint4 u = f.v[2 * c + h];
+        const f32x4 a = acc[2 * c + h];
+        float4 v;
+        v.x = fmaf(s, a[0], __uint_as_float(u.x));
+        v.y = fmaf(s, a[1], __uint_as_float(u.y));
+        v.z = fmaf(s, a[2], __uint_as_float(u.z));
+        v.w = fmaf(s, a[3], __uint_as_float(u.w));
+        stg_f4(Y + o + 4 * h, v);
+      }
     }
   }
 }
@@ -105,7 +147,7 @@ __device__ __forceinline__ void y_update16(void* Yv, int64_t ldy, int t, int o, 
 // leaving the total in wave 0.  s_red holds 2 x N x 64 f32x4.
 template <int N>
 __device__ __forceinline__ void reduce_waves(f32x4 (&acc)[N], f32x4* s_red) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, w = wave_id();
   __syncthreads();
   if (w >= 2) {
 #pragma unroll
@@ -128,61 +170,102 @@ __device__ __forceinline__ void reduce_waves(f32x4 (&acc)[N], f32x4* s_red) {
   }
 }
 
+// acc[mt * NT + nt] += X[rows of mt] A[rows of nt]^T over this wave's k-steps
+// k0 = kstart + i * kstride (k0 < kend).  xr[mt] points at a real X row and
+// ar[nt] is the element offset of a real A row; padding lanes use a clamped row,
+// and the caller discards the output rows / columns they produce.  Loads
+// come in batches of U k-steps, double buffered so one batch is in flight while
+// the previous one feeds the matrix cores.
+template <int MT, int NT, int U>
+__device__ __forceinline__ void shrink_steps(f32x4 (&acc)[MT * NT], const uint16_t* (&xr)[MT],
+                                             rsrc_t A, const uint32_t (&ar)[NT], int mt_used,
+                                             int nt_used, int kstart, int kstride, int kend) {
+  const int kg = ((threadIdx.x & 63) >> 4) * 8;
+  struct Buf {
+    bf16x8 x[U][MT];
+    bf16x8 w[U][NT];
+    bool kv[U];
+  };
+  // raw loads from clamped addresses; nothing here consumes the loaded data
+  auto load = [&](Buf& b, int kb) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int k = kb + u * kstride + kg;
+      b.kv[u] = k < kend;
+      const int kk = k < kend ? k : kend - 8;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) b.x[u][mt] = as_bf16x8(ldg16(xr[mt] + kk));
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+        b.w[u][nt] = as_bf16x8(bload16(A, (ar[nt] + (uint32_t)kk) * 2u));
+    }
+  };
+  // the K tail (k >= kend) is zeroed on the X operand where it is consumed
+  auto compute = [&](const Buf& b) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        if (mt >= mt_used) continue;
+        const bf16x8 xo = sel(b.kv[u], b.x[u][mt]);
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          if (nt >= nt_used) continue;
+          acc[mt * NT + nt] = mfma_16x16x32(xo, b.w[u][nt], acc[mt * NT + nt]);
+        }
+      }
+  };
+  if (kstart >= kend) return;
+  const int span = U * kstride;
+  Buf b0, b1;
+  load(b0, kstart);
+  for (int kb = kstart;; kb += 2 * span) {
+    const int k1 = kb + span;
+    if (k1 < kend) load(b1, k1);
+    compute(b0);
+    if (k1 >= kend) break;
+    const int k2 = k1 + span;
+    if (k2 < kend) load(b0, k2);
+    compute(b1);
+    if (k2 >= kend) break;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // shrink: H[t, :r] = X[t] A^T over row blocks of up to 64 rows
 // ---------------------------------------------------------------------------
 template <int NT>
 __global__ __launch_bounds__(256) void shrink_kernel(FwdArgs p) {
+  constexpr int U = NT <= 4 ? 2 : 1;
   __shared__ f32x4 s_red[2 * 4 * NT * 64];
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, w = wave_id();
   int first, count;
   entry_range(p, first, count);
   const XcdRange xr = xcd_range(count);
   for (int e = xr.first; e < xr.end; e += xr.step) {
-    const int4 en = p.rb[first + e];
+    const int4 en = load_entry(p.rb, first + e);
     const int a = en.x, p0 = en.y, rows = en.z;
-    const SlotMeta m = p.meta[a];
+    const Slot m = load_slot(p.meta, a);
     const int r = m.rank;
-    const uint16_t* A = reinterpret_cast<const uint16_t*>(m.A);
+    const rsrc_t A = make_rsrc(m.A, (uint32_t)r * (uint32_t)p.d_in * 2u);
     const int mt_used = (rows + 15) >> 4, nt_used = (r + 15) >> 4;
 
-    int trow[4];
-    bool rv[4];
+    const uint16_t* xrow[4];
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt) {
       const int i = mt * 16 + (lane & 15);
-      rv[mt] = i < rows;
-      trow[mt] = rv[mt] ? p.perm[p0 + i] : 0;
+      xrow[mt] = p.X + (int64_t)ldg(p.perm + p0 + (i < rows ? i : rows - 1)) * p.ldx;
+    }
+    uint32_t arow[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const int j = nt * 16 + (lane & 15);
+      arow[nt] = (uint32_t)(j < r ? j : r - 1) * (uint32_t)p.d_in;
     }
     f32x4 acc[4 * NT];
 #pragma unroll
     for (int i = 0; i < 4 * NT; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    const int kg = (lane >> 4) * 8;
-    for (int k0 = w * 32; k0 < p.d_in; k0 += 128) {
-      const int k = k0 + kg;
-      const bool kv = k < p.d_in;
-      bf16x8 xa[4], wb[NT];
-#pragma unroll
-      for (int mt = 0; mt < 4; ++mt)
-        xa[mt] = (mt < mt_used && rv[mt] && kv)
-                     ? as_bf16x8(ldg16(p.X + (int64_t)trow[mt] * p.ldx + k))
-                     : zero_bf16x8();
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const int j = nt * 16 + (lane & 15);
-        wb[nt] = (j < r && kv) ? as_bf16x8(ldg16(A + (int64_t)j * p.d_in + k)) : zero_bf16x8();
-      }
-#pragma unroll
-      for (int mt = 0; mt < 4; ++mt) {
-        if (mt >= mt_used) continue;
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          if (nt >= nt_used) continue;
-          acc[mt * NT + nt] = mfma_16x16x32(xa[mt], wb[nt], acc[mt * NT + nt]);
-        }
-      }
-    }
+    shrink_steps<4, NT, U>(acc, xrow, A, arow, mt_used, nt_used, w * 32, 128, p.d_in);
     reduce_waves<4 * NT>(acc, s_red);
     if (w == 0) {
 #pragma unroll
@@ -192,11 +275,11 @@ __global__ __launch_bounds__(256) void shrink_kernel(FwdArgs p) {
         for (int v = 0; v < 4; ++v) {
           const int i = mt * 16 + (lane >> 4) * 4 + v;
           if (i >= rows) continue;
-          float* hrow = p.H + (int64_t)p.perm[p0 + i] * p.ldh;
+          float* hrow = p.H + (int64_t)ldg(p.perm + p0 + i) * p.ldh;
 #pragma unroll
           for (int nt = 0; nt < NT; ++nt) {
             const int j = nt * 16 + (lane & 15);
-            if (j < r) hrow[j] = acc[mt * NT + nt][v];
+            if (j < r) stg(hrow + j, acc[mt * NT + nt][v]);
           }
         }
       }
@@ -205,92 +288,219 @@ __global__ __launch_bounds__(256) void shrink_kernel(FwdArgs p) {
 }
 
 // ---------------------------------------------------------------------------
-// expand: Y[t] += s H[t, :r] B^T over (row block, 256-column tile)
-// The A operand is B's rows, permuted so that lane l's four 16x16 tiles cover
-// 16 consecutive output columns: tile q, operand row m -> column
-// o_w + 16 (m / 4) + 4 q + (m % 4).
+// expand: Y[t] += s H[t, :r] B^T.  Work unit = (row block of <= 64 rows, 1024
+// output columns).  The unit's H operands (hi / lo) are loaded once; then each
+// wave streams 32-column slices (columns c0 + 128 s + 32 w), keeping two slices
+// of B and Y in flight ahead of the one feeding the matrix cores.
+//
+// Slice layout: tile q (0, 1), operand row m, covers column
+// o_w + 8 (m / 4) + 4 q + (m % 4), so lane l (og = l / 16) holds the 8
+// consecutive columns o_w + 8 og + [0, 8) of one row: one 16-byte load for a
+// bf16 Y, and the wave's load covers 64 contiguous bytes of 16 rows.
 // ---------------------------------------------------------------------------
-template <bool YBF16, bool RANK8>
+template <bool YBF16>
+struct Y8 {
+  uint4 v[YBF16 ? 1 : 2];
+};
+
+template <bool YBF16>
+__device__ __forceinline__ void y8_load(Y8<YBF16>& f, const void* Yv, int64_t ldy, int t, int o,
+                                        int d_out) {
+  o = o < d_out ? o : d_out - 8;            // clamped; such lanes are never stored
+  if (YBF16) {
+    f.v[0] = ldg16(reinterpret_cast<const uint16_t*>(Yv) + (int64_t)t * ldy + o);
+  } else {
+    const float* Y = reinterpret_cast<const float*>(Yv) + (int64_t)t * ldy + o;
+    f.v[0] = ldg16(Y);
+    f.v[1] = ldg16(Y + 4);
+  }
+}
+
+template <bool YBF16>
+__device__ __forceinline__ void y8_store(const Y8<YBF16>& f, void* Yv, int64_t ldy, int t, int o,
+                                         float s, const f32x4& a0, const f32x4& a1) {
+  if (YBF16) {
+    uint16_t* Y = reinterpret_cast<uint16_t*>(Yv) + (int64_t)t * ldy + o;
+    const uint32_t w[4] = {f.v[0].x, f.v[0].y, f.v[0].z, f.v[0].w};
+    uint32_t o4[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const f32x4& a = (i < 2) ? a0 : a1;
+      const int e0 = (2 * i) & 3;
+      const uint32_t r0 = f32_to_bf16_rne(fmaf(s, a[e0], bf16_to_f32(w[i] & 0xffffu)));
+      const uint32_t r1 = f32_to_bf16_rne(fmaf(s, a[e0 + 1], bf16_to_f32(w[i] >> 16)));
+      o4[i] = r0 | (r1 << 16);
+    }
+    stg16(Y, make_uint4(o4[0], o4[1], o4[2], o4[3]));
+  } else {
+    float* Y = reinterpret_cast<float*>(Yv) + (int64_t)t * ldy + o;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const uint4 u = f.v[h];
+      const f32x4& a = h ? a1 : a0;
+      float4 v;
+      v.x = fmaf(s, a[0], __uint_as_float(u.x));
+      v.y = fmaf(s, a[1], __uint_as_float(u.y));
+      v.z = fmaf(s, a[2], __uint_as_float(u.z));
+      v.w = fmaf(s, a[3], __uint_as_float(u.w));
+      stg_f4(Y + 4 * h, v);
+    }
+  }
+}
+
+// TT = row tiles (of 16 rows) per wave: the 4 waves form 4 / TT row groups and
+// TT column groups, so one step of the workgroup covers 64 rows x 32 TT columns.
+// DY = how many steps ahead Y is requested (HBM latency); B (L2) is double
+// buffered one step ahead.
+template <bool YBF16, bool RANK8, int KSM, int TT, int DY>
 __global__ __launch_bounds__(256) void expand_kernel(FwdArgs p) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  constexpr int CW = 1024, STEP = 32 * TT, NS = CW / STEP, R = DY + 1;
+  static_assert(R % 2 == 0, "ring length must be even");
+  const int lane = threadIdx.x & 63, w = wave_id();
+  const int og = lane >> 4, mrow = lane & 15, jg = og * 8;
+  const int rg = w % (4 / TT);     // row group: row tiles rg * TT .. rg * TT + TT - 1
+  const int cg = w / (4 / TT);     // column group: columns cg * 32 .. + 32 of every step
   int first, count;
   entry_range(p, first, count);
-  const int n_ot = (p.d_out + 255) >> 8;
-  const XcdRange xr = xcd_range(count * n_ot);
-  for (int tile = xr.first; tile < xr.end; tile += xr.step) {
-    const int e = tile / n_ot, ot = tile - e * n_ot;
-    const int o_w = ot * 256 + w * 64;
-    if (o_w >= p.d_out) continue;
-    const int4 en = p.rb[first + e];
+  const int n_ch = (p.d_out + CW - 1) / CW;
+  const XcdRange xr = xcd_range(count * n_ch);
+  for (int unit = xr.first; unit < xr.end; unit += xr.step) {
+    const int e = unit / n_ch, ch = unit - e * n_ch;
+    const int c0 = ch * CW, c1 = min(p.d_out, c0 + CW);
+    const int4 en = load_entry(p.rb, first + e);
     const int a = en.x, p0 = en.y, rows = en.z;
-    const SlotMeta m = p.meta[a];
+    if (rg * TT * 16 >= rows) continue;           // uniform: no rows for this wave
+    const Slot m = load_slot(p.meta, a);
     const int r = m.rank;
     const float s = m.scale;
-    const uint16_t* B = reinterpret_cast<const uint16_t*>(m.B);
-    const int tt_used = (rows + 15) >> 4;
+    const rsrc_t Bw = make_rsrc(m.B, (uint32_t)p.d_out * (uint32_t)r * 2u);
+    const int ks_used = (r + 31) >> 5;
+    const int tt_used = min(TT, (rows - rg * TT * 16 + 15) >> 4);
 
-    int trow[4];
-    bool rv[4];
+    int trow[TT];
+    bool rv[TT];
 #pragma unroll
-    for (int tt = 0; tt < 4; ++tt) {
-      const int i = tt * 16 + (lane & 15);
+    for (int tt = 0; tt < TT; ++tt) {
+      const int i = (rg * TT + tt) * 16 + mrow;
       rv[tt] = i < rows;
-      trow[tt] = rv[tt] ? p.perm[p0 + i] : 0;
+      trow[tt] = ldg(p.perm + p0 + (i < rows ? i : rows - 1));
     }
-    const int mrow = lane & 15;
-    int orow[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) orow[q] = o_w + (mrow >> 2) * 16 + q * 4 + (mrow & 3);
 
-    f32x4 acc[4][4];
+    // H operands of the wave's rows (hi / lo), loaded once per unit
+    bf16x8 hh[KSM][TT], hl[KSM][TT];
+    {
+      float4 hraw[KSM][TT][2];
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
+      for (int ks = 0; ks < KSM; ++ks) {
+        const int j = ks * 32 + jg;
+        const int jj = RANK8 ? (j < r ? j : r - 8) : 0;
 #pragma unroll
-      for (int tt = 0; tt < 4; ++tt) acc[q][tt] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    const int jg = (lane >> 4) * 8;
-    for (int j0 = 0; j0 < r; j0 += 32) {
-      const int j = j0 + jg;
-      bf16x8 bo[4];
+        for (int tt = 0; tt < TT; ++tt) {
+          const float* hrow = p.H + (int64_t)trow[tt] * p.ldh;
+          if (RANK8) {
+            hraw[ks][tt][0] = ldg_f4(hrow + jj);
+            hraw[ks][tt][1] = ldg_f4(hrow + jj + 4);
+          } else {
+            float h[8];
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        bo[q] = (orow[q] < p.d_out) ? load_row8(B + (int64_t)orow[q] * r, j, r, RANK8)
-                                    : zero_bf16x8();
-#pragma unroll
-      for (int tt = 0; tt < 4; ++tt) {
-        if (tt >= tt_used) continue;
-        bf16x8 hh, hl;
-        if (rv[tt]) {
-          load_h_split<RANK8>(p.H + (int64_t)trow[tt] * p.ldh, j, r, hh, hl);
-        } else {
-          hh = zero_bf16x8();
-          hl = zero_bf16x8();
+            for (int i = 0; i < 8; ++i) h[i] = (j + i < r) ? ldg(hrow + j + i) : 0.0f;
+            hraw[ks][tt][0] = make_float4(h[0], h[1], h[2], h[3]);
+            hraw[ks][tt][1] = make_float4(h[4], h[5], h[6], h[7]);
+          }
         }
+      }
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          acc[q][tt] = mfma_16x16x32(bo[q], hh, acc[q][tt]);
-          acc[q][tt] = mfma_16x16x32(bo[q], hl, acc[q][tt]);
+      for (int ks = 0; ks < KSM; ++ks) {
+        const bool jv = ks * 32 + jg < r;
+#pragma unroll
+        for (int tt = 0; tt < TT; ++tt) {
+          const bool k = jv && rv[tt];
+          const float4 a0 = hraw[ks][tt][0], a1 = hraw[ks][tt][1];
+          const float h[8] = {k ? a0.x : 0.f, k ? a0.y : 0.f, k ? a0.z : 0.f, k ? a0.w : 0.f,
+                              k ? a1.x : 0.f, k ? a1.y : 0.f, k ? a1.z : 0.f, k ? a1.w : 0.f};
+          split_hi_lo(h, hh[ks][tt], hl[ks][tt]);
         }
       }
     }
-    const int o_y = o_w + (lane >> 4) * 16;
+
+    Y8<YBF16> yb[R][TT];
+    bf16x8 bb[2][KSM][2];
+    auto load_y = [&](Y8<YBF16> (&y)[TT], int st) {
+      const int o = c0 + st * STEP + cg * 32 + 8 * og;
 #pragma unroll
-    for (int tt = 0; tt < 4; ++tt) {
-      if (tt >= tt_used || !rv[tt]) continue;
-      const f32x4 col[4] = {acc[0][tt], acc[1][tt], acc[2][tt], acc[3][tt]};
-      y_update16<YBF16>(p.Y, p.ldy, trow[tt], o_y, p.d_out, s, col);
+      for (int tt = 0; tt < TT; ++tt) y8_load<YBF16>(y[tt], p.Y, p.ldy, trow[tt], o, p.d_out);
+    };
+    auto load_b = [&](bf16x8 (&b)[KSM][2], int st) {
+      const int o_w = c0 + st * STEP + cg * 32;
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        int o = o_w + 8 * (mrow >> 2) + 4 * q + (mrow & 3);
+        o = o < p.d_out ? o : p.d_out - 1;
+#pragma unroll
+        for (int ks = 0; ks < KSM; ++ks) b[ks][q] = wrow8<RANK8>(Bw, (uint32_t)o * r, ks * 32 + jg, r);
+      }
+    };
+    auto run = [&](const bf16x8 (&b)[KSM][2], const Y8<YBF16> (&y)[TT], int st) {
+      const int o_w = c0 + st * STEP + cg * 32;
+      if (o_w >= c1) return;
+      f32x4 acc[2][TT];
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
+#pragma unroll
+        for (int tt = 0; tt < TT; ++tt) acc[q][tt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KSM; ++ks) {
+        if (ks >= ks_used) continue;
+        const bool jv = ks * 32 + jg < r;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          const bf16x8 bq = sel(jv, b[ks][q]);
+#pragma unroll
+          for (int tt = 0; tt < TT; ++tt) {
+            if (tt >= tt_used) continue;
+            acc[q][tt] = mfma_16x16x32(bq, hh[ks][tt], acc[q][tt]);
+            acc[q][tt] = mfma_16x16x32(bq, hl[ks][tt], acc[q][tt]);
+          }
+        }
+      }
+      const int o = o_w + 8 * og;
+      if (o < c1) {
+#pragma unroll
+        for (int tt = 0; tt < TT; ++tt)
+          if (rv[tt]) y8_store<YBF16>(y[tt], p.Y, p.ldy, trow[tt], o, s, acc[0][tt], acc[1][tt]);
+      }
+    };
+#pragma unroll
+    for (int d = 0; d < DY; ++d) load_y(yb[d], d);
+    load_b(bb[0], 0);
+    for (int st0 = 0; st0 < NS; st0 += R) {
+#pragma unroll
+      for (int u = 0; u < R; ++u) {
+        const int st = st0 + u;
+        if (st >= NS) break;
+        if (st + DY < NS) load_y(yb[(u + DY) % R], st + DY);
+        if (st + 1 < NS) load_b(bb[(u + 1) & 1], st + 1);
+        run(bb[u & 1], yb[u], st);
+      }
     }
   }
 }
 
 // ---------------------------------------------------------------------------
-// fused small-group kernel: entries of <= 16 rows; workgroup (entry, chunk)
+// fused small-group kernel: entries of <= 16 rows; workgroup (entry, chunk of
+// at most 1024 columns).  Each wave owns up to 4 slices of 64 columns.  The
+// chunk's B (small ranks) and Y are requested before the shrink streams A, so
+// their latency hides under it.
 // ---------------------------------------------------------------------------
 template <bool YBF16, int NT, bool RANK8>
 __global__ __launch_bounds__(256) void fused_small_kernel(FwdArgs p) {
+  constexpr int U = NT == 1 ? 8 : (NT == 2 ? 4 : (NT == 4 ? 2 : 1));
+  constexpr int KSM = (NT * 16 + 31) / 32;
+  constexpr bool B_AHEAD = KSM == 1;          // B of every slice requested up front
   __shared__ f32x4 s_red[2 * NT * 64];
   __shared__ float s_h[16][NT * 16 + 4];
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, w = wave_id();
+  const int og = lane >> 4, mrow = lane & 15;
   int first, count;
   entry_range(p, first, count);
   const int P = p.n_chunks;
@@ -299,83 +509,99 @@ __global__ __launch_bounds__(256) void fused_small_kernel(FwdArgs p) {
   const int e = 8 * (slot / P) + (int)(blockIdx.x & 7);
   const int pc = slot % P;
   if (e >= count) return;
-  const int4 en = p.rb[first + e];
+  const int4 en = load_entry(p.rb, first + e);
   const int a = en.x, p0 = en.y, rows = en.z;
-  const SlotMeta m = p.meta[a];
+  const Slot m = load_slot(p.meta, a);
   const int r = m.rank;
   const float s = m.scale;
-  const uint16_t* A = reinterpret_cast<const uint16_t*>(m.A);
-  const uint16_t* B = reinterpret_cast<const uint16_t*>(m.B);
-  const int nt_used = (r + 15) >> 4;
+  const rsrc_t A = make_rsrc(m.A, (uint32_t)r * (uint32_t)p.d_in * 2u);
+  const rsrc_t Bw = make_rsrc(m.B, (uint32_t)p.d_out * (uint32_t)r * 2u);
+  const int nt_used = (r + 15) >> 4, ks_used = (r + 31) >> 5;
 
-  const int i_l = lane & 15;
-  const bool rv = i_l < rows;
-  const int trow = rv ? p.perm[p0 + i_l] : 0;
+  const bool rv = mrow < rows;
+  const int trow = ldg(p.perm + p0 + (rv ? mrow : rows - 1));
+  const int c0 = pc * p.chunk;
+  const int c1 = min(p.d_out, c0 + p.chunk);
+
+  // ---- B (small ranks) and Y of this wave's column slices, requested first
+  bf16x8 bo_ahead[B_AHEAD ? 4 : 1][4];
+  if (B_AHEAD) {
+#pragma unroll
+    for (int sl = 0; sl < 4; ++sl) {
+      const int o_w = c0 + w * 64 + 256 * sl;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int o = out_col(o_w, q, mrow);
+        bo_ahead[B_AHEAD ? sl : 0][q] =
+            wrow8<RANK8>(Bw, (uint32_t)(o < c1 ? o : c1 - 1) * r, og * 8, r);
+      }
+    }
+  }
+  YFrag<YBF16> yf[4];
+#pragma unroll
+  for (int sl = 0; sl < 4; ++sl)
+    y_load<YBF16>(yf[sl], p.Y, p.ldy, trow, c0 + w * 64 + 256 * sl, og, c1);
 
   // ---- shrink: H[16 x r] = X[rows] A^T, d_in split over the waves
   f32x4 acc[NT];
 #pragma unroll
   for (int i = 0; i < NT; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int kg = (lane >> 4) * 8;
-  for (int k0 = w * 32; k0 < p.d_in; k0 += 128) {
-    const int k = k0 + kg;
-    const bool kv = k < p.d_in;
-    const bf16x8 xa =
-        (rv && kv) ? as_bf16x8(ldg16(p.X + (int64_t)trow * p.ldx + k)) : zero_bf16x8();
-    bf16x8 wb[NT];
+  {
+    const uint16_t* xrow[1] = {p.X + (int64_t)trow * p.ldx};
+    uint32_t arow[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      const int j = nt * 16 + (lane & 15);
-      wb[nt] = (j < r && kv) ? as_bf16x8(ldg16(A + (int64_t)j * p.d_in + k)) : zero_bf16x8();
+      const int j = nt * 16 + mrow;
+      arow[nt] = (uint32_t)(j < r ? j : r - 1) * (uint32_t)p.d_in;
     }
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-      if (nt < nt_used) acc[nt] = mfma_16x16x32(xa, wb[nt], acc[nt]);
+    shrink_steps<1, NT, U>(acc, xrow, A, arow, 1, nt_used, w * 32, 128, p.d_in);
   }
   reduce_waves<NT>(acc, s_red);
   if (w == 0) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) s_h[(lane >> 4) * 4 + v][nt * 16 + (lane & 15)] = acc[nt][v];
+      for (int v = 0; v < 4; ++v) s_h[og * 4 + v][nt * 16 + mrow] = acc[nt][v];
   }
   __syncthreads();
 
-  // ---- H operand (hi / lo) for every 32-wide rank step, kept in registers
-  constexpr int KS_MAX = (NT * 16 + 31) / 32;
-  const int ks_used = (r + 31) >> 5;
-  bf16x8 hh[KS_MAX], hl[KS_MAX];
+  // ---- H operand (hi / lo) for every 32-wide rank step
+  bf16x8 hh[KSM], hl[KSM];
 #pragma unroll
-  for (int ks = 0; ks < KS_MAX; ++ks) {
+  for (int ks = 0; ks < KSM; ++ks) {
     float h[8];
-    const int j = ks * 32 + (lane >> 4) * 8;
+    const int j = ks * 32 + og * 8;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) h[i] = (j + i < r) ? s_h[i_l][j + i] : 0.0f;
+    for (int i = 0; i < 8; ++i) h[i] = (j + i < r) ? s_h[mrow][j + i] : 0.0f;
     split_hi_lo(h, hh[ks], hl[ks]);
   }
 
-  // ---- expand over this workgroup's column chunk
-  const int c0 = pc * p.chunk;
-  const int c1 = min(p.d_out, c0 + p.chunk);
-  const int mrow = lane & 15;
-  for (int o_w = c0 + w * 64; o_w < c1; o_w += 256) {
+  // ---- expand over this wave's column slices
+#pragma unroll
+  for (int sl = 0; sl < 4; ++sl) {
+    const int o_w = c0 + w * 64 + 256 * sl;
+    if (o_w >= c1) continue;
     f32x4 acc2[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) acc2[q] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int ks = 0; ks < KS_MAX; ++ks) {
+    for (int ks = 0; ks < KSM; ++ks) {
       if (ks >= ks_used) continue;
-      const int j = ks * 32 + (lane >> 4) * 8;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const int o = o_w + (mrow >> 2) * 16 + q * 4 + (mrow & 3);
-        const bf16x8 bo =
-            (o < c1) ? load_row8(B + (int64_t)o * r, j, r, RANK8) : zero_bf16x8();
+        bf16x8 bo;
+        if (B_AHEAD) {
+          bo = bo_ahead[B_AHEAD ? sl : 0][q];
+        } else {
+          const int o = out_col(o_w, q, mrow);
+          bo = wrow8<RANK8>(Bw, (uint32_t)(o < c1 ? o : c1 - 1) * r, ks * 32 + og * 8, r);
+        }
+        bo = sel(ks * 32 + og * 8 < r, bo);
         acc2[q] = mfma_16x16x32(bo, hh[ks], acc2[q]);
         acc2[q] = mfma_16x16x32(bo, hl[ks], acc2[q]);
       }
     }
-    if (rv) y_update16<YBF16>(p.Y, p.ldy, trow, o_w + (lane >> 4) * 16, c1, s, acc2);
+    if (rv) y_store<YBF16>(yf[sl], p.Y, p.ldy, trow, o_w, og, c1, s, acc2);
   }
 }
 
@@ -386,7 +612,7 @@ hipError_t launch(K kernel, int grid, const FwdArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-int round8(int g) { return (g + 7) / 8 * 8; }
+int round8(long long g) { return (int)((g + 7) / 8 * 8); }
 
 FwdArgs base_args(const OpLaunch& o) {
   FwdArgs a{};
@@ -399,6 +625,41 @@ FwdArgs base_args(const OpLaunch& o) {
   a.count_word = o.count_word;
   a.first_word = o.first_word;
   return a;
+}
+
+int env_int(const char* name, int dflt) {
+  const char* v = std::getenv(name);
+  return (v != nullptr && *v) ? std::atoi(v) : dflt;
+}
+
+// Expand shapes: (row tiles per wave, Y prefetch depth).  The default favours
+// many resident waves; LORA_EXPAND_VARIANT selects another for measurements.
+template <bool YB, bool R8, int KSM>
+hipError_t launch_expand_variant(int grid, const FwdArgs& a, hipStream_t s) {
+  switch (env_int("LORA_EXPAND_VARIANT", 0)) {
+    case 1: return launch(expand_kernel<YB, R8, KSM, 2, 3>, grid, a, s);
+    case 2: return launch(expand_kernel<YB, R8, KSM, 1, 5>, grid, a, s);
+    case 3: return launch(expand_kernel<YB, R8, KSM, 2, 1>, grid, a, s);
+    case 4: return launch(expand_kernel<YB, R8, KSM, 4, 1>, grid, a, s);
+    default: return launch(expand_kernel<YB, R8, KSM, 1, 3>, grid, a, s);
+  }
+}
+
+template <bool YB, bool R8>
+hipError_t launch_expand_ks(const OpLaunch& o, int grid, const FwdArgs& a, hipStream_t s) {
+  const int ks = (o.r_max + 31) / 32;
+  if (ks <= 1) return launch_expand_variant<YB, R8, 1>(grid, a, s);
+  if (ks <= 2) return launch_expand_variant<YB, R8, 2>(grid, a, s);
+  return launch_expand_variant<YB, R8, 4>(grid, a, s);
+}
+
+template <bool YB, bool R8>
+hipError_t launch_fused_nt(const OpLaunch& o, int grid, const FwdArgs& a, hipStream_t s) {
+  const int nt = (o.r_max + 15) / 16;
+  if (nt <= 1) return launch(fused_small_kernel<YB, 1, R8>, grid, a, s);
+  if (nt <= 2) return launch(fused_small_kernel<YB, 2, R8>, grid, a, s);
+  if (nt <= 4) return launch(fused_small_kernel<YB, 4, R8>, grid, a, s);
+  return launch(fused_small_kernel<YB, 8, R8>, grid, a, s);
 }
 
 }  // namespace
@@ -425,22 +686,13 @@ hipError_t launch_expand_mfma(const OpLaunch& o, const float* H, int64_t ldh, vo
   a.ldh = ldh;
   a.Y = Y;
   a.ldy = ldy;
-  const long long tiles = (long long)o.rb_ub * ((o.d_out + 255) / 256);
-  const int grid = round8((int)std::min<long long>(tiles, 8192));
+  const long long units = (long long)o.rb_ub * ((o.d_out + 1023) / 1024);
+  const int grid = round8(std::min<long long>(units, 4096));
   const bool yb = y_dtype == LORA_BF16;
-  if (yb && o.rank8) return launch(expand_kernel<true, true>, grid, a, s);
-  if (yb) return launch(expand_kernel<true, false>, grid, a, s);
-  if (o.rank8) return launch(expand_kernel<false, true>, grid, a, s);
-  return launch(expand_kernel<false, false>, grid, a, s);
-}
-
-template <bool YB, bool R8>
-static hipError_t launch_fused_nt(const OpLaunch& o, int grid, const FwdArgs& a, hipStream_t s) {
-  const int nt = (o.r_max + 15) / 16;
-  if (nt <= 1) return launch(fused_small_kernel<YB, 1, R8>, grid, a, s);
-  if (nt <= 2) return launch(fused_small_kernel<YB, 2, R8>, grid, a, s);
-  if (nt <= 4) return launch(fused_small_kernel<YB, 4, R8>, grid, a, s);
-  return launch(fused_small_kernel<YB, 8, R8>, grid, a, s);
+  if (yb && o.rank8) return launch_expand_ks<true, true>(o, grid, a, s);
+  if (yb) return launch_expand_ks<true, false>(o, grid, a, s);
+  if (o.rank8) return launch_expand_ks<false, true>(o, grid, a, s);
+  return launch_expand_ks<false, false>(o, grid, a, s);
 }
 
 hipError_t launch_bgmv_mfma(const OpLaunch& o, const void* X, int64_t ldx, void* Y,
@@ -450,7 +702,8 @@ hipError_t launch_bgmv_mfma(const OpLaunch& o, const void* X, int64_t ldx, void*
   a.ldx = ldx;
   a.Y = Y;
   a.ldy = ldy;
-  const int P = std::max(1, n_chunks);
+  // each workgroup covers at most 1024 columns (4 slices of 64 per wave)
+  const int P = std::max({1, n_chunks, (o.d_out + 1023) / 1024});
   a.n_chunks = P;
   a.chunk = ((o.d_out + P - 1) / P + 63) / 64 * 64;
   const int grid = 8 * P * ((o.rb_ub + 7) / 8);

@@ -38,9 +38,9 @@ __global__ __launch_bounds__(256) void shrink_valu_kernel(ValuArgs p) {
   const int first = p.first_word >= 0 ? p.hdr[p.first_word] : 0;
   const int count = p.hdr[p.count_word] - first;
   for (int e = blockIdx.x; e < count; e += gridDim.x) {
-    const int4 en = p.rb[first + e];
+    const int4 en = load_entry(p.rb, first + e);
     const int a = en.x, p0 = en.y, rows = en.z;
-    const SlotMeta m = p.meta[a];
+    const Slot m = load_slot(p.meta, a);
     const int r = m.rank;
     for (int q = threadIdx.x; q < rows * r; q += blockDim.x) {
       const int i = q / r, j = q - i * r;
@@ -62,9 +62,9 @@ __global__ __launch_bounds__(256) void expand_valu_kernel(ValuArgs p) {
   for (int tile = blockIdx.x; tile < count * n_ot; tile += gridDim.x) {
     const int e = tile / n_ot, o = (tile - e * n_ot) * 256 + (int)threadIdx.x;
     if (o >= p.d_out) continue;
-    const int4 en = p.rb[first + e];
+    const int4 en = load_entry(p.rb, first + e);
     const int a = en.x, p0 = en.y, rows = en.z;
-    const SlotMeta m = p.meta[a];
+    const Slot m = load_slot(p.meta, a);
     const int r = m.rank;
     const float s = m.scale;
     for (int i = 0; i < rows; ++i) {

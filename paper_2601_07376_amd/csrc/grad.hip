@@ -59,7 +59,7 @@ __device__ __forceinline__ void slice(int d, int nks, int ks, int& b, int& e) {
 
 template <int N>
 __device__ __forceinline__ void reduce_waves(f32x4 (&acc)[N], f32x4* s_red) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, w = wave_id();
   __syncthreads();
   if (w >= 2) {
 #pragma unroll
@@ -90,19 +90,19 @@ __global__ __launch_bounds__(256) void hg_kernel(GradArgs g) {
   constexpr int BT_STRIDE = 128 + 8;                   // bf16 elements per staged row
   __shared__ f32x4 s_red[2 * 4 * NT * 64];
   __shared__ __align__(16) uint16_t s_bt[NT * 16 * BT_STRIDE];       // B_a slab, transposed [j][o]
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, tid = threadIdx.x;
+  const int lane = threadIdx.x & 63, w = wave_id(), tid = threadIdx.x;
   const int n_blocks = g.hdr[HDR_NMRB];
   const XcdRange xr = xcd_range(n_blocks * g.ks);
   const uint16_t* X = reinterpret_cast<const uint16_t*>(g.X);
   const uint16_t* dY = reinterpret_cast<const uint16_t*>(g.dY);
   for (int tile = xr.first; tile < xr.end; tile += xr.step) {
     const int e = tile / g.ks, ks = tile - e * g.ks;
-    const int4 en = g.mrb[e];
+    const int4 en = load_entry(g.mrb, e);
     const int a = en.x, p0 = en.y, rows = en.z;
-    const SlotMeta m = g.meta[a];
+    const Slot m = load_slot(g.meta, a);
     const int r = m.rank;
-    const uint16_t* A = reinterpret_cast<const uint16_t*>(m.A);
-    const uint16_t* B = reinterpret_cast<const uint16_t*>(m.B);
+    const rsrc_t Aw = make_rsrc(m.A, (uint32_t)r * (uint32_t)g.d_in * 2u);
+    const rsrc_t Bw = make_rsrc(m.B, (uint32_t)g.d_out * (uint32_t)r * 2u);
     const int nt_used = (r + 15) >> 4;
 
     int trow[2];
@@ -133,7 +133,7 @@ __global__ __launch_bounds__(256) void hg_kernel(GradArgs g) {
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
           const int j = nt * 16 + (lane & 15);
-          wb[nt] = (j < r && kv) ? as_bf16x8(ldg16(A + (int64_t)j * g.d_in + k)) : zero_bf16x8();
+          wb[nt] = (j < r && kv) ? as_bf16x8(bload16(Aw, ((uint32_t)j * g.d_in + k) * 2u)) : zero_bf16x8();
         }
 #pragma unroll
         for (int mt = 0; mt < 2; ++mt)
@@ -153,7 +153,7 @@ __global__ __launch_bounds__(256) void hg_kernel(GradArgs g) {
         for (int item = tid; item < 128 * r8; item += 256) {
           const int ol = item / r8, j8 = (item - ol * r8) * 8;
           const int o = oc + ol;
-          bf16x8 v = (o < oe) ? load_row8(B + (int64_t)o * r, j8, r, RANK8) : zero_bf16x8();
+          bf16x8 v = (o < oe && j8 < r) ? wrow8<RANK8>(Bw, (uint32_t)o * r, j8, r) : zero_bf16x8();
           const uint4 u = __builtin_bit_cast(uint4, v);
           const uint32_t wv[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
@@ -232,13 +232,13 @@ template <int NT>
 __global__ __launch_bounds__(256) void dadb_kernel(GradArgs g) {
   constexpr int T_STRIDE = 32 + 8;                    // staged rows per column (+pad)
   __shared__ __align__(16) uint16_t s_t[64 * T_STRIDE];             // 32 rows x 64 columns, transposed
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, tid = threadIdx.x;
+  const int lane = threadIdx.x & 63, w = wave_id(), tid = threadIdx.x;
   const int nbB = (g.d_out + 63) / 64, nbA = (g.d_in + 63) / 64, nbt = nbB + nbA;
   const XcdRange xr = xcd_range(g.slot_count * nbt);
   for (int tile = xr.first; tile < xr.end; tile += xr.step) {
     const int sl = tile / nbt, c = tile - sl * nbt;
     const int a = g.slot_base + sl;
-    const SlotMeta m = g.meta[a];
+    const Slot m = load_slot(g.meta, a);
     const int r = m.rank;
     if (r <= 0) continue;
     const bool isB = c < nbB;
@@ -332,9 +332,9 @@ template <bool XB, bool WB>
 __global__ __launch_bounds__(256) void hg_valu_kernel(GradArgs g) {
   const int n_blocks = g.hdr[HDR_NMRB];
   for (int e = blockIdx.x; e < n_blocks; e += gridDim.x) {
-    const int4 en = g.mrb[e];
+    const int4 en = load_entry(g.mrb, e);
     const int a = en.x, p0 = en.y, rows = en.z;
-    const SlotMeta m = g.meta[a];
+    const Slot m = load_slot(g.meta, a);
     const int r = m.rank;
     float* ph = plane(g, 0, 0);
     float* pg = plane(g, 1, 0);
@@ -368,7 +368,7 @@ __global__ __launch_bounds__(256) void dadb_valu_kernel(GradArgs g) {
     const int sl = (int)(q / per_slot);
     const int a = g.slot_base + sl;
     const int64_t u = q - (int64_t)sl * per_slot;
-    const SlotMeta m = g.meta[a];
+    const SlotMeta m = g.meta[a];           // per-thread slot: not made uniform
     const int r = m.rank;
     if (r <= 0) continue;
     const bool isB = u < (int64_t)LORA_MAX_RANK * g.d_out;
