@@ -41,8 +41,6 @@ BF16_PEAK_TFLOPS = 2500.0      # dense bf16 matrix cores
 FP32_PEAK_TFLOPS = 157.3       # vector fp32
 ROTATE_BYTES = 576 << 20       # >= 2 x 288 MB of rotating working set
 HEADLINE = 2
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
-KERNEL_SOURCES = ["fwd_mfma.hip", "grad.hip", "plan.hip", "fwd_valu.hip"]
 
 
 def log(msg):
@@ -63,10 +61,13 @@ def parse():
 
 
 def source_digest():
+    """Digest of the native sources (kernels, launch code, headers)."""
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, "paper_2601_07376_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+    csrc = os.path.join(ROOT, "paper_2601_07376_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith((".hip", ".cpp", ".h")):
+            with open(os.path.join(csrc, f), "rb") as fh:
+                h.update(f.encode() + b"\0" + fh.read())
     return h.hexdigest()[:16]
 
 
@@ -155,11 +156,10 @@ class Rig:
             self.sets.append(d)
         torch.cuda.synchronize()
 
-    def step(self, i, ev=None):
-        """Enqueue one step on the current stream (plan build + op)."""
+    def build_plan(self, d):
+        """Enqueue the plan build for one copy; returns the host handle."""
         L, case = self.L, self.case
         lib = L.lib()
-        d = self.sets[i % len(self.sets)]
         stream = ctypes.c_void_p(self.torch.cuda.current_stream().cuda_stream)
         h = ctypes.c_void_p()
         mask = d["mask"].data_ptr() if d["mask"] is not None else None
@@ -174,8 +174,13 @@ class Rig:
                                      d["plan_ws"].data_ptr(), d["plan_ws"].numel(), stream,
                                      ctypes.byref(h))
         assert st == 0, lib.lora_last_error()
-        if ev is not None:
-            ev[0].record()
+        return h
+
+    def run_op(self, d, h):
+        """Enqueue the forward residual (or the masked gradients) for one copy."""
+        L, case = self.L, self.case
+        lib = L.lib()
+        stream = ctypes.c_void_p(self.torch.cuda.current_stream().cuda_stream)
         X = d["X"]
         xdt = 1 if case.x_dtype == "bf16" else 0
         if case.mask is None:
@@ -189,9 +194,13 @@ class Rig:
                                dY.stride(0), None, 0, d["pA"], d["pB"], 0,
                                d["op_ws"].data_ptr(), d["op_ws"].numel(), stream)
         assert st == 0, lib.lora_last_error()
-        if ev is not None:
-            ev[1].record()
-        lib.lora_plan_destroy(h)      # host object only; enqueued work keeps its arguments
+
+    def step(self, i):
+        """Enqueue one step on the current stream: plan build, then the op."""
+        d = self.sets[i % len(self.sets)]
+        h = self.build_plan(d)
+        self.run_op(d, h)
+        self.L.lib().lora_plan_destroy(h)   # host object only; enqueued work keeps its arguments
 
 
 def sleep_rate(torch):
@@ -208,6 +217,7 @@ def sleep_rate(torch):
 def run_workload(cfg, steps, warmup, rate):
     import torch
     import workloads
+    import paper_2601_07376_amd as L
     t0 = time.time()
     case = workloads.make_config(cfg)
     counts = workload_counts(case)
@@ -224,29 +234,39 @@ def run_workload(cfg, steps, warmup, rate):
     host_ms = (time.perf_counter() - c0) * 1e3 / max(warmup, 1)
     torch.cuda.synchronize()
 
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(steps)]
-    es, ee = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    gate_ms = min(500.0, 2.0 + 2.0 * host_ms * steps)
-    torch.cuda.synchronize()
+    def timed(enqueue, k):
+        """Average GPU time per call of enqueue(i) over k back-to-back calls: the
+        calls are queued behind a GPU-side start gate, so the GPU never waits on
+        the host, and two events on the compute stream bracket them."""
+        es, ee = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        gate_ms = min(500.0, 2.0 + 2.0 * host_ms * k)
+        torch.cuda.synchronize()
+        torch.cuda._sleep(int(gate_ms * rate))
+        es.record()
+        for i in range(k):
+            enqueue(i)
+        ee.record()
+        torch.cuda.synchronize()
+        return es.elapsed_time(ee) / k
+
+    # whole steps (plan + op), the measured quantity
     w0 = time.perf_counter()
-    torch.cuda._sleep(int(gate_ms * rate))
-    es.record()
-    for i in range(steps):
-        rig.step(i, evs[i])
-    ee.record()
-    torch.cuda.synchronize()
+    ms_step = timed(rig.step, steps)
     wall_ms = (time.perf_counter() - w0) * 1e3
-    gpu_ms = es.elapsed_time(ee)
-    op_us = np.array([a.elapsed_time(b) * 1e3 for a, b in evs])
-    ms_step = gpu_ms / steps
-    op_mean = float(op_us.mean())
+    # each kernel stage alone, back to back over the same rotating copies
+    handles = [rig.build_plan(d) for d in rig.sets]
+    torch.cuda.synchronize()
+    nc = len(rig.sets)
+    op_mean = timed(lambda i: rig.run_op(rig.sets[i % nc], handles[i % nc]), steps) * 1e3
+    for h in handles:
+        L.lib().lora_plan_destroy(h)
+    plan_us = timed(lambda i: L.lib().lora_plan_destroy(rig.build_plan(rig.sets[i % nc])),
+                    steps) * 1e3
     r = dict(workload=case.name, config=cfg, copies=copies, steps=steps,
              ms_per_step=ms_step, tokens_per_s=case.n / (ms_step * 1e-3),
-             op_us_mean=op_mean, op_us_p10=float(np.percentile(op_us, 10)),
-             op_us_p90=float(np.percentile(op_us, 90)),
+             op_us_mean=op_mean, plan_us_mean=plan_us,
              op=("lora_grad" if case.mask is not None else "lora_apply"),
-             wall_ms_incl_gate=wall_ms, gate_ms=gate_ms, host_enqueue_ms_per_step=host_ms,
+             wall_ms_incl_gate=wall_ms, host_enqueue_ms_per_step=host_ms,
              **counts)
     r["op_GBps"] = counts["op_bytes"] / (op_mean * 1e-6) / 1e9
     r["op_hbm_frac"] = r["op_GBps"] / HBM_PEAK_GBS
@@ -257,8 +277,8 @@ def run_workload(cfg, steps, warmup, rate):
     r["mfma_frac_ceiling"] = min(1.0, (counts["flops"] / counts["op_bytes"]) * HBM_PEAK_GBS
                                  / 1e3 / peak_f)
     r["step_GBps"] = ws_bytes / (ms_step * 1e-3) / 1e9
-    log(f"[bench]   {r['op']}: {op_mean:.2f} us (p10 {r['op_us_p10']:.2f}, p90 "
-        f"{r['op_us_p90']:.2f}), {r['op_GBps']:.0f} GB/s = {100 * r['op_hbm_frac']:.1f}% HBM, "
+    log(f"[bench]   plan {plan_us:.2f} us; {r['op']}: {op_mean:.2f} us, "
+        f"{r['op_GBps']:.0f} GB/s = {100 * r['op_hbm_frac']:.1f}% HBM, "
         f"{r['op_TFLOPs']:.1f} TFLOP/s; step {ms_step * 1e3:.2f} us, "
         f"{r['tokens_per_s']:.3e} tokens/s")
     del rig
@@ -267,19 +287,20 @@ def run_workload(cfg, steps, warmup, rate):
 
 
 def calib_copy():
-    """A plain device copy of 1 GiB (read 1 GiB, write 1 GiB) for counter scaling."""
+    """A plain elementwise copy kernel of known size (read 1 GiB, write 1 GiB): its
+    counter readings scale the FETCH_SIZE / WRITE_SIZE counters to bytes."""
     import torch
-    a = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    a = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
     b = torch.empty_like(a)
-    a.fill_(1)
+    a.fill_(1.0)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
-    b.copy_(a)
+    torch.neg(a, out=b)
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1)
-    log(f"[bench] calibration copy 1 GiB: {ms:.3f} ms = {2 * (1 << 30) / ms / 1e6:.0f} GB/s")
+    log(f"[bench] calibration copy (neg) 1 GiB: {ms:.3f} ms = {2 * (1 << 30) / ms / 1e6:.0f} GB/s")
     return dict(bytes_read=1 << 30, bytes_written=1 << 30, ms=ms)
 
 
@@ -307,17 +328,27 @@ def cpu_baseline(case, seconds):
                        f"plan + float64 residual, {el:.1f} s")
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_bgmv.fused_small_kernel.hbm_counters.txt")
+
+
 def traffic_for(result):
-    """HBM bytes per op from committed rocprofv3 counter runs, if they were taken
-    on the current kernel sources; otherwise None."""
+    """HBM bytes per launch of the headline kernel from the committed rocprofv3
+    counter summary, if its counters were taken on the current kernel sources;
+    otherwise None."""
     if not os.path.exists(TRAFFIC_FILE):
         return None
+    kv = {}
     with open(TRAFFIC_FILE) as f:
-        t = json.load(f)
-    if t.get("source_digest") != source_digest():
+        for ln in f:
+            if ":" in ln and not ln.startswith((" ", "#", "|")):
+                k, v = ln.split(":", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("source_digest") != source_digest() or kv.get("workload") != result["workload"]:
         return None
-    w = t.get("workloads", {}).get(result["workload"])
-    return None if w is None else w.get("bytes_per_op")
+    try:
+        return int(kv["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def main():
@@ -355,7 +386,7 @@ def main():
         cpu = cpu_baseline(head_case, args.cpu_seconds)
         log(f"[bench] cpu baseline (oracle): {cpu['value']:.3e} tokens/s on {cpu['cores']} threads")
     line = {
-        "metric": "mixed-adapter LoRA tokens/s (decode step: plan + fused residual)",
+        "metric": "mixed-adapter LoRA tokens/s; decode HBM GB/s and prefill/bwd TFLOP/s vs peak",
         "value": round(h["tokens_per_s"], 1),
         "unit": "tokens/s",
         "n_gpus": 1,

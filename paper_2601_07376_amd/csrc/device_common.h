@@ -15,12 +15,17 @@ __device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
   return __uint_as_float(bits16 << 16);
 }
 
-// float -> bfloat16 bits, round to nearest even; NaN stays a quiet NaN.
+typedef __attribute__((ext_vector_type(2))) float f32x2;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+
+// float -> bfloat16, round to nearest even (gfx950 converts in hardware,
+// v_cvt_pk_bf16_f32, two values per instruction; NaN stays NaN).
+__device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {
+  const f32x2 v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
 __device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return u >> 16;
+  return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)f);
 }
 
 // Plain accessors for buffers passed as kernel arguments (the compiler knows
@@ -81,14 +86,14 @@ __device__ __forceinline__ bf16x8 pack_bf16x8(const uint32_t (&b)[8]) {
 // Split eight float32 values into hi = bf16(h) and lo = bf16(h - hi): the pair
 // carries 16 significant bits, and h - hi is exact in float32.
 __device__ __forceinline__ void split_hi_lo(const float (&h)[8], bf16x8& hi, bf16x8& lo) {
-  uint32_t bh[8], bl[8];
+  uint32_t ph[4], pl[4];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    bh[i] = f32_to_bf16_rne(h[i]);
-    bl[i] = f32_to_bf16_rne(h[i] - bf16_to_f32(bh[i]));
+  for (int i = 0; i < 4; ++i) {
+    ph[i] = pack2_bf16(h[2 * i], h[2 * i + 1]);
+    pl[i] = pack2_bf16(h[2 * i] - bf16_to_f32(ph[i] & 0xffffu), h[2 * i + 1] - bf16_to_f32(ph[i] >> 16));
   }
-  hi = pack_bf16x8(bh);
-  lo = pack_bf16x8(bl);
+  hi = as_bf16x8(make_uint4(ph[0], ph[1], ph[2], ph[3]));
+  lo = as_bf16x8(make_uint4(pl[0], pl[1], pl[2], pl[3]));
 }
 
 __device__ __forceinline__ f32x4 mfma_16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
@@ -124,6 +129,13 @@ __device__ __forceinline__ bf16x8 wrow8(rsrc_t w, uint32_t row0, int j, int len)
 // load at the join).
 __device__ __forceinline__ bf16x8 sel(bool keep, bf16x8 v) { return keep ? v : zero_bf16x8(); }
 
+
+// Wait until every vector memory operation of this wave has completed.  Placed
+// where all loads are known to be done anyway (right after the last use of a
+// load batch), it costs nothing and tells the compiler's wait insertion that
+// nothing is outstanding, so later code does not wait on the completion of
+// stores issued in between.  gfx9 encoding: vmcnt 0, expcnt 7, lgkmcnt 15.
+__device__ __forceinline__ void vmem_drained() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 // Wave-uniform views of per-tile metadata.  Entries and slot records are read
 // with vector loads; readfirstlane tells the compiler the values are the same in

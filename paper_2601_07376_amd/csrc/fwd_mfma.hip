@@ -121,9 +121,8 @@ __device__ __forceinline__ void y_store(const YFrag<YBF16>& f, void* Yv, int64_t
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int q = 2 * c + (i >> 1), e0 = (2 * i) & 3;
-        const uint32_t r0 = f32_to_bf16_rne(fmaf(s, acc[q][e0], bf16_to_f32(w[i] & 0xffffu)));
-        const uint32_t r1 = f32_to_bf16_rne(fmaf(s, acc[q][e0 + 1], bf16_to_f32(w[i] >> 16)));
-        o4[i] = r0 | (r1 << 16);
+        o4[i] = pack2_bf16(fmaf(s, acc[q][e0], bf16_to_f32(w[i] & 0xffffu)),
+                           fmaf(s, acc[q][e0 + 1], bf16_to_f32(w[i] >> 16)));
       }
       stg16(Y + o, make_uint4(o4[0], o4[1], o4[2], o4[3]));
     } else {
@@ -327,9 +326,8 @@ __device__ __forceinline__ void y8_store(const Y8<YBF16>& f, void* Yv, int64_t l
     for (int i = 0; i < 4; ++i) {
       const f32x4& a = (i < 2) ? a0 : a1;
       const int e0 = (2 * i) & 3;
-      const uint32_t r0 = f32_to_bf16_rne(fmaf(s, a[e0], bf16_to_f32(w[i] & 0xffffu)));
-      const uint32_t r1 = f32_to_bf16_rne(fmaf(s, a[e0 + 1], bf16_to_f32(w[i] >> 16)));
-      o4[i] = r0 | (r1 << 16);
+      o4[i] = pack2_bf16(fmaf(s, a[e0], bf16_to_f32(w[i] & 0xffffu)),
+                         fmaf(s, a[e0 + 1], bf16_to_f32(w[i] >> 16)));
     }
     stg16(Y, make_uint4(o4[0], o4[1], o4[2], o4[3]));
   } else {
@@ -494,7 +492,9 @@ __global__ __launch_bounds__(256) void expand_kernel(FwdArgs p) {
 // ---------------------------------------------------------------------------
 template <bool YBF16, int NT, bool RANK8>
 __global__ __launch_bounds__(256) void fused_small_kernel(FwdArgs p) {
-  constexpr int U = NT == 1 ? 8 : (NT == 2 ? 4 : (NT == 4 ? 2 : 1));
+  // k-steps per load batch: two batches of 16 cover d_in = 4096 at rank <= 16,
+  // so the whole shrink is in flight at once (one workgroup per CU anyway)
+  constexpr int U = NT == 1 ? 16 : (NT == 2 ? 8 : (NT == 4 ? 4 : 2));
   constexpr int KSM = (NT * 16 + 31) / 32;
   constexpr bool B_AHEAD = KSM == 1;          // B of every slice requested up front
   __shared__ f32x4 s_red[2 * NT * 64];
@@ -556,6 +556,7 @@ __global__ __launch_bounds__(256) void fused_small_kernel(FwdArgs p) {
     }
     shrink_steps<1, NT, U>(acc, xrow, A, arow, 1, nt_used, w * 32, 128, p.d_in);
   }
+  vmem_drained();           // B and Y were requested before the shrink loads
   reduce_waves<NT>(acc, s_red);
   if (w == 0) {
 #pragma unroll
@@ -632,16 +633,16 @@ int env_int(const char* name, int dflt) {
   return (v != nullptr && *v) ? std::atoi(v) : dflt;
 }
 
-// Expand shapes: (row tiles per wave, Y prefetch depth).  The default favours
-// many resident waves; LORA_EXPAND_VARIANT selects another for measurements.
+// Expand shapes: (TT, Y prefetch depth).  The default, all four row tiles in
+// every wave (the waves split the columns) with one slice of Y prefetched, measured fastest on the prefill and
+// mixed-rank workloads; LORA_EXPAND_VARIANT selects another for measurements.
 template <bool YB, bool R8, int KSM>
 hipError_t launch_expand_variant(int grid, const FwdArgs& a, hipStream_t s) {
   switch (env_int("LORA_EXPAND_VARIANT", 0)) {
-    case 1: return launch(expand_kernel<YB, R8, KSM, 2, 3>, grid, a, s);
-    case 2: return launch(expand_kernel<YB, R8, KSM, 1, 5>, grid, a, s);
-    case 3: return launch(expand_kernel<YB, R8, KSM, 2, 1>, grid, a, s);
-    case 4: return launch(expand_kernel<YB, R8, KSM, 4, 1>, grid, a, s);
-    default: return launch(expand_kernel<YB, R8, KSM, 1, 3>, grid, a, s);
+    case 1: return launch(expand_kernel<YB, R8, KSM, 2, 1>, grid, a, s);
+    case 2: return launch(expand_kernel<YB, R8, KSM, 1, 3>, grid, a, s);
+    case 3: return launch(expand_kernel<YB, R8, KSM, 4, 3>, grid, a, s);
+    default: return launch(expand_kernel<YB, R8, KSM, 4, 1>, grid, a, s);
   }
 }
 
