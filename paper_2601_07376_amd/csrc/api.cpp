@@ -69,16 +69,6 @@ int env_int(const char* name, int dflt) {
   return std::atoi(v);
 }
 
-// Fused small-group policy.  Batches of up to 1024 rows (decode steps) send
-// every adapter group through the fused kernel, so a decode step is a single
-// launch; larger batches send groups of up to 16 rows there and larger groups
-// through the grouped shrink + expand.
-int32_t small_max_policy(int32_t n) {
-  const int v = env_int("LORA_SMALL_MAX", -1);
-  if (v >= 0) return v;
-  return n <= 1024 ? INT32_MAX : lora::SMALL_ROWS;
-}
-
 // Output-column chunks per small-group entry (sibling workgroups).
 int32_t small_chunks_policy(int32_t d_out) {
   const int v = env_int("LORA_SMALL_CHUNKS", 0);
@@ -115,6 +105,7 @@ lora::OpLaunch op_base(const lora_plan* p) {
   lora::OpLaunch o{};
   o.hdr = p->d.hdr;
   o.rb = p->d.rb;
+  o.srec = p->d.srec;
   o.perm = p->d.perm;
   o.meta = static_cast<const lora::SlotMeta*>(p->table->dev_meta);
   o.n = p->n;
@@ -177,6 +168,7 @@ lora_status make_plan(const lora_table* t, int32_t n, const int32_t* idx,
   p->d.m_blk = reinterpret_cast<int32_t*>(b + L.m_blk);
   p->d.rb = reinterpret_cast<int4*>(b + L.rb);
   p->d.mrb = reinterpret_cast<int4*>(b + L.mrb);
+  p->d.srec = reinterpret_cast<lora::SmallRec*>(b + L.srec);
   p->d.seg_ids = reinterpret_cast<int32_t*>(b + L.seg_ids);
   p->r_max = 0;
   p->rank8 = true;
@@ -185,7 +177,7 @@ lora_status make_plan(const lora_table* t, int32_t n, const int32_t* idx,
     p->r_max = std::max(p->r_max, s.rank);
     p->rank8 = p->rank8 && (s.rank % 8 == 0);
   }
-  p->small_max = small_max_policy(n);
+  p->small_max = lora::small_max_policy(n);
 
   lora::PlanLaunch a{};
   a.d = p->d;
@@ -211,6 +203,30 @@ lora_status make_plan(const lora_table* t, int32_t n, const int32_t* idx,
 
 namespace lora {
 
+// Fused small-group policy.  Batches of up to 1024 rows (decode steps) send
+// every adapter group through the fused kernel, so a decode step is a single
+// launch; larger batches send groups of up to 16 rows there and larger groups
+// through the grouped shrink + expand.
+int32_t small_max_policy(int32_t n) {
+  const int v = env_int("LORA_SMALL_MAX", -1);
+  if (v >= 0) return v;
+  return n <= 1024 ? INT32_MAX : SMALL_ROWS;
+}
+
+// Gradient workspace: fp32 partial planes (two per d-slice), the summed bf16
+// hi / lo planes, and B^T of every slot.
+GradLayout grad_layout(int32_t mrb_ub, int32_t r_max, int32_t num_slots, int32_t d_out) {
+  GradLayout G{};
+  const size_t r_pad = (size_t)(std::max(r_max, 1) + 15) / 16 * 16;
+  const size_t p_stride = (size_t)mrb_ub * MRB_ROWS;
+  size_t o = 0;
+  G.partial = o; o += al256(2 * GRAD_SPLITS_MAX * r_pad * p_stride * 4);
+  G.fin = o;     o += al256(2 * 2 * r_pad * p_stride * 2);
+  G.bt = o;      o += al256((size_t)num_slots * r_pad * (size_t)d_out * 2);
+  G.total = o;
+  return G;
+}
+
 PlanLayout plan_layout(int32_t n, int32_t S) {
   PlanLayout L{};
   const size_t nn = (size_t)std::max(n, 1);
@@ -230,6 +246,16 @@ PlanLayout plan_layout(int32_t n, int32_t S) {
   L.mrb_max = n / MRB_ROWS + std::min(S, n) + 1;
   L.rb = o;          o += al256((size_t)L.rb_max * 16);
   L.mrb = o;         o += al256((size_t)L.mrb_max * 16);
+  {
+    // small-group records: every group may be small, or at most
+    // ceil(small_max / 16) records for each adapter
+    const int32_t sm = small_max_policy(n);
+    int64_t m = L.rb_max;
+    if (sm != INT32_MAX)
+      m = std::min<int64_t>(m, (int64_t)std::min(S, n) * ((sm + SMALL_ROWS - 1) / SMALL_ROWS) + 1);
+    L.srec_max = (int32_t)std::max<int64_t>(m, 1);
+  }
+  L.srec = o;        o += al256((size_t)L.srec_max * sizeof(SmallRec));
   L.seg_ids = o;     o += al256(nn * 4);
   L.total = o;
   return L;
@@ -488,8 +514,8 @@ lora_status lora_apply(const lora_plan* p, const void* X, lora_dtype x_dtype, in
       if (e == hipSuccess) e = lora::launch_expand_mfma(o, H, ldh, Y, y_dtype, ldy, s);
       if (e != hipSuccess) return hip_fail(e, "grouped shrink/expand launch");
     }
-    o.count_word = lora::HDR_NRB_TOTAL;
-    o.first_word = lora::HDR_NRB_LARGE;
+    o.count_word = lora::HDR_NSMALL;
+    o.first_word = -1;
     o.rb_ub = ub_small(p);
     e = lora::launch_bgmv_mfma(o, X, ldx, Y, y_dtype, ldy, small_chunks_policy(t->d_out), s);
     if (e != hipSuccess) return hip_fail(e, "fused small-group launch");
@@ -508,9 +534,7 @@ lora_status lora_apply(const lora_plan* p, const void* X, lora_dtype x_dtype, in
 
 size_t lora_grad_workspace_bytes(const lora_plan* p) {
   if (p == nullptr) return 0;
-  const size_t r_pad = (size_t)(std::max(p->r_max, 1) + 15) / 16 * 16;
-  const size_t p_stride = (size_t)ub_mrb(p) * lora::MRB_ROWS;
-  return al256(2 * GRAD_SPLITS_MAX * r_pad * p_stride * 4);
+  return lora::grad_layout(ub_mrb(p), p->r_max, p->table->num_slots, p->table->d_out).total;
 }
 
 lora_status lora_grad(const lora_plan* p, const void* X, lora_dtype x_dtype, int64_t ldx,
@@ -559,7 +583,11 @@ lora_status lora_grad(const lora_plan* p, const void* X, lora_dtype x_dtype, int
   g.dA = dA;
   g.dB = dB;
   g.accumulate = accumulate;
-  g.hg = static_cast<float*>(ws);
+  const lora::GradLayout GL = lora::grad_layout(ub_mrb(p), p->r_max, t->num_slots, t->d_out);
+  char* wsb = static_cast<char*>(ws);
+  g.hg = reinterpret_cast<float*>(wsb + GL.partial);
+  g.fin = reinterpret_cast<uint16_t*>(wsb + GL.fin);
+  g.bt = reinterpret_cast<uint16_t*>(wsb + GL.bt);
   g.k_splits = mfma ? grad_splits_policy(t->d_in, t->d_out) : 1;
   g.p_stride = ub_mrb(p) * lora::MRB_ROWS;
   g.r_pad = (std::max(p->r_max, 1) + 15) / 16 * 16;

@@ -100,6 +100,19 @@ __device__ __forceinline__ f32x4 mfma_16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
+// Wait states between the last matrix-core instruction of a sequence and the
+// first vector instruction that reads its result.  The hardware does not
+// interlock that dependency; the compiler inserts the wait states itself
+// within straight-line code but has been seen to miss them when the reader
+// sits behind a branch (the first accumulator register then reads stale).
+// Call this after every matrix-core loop whose results are read after control
+// flow: 3 x 8 wait states cover the longest (16-pass) instructions.
+__device__ __forceinline__ void mfma_fence() {
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+}
+
 // Eight consecutive bf16 weights of a row that starts at element `row0` of a
 // weight buffer, columns [j, j + 8) of a row of len.  With RANK8 (len a multiple
 // of 8) this is one 16-byte load from a clamped column and the lanes with
@@ -176,6 +189,33 @@ __device__ __forceinline__ Slot load_slot(const Meta* meta, int a) {
   s.scale = __int_as_float(uni(__float_as_int(m.scale)));
   return s;
 }
+
+// Lane shuffles through DPP (gfx9): a few cycles each, where ds_bpermute
+// (__shfl and friends) costs an LDS round trip.
+//   row_incl_scan   inclusive prefix sum inside each row of 16 lanes
+//   wave_incl_scan  inclusive prefix sum over the 64 lanes (row scans, then the
+//                   last lane of row 0 / row 1 broadcast into the later rows)
+//   lane_prev/next  the value of lane - 1 / lane + 1 (`edge` at the wave ends)
+__device__ __forceinline__ int row_incl_scan(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, true);   // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, true);   // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, true);   // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, true);   // row_shr:8
+  return x;
+}
+__device__ __forceinline__ int wave_incl_scan(int x) {
+  x = row_incl_scan(x);
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);  // row_bcast:31
+  return x;
+}
+__device__ __forceinline__ int lane_prev(int x, int edge) {
+  return __builtin_amdgcn_update_dpp(edge, x, 0x138, 0xf, 0xf, false);  // wave_shr:1
+}
+__device__ __forceinline__ int lane_next(int x, int edge) {
+  return __builtin_amdgcn_update_dpp(edge, x, 0x130, 0xf, 0xf, false);  // wave_shl:1
+}
+__device__ __forceinline__ int lane_value(int x, int l) { return __builtin_amdgcn_readlane(x, l); }
 
 // Tile range of the XCD this workgroup runs on.  Workgroups are dispatched to
 // the 8 XCDs round-robin by id, so workgroup g runs on XCD g % 8.  Giving each

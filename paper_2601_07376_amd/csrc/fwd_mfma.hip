@@ -43,6 +43,8 @@ struct FwdArgs {
   void* Y;
   int64_t ldy;
   int32_t n_chunks, chunk;
+  const SmallRec* srec;     // fused path: small-group records
+  int32_t n_rec;            // records the array holds (host bound)
 };
 
 __device__ __forceinline__ void entry_range(const FwdArgs& p, int& first, int& count) {
@@ -177,8 +179,8 @@ __device__ __forceinline__ void reduce_waves(f32x4 (&acc)[N], f32x4* s_red) {
 // the previous one feeds the matrix cores.
 template <int MT, int NT, int U>
 __device__ __forceinline__ void shrink_steps(f32x4 (&acc)[MT * NT], const uint16_t* (&xr)[MT],
-                                             rsrc_t A, const uint32_t (&ar)[NT], int mt_used,
-                                             int nt_used, int kstart, int kstride, int kend) {
+                                             rsrc_t A, const uint32_t (&ar)[NT], int kstart,
+                                             int kstride, int kend) {
   const int kg = ((threadIdx.x & 63) >> 4) * 8;
   struct Buf {
     bf16x8 x[U][MT];
@@ -199,35 +201,37 @@ __device__ __forceinline__ void shrink_steps(f32x4 (&acc)[MT * NT], const uint16
         b.w[u][nt] = as_bf16x8(bload16(A, (ar[nt] + (uint32_t)kk) * 2u));
     }
   };
-  // the K tail (k >= kend) is zeroed on the X operand where it is consumed
+  // the K tail (k >= kend) is zeroed on the X operand where it is consumed.
+  // Every tile is computed (tiles past the rows or the rank hold values that
+  // are never stored): no branch separates a matrix-core instruction from its
+  // reader.
   auto compute = [&](const Buf& b) {
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
-        if (mt >= mt_used) continue;
         const bf16x8 xo = sel(b.kv[u], b.x[u][mt]);
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          if (nt >= nt_used) continue;
+        for (int nt = 0; nt < NT; ++nt)
           acc[mt * NT + nt] = mfma_16x16x32(xo, b.w[u][nt], acc[mt * NT + nt]);
-        }
       }
   };
-  if (kstart >= kend) return;
-  const int span = U * kstride;
-  Buf b0, b1;
-  load(b0, kstart);
-  for (int kb = kstart;; kb += 2 * span) {
-    const int k1 = kb + span;
-    if (k1 < kend) load(b1, k1);
-    compute(b0);
-    if (k1 >= kend) break;
-    const int k2 = k1 + span;
-    if (k2 < kend) load(b0, k2);
-    compute(b1);
-    if (k2 >= kend) break;
+  if (kstart < kend) {
+    const int span = U * kstride;
+    Buf b0, b1;
+    load(b0, kstart);
+    for (int kb = kstart;; kb += 2 * span) {
+      const int k1 = kb + span;
+      if (k1 < kend) load(b1, k1);
+      compute(b0);
+      if (k1 >= kend) break;
+      const int k2 = k1 + span;
+      if (k2 < kend) load(b0, k2);
+      compute(b1);
+      if (k2 >= kend) break;
+    }
   }
+  mfma_fence();
 }
 
 // ---------------------------------------------------------------------------
@@ -247,7 +251,7 @@ __global__ __launch_bounds__(256) void shrink_kernel(FwdArgs p) {
     const Slot m = load_slot(p.meta, a);
     const int r = m.rank;
     const rsrc_t A = make_rsrc(m.A, (uint32_t)r * (uint32_t)p.d_in * 2u);
-    const int mt_used = (rows + 15) >> 4, nt_used = (r + 15) >> 4;
+    const int mt_used = (rows + 15) >> 4;
 
     const uint16_t* xrow[4];
 #pragma unroll
@@ -264,7 +268,7 @@ __global__ __launch_bounds__(256) void shrink_kernel(FwdArgs p) {
     f32x4 acc[4 * NT];
 #pragma unroll
     for (int i = 0; i < 4 * NT; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    shrink_steps<4, NT, U>(acc, xrow, A, arow, mt_used, nt_used, w * 32, 128, p.d_in);
+    shrink_steps<4, NT, U>(acc, xrow, A, arow, w * 32, 128, p.d_in);
     reduce_waves<4 * NT>(acc, s_red);
     if (w == 0) {
 #pragma unroll
@@ -372,9 +376,6 @@ __global__ __launch_bounds__(256) void expand_kernel(FwdArgs p) {
     const int r = m.rank;
     const float s = m.scale;
     const rsrc_t Bw = make_rsrc(m.B, (uint32_t)p.d_out * (uint32_t)r * 2u);
-    const int ks_used = (r + 31) >> 5;
-    const int tt_used = min(TT, (rows - rg * TT * 16 + 15) >> 4);
-
     int trow[TT];
     bool rv[TT];
 #pragma unroll
@@ -448,19 +449,18 @@ __global__ __launch_bounds__(256) void expand_kernel(FwdArgs p) {
         for (int tt = 0; tt < TT; ++tt) acc[q][tt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < KSM; ++ks) {
-        if (ks >= ks_used) continue;
         const bool jv = ks * 32 + jg < r;
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
           const bf16x8 bq = sel(jv, b[ks][q]);
 #pragma unroll
           for (int tt = 0; tt < TT; ++tt) {
-            if (tt >= tt_used) continue;
             acc[q][tt] = mfma_16x16x32(bq, hh[ks][tt], acc[q][tt]);
             acc[q][tt] = mfma_16x16x32(bq, hl[ks][tt], acc[q][tt]);
           }
         }
       }
+      mfma_fence();
       const int o = o_w + 8 * og;
       if (o < c1) {
 #pragma unroll
@@ -485,50 +485,62 @@ __global__ __launch_bounds__(256) void expand_kernel(FwdArgs p) {
 }
 
 // ---------------------------------------------------------------------------
-// fused small-group kernel: entries of <= 16 rows; workgroup (entry, chunk of
-// at most 1024 columns).  Each wave owns up to 4 slices of 64 columns.  The
-// chunk's B (small ranks) and Y are requested before the shrink streams A, so
-// their latency hides under it.
+// fused small-group kernel: one small-group record (<= 16 rows of one adapter)
+// per workgroup, and a chunk of at most 64 * FW * FSL output columns.
+//
+// The record (128 bytes, written by the plan) holds the weight pointers, rank,
+// scale and row ids, so one round trip yields everything; the chunk's B (small
+// ranks) and Y are then requested before the shrink streams X and A, whose k-
+// steps are spread over all FW waves.  The waves' partial H are summed in a
+// fixed order through LDS; H (hi / lo) feeds the expand of each wave's column
+// slices.  Sibling workgroups (same record, other column chunks) share
+// blockIdx % 8, so they run on one XCD and read A from its L2.
 // ---------------------------------------------------------------------------
+constexpr int FW = 8;     // waves per fused workgroup
+constexpr int FSL = 2;    // 64-column slices per wave
+
 template <bool YBF16, int NT, bool RANK8>
-__global__ __launch_bounds__(256) void fused_small_kernel(FwdArgs p) {
-  // k-steps per load batch: two batches of 16 cover d_in = 4096 at rank <= 16,
-  // so the whole shrink is in flight at once (one workgroup per CU anyway)
-  constexpr int U = NT == 1 ? 16 : (NT == 2 ? 8 : (NT == 4 ? 4 : 2));
+__global__ __launch_bounds__(FW * 64) void fused_small_kernel(FwdArgs p) {
+  // k-steps per load batch (two batches in flight)
+  constexpr int U = NT == 1 ? 8 : (NT == 2 ? 4 : (NT == 4 ? 2 : 1));
   constexpr int KSM = (NT * 16 + 31) / 32;
   constexpr bool B_AHEAD = KSM == 1;          // B of every slice requested up front
-  __shared__ f32x4 s_red[2 * NT * 64];
+  __shared__ f32x4 s_red[FW * NT * 64];
   __shared__ float s_h[16][NT * 16 + 4];
   const int lane = threadIdx.x & 63, w = wave_id();
   const int og = lane >> 4, mrow = lane & 15;
-  int first, count;
-  entry_range(p, first, count);
   const int P = p.n_chunks;
-  // siblings (same entry, different column chunk) share blockIdx % 8, i.e. one XCD
+  // siblings (same record, different column chunk) share blockIdx % 8, i.e. one XCD
   const int slot = (int)(blockIdx.x >> 3);
   const int e = 8 * (slot / P) + (int)(blockIdx.x & 7);
   const int pc = slot % P;
-  if (e >= count) return;
-  const int4 en = load_entry(p.rb, first + e);
-  const int a = en.x, p0 = en.y, rows = en.z;
-  const Slot m = load_slot(p.meta, a);
-  const int r = m.rank;
-  const float s = m.scale;
-  const rsrc_t A = make_rsrc(m.A, (uint32_t)r * (uint32_t)p.d_in * 2u);
-  const rsrc_t Bw = make_rsrc(m.B, (uint32_t)p.d_out * (uint32_t)r * 2u);
-  const int nt_used = (r + 15) >> 4, ks_used = (r + 31) >> 5;
 
+  // ---- the record and the entry count, in one round trip (the record index is
+  // clamped to the array; records at or past the count are never used)
+  const int er = min(e, p.n_rec - 1);
+  const int4* rec = reinterpret_cast<const int4*>(p.srec + er);
+  const int4 h0 = rec[0], h1 = rec[1];
+  const int trow = ldg(&p.srec[er].row[mrow]);
+  const int count = p.hdr[p.count_word];
+  if (e >= count) return;
+  const void* Ap = uni_ptr(reinterpret_cast<const void*>(
+      (uint64_t)(uint32_t)h0.x | ((uint64_t)(uint32_t)h0.y << 32)));
+  const void* Bp = uni_ptr(reinterpret_cast<const void*>(
+      (uint64_t)(uint32_t)h0.z | ((uint64_t)(uint32_t)h0.w << 32)));
+  const int rows = uni(h1.x), r = uni(h1.y);
+  const float s = __int_as_float(uni(h1.z));
+  const rsrc_t A = make_rsrc(Ap, (uint32_t)r * (uint32_t)p.d_in * 2u);
+  const rsrc_t Bw = make_rsrc(Bp, (uint32_t)p.d_out * (uint32_t)r * 2u);
   const bool rv = mrow < rows;
-  const int trow = ldg(p.perm + p0 + (rv ? mrow : rows - 1));
   const int c0 = pc * p.chunk;
   const int c1 = min(p.d_out, c0 + p.chunk);
 
   // ---- B (small ranks) and Y of this wave's column slices, requested first
-  bf16x8 bo_ahead[B_AHEAD ? 4 : 1][4];
+  bf16x8 bo_ahead[B_AHEAD ? FSL : 1][4];
   if (B_AHEAD) {
 #pragma unroll
-    for (int sl = 0; sl < 4; ++sl) {
-      const int o_w = c0 + w * 64 + 256 * sl;
+    for (int sl = 0; sl < FSL; ++sl) {
+      const int o_w = c0 + 64 * (w + FW * sl);
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int o = out_col(o_w, q, mrow);
@@ -537,12 +549,12 @@ __global__ __launch_bounds__(256) void fused_small_kernel(FwdArgs p) {
       }
     }
   }
-  YFrag<YBF16> yf[4];
+  YFrag<YBF16> yf[FSL];
 #pragma unroll
-  for (int sl = 0; sl < 4; ++sl)
-    y_load<YBF16>(yf[sl], p.Y, p.ldy, trow, c0 + w * 64 + 256 * sl, og, c1);
+  for (int sl = 0; sl < FSL; ++sl)
+    y_load<YBF16>(yf[sl], p.Y, p.ldy, trow, c0 + 64 * (w + FW * sl), og, c1);
 
-  // ---- shrink: H[16 x r] = X[rows] A^T, d_in split over the waves
+  // ---- shrink: H[16 x r] = X[rows] A^T, the k-steps spread over the waves
   f32x4 acc[NT];
 #pragma unroll
   for (int i = 0; i < NT; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -554,15 +566,23 @@ __global__ __launch_bounds__(256) void fused_small_kernel(FwdArgs p) {
       const int j = nt * 16 + mrow;
       arow[nt] = (uint32_t)(j < r ? j : r - 1) * (uint32_t)p.d_in;
     }
-    shrink_steps<1, NT, U>(acc, xrow, A, arow, 1, nt_used, w * 32, 128, p.d_in);
+    shrink_steps<1, NT, U>(acc, xrow, A, arow, w * 32, 32 * FW, p.d_in);
   }
   vmem_drained();           // B and Y were requested before the shrink loads
-  reduce_waves<NT>(acc, s_red);
-  if (w == 0) {
+
+  // ---- sum the waves' partial H in a fixed order (wave 0, 1, ..., FW - 1)
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
+  for (int nt = 0; nt < NT; ++nt) s_red[(w * NT + nt) * 64 + lane] = acc[nt];
+  __syncthreads();
+  {
+    const float* red = reinterpret_cast<const float*>(s_red);
+    for (int i = threadIdx.x; i < NT * 256; i += FW * 64) {
+      const int nt = i >> 8, l = (i >> 2) & 63, v = i & 3;
+      float sum = red[((0 * NT + nt) * 64 + l) * 4 + v];
 #pragma unroll
-      for (int v = 0; v < 4; ++v) s_h[og * 4 + v][nt * 16 + mrow] = acc[nt][v];
+      for (int ww = 1; ww < FW; ++ww) sum += red[((ww * NT + nt) * 64 + l) * 4 + v];
+      s_h[(l >> 4) * 4 + v][nt * 16 + (l & 15)] = sum;
+    }
   }
   __syncthreads();
 
@@ -579,15 +599,14 @@ __global__ __launch_bounds__(256) void fused_small_kernel(FwdArgs p) {
 
   // ---- expand over this wave's column slices
 #pragma unroll
-  for (int sl = 0; sl < 4; ++sl) {
-    const int o_w = c0 + w * 64 + 256 * sl;
+  for (int sl = 0; sl < FSL; ++sl) {
+    const int o_w = c0 + 64 * (w + FW * sl);
     if (o_w >= c1) continue;
     f32x4 acc2[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) acc2[q] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < KSM; ++ks) {
-      if (ks >= ks_used) continue;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         bf16x8 bo;
@@ -602,14 +621,15 @@ __global__ __launch_bounds__(256) void fused_small_kernel(FwdArgs p) {
         acc2[q] = mfma_16x16x32(bo, hl[ks], acc2[q]);
       }
     }
+    mfma_fence();
     if (rv) y_store<YBF16>(yf[sl], p.Y, p.ldy, trow, o_w, og, c1, s, acc2);
   }
 }
 
 template <typename K>
-hipError_t launch(K kernel, int grid, const FwdArgs& a, hipStream_t s) {
+hipError_t launch(K kernel, int grid, const FwdArgs& a, hipStream_t s, int threads = 256) {
   if (grid <= 0) return hipSuccess;
-  hipLaunchKernelGGL(kernel, dim3(grid), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(kernel, dim3(grid), dim3(threads), 0, s, a);
   return hipGetLastError();
 }
 
@@ -657,10 +677,11 @@ hipError_t launch_expand_ks(const OpLaunch& o, int grid, const FwdArgs& a, hipSt
 template <bool YB, bool R8>
 hipError_t launch_fused_nt(const OpLaunch& o, int grid, const FwdArgs& a, hipStream_t s) {
   const int nt = (o.r_max + 15) / 16;
-  if (nt <= 1) return launch(fused_small_kernel<YB, 1, R8>, grid, a, s);
-  if (nt <= 2) return launch(fused_small_kernel<YB, 2, R8>, grid, a, s);
-  if (nt <= 4) return launch(fused_small_kernel<YB, 4, R8>, grid, a, s);
-  return launch(fused_small_kernel<YB, 8, R8>, grid, a, s);
+  constexpr int T = FW * 64;
+  if (nt <= 1) return launch(fused_small_kernel<YB, 1, R8>, grid, a, s, T);
+  if (nt <= 2) return launch(fused_small_kernel<YB, 2, R8>, grid, a, s, T);
+  if (nt <= 4) return launch(fused_small_kernel<YB, 4, R8>, grid, a, s, T);
+  return launch(fused_small_kernel<YB, 8, R8>, grid, a, s, T);
 }
 
 }  // namespace
@@ -703,10 +724,13 @@ hipError_t launch_bgmv_mfma(const OpLaunch& o, const void* X, int64_t ldx, void*
   a.ldx = ldx;
   a.Y = Y;
   a.ldy = ldy;
-  // each workgroup covers at most 1024 columns (4 slices of 64 per wave)
-  const int P = std::max({1, n_chunks, (o.d_out + 1023) / 1024});
+  // each workgroup covers at most CW columns (FSL slices of 64 per wave)
+  constexpr int CW = 64 * FW * FSL;
+  const int P = std::max({1, n_chunks, (o.d_out + CW - 1) / CW});
   a.n_chunks = P;
   a.chunk = ((o.d_out + P - 1) / P + 63) / 64 * 64;
+  a.srec = o.srec;
+  a.n_rec = std::max(o.rb_ub, 1);
   const int grid = 8 * P * ((o.rb_ub + 7) / 8);
   const bool yb = y_dtype == LORA_BF16;
   if (yb && o.rank8) return launch_fused_nt<true, true>(o, grid, a, s);

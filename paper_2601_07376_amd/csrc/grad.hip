@@ -5,13 +5,19 @@
 //
 //   H = X_m A_a^T,  G = dY_m B_a,  dB_a = s_a dY_m^T H,  dA_a = s_a G^T X_m.
 //
-// Stage 1 (per trainable row block of <= 32 rows and d-slice ks): partial H and
-// G over the slice, written transposed into "planes" [j][column], where row i
-// of block e sits in column 32 e + i (32-aligned, so stage 2 loads float4).
-// Stage 2 (per adapter and 64-wide column block of dB or dA): a fixed-order
-// reduction over the adapter's trainable rows, 32 rows per step; the partial
-// planes are summed in slice order.  Rows outside T_a^m are never read.  No
-// floating-point atomics anywhere, so the result is the same bytes run to run.
+// Matrix-core path, four launches:
+//  0. B_a^T of every live slot into the workspace, so that G reads its second
+//     operand with d_out contiguous, as H reads A_a with d_in contiguous.
+//  1. per trainable row block (<= 32 rows) and d-slice: partial H and G over
+//     the slice, written transposed into fp32 "planes" [j][column], where row i
+//     of block e sits in column 32 e + i.
+//  2. the slice planes summed in slice order and split into bf16 hi + lo.
+//  3. per adapter and 128-wide column tile of dB or dA: a fixed-order
+//     reduction over the adapter's trainable rows, 32 rows per step; the row
+//     tile is transposed through LDS and meets the hi / lo planes on the
+//     matrix cores.
+// Rows outside T_a^m are never read.  No floating-point atomics anywhere, so
+// the result is the same bytes run to run.
 #include <algorithm>
 
 #include "device_common.h"
@@ -44,7 +50,13 @@ struct GradArgs {
   int32_t ks;
   int32_t p_stride;
   int32_t r_pad;
+  uint16_t* fin;            // summed planes, bf16: [which][hi, lo][j][column]
+  uint16_t* bt;             // B_a^T per slot: [slot][r_pad][d_out]
 };
+
+__device__ __forceinline__ uint16_t* fin_plane(const GradArgs& g, int which, int hl) {
+  return g.fin + ((int64_t)(which * 2 + hl) * g.r_pad) * g.p_stride;
+}
 
 __device__ __forceinline__ float* plane(const GradArgs& g, int which, int ks) {
   return g.hg + ((int64_t)(which * g.ks + ks) * g.r_pad) * g.p_stride;
@@ -83,14 +95,96 @@ __device__ __forceinline__ void reduce_waves(f32x4 (&acc)[N], f32x4* s_red) {
 }
 
 // ---------------------------------------------------------------------------
-// stage 1 (matrix cores): partial H and G for one (row block, slice)
+// stage 0: B_a^T of every live slot, 64 rows of B per tile, through LDS
 // ---------------------------------------------------------------------------
-template <int NT, bool RANK8>
+__global__ __launch_bounds__(256) void bt_kernel(GradArgs g) {
+  __shared__ uint16_t s_b[64][LORA_MAX_RANK + 2];
+  const int tid = threadIdx.x;
+  const int tpo = (g.d_out + 63) / 64;
+  for (int tile = blockIdx.x; tile < g.num_slots * tpo; tile += gridDim.x) {
+    const int a = tile / tpo, o0 = (tile - a * tpo) * 64;
+    const Slot m = load_slot(g.meta, a);
+    const int r = m.rank;
+    if (r <= 0) continue;
+    const rsrc_t Bw = make_rsrc(m.B, (uint32_t)g.d_out * (uint32_t)r * 2u);
+    const int orows = min(64, g.d_out - o0);
+    __syncthreads();
+    for (int i = tid; i < orows * r; i += 256) {          // B[o0 .. o0 + orows) is contiguous
+      const int o = i / r, j = i - o * r;
+      s_b[o][j] = (uint16_t)bload_u16(Bw, ((uint32_t)o0 * r + i) * 2u);
+    }
+    __syncthreads();
+    uint16_t* bt = g.bt + (int64_t)a * g.r_pad * g.d_out + o0;
+    for (int i = tid; i < r * 64; i += 256) {
+      const int j = i >> 6, o = i & 63;
+      if (o < orows) bt[(int64_t)j * g.d_out + o] = s_b[o][j];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// stage 1 (matrix cores): partial H and G for one (row block, slice).  Both are
+// shrink-shaped products (rows x d-slice times rank x d-slice), streamed with
+// double-buffered 16-byte loads.
+// ---------------------------------------------------------------------------
+template <int MT, int NT, int U>
+__device__ __forceinline__ void rows_times_w(f32x4 (&acc)[MT * NT], const uint16_t* (&xr)[MT],
+                                             rsrc_t W, const uint32_t (&wr)[NT], int kstart,
+                                             int kstride, int kend) {
+  const int kg = ((threadIdx.x & 63) >> 4) * 8;
+  struct Buf {
+    bf16x8 x[U][MT];
+    bf16x8 w[U][NT];
+    bool kv[U];
+  };
+  auto load = [&](Buf& b, int kb) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int k = kb + u * kstride + kg;
+      b.kv[u] = k < kend;
+      const int kk = k < kend ? k : kend - 8;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) b.x[u][mt] = as_bf16x8(ldg16(xr[mt] + kk));
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) b.w[u][nt] = as_bf16x8(bload16(W, (wr[nt] + (uint32_t)kk) * 2u));
+    }
+  };
+  // every tile is computed: no branch between a matrix-core instruction and
+  // its reader (tiles past the rows or the rank are never stored)
+  auto compute = [&](const Buf& b) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const bf16x8 xo = sel(b.kv[u], b.x[u][mt]);
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+          acc[mt * NT + nt] = mfma_16x16x32(xo, b.w[u][nt], acc[mt * NT + nt]);
+      }
+  };
+  if (kstart < kend) {
+    const int span = U * kstride;
+    Buf b0, b1;
+    load(b0, kstart);
+    for (int kb = kstart;; kb += 2 * span) {
+      const int k1 = kb + span;
+      if (k1 < kend) load(b1, k1);
+      compute(b0);
+      if (k1 >= kend) break;
+      const int k2 = k1 + span;
+      if (k2 < kend) load(b0, k2);
+      compute(b1);
+      if (k2 >= kend) break;
+    }
+  }
+  mfma_fence();
+}
+
+template <int NT>
 __global__ __launch_bounds__(256) void hg_kernel(GradArgs g) {
-  constexpr int BT_STRIDE = 128 + 8;                   // bf16 elements per staged row
+  constexpr int U = NT <= 2 ? 2 : 1;
   __shared__ f32x4 s_red[2 * 4 * NT * 64];
-  __shared__ __align__(16) uint16_t s_bt[NT * 16 * BT_STRIDE];       // B_a slab, transposed [j][o]
-  const int lane = threadIdx.x & 63, w = wave_id(), tid = threadIdx.x;
+  const int lane = threadIdx.x & 63, w = wave_id();
   const int n_blocks = g.hdr[HDR_NMRB];
   const XcdRange xr = xcd_range(n_blocks * g.ks);
   const uint16_t* X = reinterpret_cast<const uint16_t*>(g.X);
@@ -102,85 +196,41 @@ __global__ __launch_bounds__(256) void hg_kernel(GradArgs g) {
     const Slot m = load_slot(g.meta, a);
     const int r = m.rank;
     const rsrc_t Aw = make_rsrc(m.A, (uint32_t)r * (uint32_t)g.d_in * 2u);
-    const rsrc_t Bw = make_rsrc(m.B, (uint32_t)g.d_out * (uint32_t)r * 2u);
-    const int nt_used = (r + 15) >> 4;
-
-    int trow[2];
-    bool rv[2];
+    const rsrc_t Btw = make_rsrc(g.bt + (int64_t)a * g.r_pad * g.d_out,
+                                 (uint32_t)r * (uint32_t)g.d_out * 2u);
+    const uint16_t* xrow[2];
+    const uint16_t* yrow[2];
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
       const int i = mt * 16 + (lane & 15);
-      rv[mt] = i < rows;
-      trow[mt] = rv[mt] ? g.m_perm[p0 + i] : 0;
+      const int t = g.m_perm[p0 + (i < rows ? i : rows - 1)];
+      xrow[mt] = X + (int64_t)t * g.ldx;
+      yrow[mt] = dY + (int64_t)t * g.lddy;
+    }
+    uint32_t arow[NT], brow[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const int j = nt * 16 + (lane & 15);
+      arow[nt] = (uint32_t)(j < r ? j : r - 1) * (uint32_t)g.d_in;
+      brow[nt] = (uint32_t)(j < r ? j : r - 1) * (uint32_t)g.d_out;
     }
     // acc[0 .. 2NT) : H tiles (mt, nt); acc[2NT .. 4NT) : G tiles
     f32x4 acc[4 * NT];
 #pragma unroll
     for (int i = 0; i < 4 * NT; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const int kg = (lane >> 4) * 8;
-
+    f32x4 (&acc_h)[2 * NT] = *reinterpret_cast<f32x4(*)[2 * NT]>(&acc[0]);
+    f32x4 (&acc_g)[2 * NT] = *reinterpret_cast<f32x4(*)[2 * NT]>(&acc[2 * NT]);
     if (g.H_saved == nullptr) {
       int kb, ke;
       slice(g.d_in, g.ks, ks, kb, ke);
-      for (int k0 = kb + w * 32; k0 < ke; k0 += 128) {
-        const int k = k0 + kg;
-        const bool kv = k < ke;
-        bf16x8 xa[2], wb[NT];
-#pragma unroll
-        for (int mt = 0; mt < 2; ++mt)
-          xa[mt] = (rv[mt] && kv) ? as_bf16x8(ldg16(X + (int64_t)trow[mt] * g.ldx + k))
-                                  : zero_bf16x8();
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          const int j = nt * 16 + (lane & 15);
-          wb[nt] = (j < r && kv) ? as_bf16x8(bload16(Aw, ((uint32_t)j * g.d_in + k) * 2u)) : zero_bf16x8();
-        }
-#pragma unroll
-        for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-          for (int nt = 0; nt < NT; ++nt)
-            if (nt < nt_used) acc[mt * NT + nt] = mfma_16x16x32(xa[mt], wb[nt], acc[mt * NT + nt]);
-      }
+      rows_times_w<2, NT, U>(acc_h, xrow, Aw, arow, kb + w * 32, 128, ke);
     }
-
     {
       int ob, oe;
       slice(g.d_out, g.ks, ks, ob, oe);
-      const int r8 = (r + 7) >> 3;
-      for (int oc = ob; oc < oe; oc += 128) {
-        __syncthreads();
-        // stage B[oc .. oc+128, 0 .. r) transposed into s_bt[j][o - oc]
-        for (int item = tid; item < 128 * r8; item += 256) {
-          const int ol = item / r8, j8 = (item - ol * r8) * 8;
-          const int o = oc + ol;
-          bf16x8 v = (o < oe && j8 < r) ? wrow8<RANK8>(Bw, (uint32_t)o * r, j8, r) : zero_bf16x8();
-          const uint4 u = __builtin_bit_cast(uint4, v);
-          const uint32_t wv[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-          for (int i = 0; i < 8; ++i)
-            s_bt[(j8 + i) * BT_STRIDE + ol] = (uint16_t)(wv[i >> 1] >> (16 * (i & 1)));
-        }
-        __syncthreads();
-        const int o = oc + w * 32 + kg;
-        const bool ov = o < oe;
-        bf16x8 ya[2], bb[NT];
-#pragma unroll
-        for (int mt = 0; mt < 2; ++mt)
-          ya[mt] = (rv[mt] && ov) ? as_bf16x8(ldg16(dY + (int64_t)trow[mt] * g.lddy + o))
-                                  : zero_bf16x8();
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          const int j = nt * 16 + (lane & 15);
-          bb[nt] = as_bf16x8(*reinterpret_cast<const uint4*>(&s_bt[j * BT_STRIDE + w * 32 + kg]));
-        }
-#pragma unroll
-        for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-          for (int nt = 0; nt < NT; ++nt)
-            if (nt < nt_used)
-              acc[2 * NT + mt * NT + nt] = mfma_16x16x32(ya[mt], bb[nt], acc[2 * NT + mt * NT + nt]);
-      }
+      rows_times_w<2, NT, U>(acc_g, yrow, Btw, brow, ob + w * 32, 128, oe);
     }
+    vmem_drained();
     reduce_waves<4 * NT>(acc, s_red);
     if (w == 0) {
       float* ph = plane(g, 0, ks);
@@ -211,29 +261,54 @@ __global__ __launch_bounds__(256) void hg_kernel(GradArgs g) {
   }
 }
 
-// Sum of the slice planes for rows [c, c+8) of plane `which`, column j; split hi / lo.
-__device__ __forceinline__ void plane8_split(const GradArgs& g, int which, int j, int col,
-                                             bf16x8& hi, bf16x8& lo) {
-  float h[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  for (int ks = 0; ks < g.ks; ++ks) {
-    const float* p = plane(g, which, ks) + (int64_t)j * g.p_stride + col;
-    const float4 a = *reinterpret_cast<const float4*>(p);
-    const float4 b = *reinterpret_cast<const float4*>(p + 4);
-    h[0] += a.x; h[1] += a.y; h[2] += a.z; h[3] += a.w;
-    h[4] += b.x; h[5] += b.y; h[6] += b.z; h[7] += b.w;
+// ---------------------------------------------------------------------------
+// stage 2: planes summed in slice order, split into bf16 hi / lo (8 columns per
+// thread)
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void hgsum_kernel(GradArgs g) {
+  const int n8 = g.hdr[HDR_NMRB] * 4;                 // 8-column groups per plane row
+  const int64_t per = (int64_t)g.r_pad * n8;
+  for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < 2 * per;
+       q += (int64_t)gridDim.x * 256) {
+    const int which = (int)(q / per);
+    const int64_t u = q - which * per;
+    const int j = (int)(u / n8), c = (int)(u - (int64_t)j * n8) * 8;
+    float h[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int ks = 0; ks < g.ks; ++ks) {
+      const float* p = plane(g, which, ks) + (int64_t)j * g.p_stride + c;
+      const float4 x0 = ldg_f4(p), x1 = ldg_f4(p + 4);
+      h[0] += x0.x; h[1] += x0.y; h[2] += x0.z; h[3] += x0.w;
+      h[4] += x1.x; h[5] += x1.y; h[6] += x1.z; h[7] += x1.w;
+    }
+    bf16x8 hi, lo;
+    split_hi_lo(h, hi, lo);
+    stg16(fin_plane(g, which, 0) + (int64_t)j * g.p_stride + c, __builtin_bit_cast(uint4, hi));
+    stg16(fin_plane(g, which, 1) + (int64_t)j * g.p_stride + c, __builtin_bit_cast(uint4, lo));
   }
-  split_hi_lo(h, hi, lo);
 }
 
 // ---------------------------------------------------------------------------
-// stage 2 (matrix cores): one workgroup per (adapter, 64-column block of dB or dA)
+// stage 3 (matrix cores): one workgroup per (slot, dB or dA, 128-column tile).
+// Per 32-row step: the row tile of dY (for dB) or X (for dA) is loaded two
+// steps ahead, transposed into LDS next to the step's hi / lo plane columns,
+// and multiplied; LDS is double buffered, one barrier per step.
+//   dB[o][j] = s sum_t dY[t][o] H[t][j]:  A operand = dY^T tile, B = H plane
+//   dA[j][k] = s sum_t G[t][j] X[t][k]:   A operand = G plane, B = X^T tile
 // ---------------------------------------------------------------------------
+constexpr int DT_CT = 128;            // tile columns
+constexpr int DT_TS = 32 + 8;         // LDS stride (bf16) of one transposed column
+constexpr int DT_WIN = 512;           // row ids staged per window
+
 template <int NT>
 __global__ __launch_bounds__(256) void dadb_kernel(GradArgs g) {
-  constexpr int T_STRIDE = 32 + 8;                    // staged rows per column (+pad)
-  __shared__ __align__(16) uint16_t s_t[64 * T_STRIDE];             // 32 rows x 64 columns, transposed
+  constexpr int CT = DT_CT, TS = DT_TS, PSEG = 2 * NT * 16 * 4;   // 16-byte plane pieces per step
+  constexpr int PPT = (PSEG + 255) / 256;                           // per thread
+  constexpr int R = 3;                                              // register ring (2 steps ahead)
+  __shared__ __align__(16) uint16_t s_t[2][CT * TS];
+  __shared__ __align__(16) uint16_t s_p[2][2 * NT * 16 * TS];     // [hl][j][t]
+  __shared__ int s_rows[DT_WIN];
   const int lane = threadIdx.x & 63, w = wave_id(), tid = threadIdx.x;
-  const int nbB = (g.d_out + 63) / 64, nbA = (g.d_in + 63) / 64, nbt = nbB + nbA;
+  const int nbB = (g.d_out + CT - 1) / CT, nbA = (g.d_in + CT - 1) / CT, nbt = nbB + nbA;
   const XcdRange xr = xcd_range(g.slot_count * nbt);
   for (int tile = xr.first; tile < xr.end; tile += xr.step) {
     const int sl = tile / nbt, c = tile - sl * nbt;
@@ -244,78 +319,132 @@ __global__ __launch_bounds__(256) void dadb_kernel(GradArgs g) {
     const bool isB = c < nbB;
     float* out = isB ? g.dB[sl] : g.dA[sl];
     if (out == nullptr) continue;
-    const int c0 = (isB ? c : c - nbB) * 64;
-    const int dcol = isB ? g.d_out : g.d_in;        // columns of the contracted input
-    const int mc = g.m_counts[a], moff = g.m_offsets[a], blk0 = g.m_blk[a];
+    const int c0 = (isB ? c : c - nbB) * CT;
+    const int dcol = isB ? g.d_out : g.d_in;
+    const int mc = uni(g.m_counts[a]), moff = uni(g.m_offsets[a]), blk0 = uni(g.m_blk[a]);
     const float s = m.scale;
-    const int nt_used = (r + 15) >> 4;
     const uint16_t* src = reinterpret_cast<const uint16_t*>(isB ? g.dY : g.X);
-    const int64_t lds = isB ? g.lddy : g.ldx;
+    const int64_t ld = isB ? g.lddy : g.ldx;
+    const uint16_t* fin0 = fin_plane(g, isB ? 0 : 1, 0);
+    const uint16_t* fin1 = fin_plane(g, isB ? 0 : 1, 1);
 
-    f32x4 acc[NT];
+    f32x4 acc[2][NT];
 #pragma unroll
-    for (int i = 0; i < NT; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) acc[i][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    for (int pb = 0; pb < mc; pb += 32) {
+    const int nch = (mc + 31) >> 5;
+    for (int w0 = 0; w0 < nch; w0 += DT_WIN / 32) {
+      const int wch = min(DT_WIN / 32, nch - w0);
       __syncthreads();
-      {
-        const int pl = tid >> 3, cc = (tid & 7) * 8;
-        const int p = pb + pl;
-        uint4 u = make_uint4(0u, 0u, 0u, 0u);
-        if (p < mc && c0 + cc < dcol) {
-          const int t = g.m_perm[moff + p];
-          u = ldg16(src + (int64_t)t * lds + c0 + cc);
-        }
-        const uint32_t wv[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-        for (int i = 0; i < 8; ++i)
-          s_t[(cc + i) * T_STRIDE + pl] = (uint16_t)(wv[i >> 1] >> (16 * (i & 1)));
+      for (int i = tid; i < DT_WIN; i += 256) {
+        const int p = w0 * 32 + i;
+        s_rows[i] = g.m_perm[moff + (p < mc ? p : mc - 1)];
       }
       __syncthreads();
-      const int col = (blk0 + (pb >> 5)) * 32 + (lane >> 4) * 8;
-      const bf16x8 tv =
-          as_bf16x8(*reinterpret_cast<const uint4*>(&s_t[(w * 16 + (lane & 15)) * T_STRIDE + (lane >> 4) * 8]));
+
+      uint4 tr[R][2], pr[R][PPT];
+      // raw loads of step cc into ring slot q (clamped addresses; masked at the LDS write)
+      auto load = [&](int q, int cc) {
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        if (nt >= nt_used) continue;
-        const int j = nt * 16 + (lane & 15);
-        bf16x8 hi, lo;
-        if (j < r) {
-          plane8_split(g, isB ? 0 : 1, j, col, hi, lo);
-        } else {
-          hi = zero_bf16x8();
-          lo = zero_bf16x8();
+        for (int h = 0; h < 2; ++h) {
+          const int sgm = tid + 256 * h, i = sgm >> 4, cs = (sgm & 15) * 8;
+          const int col = c0 + cs < dcol ? c0 + cs : dcol - 8;
+          tr[q][h] = ldg16(src + (int64_t)s_rows[cc * 32 + i] * ld + col);
         }
-        if (isB) {   // C[o][j]: A operand = staged dY^T (rows o), B operand = H (columns j)
-          acc[nt] = mfma_16x16x32(tv, hi, acc[nt]);
-          acc[nt] = mfma_16x16x32(tv, lo, acc[nt]);
-        } else {     // C[j][k]: A operand = G^T (rows j), B operand = staged X (columns k)
-          acc[nt] = mfma_16x16x32(hi, tv, acc[nt]);
-          acc[nt] = mfma_16x16x32(lo, tv, acc[nt]);
+        const int col0 = (blk0 + w0 + cc) * 32;
+#pragma unroll
+        for (int h = 0; h < PPT; ++h) {
+          int sgm = tid + 256 * h;
+          sgm = sgm < PSEG ? sgm : PSEG - 1;
+          const int hl = sgm / (NT * 64), rem = sgm - hl * (NT * 64);
+          const int j = rem >> 2, part = (rem & 3) * 8;
+          pr[q][h] = ldg16((hl ? fin1 : fin0) + (int64_t)j * g.p_stride + col0 + part);
+        }
+      };
+      auto stage = [&](int q, int cc, int buf) {
+        const int rows_left = mc - (w0 + cc) * 32;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int sgm = tid + 256 * h, i = sgm >> 4, cs = (sgm & 15) * 8;
+          const bool ok = i < rows_left && c0 + cs < dcol;
+          const uint4 u = ok ? tr[q][h] : make_uint4(0u, 0u, 0u, 0u);
+          const uint32_t wv[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+          for (int k = 0; k < 8; ++k)
+            s_t[buf][(cs + k) * TS + i] = (uint16_t)(wv[k >> 1] >> (16 * (k & 1)));
+        }
+#pragma unroll
+        for (int h = 0; h < PPT; ++h) {
+          const int sgm = tid + 256 * h;
+          if (sgm >= PSEG) continue;
+          const int hl = sgm / (NT * 64), rem = sgm - hl * (NT * 64);
+          const int j = rem >> 2, part = (rem & 3) * 8;
+          *reinterpret_cast<uint4*>(&s_p[buf][(hl * NT * 16 + j) * TS + part]) = pr[q][h];
+        }
+      };
+      auto mma = [&](int buf) {
+        const int tg = (lane >> 4) * 8, n = lane & 15;
+#pragma unroll
+        for (int i2 = 0; i2 < 2; ++i2) {
+          const bf16x8 tv = as_bf16x8(
+              *reinterpret_cast<const uint4*>(&s_t[buf][(w * 32 + i2 * 16 + n) * TS + tg]));
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt) {
+            const bf16x8 hi = as_bf16x8(
+                *reinterpret_cast<const uint4*>(&s_p[buf][(nt * 16 + n) * TS + tg]));
+            const bf16x8 lo = as_bf16x8(
+                *reinterpret_cast<const uint4*>(&s_p[buf][((NT + nt) * 16 + n) * TS + tg]));
+            if (isB) {
+              acc[i2][nt] = mfma_16x16x32(tv, hi, acc[i2][nt]);
+              acc[i2][nt] = mfma_16x16x32(tv, lo, acc[i2][nt]);
+            } else {
+              acc[i2][nt] = mfma_16x16x32(hi, tv, acc[i2][nt]);
+              acc[i2][nt] = mfma_16x16x32(lo, tv, acc[i2][nt]);
+            }
+          }
+        }
+      };
+      load(0, 0);
+      if (wch > 1) load(1, 1);
+      for (int cc0 = 0; cc0 < wch; cc0 += R) {
+#pragma unroll
+        for (int u = 0; u < R; ++u) {
+          const int cc = cc0 + u;
+          if (cc >= wch) break;
+          if (cc + 2 < wch) load((u + 2) % R, cc + 2);
+          stage(u, cc, cc & 1);
+          __syncthreads();
+          mma(cc & 1);
         }
       }
     }
+
+    mfma_fence();
     if (mc == 0 && g.accumulate) continue;
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      if (nt >= nt_used) continue;
+    for (int i2 = 0; i2 < 2; ++i2)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        int oidx, valid;
-        if (isB) {
-          const int o = c0 + w * 16 + (lane >> 4) * 4 + v, j = nt * 16 + (lane & 15);
-          valid = o < g.d_out && j < r;
-          oidx = o * r + j;
-        } else {
-          const int j = nt * 16 + (lane >> 4) * 4 + v, k = c0 + w * 16 + (lane & 15);
-          valid = j < r && k < g.d_in;
-          oidx = j * g.d_in + k;
+      for (int nt = 0; nt < NT; ++nt) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          int64_t oidx;
+          bool valid;
+          if (isB) {
+            const int o = c0 + w * 32 + i2 * 16 + (lane >> 4) * 4 + v, j = nt * 16 + (lane & 15);
+            valid = o < g.d_out && j < r;
+            oidx = (int64_t)o * r + j;
+          } else {
+            const int j = nt * 16 + (lane >> 4) * 4 + v, k = c0 + w * 32 + i2 * 16 + (lane & 15);
+            valid = j < r && k < g.d_in;
+            oidx = (int64_t)j * g.d_in + k;
+          }
+          if (!valid) continue;
+          const float val = (mc == 0) ? 0.0f : s * acc[i2][nt][v];
+          out[oidx] = g.accumulate ? out[oidx] + val : val;
         }
-        if (!valid) continue;
-        const float val = (mc == 0) ? 0.0f : s * acc[nt][v];
-        out[oidx] = g.accumulate ? out[oidx] + val : val;
       }
-    }
   }
 }
 
@@ -423,6 +552,8 @@ GradArgs make_args(const GradLaunch& l) {
   g.ks = l.k_splits;
   g.p_stride = l.p_stride;
   g.r_pad = l.r_pad;
+  g.fin = l.fin;
+  g.bt = l.bt;
   return g;
 }
 
@@ -444,22 +575,26 @@ bool set_group(const GradLaunch& l, GradArgs& g, int base) {
 
 template <int NT>
 hipError_t launch_nt(const GradLaunch& l, const GradArgs& g, hipStream_t s) {
-  const int grid1 = round8(std::min<long long>((long long)l.o.rb_ub * l.k_splits, 4096));
-  if (l.o.rank8)
-    hipLaunchKernelGGL((hg_kernel<NT, true>), dim3(grid1), dim3(256), 0, s, g);
-  else
-    hipLaunchKernelGGL((hg_kernel<NT, false>), dim3(grid1), dim3(256), 0, s, g);
+  const int tpo = (l.o.d_out + 63) / 64;
+  const int grid0 = std::min(l.o.num_slots * tpo, 8192);
+  hipLaunchKernelGGL(bt_kernel, dim3(grid0), dim3(256), 0, s, g);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
+  const int grid1 = round8(std::min<long long>((long long)l.o.rb_ub * l.k_splits, 4096));
+  hipLaunchKernelGGL((hg_kernel<NT>), dim3(grid1), dim3(256), 0, s, g);
+  if ((err = hipGetLastError()) != hipSuccess) return err;
+  const long long groups = 2LL * l.r_pad * l.o.rb_ub * 4;       // 8-column groups (upper bound)
+  const int grid2 = (int)std::max<long long>(1, std::min<long long>((groups + 255) / 256, 4096));
+  hipLaunchKernelGGL(hgsum_kernel, dim3(grid2), dim3(256), 0, s, g);
+  if ((err = hipGetLastError()) != hipSuccess) return err;
   for (int base = 0; base < l.o.num_slots; base += GRAD_SLOT_GROUP) {
     GradArgs gg = g;
     if (!set_group(l, gg, base)) continue;
-    const long long tiles =
-        (long long)gg.slot_count * ((l.o.d_out + 63) / 64 + (l.o.d_in + 63) / 64);
-    const int grid2 = round8(std::min<long long>(tiles, 8192));
-    hipLaunchKernelGGL((dadb_kernel<NT>), dim3(grid2), dim3(256), 0, s, gg);
-    err = hipGetLastError();
-    if (err != hipSuccess) return err;
+    const long long tiles = (long long)gg.slot_count *
+                            ((l.o.d_out + DT_CT - 1) / DT_CT + (l.o.d_in + DT_CT - 1) / DT_CT);
+    const int grid3 = round8(std::min<long long>(tiles, 8192));
+    hipLaunchKernelGGL((dadb_kernel<NT>), dim3(grid3), dim3(256), 0, s, gg);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
   }
   return hipSuccess;
 }

@@ -29,6 +29,7 @@ enum : int {
   HDR_NRB_LARGE = 4,  // row-block entries of large groups (grouped matrix-core path)
   HDR_NRB_TOTAL = 5,  // all entries: large-group blocks, then small-group entries
   HDR_NMRB = 6,       // trainable row-block entries (gradient path)
+  HDR_NSMALL = 7,     // small-group records (fused path); equals NRB_TOTAL - NRB_LARGE
   HDR_WORDS = 64
 };
 
@@ -38,11 +39,27 @@ constexpr int MRB_ROWS = 32;     // trainable rows per gradient row block
 constexpr int PLAN_THREADS = 1024;
 constexpr int PLAN_WAVES = PLAN_THREADS / 64;
 
+// One small-group entry as the fused kernel reads it: everything a workgroup
+// needs in one 128-byte line, so the kernel's first memory round trip already
+// yields the weight pointers and the row ids.  row[i] for i >= rows repeats the
+// last row (a real row, so padding lanes read valid memory).
+struct SmallRec {
+  const void* A;
+  const void* B;
+  int32_t rows;
+  int32_t rank;
+  float scale;
+  int32_t adapter;
+  int32_t row[SMALL_ROWS];
+  int32_t pad[8];
+};
+static_assert(sizeof(SmallRec) == 128, "small-group record layout");
+
 // Byte offsets of the plan arrays inside the caller's workspace.
 struct PlanLayout {
   size_t hdr, counts, offsets, perm, run_start, run_len, run_adapter;
-  size_t m_counts, m_offsets, m_perm, m_blk, rb, mrb, seg_ids, total;
-  int32_t rb_max, mrb_max;
+  size_t m_counts, m_offsets, m_perm, m_blk, rb, mrb, srec, seg_ids, total;
+  int32_t rb_max, mrb_max, srec_max;
 };
 
 // Device pointers into one plan workspace.
@@ -60,9 +77,12 @@ struct PlanDev {
   int32_t* m_blk;  // first trainable row block of each adapter
   int4* rb;     // {adapter, first index into perm, rows, 0}
   int4* mrb;    // {adapter, first index into m_perm, rows, 0}
+  SmallRec* srec;  // small-group records, in the order of the small rb entries
   int32_t* seg_ids;
 };
 
+// Groups of at most this many rows take the fused small-group path.
+int32_t small_max_policy(int32_t n);
 PlanLayout plan_layout(int32_t n, int32_t num_slots);
 
 // ---- launchers (defined in the .hip files) --------------------------------
@@ -84,6 +104,7 @@ hipError_t launch_plan(const PlanLaunch& a, hipStream_t s);
 struct OpLaunch {
   const int32_t* hdr;
   const int4* rb;
+  const SmallRec* srec;
   const int32_t* perm;
   const SlotMeta* meta;
   int32_t n, d_in, d_out, num_slots;
@@ -133,7 +154,15 @@ struct GradLaunch {
   int32_t k_splits;
   int32_t p_stride;              // row stride (elements) of the H^T / G^T planes
   int32_t r_pad;                 // rank padding of the planes
+  uint16_t* fin;                 // workspace: summed planes, bf16 hi / lo
+  uint16_t* bt;                  // workspace: B_a^T per slot [num_slots][r_pad][d_out]
 };
+
+// Byte offsets of the gradient workspace parts.
+struct GradLayout {
+  size_t partial, fin, bt, total;
+};
+GradLayout grad_layout(int32_t mrb_ub, int32_t r_max, int32_t num_slots, int32_t d_out);
 hipError_t launch_grad_mfma(const GradLaunch& g, hipStream_t s);
 hipError_t launch_grad_valu(const GradLaunch& g, lora_dtype x_dtype, lora_dtype w_dtype,
                             hipStream_t s);

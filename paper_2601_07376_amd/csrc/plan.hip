@@ -39,23 +39,13 @@ __device__ __forceinline__ uint64_t match_peers(int key, int nbits) {
 // Exclusive prefix sum over the 1024 threads of the block (all must call).
 __device__ int block_excl_scan(int v, int* s_wsum, int& total) {
   const int lane = threadIdx.x & 63, w = wave_id();
-  int x = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(x, o);
-    if (lane >= o) x += y;
-  }
+  const int x = wave_incl_scan(v);
   if (lane == 63) s_wsum[w] = x;
   __syncthreads();
-  int base = 0, tot = 0;
-#pragma unroll
-  for (int i = 0; i < PLAN_WAVES; ++i) {
-    const int s = s_wsum[i];
-    base += (i < w) ? s : 0;
-    tot += s;
-  }
+  const int c = row_incl_scan(lane < PLAN_WAVES ? s_wsum[lane] : 0);   // lanes 0..15
+  const int base = lane_value(c, w) - lane_value(x, 63);
+  total = lane_value(c, PLAN_WAVES - 1);
   __syncthreads();
-  total = tot;
   return base + x - v;
 }
 
@@ -81,8 +71,9 @@ struct Out {
 
 // One stable grouping pass.  Returns, for thread a < S, the count and offset of
 // adapter a, and (in every thread) the number of grouped rows and of runs.
+// s_hist holds one counter per (adapter, wave), adapter-major: [a * 16 + w].
 template <bool MASKED, bool RUNS, bool DUP>
-__device__ void group_pass(const Rows& R, int S, int (*s_hist)[LORA_MAX_SLOTS], int* s_wsum,
+__device__ void group_pass(const Rows& R, int S, int* s_hist, int* s_cnt, int* s_wsum,
                            int (*s_runs)[PLAN_WAVES], int* s_scalar, const Out& out,
                            int& my_count, int& my_offset, int& n_act, int& n_runs) {
   const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
@@ -91,9 +82,7 @@ __device__ void group_pass(const Rows& R, int S, int (*s_hist)[LORA_MAX_SLOTS], 
   const int L = (((n + PLAN_WAVES - 1) / PLAN_WAVES) + 63) / 64 * 64;
   const int beg = min(n, w * L), end = min(n, beg + L);
 
-  for (int i = tid; i < PLAN_WAVES * LORA_MAX_SLOTS; i += PLAN_THREADS) {
-    if ((i % LORA_MAX_SLOTS) < S) s_hist[i / LORA_MAX_SLOTS][i % LORA_MAX_SLOTS] = 0;
-  }
+  for (int i = tid; i < S * PLAN_WAVES; i += PLAN_THREADS) s_hist[i] = 0;
   __syncthreads();
 
   // ---- pass A: per-wave histograms and run counts
@@ -104,7 +93,7 @@ __device__ void group_pass(const Rows& R, int S, int (*s_hist)[LORA_MAX_SLOTS], 
     const int e = valid ? (MASKED ? R.eff_m(t) : R.eff(t)) : -1;
     const uint64_t peers = match_peers(e + 1, nbits);
     if (e >= 0 && lane == __ffsll((unsigned long long)peers) - 1)
-      s_hist[w][e] += __popcll(peers);
+      s_hist[e * PLAN_WAVES + w] += __popcll(peers);
     if (RUNS) {
       bool st = false, ed = false;
       if (valid && e >= 0) {
@@ -121,17 +110,22 @@ __device__ void group_pass(const Rows& R, int S, int (*s_hist)[LORA_MAX_SLOTS], 
   }
   __syncthreads();
 
-  // ---- cursors: per adapter, the prefix over waves; then the prefix over adapters
-  int cnt = 0;
-  if (tid < S) {
-    for (int ww = 0; ww < PLAN_WAVES; ++ww) {
-      const int v = s_hist[ww][tid];
-      s_hist[ww][tid] = cnt;
-      cnt += v;
+  // ---- cursors: per adapter, the prefix over its 16 wave counters (one row of
+  // 16 lanes per adapter); then the prefix over adapters
+  for (int k0 = 0; k0 < S * PLAN_WAVES; k0 += PLAN_THREADS) {
+    const int k = k0 + tid;
+    const bool act = k < S * PLAN_WAVES;
+    const int v = act ? s_hist[k] : 0;
+    const int incl = row_incl_scan(v);
+    if (act) {
+      s_hist[k] = incl - v;
+      if ((k & 15) == 15) s_cnt[k >> 4] = incl;
     }
   }
+  __syncthreads();
+  const int cnt = tid < S ? s_cnt[tid] : 0;
   int total;
-  const int off = block_excl_scan(tid < S ? cnt : 0, s_wsum, total);
+  const int off = block_excl_scan(cnt, s_wsum, total);
   if (tid < S) {
     out.counts[tid] = cnt;
     out.offsets[tid] = off;
@@ -139,7 +133,7 @@ __device__ void group_pass(const Rows& R, int S, int (*s_hist)[LORA_MAX_SLOTS], 
       out.dup_counts[tid] = cnt;
       out.dup_offsets[tid] = off;
     }
-    for (int ww = 0; ww < PLAN_WAVES; ++ww) s_hist[ww][tid] += off;
+    s_cnt[tid] = off;
   }
   if (tid == 0) {
     out.offsets[S] = total;
@@ -170,13 +164,13 @@ __device__ void group_pass(const Rows& R, int S, int (*s_hist)[LORA_MAX_SLOTS], 
     const uint64_t peers = match_peers(e + 1, nbits);
     const bool leader = e >= 0 && lane == __ffsll((unsigned long long)peers) - 1;
     int cur = 0;
-    if (e >= 0) cur = s_hist[w][e];
+    if (e >= 0) cur = s_cnt[e] + s_hist[e * PLAN_WAVES + w];
     if (e >= 0) {
       const int pos = cur + __popcll(peers & lanemask_lt());
       out.perm[pos] = t;
       if (DUP) out.dup_perm[pos] = t;
     }
-    if (leader) s_hist[w][e] = cur + __popcll(peers);
+    if (leader) s_hist[e * PLAN_WAVES + w] += __popcll(peers);
     if (RUNS) {
       bool st = false, ed = false;
       if (valid && e >= 0) {
@@ -210,8 +204,9 @@ __device__ void group_pass(const Rows& R, int S, int (*s_hist)[LORA_MAX_SLOTS], 
 // compiles to generic loads that wait on both memory counters).
 template <bool PK_LDS, bool SEG_LDS>
 __global__ __launch_bounds__(PLAN_THREADS) void plan_kernel(PlanLaunch a) {
-  __shared__ int s_hist[PLAN_WAVES][LORA_MAX_SLOTS];
+  __shared__ int s_hist[PLAN_WAVES * LORA_MAX_SLOTS];
   __shared__ int s_rank[LORA_MAX_SLOTS];
+  __shared__ int s_cnt[LORA_MAX_SLOTS];
   __shared__ int32_t s_pk[LDS_ROWS];
   __shared__ int s_wsum[PLAN_WAVES];
   __shared__ int s_runs[2][PLAN_WAVES];
@@ -222,12 +217,14 @@ __global__ __launch_bounds__(PLAN_THREADS) void plan_kernel(PlanLaunch a) {
   const int n = a.n, S = a.num_slots;
   if (tid == 0) s_flags = 0u;
   for (int i = tid; i < S; i += PLAN_THREADS) s_rank[i] = a.meta[i].rank;
+  SlotMeta my_meta{};
+  if (tid < S) my_meta = a.meta[tid];
   uint32_t flags = 0u;
 
   // ---- segment table: staged in LDS (in the histogram area) when it fits
   const bool seg = a.seg_offsets != nullptr;
   const int ns = a.num_segs;
-  int* s_seg = &s_hist[0][0];
+  int* s_seg = s_hist;
   const int32_t* seg_off = SEG_LDS ? s_seg : a.seg_offsets;
   const int32_t* seg_ad = SEG_LDS ? s_seg + ns + 1 : a.seg_adapter;
   int any_bad = 0;
@@ -299,17 +296,17 @@ __global__ __launch_bounds__(PLAN_THREADS) void plan_kernel(PlanLaunch a) {
   const Out out{a.d.counts, a.d.offsets, a.d.perm, a.d.m_counts, a.d.m_offsets, a.d.m_perm,
                 a.d.run_start, a.d.run_len, a.d.run_adapter};
   if (a.mask == nullptr) {
-    group_pass<false, true, true>(R, S, s_hist, s_wsum, s_runs, s_scalar, out, cnt, off, n_act,
+    group_pass<false, true, true>(R, S, s_hist, s_cnt, s_wsum, s_runs, s_scalar, out, cnt, off, n_act,
                                   n_runs);
     mcnt = cnt;
     moff = off;
     m_n_act = n_act;
   } else {
-    group_pass<false, true, false>(R, S, s_hist, s_wsum, s_runs, s_scalar, out, cnt, off, n_act,
+    group_pass<false, true, false>(R, S, s_hist, s_cnt, s_wsum, s_runs, s_scalar, out, cnt, off, n_act,
                                    n_runs);
     const Out mout{a.d.m_counts, a.d.m_offsets, a.d.m_perm, nullptr, nullptr, nullptr,
                    nullptr, nullptr, nullptr};
-    group_pass<true, false, false>(R, S, s_hist, s_wsum, s_runs, s_scalar, mout, mcnt, moff,
+    group_pass<true, false, false>(R, S, s_hist, s_cnt, s_wsum, s_runs, s_scalar, mout, mcnt, moff,
                                    m_n_act, unused);
   }
 
@@ -326,15 +323,30 @@ __global__ __launch_bounds__(PLAN_THREADS) void plan_kernel(PlanLaunch a) {
   const int pm = block_excl_scan(nbm, s_wsum, tot_m);
   for (int i = 0; i < nbl; ++i)
     a.d.rb[pl + i] = make_int4(tid, off + i * RB_ROWS, min(RB_ROWS, cnt - i * RB_ROWS), 0);
-  for (int i = 0; i < nbs; ++i)
-    a.d.rb[tot_l + ps + i] =
-        make_int4(tid, off + i * SMALL_ROWS, min(SMALL_ROWS, cnt - i * SMALL_ROWS), 1);
+  for (int i = 0; i < nbs; ++i) {
+    const int rows = min(SMALL_ROWS, cnt - i * SMALL_ROWS);
+    a.d.rb[tot_l + ps + i] = make_int4(tid, off + i * SMALL_ROWS, rows, 1);
+    SmallRec* r = a.d.srec + ps + i;
+    r->A = my_meta.A;
+    r->B = my_meta.B;
+    r->rows = rows;
+    r->rank = my_meta.rank;
+    r->scale = my_meta.scale;
+    r->adapter = tid;
+  }
   if (live) a.d.m_blk[tid] = pm;
   for (int i = 0; i < nbm; ++i)
     a.d.mrb[pm + i] = make_int4(tid, moff + i * MRB_ROWS, min(MRB_ROWS, mcnt - i * MRB_ROWS), 0);
 
   if (flags) atomicOr(&s_flags, flags);
   __syncthreads();
+  // record rows, from the entries and perm just written (visible to the whole
+  // workgroup after the barrier); padding slots repeat the entry's last row
+  for (int k = tid; k < tot_s * SMALL_ROWS; k += PLAN_THREADS) {
+    const int q = k / SMALL_ROWS, j = k % SMALL_ROWS;
+    const int4 en = a.d.rb[tot_l + q];
+    a.d.srec[q].row[j] = a.d.perm[en.y + min(j, en.z - 1)];
+  }
   if (tid == 0) {
     int32_t* h = a.d.hdr;
     h[HDR_FLAGS] = (int32_t)s_flags;
@@ -344,12 +356,268 @@ __global__ __launch_bounds__(PLAN_THREADS) void plan_kernel(PlanLaunch a) {
     h[HDR_NRB_LARGE] = tot_l;
     h[HDR_NRB_TOTAL] = tot_l + tot_s;
     h[HDR_NMRB] = tot_m;
+    h[HDR_NSMALL] = tot_s;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Batches of at most PLAN_THREADS rows (decode steps).  Thread t owns row t, so
+// every step is a single parallel pass and nothing is read from memory twice:
+//   1. ids, mask, slot ranks and (adapter threads) slot records are loaded at
+//      once, and the per-(adapter, wave) counters are cleared;
+//   2. ids are validated; ballots group each wave's rows by id and the lowest
+//      lane of each group stores the group's size;
+//   3. a 16-wide scan per adapter turns the per-wave sizes into cursors, and
+//      rows find the starts and ends of maximal runs;
+//   4. one block-wide scan gives adapter offsets, entry positions and run
+//      indices together; adapter threads write counts, offsets and entries;
+//   5. rows scatter themselves to perm (and m_perm), to their record slot and
+//      to their run.
+// ---------------------------------------------------------------------------
+constexpr int SEG_STAGE = 4096;   // LDS words for the segment table
+
+// Exclusive scan of N values per thread over the block; total[i] = sum.
+template <int N>
+__device__ __forceinline__ void block_scan_n(int (&v)[N], int (&total)[N],
+                                             int (*s_w)[PLAN_WAVES]) {
+  const int lane = threadIdx.x & 63, w = wave_id();
+  int x[N];
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    x[i] = wave_incl_scan(v[i]);
+    if (lane == 63) s_w[i][w] = x[i];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    const int c = row_incl_scan(lane < PLAN_WAVES ? s_w[i][lane] : 0);   // lanes 0..15
+    total[i] = lane_value(c, PLAN_WAVES - 1);
+    v[i] = lane_value(c, w) - lane_value(x[i], 63) + x[i] - v[i];
+  }
+  __syncthreads();
+}
+
+template <bool MASKED, bool SEG>
+__global__ __launch_bounds__(PLAN_THREADS) void plan_small_kernel(PlanLaunch a) {
+  __shared__ int s_rank[LORA_MAX_SLOTS];
+  __shared__ unsigned short s_wc[LORA_MAX_SLOTS * PLAN_WAVES];    // [adapter][wave]
+  __shared__ unsigned short s_wcm[MASKED ? LORA_MAX_SLOTS * PLAN_WAVES : 1];
+  __shared__ int s_cnt[LORA_MAX_SLOTS];
+  __shared__ int s_mcnt[MASKED ? LORA_MAX_SLOTS : 1];
+  __shared__ int s_off[LORA_MAX_SLOTS];
+  __shared__ int s_moff[MASKED ? LORA_MAX_SLOTS : 1];
+  __shared__ int s_sbase[LORA_MAX_SLOTS];
+  __shared__ int s_seg[SEG ? SEG_STAGE : 1];
+  __shared__ int s_efirst[PLAN_WAVES], s_elast[PLAN_WAVES];
+  __shared__ int s_rs[PLAN_THREADS], s_re[PLAN_THREADS];
+  __shared__ int s_w[7][PLAN_WAVES];
+  __shared__ unsigned s_flags;
+
+  const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
+  const int n = a.n, S = a.num_slots, ns = a.num_segs;
+  const PlanDev& d = a.d;
+
+  // ---- 1. loads
+  if (tid == 0) s_flags = 0u;
+  int raw = -1, mk = 1;
+  SlotMeta my{};
+  if (tid < S) my = a.meta[tid];
+  if (!SEG) {
+    if (tid < n) raw = a.idx[tid];
+  } else {
+    for (int i = tid; i <= ns; i += PLAN_THREADS) s_seg[i] = a.seg_offsets[i];
+    for (int i = tid; i < ns; i += PLAN_THREADS) s_seg[ns + 1 + i] = a.seg_adapter[i];
+  }
+  if (MASKED && tid < n) mk = a.mask[tid];
+  for (int i = tid; i < S * PLAN_WAVES; i += PLAN_THREADS) {
+    s_wc[i] = 0;
+    if (MASKED) s_wcm[i] = 0;
+  }
+  if (tid < S) s_rank[tid] = my.rank;
+  __syncthreads();
+
+  uint32_t flags = 0u;
+  if (SEG) {
+    bool bad = false;
+    for (int i = tid; i <= ns; i += PLAN_THREADS) {
+      const int o = s_seg[i];
+      if (i == 0 && o != 0) bad = true;
+      if (i == ns && o != n) bad = true;
+      if (i < ns && s_seg[i + 1] < o) bad = true;
+    }
+    if (__syncthreads_or(bad ? 1 : 0)) {
+      flags |= LORA_DATA_BAD_SEGMENTS;
+    } else if (tid < n) {
+      int lo = 0, hi = ns;             // s_seg[lo] <= tid < s_seg[hi]
+      while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (s_seg[mid] <= tid) lo = mid;
+        else hi = mid;
+      }
+      raw = s_seg[ns + 1 + lo];
+    }
+  }
+
+  // ---- 2. validation and per-wave group sizes
+  int e = -1;
+  if (tid < n) {
+    int v = raw;
+    if (v < -1 || v >= S) {
+      flags |= LORA_DATA_BAD_ID;
+      v = -1;
+    } else if (v >= 0 && s_rank[v] <= 0) {
+      flags |= LORA_DATA_EMPTY_SLOT;
+      v = -1;
+    }
+    e = v;
+  }
+  const int em = (MASKED && !mk) ? -1 : e;
+  const int nbits = 32 - __clz(S);
+  const uint64_t lt = lanemask_lt();
+  const uint64_t peers = match_peers(e + 1, nbits);
+  const int rank_in = __popcll(peers & lt);
+  if (e >= 0 && rank_in == 0) s_wc[e * PLAN_WAVES + w] = (unsigned short)__popcll(peers);
+  int mrank_in = 0;
+  if (MASKED) {
+    const uint64_t mpeers = match_peers(em + 1, nbits);
+    mrank_in = __popcll(mpeers & lt);
+    if (em >= 0 && mrank_in == 0) s_wcm[em * PLAN_WAVES + w] = (unsigned short)__popcll(mpeers);
+  }
+  if (lane == 0) s_efirst[w] = e;
+  if (lane == 63) s_elast[w] = e;
+  __syncthreads();
+
+  // ---- 3. cursors (exclusive prefix over waves) and run boundaries
+  for (int k0 = 0; k0 < S * PLAN_WAVES; k0 += PLAN_THREADS) {
+    const int k = k0 + tid;
+    const bool act = k < S * PLAN_WAVES;
+    const int v = act ? (int)s_wc[k] : 0;
+    const int incl = row_incl_scan(v);
+    if (act) {
+      s_wc[k] = (unsigned short)(incl - v);
+      if ((k & 15) == 15) s_cnt[k >> 4] = incl;
+    }
+    if (MASKED) {
+      const int vm = act ? (int)s_wcm[k] : 0;
+      const int im = row_incl_scan(vm);
+      if (act) {
+        s_wcm[k] = (unsigned short)(im - vm);
+        if ((k & 15) == 15) s_mcnt[k >> 4] = im;
+      }
+    }
+  }
+  const int ep = lane_prev(e, w > 0 ? s_elast[w - 1] : -1);
+  const int en = lane_next(e, w + 1 < PLAN_WAVES ? s_efirst[w + 1] : -1);
+  const bool st = e >= 0 && ep != e;
+  const bool ed = e >= 0 && en != e;
+  __syncthreads();
+
+  // ---- 4. offsets, entry positions and run indices in one scan
+  const bool live = tid < S;
+  const int cnt = live ? s_cnt[tid] : 0;
+  const int mcnt = MASKED ? (live ? s_mcnt[tid] : 0) : cnt;
+  const bool small = live && cnt > 0 && cnt <= a.small_max;
+  const int nbl = (live && cnt > a.small_max) ? (cnt + RB_ROWS - 1) / RB_ROWS : 0;
+  const int nbs = small ? (cnt + SMALL_ROWS - 1) / SMALL_ROWS : 0;
+  const int nbm = live ? (mcnt + MRB_ROWS - 1) / MRB_ROWS : 0;
+  int v[7] = {cnt, mcnt, nbl, nbs, nbm, st ? 1 : 0, ed ? 1 : 0};
+  int tot[7];
+  block_scan_n<7>(v, tot, s_w);
+  const int off = v[0], moff = v[1], pl = v[2], ps = v[3], pm = v[4];
+  if (live) {
+    d.counts[tid] = cnt;
+    d.offsets[tid] = off;
+    d.m_counts[tid] = mcnt;
+    d.m_offsets[tid] = moff;
+    d.m_blk[tid] = pm;
+    s_off[tid] = off;
+    if (MASKED) s_moff[tid] = moff;
+    s_sbase[tid] = small ? ps : -1;
+    for (int i = 0; i < nbl; ++i)
+      d.rb[pl + i] = make_int4(tid, off + i * RB_ROWS, min(RB_ROWS, cnt - i * RB_ROWS), 0);
+    for (int i = 0; i < nbs; ++i) {
+      const int rows = min(SMALL_ROWS, cnt - i * SMALL_ROWS);
+      d.rb[tot[2] + ps + i] = make_int4(tid, off + i * SMALL_ROWS, rows, 1);
+      SmallRec* r = d.srec + ps + i;
+      r->A = my.A;
+      r->B = my.B;
+      r->rows = rows;
+      r->rank = my.rank;
+      r->scale = my.scale;
+      r->adapter = tid;
+    }
+    for (int i = 0; i < nbm; ++i)
+      d.mrb[pm + i] = make_int4(tid, moff + i * MRB_ROWS, min(MRB_ROWS, mcnt - i * MRB_ROWS), 0);
+  }
+  if (tid == 0) {
+    d.offsets[S] = tot[0];
+    d.m_offsets[S] = tot[1];
+  }
+  if (flags) atomicOr(&s_flags, flags);
+  __syncthreads();
+
+  // ---- 5. scatter
+  // (every index below is < n or < the record count by construction; the
+  // guards only keep a broken invariant from writing outside the arrays)
+  if (e >= 0) {
+    const int o = s_off[e];
+    const int pos = o + (int)s_wc[e * PLAN_WAVES + w] + rank_in;
+    if ((unsigned)pos < (unsigned)n) {
+      d.perm[pos] = tid;
+      if (!MASKED) d.m_perm[pos] = tid;
+    }
+    const int sb = s_sbase[e];
+    const int rel = pos - o;
+    const int q = sb + rel / SMALL_ROWS;
+    if (sb >= 0 && rel >= 0 && q < tot[3]) {
+      SmallRec* r = d.srec + q;
+      const int j = rel % SMALL_ROWS;
+      r->row[j] = tid;
+      if (rel == s_cnt[e] - 1)
+        for (int jj = j + 1; jj < SMALL_ROWS; ++jj) r->row[jj] = tid;
+    }
+  }
+  if (MASKED && em >= 0) {
+    const int pos = s_moff[em] + (int)s_wcm[em * PLAN_WAVES + w] + mrank_in;
+    if ((unsigned)pos < (unsigned)n) d.m_perm[pos] = tid;
+  }
+  if (st && (unsigned)v[5] < (unsigned)n) {
+    d.run_start[v[5]] = tid;
+    d.run_adapter[v[5]] = e;
+    s_rs[v[5]] = tid;
+  }
+  if (ed && (unsigned)v[6] < (unsigned)n) s_re[v[6]] = tid;
+  __syncthreads();
+  for (int k = tid; k < min(tot[5], n); k += PLAN_THREADS) d.run_len[k] = s_re[k] - s_rs[k] + 1;
+  if (tid == 0) {
+    int32_t* h = d.hdr;
+    h[HDR_FLAGS] = (int32_t)s_flags;
+    h[HDR_NACT] = tot[0];
+    h[HDR_NRUNS] = tot[5];
+    h[HDR_MNACT] = tot[1];
+    h[HDR_NRB_LARGE] = tot[2];
+    h[HDR_NRB_TOTAL] = tot[2] + tot[3];
+    h[HDR_NMRB] = tot[4];
+    h[HDR_NSMALL] = tot[3];
   }
 }
 
 }  // namespace
 
 hipError_t launch_plan(const PlanLaunch& a, hipStream_t s) {
+  const bool seg = a.seg_offsets != nullptr;
+  if (a.n <= PLAN_THREADS && (!seg || 2 * a.num_segs + 1 <= SEG_STAGE)) {
+    const bool m = a.mask != nullptr;
+    if (m && seg)
+      hipLaunchKernelGGL((plan_small_kernel<true, true>), dim3(1), dim3(PLAN_THREADS), 0, s, a);
+    else if (m)
+      hipLaunchKernelGGL((plan_small_kernel<true, false>), dim3(1), dim3(PLAN_THREADS), 0, s, a);
+    else if (seg)
+      hipLaunchKernelGGL((plan_small_kernel<false, true>), dim3(1), dim3(PLAN_THREADS), 0, s, a);
+    else
+      hipLaunchKernelGGL((plan_small_kernel<false, false>), dim3(1), dim3(PLAN_THREADS), 0, s, a);
+    return hipGetLastError();
+  }
   const bool pk_lds = a.n <= LDS_ROWS;
   const bool seg_lds = a.seg_offsets != nullptr && 2 * a.num_segs + 1 <= LDS_SEG_WORDS;
   if (pk_lds && seg_lds)
