@@ -76,11 +76,12 @@ int32_t small_chunks_policy(int32_t d_out) {
   return std::max(1, std::min(16, (d_out + 1023) / 1024));
 }
 
-// d-slices of the gradient's first stage.
+// Most d-slices of the gradient's first stage (the kernel uses fewer when
+// there are enough row blocks to fill the chip).
 int32_t grad_splits_policy(int32_t d_in, int32_t d_out) {
   const int v = env_int("LORA_GRAD_SPLITS", 0);
   if (v > 0) return std::min(v, 8);
-  return (std::min(d_in, d_out) >= 1024) ? 4 : 1;
+  return std::max(1, std::min(8, (std::min(d_in, d_out) + 511) / 512));   // slices of >= 512
 }
 constexpr int32_t GRAD_SPLITS_MAX = 8;
 

@@ -220,13 +220,16 @@ __device__ __forceinline__ void shrink_steps(f32x4 (&acc)[MT * NT], const uint16
     const int span = U * kstride;
     Buf b0, b1;
     load(b0, kstart);
+    // the next batch is requested unconditionally (past the end every lane
+    // reads a clamped address and the batch is never consumed): a load behind a
+    // branch would make the compiler wait for every outstanding load at the join
     for (int kb = kstart;; kb += 2 * span) {
       const int k1 = kb + span;
-      if (k1 < kend) load(b1, k1);
+      load(b1, k1);
       compute(b0);
       if (k1 >= kend) break;
       const int k2 = k1 + span;
-      if (k2 < kend) load(b0, k2);
+      load(b0, k2);
       compute(b1);
       if (k2 >= kend) break;
     }
@@ -468,16 +471,18 @@ __global__ __launch_bounds__(256) void expand_kernel(FwdArgs p) {
           if (rv[tt]) y8_store<YBF16>(y[tt], p.Y, p.ldy, trow[tt], o, s, acc[0][tt], acc[1][tt]);
       }
     };
+    // Y and B run ahead unconditionally (past the last step they repeat it):
+    // a load behind a branch would drain every outstanding load at the join
 #pragma unroll
-    for (int d = 0; d < DY; ++d) load_y(yb[d], d);
+    for (int d = 0; d < DY; ++d) load_y(yb[d], min(d, NS - 1));
     load_b(bb[0], 0);
     for (int st0 = 0; st0 < NS; st0 += R) {
 #pragma unroll
       for (int u = 0; u < R; ++u) {
         const int st = st0 + u;
         if (st >= NS) break;
-        if (st + DY < NS) load_y(yb[(u + DY) % R], st + DY);
-        if (st + 1 < NS) load_b(bb[(u + 1) & 1], st + 1);
+        load_y(yb[(u + DY) % R], min(st + DY, NS - 1));
+        load_b(bb[(u + 1) & 1], min(st + 1, NS - 1));
         run(bb[u & 1], yb[u], st);
       }
     }

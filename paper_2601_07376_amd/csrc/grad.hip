@@ -8,9 +8,9 @@
 // Matrix-core path, four launches:
 //  0. B_a^T of every live slot into the workspace, so that G reads its second
 //     operand with d_out contiguous, as H reads A_a with d_in contiguous.
-//  1. per trainable row block (<= 32 rows) and d-slice: partial H and G over
+//  1. per trainable row block (<= 64 rows) and d-slice: partial H and G over
 //     the slice, written transposed into fp32 "planes" [j][column], where row i
-//     of block e sits in column 32 e + i.
+//     of block e sits in column 64 e + i.
 //  2. the slice planes summed in slice order and split into bf16 hi + lo.
 //  3. per adapter and 128-wide column tile of dB or dA: a fixed-order
 //     reduction over the adapter's trainable rows, 32 rows per step; the row
@@ -62,6 +62,12 @@ __device__ __forceinline__ float* plane(const GradArgs& g, int which, int ks) {
   return g.hg + ((int64_t)(which * g.ks + ks) * g.r_pad) * g.p_stride;
 }
 
+// d-slices actually used: enough (row block, slice) tiles to cover the chip
+// once (about 256), at most g.ks (the workspace holds g.ks slice planes)
+__device__ __forceinline__ int active_splits(const GradArgs& g, int n_blocks) {
+  return max(1, min(g.ks, 256 / max(n_blocks, 1)));
+}
+
 // slice of a dimension for split ks, in multiples of 128
 __device__ __forceinline__ void slice(int d, int nks, int ks, int& b, int& e) {
   const int w = ((d + nks - 1) / nks + 127) / 128 * 128;
@@ -69,28 +75,39 @@ __device__ __forceinline__ void slice(int d, int nks, int ks, int& b, int& e) {
   e = min(d, b + w);
 }
 
-template <int N>
+// Sum the four waves' accumulators in a fixed order, ((w0 + w2) + (w1 + w3)),
+// leaving the total in wave 0; CH accumulators at a time through s_red
+// (2 x CH x 64 f32x4).
+template <int N, int CH>
 __device__ __forceinline__ void reduce_waves(f32x4 (&acc)[N], f32x4* s_red) {
   const int lane = threadIdx.x & 63, w = wave_id();
-  __syncthreads();
-  if (w >= 2) {
 #pragma unroll
-    for (int i = 0; i < N; ++i) s_red[((w - 2) * N + i) * 64 + lane] = acc[i];
-  }
-  __syncthreads();
-  if (w < 2) {
+  for (int c0 = 0; c0 < N; c0 += CH) {
+    constexpr int C = CH;
+    __syncthreads();
+    if (w >= 2) {
 #pragma unroll
-    for (int i = 0; i < N; ++i) acc[i] += s_red[(w * N + i) * 64 + lane];
-  }
-  __syncthreads();
-  if (w == 1) {
+      for (int i = 0; i < C; ++i)
+        if (c0 + i < N) s_red[((w - 2) * C + i) * 64 + lane] = acc[c0 + i];
+    }
+    __syncthreads();
+    if (w < 2) {
 #pragma unroll
-    for (int i = 0; i < N; ++i) s_red[i * 64 + lane] = acc[i];
-  }
-  __syncthreads();
-  if (w == 0) {
+      for (int i = 0; i < C; ++i)
+        if (c0 + i < N) acc[c0 + i] += s_red[(w * C + i) * 64 + lane];
+    }
+    __syncthreads();
+    if (w == 1) {
 #pragma unroll
-    for (int i = 0; i < N; ++i) acc[i] += s_red[i * 64 + lane];
+      for (int i = 0; i < C; ++i)
+        if (c0 + i < N) s_red[i * 64 + lane] = acc[c0 + i];
+    }
+    __syncthreads();
+    if (w == 0) {
+#pragma unroll
+      for (int i = 0; i < C; ++i)
+        if (c0 + i < N) acc[c0 + i] += s_red[i * 64 + lane];
+    }
   }
 }
 
@@ -107,17 +124,27 @@ __global__ __launch_bounds__(256) void bt_kernel(GradArgs g) {
     const int r = m.rank;
     if (r <= 0) continue;
     const rsrc_t Bw = make_rsrc(m.B, (uint32_t)g.d_out * (uint32_t)r * 2u);
-    const int orows = min(64, g.d_out - o0);
+    const int orows = min(64, g.d_out - o0);     // a multiple of 8
     __syncthreads();
-    for (int i = tid; i < orows * r; i += 256) {          // B[o0 .. o0 + orows) is contiguous
-      const int o = i / r, j = i - o * r;
-      s_b[o][j] = (uint16_t)bload_u16(Bw, ((uint32_t)o0 * r + i) * 2u);
+    // B[o0 .. o0 + orows) is one contiguous run of orows * r elements
+    for (int i = tid; i < orows * r / 8; i += 256) {
+      const uint4 u = bload16(Bw, ((uint32_t)o0 * r + 8u * i) * 2u);
+      const uint32_t wv[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const int e = 8 * i + q, o = e / r, j = e - o * r;
+        s_b[o][j] = (uint16_t)(wv[q >> 1] >> (16 * (q & 1)));
+      }
     }
     __syncthreads();
     uint16_t* bt = g.bt + (int64_t)a * g.r_pad * g.d_out + o0;
-    for (int i = tid; i < r * 64; i += 256) {
-      const int j = i >> 6, o = i & 63;
-      if (o < orows) bt[(int64_t)j * g.d_out + o] = s_b[o][j];
+    for (int i = tid; i < r * (orows / 8); i += 256) {
+      const int j = i / (orows / 8), o8 = (i - j * (orows / 8)) * 8;
+      uint32_t b[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) b[q] = s_b[o8 + q][j];
+      stg16(bt + (int64_t)j * g.d_out + o8,
+            make_uint4(b[0] | (b[1] << 16), b[2] | (b[3] << 16), b[4] | (b[5] << 16), b[6] | (b[7] << 16)));
     }
   }
 }
@@ -127,31 +154,38 @@ __global__ __launch_bounds__(256) void bt_kernel(GradArgs g) {
 // shrink-shaped products (rows x d-slice times rank x d-slice), streamed with
 // double-buffered 16-byte loads.
 // ---------------------------------------------------------------------------
+// acc_h += rows(xr) W1^T over k in [k1b, k1e) and acc_g += rows(yr) W2^T over
+// k in [k2b, k2e), both with k-steps kb + w * 32 + i * 128.  Each round requests
+// one batch of U k-steps of both products (every load unconditional, from a
+// clamped address) and then feeds the matrix cores, so the second product's
+// loads overlap the first one's arithmetic and nothing waits behind a branch.
+// Every tile is computed (tiles past the rows or the rank are never stored).
 template <int MT, int NT, int U>
-__device__ __forceinline__ void rows_times_w(f32x4 (&acc)[MT * NT], const uint16_t* (&xr)[MT],
-                                             rsrc_t W, const uint32_t (&wr)[NT], int kstart,
-                                             int kstride, int kend) {
-  const int kg = ((threadIdx.x & 63) >> 4) * 8;
+__device__ __forceinline__ void rows_times_w2(f32x4 (&acc_h)[MT * NT], f32x4 (&acc_g)[MT * NT],
+                                              const uint16_t* (&xr)[MT], rsrc_t W1,
+                                              const uint32_t (&wr1)[NT], int k1b, int k1e,
+                                              const uint16_t* (&yr)[MT], rsrc_t W2,
+                                              const uint32_t (&wr2)[NT], int k2b, int k2e) {
+  const int kg = ((threadIdx.x & 63) >> 4) * 8 + wave_id() * 32;
   struct Buf {
     bf16x8 x[U][MT];
     bf16x8 w[U][NT];
     bool kv[U];
   };
-  auto load = [&](Buf& b, int kb) {
+  auto load = [&](Buf& b, const uint16_t* (&rr)[MT], rsrc_t W, const uint32_t (&wr)[NT], int kb,
+                  int ke) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int k = kb + u * kstride + kg;
-      b.kv[u] = k < kend;
-      const int kk = k < kend ? k : kend - 8;
+      const int k = kb + u * 128 + kg;
+      b.kv[u] = k < ke;
+      const int kk = k < ke ? k : ke - 8;
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) b.x[u][mt] = as_bf16x8(ldg16(xr[mt] + kk));
+      for (int mt = 0; mt < MT; ++mt) b.x[u][mt] = as_bf16x8(ldg16(rr[mt] + kk));
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) b.w[u][nt] = as_bf16x8(bload16(W, (wr[nt] + (uint32_t)kk) * 2u));
     }
   };
-  // every tile is computed: no branch between a matrix-core instruction and
-  // its reader (tiles past the rows or the rank are never stored)
-  auto compute = [&](const Buf& b) {
+  auto compute = [&](const Buf& b, f32x4 (&acc)[MT * NT]) {
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
@@ -162,35 +196,36 @@ __device__ __forceinline__ void rows_times_w(f32x4 (&acc)[MT * NT], const uint16
           acc[mt * NT + nt] = mfma_16x16x32(xo, b.w[u][nt], acc[mt * NT + nt]);
       }
   };
-  if (kstart < kend) {
-    const int span = U * kstride;
-    Buf b0, b1;
-    load(b0, kstart);
-    for (int kb = kstart;; kb += 2 * span) {
-      const int k1 = kb + span;
-      if (k1 < kend) load(b1, k1);
-      compute(b0);
-      if (k1 >= kend) break;
-      const int k2 = k1 + span;
-      if (k2 < kend) load(b0, k2);
-      compute(b1);
-      if (k2 >= kend) break;
-    }
+  const int n1 = max(0, (k1e - k1b + U * 128 - 1) / (U * 128));
+  const int n2 = max(0, (k2e - k2b + U * 128 - 1) / (U * 128));
+  const int rounds = max(n1, n2);
+  for (int i = 0; i < rounds; ++i) {
+    Buf bh, bg;
+    load(bh, xr, W1, wr1, k1b + i * U * 128, max(k1e, 8));
+    load(bg, yr, W2, wr2, k2b + i * U * 128, max(k2e, 8));
+    // keep the whole round's loads ahead of its arithmetic (the scheduler
+    // would otherwise interleave them to save registers, and wait on each)
+    __builtin_amdgcn_sched_barrier(0);
+    compute(bh, acc_h);
+    compute(bg, acc_g);
   }
   mfma_fence();
 }
 
 template <int NT>
 __global__ __launch_bounds__(256) void hg_kernel(GradArgs g) {
-  constexpr int U = NT <= 2 ? 2 : 1;
-  __shared__ f32x4 s_red[2 * 4 * NT * 64];
+  constexpr int MT = MRB_ROWS / 16;                      // row tiles per block
+  constexpr int U = NT <= 2 ? 4 : (NT == 4 ? 2 : 1);     // k-steps per wave and round
+  constexpr int N = 2 * MT * NT, CH = N < 16 ? N : 16;
+  __shared__ f32x4 s_red[2 * CH * 64];
   const int lane = threadIdx.x & 63, w = wave_id();
   const int n_blocks = g.hdr[HDR_NMRB];
-  const XcdRange xr = xcd_range(n_blocks * g.ks);
+  const int nks = active_splits(g, n_blocks);
+  const XcdRange xr = xcd_range(n_blocks * nks);
   const uint16_t* X = reinterpret_cast<const uint16_t*>(g.X);
   const uint16_t* dY = reinterpret_cast<const uint16_t*>(g.dY);
   for (int tile = xr.first; tile < xr.end; tile += xr.step) {
-    const int e = tile / g.ks, ks = tile - e * g.ks;
+    const int e = tile / nks, ks = tile - e * nks;
     const int4 en = load_entry(g.mrb, e);
     const int a = en.x, p0 = en.y, rows = en.z;
     const Slot m = load_slot(g.meta, a);
@@ -198,10 +233,10 @@ __global__ __launch_bounds__(256) void hg_kernel(GradArgs g) {
     const rsrc_t Aw = make_rsrc(m.A, (uint32_t)r * (uint32_t)g.d_in * 2u);
     const rsrc_t Btw = make_rsrc(g.bt + (int64_t)a * g.r_pad * g.d_out,
                                  (uint32_t)r * (uint32_t)g.d_out * 2u);
-    const uint16_t* xrow[2];
-    const uint16_t* yrow[2];
+    const uint16_t* xrow[MT];
+    const uint16_t* yrow[MT];
 #pragma unroll
-    for (int mt = 0; mt < 2; ++mt) {
+    for (int mt = 0; mt < MT; ++mt) {
       const int i = mt * 16 + (lane & 15);
       const int t = g.m_perm[p0 + (i < rows ? i : rows - 1)];
       xrow[mt] = X + (int64_t)t * g.ldx;
@@ -214,30 +249,27 @@ __global__ __launch_bounds__(256) void hg_kernel(GradArgs g) {
       arow[nt] = (uint32_t)(j < r ? j : r - 1) * (uint32_t)g.d_in;
       brow[nt] = (uint32_t)(j < r ? j : r - 1) * (uint32_t)g.d_out;
     }
-    // acc[0 .. 2NT) : H tiles (mt, nt); acc[2NT .. 4NT) : G tiles
-    f32x4 acc[4 * NT];
+    // acc[0 .. MT NT) : H tiles (mt, nt); acc[MT NT .. 2 MT NT) : G tiles
+    f32x4 acc[N];
 #pragma unroll
-    for (int i = 0; i < 4 * NT; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    f32x4 (&acc_h)[2 * NT] = *reinterpret_cast<f32x4(*)[2 * NT]>(&acc[0]);
-    f32x4 (&acc_g)[2 * NT] = *reinterpret_cast<f32x4(*)[2 * NT]>(&acc[2 * NT]);
-    if (g.H_saved == nullptr) {
-      int kb, ke;
-      slice(g.d_in, g.ks, ks, kb, ke);
-      rows_times_w<2, NT, U>(acc_h, xrow, Aw, arow, kb + w * 32, 128, ke);
-    }
+    for (int i = 0; i < N; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    f32x4 (&acc_h)[MT * NT] = *reinterpret_cast<f32x4(*)[MT * NT]>(&acc[0]);
+    f32x4 (&acc_g)[MT * NT] = *reinterpret_cast<f32x4(*)[MT * NT]>(&acc[MT * NT]);
     {
-      int ob, oe;
-      slice(g.d_out, g.ks, ks, ob, oe);
-      rows_times_w<2, NT, U>(acc_g, yrow, Btw, brow, ob + w * 32, 128, oe);
+      int kb, ke, ob, oe;
+      slice(g.d_in, nks, ks, kb, ke);
+      slice(g.d_out, nks, ks, ob, oe);
+      if (g.H_saved != nullptr) ke = kb;          // H comes from the caller
+      rows_times_w2<MT, NT, U>(acc_h, acc_g, xrow, Aw, arow, kb, ke, yrow, Btw, brow, ob, oe);
     }
     vmem_drained();
-    reduce_waves<4 * NT>(acc, s_red);
+    reduce_waves<N, CH>(acc, s_red);
     if (w == 0) {
       float* ph = plane(g, 0, ks);
       float* pg = plane(g, 1, ks);
-      const int col0 = e * 32;
+      const int col0 = e * MRB_ROWS;
 #pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
+      for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
@@ -247,10 +279,10 @@ __global__ __launch_bounds__(256) void hg_kernel(GradArgs g) {
             if (j >= g.r_pad) continue;
             const bool in = i < rows;
             if (g.H_saved == nullptr) ph[(int64_t)j * g.p_stride + col0 + i] = in ? acc[mt * NT + nt][v] : 0.0f;
-            pg[(int64_t)j * g.p_stride + col0 + i] = in ? acc[2 * NT + mt * NT + nt][v] : 0.0f;
+            pg[(int64_t)j * g.p_stride + col0 + i] = in ? acc[MT * NT + mt * NT + nt][v] : 0.0f;
           }
       if (g.H_saved != nullptr) {
-        for (int q = lane; q < 32 * g.r_pad; q += 64) {
+        for (int q = lane; q < MRB_ROWS * g.r_pad; q += 64) {
           const int i = q / g.r_pad, j = q - i * g.r_pad;
           float h = 0.0f;
           if (ks == 0 && i < rows && j < r) h = g.H_saved[(int64_t)g.m_perm[p0 + i] * g.ldh + j];
@@ -266,7 +298,9 @@ __global__ __launch_bounds__(256) void hg_kernel(GradArgs g) {
 // thread)
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void hgsum_kernel(GradArgs g) {
-  const int n8 = g.hdr[HDR_NMRB] * 4;                 // 8-column groups per plane row
+  const int n_blocks = g.hdr[HDR_NMRB];
+  const int nks = active_splits(g, n_blocks);
+  const int n8 = n_blocks * (MRB_ROWS / 8);           // 8-column groups per plane row
   const int64_t per = (int64_t)g.r_pad * n8;
   for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < 2 * per;
        q += (int64_t)gridDim.x * 256) {
@@ -274,7 +308,7 @@ __global__ __launch_bounds__(256) void hgsum_kernel(GradArgs g) {
     const int64_t u = q - which * per;
     const int j = (int)(u / n8), c = (int)(u - (int64_t)j * n8) * 8;
     float h[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (int ks = 0; ks < g.ks; ++ks) {
+    for (int ks = 0; ks < nks; ++ks) {
       const float* p = plane(g, which, ks) + (int64_t)j * g.p_stride + c;
       const float4 x0 = ldg_f4(p), x1 = ldg_f4(p + 4);
       h[0] += x0.x; h[1] += x0.y; h[2] += x0.z; h[3] += x0.w;
@@ -288,163 +322,199 @@ __global__ __launch_bounds__(256) void hgsum_kernel(GradArgs g) {
 }
 
 // ---------------------------------------------------------------------------
-// stage 3 (matrix cores): one workgroup per (slot, dB or dA, 128-column tile).
-// Per 32-row step: the row tile of dY (for dB) or X (for dA) is loaded two
-// steps ahead, transposed into LDS next to the step's hi / lo plane columns,
-// and multiplied; LDS is double buffered, one barrier per step.
+// stage 3 (matrix cores): one workgroup per (slot, dB or dA, 256-column tile).
+// Per 32-row step every thread loads four rows x 8 columns of dY (for dB) or
+// X (for dA), transposes them in registers and writes 8 columns x 4 rows into
+// LDS (column-major, 16-byte chunks swizzled by column), next to the step's
+// hi / lo plane columns; loads run several steps ahead and LDS is double
+// buffered with one barrier per step.
 //   dB[o][j] = s sum_t dY[t][o] H[t][j]:  A operand = dY^T tile, B = H plane
 //   dA[j][k] = s sum_t G[t][j] X[t][k]:   A operand = G plane, B = X^T tile
 // ---------------------------------------------------------------------------
-constexpr int DT_CT = 128;            // tile columns
+// tile columns: 256, or 128 for ranks above 64 (register budget)
+constexpr int dt_ct(int NT) { return NT <= 4 ? 256 : 128; }
 constexpr int DT_TS = 32 + 8;         // LDS stride (bf16) of one transposed column
 constexpr int DT_WIN = 512;           // row ids staged per window
 
+// 16-byte chunk g (rows 8g .. 8g + 7 of a step) of column `col` in the tile
+__device__ __forceinline__ int dt_chunk(int col, int g) { return g ^ ((col >> 3) & 3); }
+
+// One (slot, column tile) of dB (IS_B) or dA: the whole reduction over the
+// slot's trainable rows, then the scaled store.
+template <int NT, bool IS_B>
+__device__ __forceinline__ void dadb_tile(const GradArgs& g, int sl, int c0, uint16_t (*s_t)[dt_ct(NT) * DT_TS],
+                                          uint16_t (*s_p)[2 * NT * 16 * DT_TS], int* s_rows) {
+  constexpr int CT = dt_ct(NT), TS = DT_TS, PSEG = 2 * NT * 16 * 4;   // 16-byte plane pieces per step
+  constexpr int PPT = (PSEG + 255) / 256;                               // per thread
+  constexpr int AHEAD = NT <= 2 ? 4 : 2;                                // steps in flight
+  constexpr int R = AHEAD + 1;                                          // register ring
+  constexpr int CSN = CT / 8, I4 = CT / 64;     // loader column segments; 16-column tiles per wave
+  const int lane = threadIdx.x & 63, w = wave_id(), tid = threadIdx.x;
+  // loader: columns 8 cs .., rows 4 tq ..; with 128-column tiles the upper
+  // half of the threads repeats the lower half (same values, same addresses)
+  const int cs = tid % CSN, tq = (tid / CSN) & 7;
+  const int a = g.slot_base + sl;
+  const Slot m = load_slot(g.meta, a);
+  const int r = m.rank;
+  float* out = IS_B ? g.dB[sl] : g.dA[sl];
+  const int dcol = IS_B ? g.d_out : g.d_in;
+  const int mc = uni(g.m_counts[a]), moff = uni(g.m_offsets[a]), blk0 = uni(g.m_blk[a]);
+  const float s = m.scale;
+  const uint16_t* src = reinterpret_cast<const uint16_t*>(IS_B ? g.dY : g.X);
+  const int64_t ld = IS_B ? g.lddy : g.ldx;
+  const uint16_t* fin0 = fin_plane(g, IS_B ? 0 : 1, 0);
+  const uint16_t* fin1 = fin_plane(g, IS_B ? 0 : 1, 1);
+  const int lcol = c0 + cs * 8 < dcol ? c0 + cs * 8 : dcol - 8;   // clamped loader column
+  const bool lcol_ok = c0 + cs * 8 < dcol;
+
+  f32x4 acc[I4][NT];
+#pragma unroll
+  for (int i = 0; i < I4; ++i)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) acc[i][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int nch = (mc + 31) >> 5;
+  for (int w0 = 0; w0 < nch; w0 += DT_WIN / 32) {
+    const int wch = min(DT_WIN / 32, nch - w0);
+    __syncthreads();
+    for (int i = tid; i < DT_WIN; i += 256) {
+      const int p = w0 * 32 + i;
+      s_rows[i] = g.m_perm[moff + (p < mc ? p : mc - 1)];
+    }
+    __syncthreads();
+
+    uint4 tr[R][4], pr[R][PPT];
+    // raw loads of step cc into ring slot q (clamped addresses; masked at the LDS write)
+    auto load = [&](int q, int cc) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        tr[q][i] = ldg16(src + (int64_t)s_rows[cc * 32 + tq * 4 + i] * ld + lcol);
+      const int col0 = blk0 * MRB_ROWS + (w0 + cc) * 32;
+#pragma unroll
+      for (int h = 0; h < PPT; ++h) {
+        const int sgm = (tid + 256 * h) & (PSEG - 1);
+        const int hl = sgm / (NT * 64), rem = sgm - hl * (NT * 64);
+        const int j = rem >> 2, part = (rem & 3) * 8;
+        pr[q][h] = ldg16((hl ? fin1 : fin0) + (int64_t)j * g.p_stride + col0 + part);
+      }
+    };
+    auto stage = [&](int q, int cc, int buf) {
+      const int rows_left = mc - (w0 + cc) * 32;
+      uint32_t v[4][4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const bool ok = lcol_ok && tq * 4 + i < rows_left;
+        v[i][0] = ok ? tr[q][i].x : 0u;
+        v[i][1] = ok ? tr[q][i].y : 0u;
+        v[i][2] = ok ? tr[q][i].z : 0u;
+        v[i][3] = ok ? tr[q][i].w : 0u;
+      }
+      // 4 rows x 8 columns -> 8 columns x 4 rows (bf16 pairs through byte permutes)
+#pragma unroll
+      for (int wd = 0; wd < 4; ++wd) {
+        const uint32_t e01 = __builtin_amdgcn_perm(v[1][wd], v[0][wd], 0x05040100u);
+        const uint32_t o01 = __builtin_amdgcn_perm(v[1][wd], v[0][wd], 0x07060302u);
+        const uint32_t e23 = __builtin_amdgcn_perm(v[3][wd], v[2][wd], 0x05040100u);
+        const uint32_t o23 = __builtin_amdgcn_perm(v[3][wd], v[2][wd], 0x07060302u);
+        const int col_e = cs * 8 + 2 * wd, col_o = col_e + 1;
+        const int off = (tq & 1) * 4;
+        *reinterpret_cast<uint2*>(&s_t[buf][col_e * TS + dt_chunk(col_e, tq >> 1) * 8 + off]) =
+            make_uint2(e01, e23);
+        *reinterpret_cast<uint2*>(&s_t[buf][col_o * TS + dt_chunk(col_o, tq >> 1) * 8 + off]) =
+            make_uint2(o01, o23);
+      }
+#pragma unroll
+      for (int h = 0; h < PPT; ++h) {
+        const int sgm = (tid + 256 * h) & (PSEG - 1);
+        const int hl = sgm / (NT * 64), rem = sgm - hl * (NT * 64);
+        const int j = rem >> 2, part = (rem & 3) * 8;
+        *reinterpret_cast<uint4*>(&s_p[buf][(hl * NT * 16 + j) * TS + part]) = pr[q][h];
+      }
+    };
+    auto mma = [&](int buf) {
+      const int gq = lane >> 4, n = lane & 15;
+#pragma unroll
+      for (int i4 = 0; i4 < I4; ++i4) {
+        const int col = w * (16 * I4) + i4 * 16 + n;
+        const bf16x8 tv = as_bf16x8(
+            *reinterpret_cast<const uint4*>(&s_t[buf][col * TS + dt_chunk(col, gq) * 8]));
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const bf16x8 hi = as_bf16x8(
+              *reinterpret_cast<const uint4*>(&s_p[buf][(nt * 16 + n) * TS + gq * 8]));
+          const bf16x8 lo = as_bf16x8(
+              *reinterpret_cast<const uint4*>(&s_p[buf][((NT + nt) * 16 + n) * TS + gq * 8]));
+          if (IS_B) {
+            acc[i4][nt] = mfma_16x16x32(tv, hi, acc[i4][nt]);
+            acc[i4][nt] = mfma_16x16x32(tv, lo, acc[i4][nt]);
+          } else {
+            acc[i4][nt] = mfma_16x16x32(hi, tv, acc[i4][nt]);
+            acc[i4][nt] = mfma_16x16x32(lo, tv, acc[i4][nt]);
+          }
+        }
+      }
+    };
+    // loads run AHEAD steps ahead, unconditionally (past the last step they
+    // repeat it): a load behind a branch would drain the whole pipeline
+#pragma unroll
+    for (int q = 0; q < AHEAD; ++q) load(q, min(q, wch - 1));
+    for (int cc0 = 0; cc0 < wch; cc0 += R) {
+#pragma unroll
+      for (int u = 0; u < R; ++u) {
+        const int cc = cc0 + u;
+        if (cc >= wch) break;
+        load((u + AHEAD) % R, min(cc + AHEAD, wch - 1));
+        __builtin_amdgcn_sched_barrier(0);     // requests stay ahead of the staging
+        stage(u, cc, cc & 1);
+        __syncthreads();
+        mma(cc & 1);
+      }
+    }
+  }
+
+  mfma_fence();
+  if (mc == 0 && g.accumulate) return;
+#pragma unroll
+  for (int i4 = 0; i4 < I4; ++i4)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        int64_t oidx;
+        bool valid;
+        if (IS_B) {
+          const int o = c0 + w * (16 * I4) + i4 * 16 + (lane >> 4) * 4 + v, j = nt * 16 + (lane & 15);
+          valid = o < g.d_out && j < r;
+          oidx = (int64_t)o * r + j;
+        } else {
+          const int j = nt * 16 + (lane >> 4) * 4 + v, k = c0 + w * (16 * I4) + i4 * 16 + (lane & 15);
+          valid = j < r && k < g.d_in;
+          oidx = (int64_t)j * g.d_in + k;
+        }
+        if (!valid) continue;
+        const float val = (mc == 0) ? 0.0f : s * acc[i4][nt][v];
+        out[oidx] = g.accumulate ? out[oidx] + val : val;
+      }
+    }
+}
+
 template <int NT>
 __global__ __launch_bounds__(256) void dadb_kernel(GradArgs g) {
-  constexpr int CT = DT_CT, TS = DT_TS, PSEG = 2 * NT * 16 * 4;   // 16-byte plane pieces per step
-  constexpr int PPT = (PSEG + 255) / 256;                           // per thread
-  constexpr int R = 3;                                              // register ring (2 steps ahead)
-  __shared__ __align__(16) uint16_t s_t[2][CT * TS];
-  __shared__ __align__(16) uint16_t s_p[2][2 * NT * 16 * TS];     // [hl][j][t]
+  constexpr int CT = dt_ct(NT);
+  __shared__ __align__(16) uint16_t s_t[2][CT * DT_TS];
+  __shared__ __align__(16) uint16_t s_p[2][2 * NT * 16 * DT_TS];     // [hl][j][t]
   __shared__ int s_rows[DT_WIN];
-  const int lane = threadIdx.x & 63, w = wave_id(), tid = threadIdx.x;
   const int nbB = (g.d_out + CT - 1) / CT, nbA = (g.d_in + CT - 1) / CT, nbt = nbB + nbA;
   const XcdRange xr = xcd_range(g.slot_count * nbt);
   for (int tile = xr.first; tile < xr.end; tile += xr.step) {
     const int sl = tile / nbt, c = tile - sl * nbt;
-    const int a = g.slot_base + sl;
-    const Slot m = load_slot(g.meta, a);
-    const int r = m.rank;
+    const int r = uni(g.meta[g.slot_base + sl].rank);
     if (r <= 0) continue;
-    const bool isB = c < nbB;
-    float* out = isB ? g.dB[sl] : g.dA[sl];
-    if (out == nullptr) continue;
-    const int c0 = (isB ? c : c - nbB) * CT;
-    const int dcol = isB ? g.d_out : g.d_in;
-    const int mc = uni(g.m_counts[a]), moff = uni(g.m_offsets[a]), blk0 = uni(g.m_blk[a]);
-    const float s = m.scale;
-    const uint16_t* src = reinterpret_cast<const uint16_t*>(isB ? g.dY : g.X);
-    const int64_t ld = isB ? g.lddy : g.ldx;
-    const uint16_t* fin0 = fin_plane(g, isB ? 0 : 1, 0);
-    const uint16_t* fin1 = fin_plane(g, isB ? 0 : 1, 1);
-
-    f32x4 acc[2][NT];
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) acc[i][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    const int nch = (mc + 31) >> 5;
-    for (int w0 = 0; w0 < nch; w0 += DT_WIN / 32) {
-      const int wch = min(DT_WIN / 32, nch - w0);
-      __syncthreads();
-      for (int i = tid; i < DT_WIN; i += 256) {
-        const int p = w0 * 32 + i;
-        s_rows[i] = g.m_perm[moff + (p < mc ? p : mc - 1)];
-      }
-      __syncthreads();
-
-      uint4 tr[R][2], pr[R][PPT];
-      // raw loads of step cc into ring slot q (clamped addresses; masked at the LDS write)
-      auto load = [&](int q, int cc) {
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int sgm = tid + 256 * h, i = sgm >> 4, cs = (sgm & 15) * 8;
-          const int col = c0 + cs < dcol ? c0 + cs : dcol - 8;
-          tr[q][h] = ldg16(src + (int64_t)s_rows[cc * 32 + i] * ld + col);
-        }
-        const int col0 = (blk0 + w0 + cc) * 32;
-#pragma unroll
-        for (int h = 0; h < PPT; ++h) {
-          int sgm = tid + 256 * h;
-          sgm = sgm < PSEG ? sgm : PSEG - 1;
-          const int hl = sgm / (NT * 64), rem = sgm - hl * (NT * 64);
-          const int j = rem >> 2, part = (rem & 3) * 8;
-          pr[q][h] = ldg16((hl ? fin1 : fin0) + (int64_t)j * g.p_stride + col0 + part);
-        }
-      };
-      auto stage = [&](int q, int cc, int buf) {
-        const int rows_left = mc - (w0 + cc) * 32;
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int sgm = tid + 256 * h, i = sgm >> 4, cs = (sgm & 15) * 8;
-          const bool ok = i < rows_left && c0 + cs < dcol;
-          const uint4 u = ok ? tr[q][h] : make_uint4(0u, 0u, 0u, 0u);
-          const uint32_t wv[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-          for (int k = 0; k < 8; ++k)
-            s_t[buf][(cs + k) * TS + i] = (uint16_t)(wv[k >> 1] >> (16 * (k & 1)));
-        }
-#pragma unroll
-        for (int h = 0; h < PPT; ++h) {
-          const int sgm = tid + 256 * h;
-          if (sgm >= PSEG) continue;
-          const int hl = sgm / (NT * 64), rem = sgm - hl * (NT * 64);
-          const int j = rem >> 2, part = (rem & 3) * 8;
-          *reinterpret_cast<uint4*>(&s_p[buf][(hl * NT * 16 + j) * TS + part]) = pr[q][h];
-        }
-      };
-      auto mma = [&](int buf) {
-        const int tg = (lane >> 4) * 8, n = lane & 15;
-#pragma unroll
-        for (int i2 = 0; i2 < 2; ++i2) {
-          const bf16x8 tv = as_bf16x8(
-              *reinterpret_cast<const uint4*>(&s_t[buf][(w * 32 + i2 * 16 + n) * TS + tg]));
-#pragma unroll
-          for (int nt = 0; nt < NT; ++nt) {
-            const bf16x8 hi = as_bf16x8(
-                *reinterpret_cast<const uint4*>(&s_p[buf][(nt * 16 + n) * TS + tg]));
-            const bf16x8 lo = as_bf16x8(
-                *reinterpret_cast<const uint4*>(&s_p[buf][((NT + nt) * 16 + n) * TS + tg]));
-            if (isB) {
-              acc[i2][nt] = mfma_16x16x32(tv, hi, acc[i2][nt]);
-              acc[i2][nt] = mfma_16x16x32(tv, lo, acc[i2][nt]);
-            } else {
-              acc[i2][nt] = mfma_16x16x32(hi, tv, acc[i2][nt]);
-              acc[i2][nt] = mfma_16x16x32(lo, tv, acc[i2][nt]);
-            }
-          }
-        }
-      };
-      load(0, 0);
-      if (wch > 1) load(1, 1);
-      for (int cc0 = 0; cc0 < wch; cc0 += R) {
-#pragma unroll
-        for (int u = 0; u < R; ++u) {
-          const int cc = cc0 + u;
-          if (cc >= wch) break;
-          if (cc + 2 < wch) load((u + 2) % R, cc + 2);
-          stage(u, cc, cc & 1);
-          __syncthreads();
-          mma(cc & 1);
-        }
-      }
+    if (c < nbB) {
+      if (g.dB[sl] != nullptr) dadb_tile<NT, true>(g, sl, c * CT, s_t, s_p, s_rows);
+    } else {
+      if (g.dA[sl] != nullptr) dadb_tile<NT, false>(g, sl, (c - nbB) * CT, s_t, s_p, s_rows);
     }
-
-    mfma_fence();
-    if (mc == 0 && g.accumulate) continue;
-#pragma unroll
-    for (int i2 = 0; i2 < 2; ++i2)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          int64_t oidx;
-          bool valid;
-          if (isB) {
-            const int o = c0 + w * 32 + i2 * 16 + (lane >> 4) * 4 + v, j = nt * 16 + (lane & 15);
-            valid = o < g.d_out && j < r;
-            oidx = (int64_t)o * r + j;
-          } else {
-            const int j = nt * 16 + (lane >> 4) * 4 + v, k = c0 + w * 32 + i2 * 16 + (lane & 15);
-            valid = j < r && k < g.d_in;
-            oidx = (int64_t)j * g.d_in + k;
-          }
-          if (!valid) continue;
-          const float val = (mc == 0) ? 0.0f : s * acc[i2][nt][v];
-          out[oidx] = g.accumulate ? out[oidx] + val : val;
-        }
-      }
   }
 }
 
@@ -467,7 +537,7 @@ __global__ __launch_bounds__(256) void hg_valu_kernel(GradArgs g) {
     const int r = m.rank;
     float* ph = plane(g, 0, 0);
     float* pg = plane(g, 1, 0);
-    for (int q = threadIdx.x; q < 32 * g.r_pad; q += blockDim.x) {
+    for (int q = threadIdx.x; q < MRB_ROWS * g.r_pad; q += blockDim.x) {
       const int i = q / g.r_pad, j = q - i * g.r_pad;
       float h = 0.0f, gg = 0.0f;
       if (i < rows && j < r) {
@@ -481,8 +551,8 @@ __global__ __launch_bounds__(256) void hg_valu_kernel(GradArgs g) {
         for (int o = 0; o < g.d_out; ++o)
           gg = fmaf(ldv<XB>(g.dY, (int64_t)t * g.lddy + o), ldv<WB>(m.B, (int64_t)o * r + j), gg);
       }
-      ph[(int64_t)j * g.p_stride + e * 32 + i] = h;
-      pg[(int64_t)j * g.p_stride + e * 32 + i] = gg;
+      ph[(int64_t)j * g.p_stride + e * MRB_ROWS + i] = h;
+      pg[(int64_t)j * g.p_stride + e * MRB_ROWS + i] = gg;
     }
   }
 }
@@ -519,7 +589,7 @@ __global__ __launch_bounds__(256) void dadb_valu_kernel(GradArgs g) {
     float acc = 0.0f;
     for (int p = 0; p < mc; ++p) {
       const int t = g.m_perm[moff + p];
-      const float hv = pl[(blk0 + (p >> 5)) * 32 + (p & 31)];
+      const float hv = pl[blk0 * MRB_ROWS + p];
       const float xv = isB ? ldv<XB>(g.dY, (int64_t)t * g.lddy + col) : ldv<XB>(g.X, (int64_t)t * g.ldx + col);
       acc = fmaf(xv, hv, acc);
     }
@@ -583,15 +653,16 @@ hipError_t launch_nt(const GradLaunch& l, const GradArgs& g, hipStream_t s) {
   const int grid1 = round8(std::min<long long>((long long)l.o.rb_ub * l.k_splits, 4096));
   hipLaunchKernelGGL((hg_kernel<NT>), dim3(grid1), dim3(256), 0, s, g);
   if ((err = hipGetLastError()) != hipSuccess) return err;
-  const long long groups = 2LL * l.r_pad * l.o.rb_ub * 4;       // 8-column groups (upper bound)
+  const long long groups = 2LL * l.r_pad * l.o.rb_ub * (MRB_ROWS / 8);   // 8-column groups (upper bound)
   const int grid2 = (int)std::max<long long>(1, std::min<long long>((groups + 255) / 256, 4096));
   hipLaunchKernelGGL(hgsum_kernel, dim3(grid2), dim3(256), 0, s, g);
   if ((err = hipGetLastError()) != hipSuccess) return err;
   for (int base = 0; base < l.o.num_slots; base += GRAD_SLOT_GROUP) {
     GradArgs gg = g;
     if (!set_group(l, gg, base)) continue;
+    constexpr int CT = dt_ct(NT);
     const long long tiles = (long long)gg.slot_count *
-                            ((l.o.d_out + DT_CT - 1) / DT_CT + (l.o.d_in + DT_CT - 1) / DT_CT);
+                            ((l.o.d_out + CT - 1) / CT + (l.o.d_in + CT - 1) / CT);
     const int grid3 = round8(std::min<long long>(tiles, 8192));
     hipLaunchKernelGGL((dadb_kernel<NT>), dim3(grid3), dim3(256), 0, s, gg);
     if ((err = hipGetLastError()) != hipSuccess) return err;

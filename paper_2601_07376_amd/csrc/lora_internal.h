@@ -35,7 +35,7 @@ enum : int {
 
 constexpr int RB_ROWS = 64;      // rows per large-group row block
 constexpr int SMALL_ROWS = 16;   // rows per small-group entry (one matrix-core column tile)
-constexpr int MRB_ROWS = 32;     // trainable rows per gradient row block
+constexpr int MRB_ROWS = 64;     // trainable rows per gradient row block
 constexpr int PLAN_THREADS = 1024;
 constexpr int PLAN_WAVES = PLAN_THREADS / 64;
 
