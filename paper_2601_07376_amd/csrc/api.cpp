@@ -161,7 +161,7 @@ lora_status make_plan(const lora_table* t, int32_t n, const int32_t* idx,
   p->d.offsets = reinterpret_cast<int32_t*>(b + L.offsets);
   p->d.perm = reinterpret_cast<int32_t*>(b + L.perm);
   p->d.run_start = reinterpret_cast<int32_t*>(b + L.run_start);
-  p->d.run_len = reinterpret_cast<int32_t*>(b + L.run_len);
+  p->d.run_end = reinterpret_cast<int32_t*>(b + L.run_end);
   p->d.run_adapter = reinterpret_cast<int32_t*>(b + L.run_adapter);
   p->d.m_counts = reinterpret_cast<int32_t*>(b + L.m_counts);
   p->d.m_offsets = reinterpret_cast<int32_t*>(b + L.m_offsets);
@@ -171,6 +171,12 @@ lora_status make_plan(const lora_table* t, int32_t n, const int32_t* idx,
   p->d.mrb = reinterpret_cast<int4*>(b + L.mrb);
   p->d.srec = reinterpret_cast<lora::SmallRec*>(b + L.srec);
   p->d.seg_ids = reinterpret_cast<int32_t*>(b + L.seg_ids);
+  p->d.ch_hist = reinterpret_cast<int32_t*>(b + L.ch_hist);
+  p->d.ch_mhist = reinterpret_cast<int32_t*>(b + L.ch_mhist);
+  p->d.ch_runs = reinterpret_cast<int32_t*>(b + L.ch_runs);
+  p->d.ch_flags = reinterpret_cast<int32_t*>(b + L.ch_flags);
+  p->d.minfo = reinterpret_cast<int32_t*>(b + L.minfo);
+  p->d.chunks = L.chunks;
   p->r_max = 0;
   p->rank8 = true;
   for (const auto& s : t->host) {
@@ -237,7 +243,7 @@ PlanLayout plan_layout(int32_t n, int32_t S) {
   L.offsets = o;     o += al256((size_t)(S + 1) * 4);
   L.perm = o;        o += al256(nn * 4);
   L.run_start = o;   o += al256(nn * 4);
-  L.run_len = o;     o += al256(nn * 4);
+  L.run_end = o;     o += al256(nn * 4);
   L.run_adapter = o; o += al256(nn * 4);
   L.m_counts = o;    o += al256((size_t)S * 4);
   L.m_offsets = o;   o += al256((size_t)(S + 1) * 4);
@@ -258,6 +264,13 @@ PlanLayout plan_layout(int32_t n, int32_t S) {
   }
   L.srec = o;        o += al256((size_t)L.srec_max * sizeof(SmallRec));
   L.seg_ids = o;     o += al256(nn * 4);
+  L.chunks = (n > PLAN_THREADS && n <= PLAN_MULTI_MAX) ? (n + PLAN_THREADS - 1) / PLAN_THREADS : 0;
+  const size_t ch = (size_t)L.chunks;
+  L.ch_hist = o;     o += al256(ch * S * 4);
+  L.ch_mhist = o;    o += al256(ch * S * 4);
+  L.ch_runs = o;     o += al256(ch * 4);
+  L.ch_flags = o;    o += al256(ch * 4);
+  L.minfo = o;       o += al256(ch ? nn * 4 : 0);
   L.total = o;
   return L;
 }
@@ -388,6 +401,13 @@ lora_status lora_plan_export(const lora_plan* p, int32_t* counts, int32_t* offse
   if (st != LORA_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
   const size_t S = p->table->num_slots, n = p->n;
+  // the device keeps the last row of each run; the length needs the start too
+  std::vector<int32_t> start_tmp;
+  int32_t* run_start_h = run_start;
+  if (run_len != nullptr && run_start_h == nullptr) {
+    start_tmp.resize(std::max<size_t>(n, 1));
+    run_start_h = start_tmp.data();
+  }
   struct Item {
     void* dst;
     const void* src;
@@ -399,8 +419,8 @@ lora_status lora_plan_export(const lora_plan* p, int32_t* counts, int32_t* offse
       {counts, p->d.counts, S * 4},
       {offsets, p->d.offsets, (S + 1) * 4},
       {perm, p->d.perm, n * 4},
-      {run_start, p->d.run_start, n * 4},
-      {run_len, p->d.run_len, n * 4},
+      {run_start_h, p->d.run_start, n * 4},
+      {run_len, p->d.run_end, n * 4},
       {run_adapter, p->d.run_adapter, n * 4},
       {m_counts, p->d.m_counts, S * 4},
       {m_offsets, p->d.m_offsets, (S + 1) * 4},
@@ -413,7 +433,10 @@ lora_status lora_plan_export(const lora_plan* p, int32_t* counts, int32_t* offse
   }
   hipError_t e = hipStreamSynchronize(s);
   if (e != hipSuccess) return hip_fail(e, "plan export sync");
-  if (n_runs != nullptr) *n_runs = hdr[lora::HDR_NRUNS];
+  const int32_t nr = hdr[lora::HDR_NRUNS];
+  if (run_len != nullptr)
+    for (int32_t k = 0; k < nr; ++k) run_len[k] = run_len[k] - run_start_h[k] + 1;
+  if (n_runs != nullptr) *n_runs = nr;
   if (data_flags != nullptr) *data_flags = (uint32_t)hdr[lora::HDR_FLAGS];
   return ok();
 }

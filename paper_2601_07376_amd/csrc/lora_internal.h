@@ -38,6 +38,9 @@ constexpr int SMALL_ROWS = 16;   // rows per small-group entry (one matrix-core 
 constexpr int MRB_ROWS = 64;     // trainable rows per gradient row block
 constexpr int PLAN_THREADS = 1024;
 constexpr int PLAN_WAVES = PLAN_THREADS / 64;
+// batches of (PLAN_THREADS, PLAN_MULTI_MAX] rows are grouped by two launches over
+// chunks of PLAN_THREADS rows; longer ones by one workgroup
+constexpr int PLAN_MULTI_MAX = 65536;
 
 // One small-group entry as the fused kernel reads it: everything a workgroup
 // needs in one 128-byte line, so the kernel's first memory round trip already
@@ -57,9 +60,10 @@ static_assert(sizeof(SmallRec) == 128, "small-group record layout");
 
 // Byte offsets of the plan arrays inside the caller's workspace.
 struct PlanLayout {
-  size_t hdr, counts, offsets, perm, run_start, run_len, run_adapter;
-  size_t m_counts, m_offsets, m_perm, m_blk, rb, mrb, srec, seg_ids, total;
-  int32_t rb_max, mrb_max, srec_max;
+  size_t hdr, counts, offsets, perm, run_start, run_end, run_adapter;
+  size_t m_counts, m_offsets, m_perm, m_blk, rb, mrb, srec, seg_ids;
+  size_t ch_hist, ch_mhist, ch_runs, ch_flags, minfo, total;   // chunked grouping
+  int32_t rb_max, mrb_max, srec_max, chunks;
 };
 
 // Device pointers into one plan workspace.
@@ -69,7 +73,7 @@ struct PlanDev {
   int32_t* offsets;
   int32_t* perm;
   int32_t* run_start;
-  int32_t* run_len;
+  int32_t* run_end;    // last row of each run (lora_plan_export turns it into a length)
   int32_t* run_adapter;
   int32_t* m_counts;
   int32_t* m_offsets;
@@ -78,7 +82,13 @@ struct PlanDev {
   int4* rb;     // {adapter, first index into perm, rows, 0}
   int4* mrb;    // {adapter, first index into m_perm, rows, 0}
   SmallRec* srec;  // small-group records, in the order of the small rb entries
-  int32_t* seg_ids;
+  int32_t* seg_ids;   // packed ids (one workgroup), or per-row id and rank (chunked)
+  int32_t* ch_hist;   // chunked grouping: [chunk][adapter] row counts
+  int32_t* ch_mhist;  //   ... of trainable rows
+  int32_t* ch_runs;   //   [chunk] run starts
+  int32_t* ch_flags;  //   [chunk] data flags
+  int32_t* minfo;     //   per-row trainable id and rank
+  int32_t chunks;     //   chunks of PLAN_THREADS rows (0: not chunked)
 };
 
 // Groups of at most this many rows take the fused small-group path.

@@ -65,7 +65,7 @@ struct Out {
   int32_t* dup_offsets;
   int32_t* dup_perm;
   int32_t* run_start;
-  int32_t* run_len;
+  int32_t* run_end;
   int32_t* run_adapter;
 };
 
@@ -183,19 +183,13 @@ __device__ void group_pass(const Rows& R, int S, int* s_hist, int* s_cnt, int* s
         out.run_start[k] = t;
         out.run_adapter[k] = e;
       }
-      if (ed) out.run_len[reb + __popcll(eb & lanemask_lt())] = t;  // last row; length below
+      if (ed) out.run_end[reb + __popcll(eb & lanemask_lt())] = t;
       rsb += __popcll(sb);
       reb += __popcll(eb);
     }
   }
   __syncthreads();
-  n_runs = 0;
-  if (RUNS) {
-    n_runs = s_scalar[0];
-    for (int k = tid; k < n_runs; k += PLAN_THREADS)
-      out.run_len[k] = out.run_len[k] - out.run_start[k] + 1;
-    __syncthreads();
-  }
+  n_runs = RUNS ? s_scalar[0] : 0;
 }
 
 // PK_LDS: the packed ids live in LDS (n <= LDS_ROWS), else in the workspace.
@@ -294,7 +288,7 @@ __global__ __launch_bounds__(PLAN_THREADS) void plan_kernel(PlanLaunch a) {
   int cnt, off, n_act, n_runs;
   int mcnt, moff, m_n_act, unused;
   const Out out{a.d.counts, a.d.offsets, a.d.perm, a.d.m_counts, a.d.m_offsets, a.d.m_perm,
-                a.d.run_start, a.d.run_len, a.d.run_adapter};
+                a.d.run_start, a.d.run_end, a.d.run_adapter};
   if (a.mask == nullptr) {
     group_pass<false, true, true>(R, S, s_hist, s_cnt, s_wsum, s_runs, s_scalar, out, cnt, off, n_act,
                                   n_runs);
@@ -372,7 +366,7 @@ __global__ __launch_bounds__(PLAN_THREADS) void plan_kernel(PlanLaunch a) {
 //   4. one block-wide scan gives adapter offsets, entry positions and run
 //      indices together; adapter threads write counts, offsets and entries;
 //   5. rows scatter themselves to perm (and m_perm), to their record slot and
-//      to their run.
+//      to their run (start, adapter and last row).
 // ---------------------------------------------------------------------------
 constexpr int SEG_STAGE = 4096;   // LDS words for the segment table
 
@@ -409,7 +403,6 @@ __global__ __launch_bounds__(PLAN_THREADS) void plan_small_kernel(PlanLaunch a) 
   __shared__ int s_sbase[LORA_MAX_SLOTS];
   __shared__ int s_seg[SEG ? SEG_STAGE : 1];
   __shared__ int s_efirst[PLAN_WAVES], s_elast[PLAN_WAVES];
-  __shared__ int s_rs[PLAN_THREADS], s_re[PLAN_THREADS];
   __shared__ int s_w[7][PLAN_WAVES];
   __shared__ unsigned s_flags;
 
@@ -584,11 +577,8 @@ __global__ __launch_bounds__(PLAN_THREADS) void plan_small_kernel(PlanLaunch a) 
   if (st && (unsigned)v[5] < (unsigned)n) {
     d.run_start[v[5]] = tid;
     d.run_adapter[v[5]] = e;
-    s_rs[v[5]] = tid;
   }
-  if (ed && (unsigned)v[6] < (unsigned)n) s_re[v[6]] = tid;
-  __syncthreads();
-  for (int k = tid; k < min(tot[5], n); k += PLAN_THREADS) d.run_len[k] = s_re[k] - s_rs[k] + 1;
+  if (ed && (unsigned)v[6] < (unsigned)n) d.run_end[v[6]] = tid;
   if (tid == 0) {
     int32_t* h = d.hdr;
     h[HDR_FLAGS] = (int32_t)s_flags;
@@ -600,6 +590,297 @@ __global__ __launch_bounds__(PLAN_THREADS) void plan_small_kernel(PlanLaunch a) 
     h[HDR_NMRB] = tot[4];
     h[HDR_NSMALL] = tot[3];
   }
+}
+
+
+// ---------------------------------------------------------------------------
+// Batches of (PLAN_THREADS, PLAN_MULTI_MAX] rows: two launches over chunks of
+// PLAN_THREADS rows, one workgroup per chunk.
+//   count:   ids validated; each row's rank among its chunk's rows of the same
+//            adapter (and under the mask); per-chunk adapter histograms, run
+//            starts and data flags.
+//   scatter: each chunk adds the histograms of the chunks before it (and of
+//            all chunks, for the adapter offsets), then its rows scatter to
+//            perm, m_perm, their record slot and their run; the first chunk
+//            writes counts, offsets, entry lists and the header.
+// ---------------------------------------------------------------------------
+template <bool MASKED, bool SEG>
+__global__ __launch_bounds__(PLAN_THREADS) void plan_count_kernel(PlanLaunch a) {
+  __shared__ int s_rank[LORA_MAX_SLOTS];
+  __shared__ unsigned short s_wc[LORA_MAX_SLOTS * PLAN_WAVES];    // [adapter][wave]
+  __shared__ unsigned short s_wcm[MASKED ? LORA_MAX_SLOTS * PLAN_WAVES : 1];
+  __shared__ int s_seg[SEG ? SEG_STAGE : 1];
+  __shared__ int s_elast[PLAN_WAVES];
+  __shared__ int s_nst;
+  __shared__ unsigned s_flags;
+
+  const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
+  const int n = a.n, S = a.num_slots, ns = a.num_segs;
+  const int c = blockIdx.x, t = c * PLAN_THREADS + tid;
+  const PlanDev& d = a.d;
+
+  if (tid == 0) {
+    s_flags = 0u;
+    s_nst = 0;
+  }
+  int raw = -1, rawp = -1, mk = 1;
+  if (!SEG) {
+    if (t < n) raw = a.idx[t];
+    if (tid == 0 && t > 0) rawp = a.idx[t - 1];
+  } else {
+    for (int i = tid; i <= ns; i += PLAN_THREADS) s_seg[i] = a.seg_offsets[i];
+    for (int i = tid; i < ns; i += PLAN_THREADS) s_seg[ns + 1 + i] = a.seg_adapter[i];
+  }
+  if (MASKED && t < n) mk = a.mask[t];
+  for (int i = tid; i < S * PLAN_WAVES; i += PLAN_THREADS) {
+    s_wc[i] = 0;
+    if (MASKED) s_wcm[i] = 0;
+  }
+  if (tid < S) s_rank[tid] = a.meta[tid].rank;
+  __syncthreads();
+
+  uint32_t flags = 0u;
+  if (SEG) {
+    bool bad = false;
+    for (int i = tid; i <= ns; i += PLAN_THREADS) {
+      const int o = s_seg[i];
+      if (i == 0 && o != 0) bad = true;
+      if (i == ns && o != n) bad = true;
+      if (i < ns && s_seg[i + 1] < o) bad = true;
+    }
+    if (__syncthreads_or(bad ? 1 : 0)) {
+      flags |= LORA_DATA_BAD_SEGMENTS;
+    } else {
+      auto seg_of = [&](int row) {
+        int lo = 0, hi = ns;             // s_seg[lo] <= row < s_seg[hi]
+        while (hi - lo > 1) {
+          const int mid = (lo + hi) >> 1;
+          if (s_seg[mid] <= row) lo = mid;
+          else hi = mid;
+        }
+        return s_seg[ns + 1 + lo];
+      };
+      if (t < n) raw = seg_of(t);
+      if (tid == 0 && t > 0) rawp = seg_of(t - 1);
+    }
+  }
+  auto validate = [&](int v, bool report) {
+    if (v < -1 || v >= S) {
+      if (report) flags |= LORA_DATA_BAD_ID;
+      return -1;
+    }
+    if (v >= 0 && s_rank[v] <= 0) {
+      if (report) flags |= LORA_DATA_EMPTY_SLOT;
+      return -1;
+    }
+    return v;
+  };
+  const int e = t < n ? validate(raw, true) : -1;
+  const int ep0 = (tid == 0 && t > 0) ? validate(rawp, false) : -1;   // previous chunk's last row
+  const int em = (MASKED && !mk) ? -1 : e;
+  const int nbits = 32 - __clz(S);
+  const uint64_t lt = lanemask_lt();
+  const uint64_t peers = match_peers(e + 1, nbits);
+  const int rank_in = __popcll(peers & lt);
+  if (e >= 0 && rank_in == 0) s_wc[e * PLAN_WAVES + w] = (unsigned short)__popcll(peers);
+  int mrank_in = 0;
+  if (MASKED) {
+    const uint64_t mpeers = match_peers(em + 1, nbits);
+    mrank_in = __popcll(mpeers & lt);
+    if (em >= 0 && mrank_in == 0) s_wcm[em * PLAN_WAVES + w] = (unsigned short)__popcll(mpeers);
+  }
+  if (lane == 63) s_elast[w] = e;
+  __syncthreads();
+
+  // per adapter: exclusive prefix over waves, chunk total to the histogram
+  for (int k0 = 0; k0 < S * PLAN_WAVES; k0 += PLAN_THREADS) {
+    const int k = k0 + tid;
+    const bool act = k < S * PLAN_WAVES;
+    const int v = act ? (int)s_wc[k] : 0;
+    const int incl = row_incl_scan(v);
+    if (act) {
+      s_wc[k] = (unsigned short)(incl - v);
+      if ((k & 15) == 15) d.ch_hist[c * S + (k >> 4)] = incl;
+    }
+    if (MASKED) {
+      const int vm = act ? (int)s_wcm[k] : 0;
+      const int im = row_incl_scan(vm);
+      if (act) {
+        s_wcm[k] = (unsigned short)(im - vm);
+        if ((k & 15) == 15) d.ch_mhist[c * S + (k >> 4)] = im;
+      }
+    }
+  }
+  const int ep = lane_prev(e, w > 0 ? s_elast[w - 1] : ep0);
+  const uint64_t stb = __ballot(e >= 0 && ep != e);
+  if (lane == 0 && stb) atomicAdd(&s_nst, __popcll(stb));
+  __syncthreads();
+
+  if (t < n) {
+    d.seg_ids[t] = e >= 0 ? (e + 1) | (((int)s_wc[e * PLAN_WAVES + w] + rank_in) << 16) : 0;
+    if (MASKED)
+      d.minfo[t] = em >= 0 ? (em + 1) | (((int)s_wcm[em * PLAN_WAVES + w] + mrank_in) << 16) : 0;
+  }
+  if (flags) atomicOr(&s_flags, flags);
+  __syncthreads();
+  if (tid == 0) {
+    d.ch_runs[c] = s_nst;
+    d.ch_flags[c] = (int32_t)s_flags;
+  }
+}
+
+template <bool MASKED>
+__global__ __launch_bounds__(PLAN_THREADS) void plan_scatter_kernel(PlanLaunch a) {
+  __shared__ int s_base[LORA_MAX_SLOTS];      // adapter offset + its rows in earlier chunks
+  __shared__ int s_mbase[MASKED ? LORA_MAX_SLOTS : 1];
+  __shared__ int s_off[LORA_MAX_SLOTS];
+  __shared__ int s_cnt[LORA_MAX_SLOTS];
+  __shared__ int s_sbase[LORA_MAX_SLOTS];
+  __shared__ int s_w[7][PLAN_WAVES];
+  __shared__ int s_misc[4];
+
+  const int tid = threadIdx.x;
+  const int n = a.n, S = a.num_slots;
+  const PlanDev& d = a.d;
+  const int C = d.chunks, c = blockIdx.x, t = c * PLAN_THREADS + tid;
+  const int t0 = c * PLAN_THREADS;
+
+  // this chunk's rows (and their neighbours, for the run boundaries)
+  const int info = t < n ? d.seg_ids[t] : 0;
+  const int infop = (t > 0 && t - 1 < n) ? d.seg_ids[t - 1] : 0;
+  const int infon = t + 1 < n ? d.seg_ids[t + 1] : 0;
+  const int minf = (MASKED && t < n) ? d.minfo[t] : 0;
+
+  // per adapter: rows in all chunks and in the chunks before this one
+  int cnt = 0, pre = 0, mcnt = 0, mpre = 0;
+  if (tid < S) {
+    for (int cc = 0; cc < C; ++cc) {
+      const int v = d.ch_hist[cc * S + tid];
+      cnt += v;
+      pre += cc < c ? v : 0;
+      if (MASKED) {
+        const int vm = d.ch_mhist[cc * S + tid];
+        mcnt += vm;
+        mpre += cc < c ? vm : 0;
+      }
+    }
+  }
+  if (!MASKED) {
+    mcnt = cnt;
+    mpre = pre;
+  }
+  if (tid == 0) {
+    int rpre = 0, rtot = 0;
+    uint32_t fl = 0u;
+    for (int cc = 0; cc < C; ++cc) {
+      const int r = d.ch_runs[cc];
+      rtot += r;
+      rpre += cc < c ? r : 0;
+      fl |= (uint32_t)d.ch_flags[cc];
+    }
+    // a run that crosses into this chunk ends here, not before it
+    const int eb = t0 > 0 ? (d.seg_ids[t0 - 1] & 0xffff) - 1 : -1;
+    const int ef = (d.seg_ids[t0] & 0xffff) - 1;
+    s_misc[0] = rpre;
+    s_misc[1] = rtot;
+    s_misc[2] = (int)fl;
+    s_misc[3] = rpre - ((eb >= 0 && eb == ef) ? 1 : 0);
+  }
+
+  const int e = (info & 0xffff) - 1;
+  const int ep = t > 0 ? (infop & 0xffff) - 1 : -1;
+  const int en = t + 1 < n ? (infon & 0xffff) - 1 : -1;
+  const bool st = e >= 0 && ep != e;
+  const bool ed = e >= 0 && en != e;
+
+  const bool live = tid < S;
+  const bool small = live && cnt > 0 && cnt <= a.small_max;
+  const int nbl = (live && cnt > a.small_max) ? (cnt + RB_ROWS - 1) / RB_ROWS : 0;
+  const int nbs = small ? (cnt + SMALL_ROWS - 1) / SMALL_ROWS : 0;
+  const int nbm = live ? (mcnt + MRB_ROWS - 1) / MRB_ROWS : 0;
+  int v[7] = {cnt, mcnt, nbl, nbs, nbm, st ? 1 : 0, ed ? 1 : 0};
+  int tot[7];
+  block_scan_n<7>(v, tot, s_w);            // (barriers inside: s_misc is visible after it)
+  const int off = v[0], moff = v[1], pl = v[2], ps = v[3], pm = v[4];
+  if (live) {
+    s_base[tid] = off + pre;
+    if (MASKED) s_mbase[tid] = moff + mpre;
+    s_off[tid] = off;
+    s_cnt[tid] = cnt;
+    s_sbase[tid] = small ? ps : -1;
+  }
+  if (c == 0) {
+    if (live) {
+      const SlotMeta my = a.meta[tid];
+      d.counts[tid] = cnt;
+      d.offsets[tid] = off;
+      d.m_counts[tid] = mcnt;
+      d.m_offsets[tid] = moff;
+      d.m_blk[tid] = pm;
+      for (int i = 0; i < nbl; ++i)
+        d.rb[pl + i] = make_int4(tid, off + i * RB_ROWS, min(RB_ROWS, cnt - i * RB_ROWS), 0);
+      for (int i = 0; i < nbs; ++i) {
+        const int rows = min(SMALL_ROWS, cnt - i * SMALL_ROWS);
+        d.rb[tot[2] + ps + i] = make_int4(tid, off + i * SMALL_ROWS, rows, 1);
+        SmallRec* r = d.srec + ps + i;
+        r->A = my.A;
+        r->B = my.B;
+        r->rows = rows;
+        r->rank = my.rank;
+        r->scale = my.scale;
+        r->adapter = tid;
+      }
+      for (int i = 0; i < nbm; ++i)
+        d.mrb[pm + i] = make_int4(tid, moff + i * MRB_ROWS, min(MRB_ROWS, mcnt - i * MRB_ROWS), 0);
+    }
+    if (tid == 0) {
+      d.offsets[S] = tot[0];
+      d.m_offsets[S] = tot[1];
+      int32_t* h = d.hdr;
+      h[HDR_FLAGS] = s_misc[2];
+      h[HDR_NACT] = tot[0];
+      h[HDR_NRUNS] = s_misc[1];
+      h[HDR_MNACT] = tot[1];
+      h[HDR_NRB_LARGE] = tot[2];
+      h[HDR_NRB_TOTAL] = tot[2] + tot[3];
+      h[HDR_NMRB] = tot[4];
+      h[HDR_NSMALL] = tot[3];
+    }
+  }
+  __syncthreads();
+
+  // (every index below is < n or < the record count by construction; the
+  // guards only keep a broken invariant from writing outside the arrays)
+  if (e >= 0) {
+    const int pos = s_base[e] + (info >> 16);
+    if ((unsigned)pos < (unsigned)n) {
+      d.perm[pos] = t;
+      if (!MASKED) d.m_perm[pos] = t;
+    }
+    const int sb = s_sbase[e];
+    const int rel = pos - s_off[e];
+    const int q = sb + rel / SMALL_ROWS;
+    if (sb >= 0 && rel >= 0 && q < tot[3]) {
+      SmallRec* r = d.srec + q;
+      const int j = rel % SMALL_ROWS;
+      r->row[j] = t;
+      if (rel == s_cnt[e] - 1)
+        for (int jj = j + 1; jj < SMALL_ROWS; ++jj) r->row[jj] = t;
+    }
+  }
+  if (MASKED) {
+    const int em = (minf & 0xffff) - 1;
+    if (em >= 0) {
+      const int pos = s_mbase[em] + (minf >> 16);
+      if ((unsigned)pos < (unsigned)n) d.m_perm[pos] = t;
+    }
+  }
+  const int ks = s_misc[0] + v[5], ke = s_misc[3] + v[6];
+  if (st && (unsigned)ks < (unsigned)n) {
+    d.run_start[ks] = t;
+    d.run_adapter[ks] = e;
+  }
+  if (ed && (unsigned)ke < (unsigned)n) d.run_end[ke] = t;
 }
 
 }  // namespace
@@ -616,6 +897,19 @@ hipError_t launch_plan(const PlanLaunch& a, hipStream_t s) {
       hipLaunchKernelGGL((plan_small_kernel<false, true>), dim3(1), dim3(PLAN_THREADS), 0, s, a);
     else
       hipLaunchKernelGGL((plan_small_kernel<false, false>), dim3(1), dim3(PLAN_THREADS), 0, s, a);
+    return hipGetLastError();
+  }
+  if (a.d.chunks > 0 && (!seg || 2 * a.num_segs + 1 <= SEG_STAGE)) {
+    const dim3 g(a.d.chunks), b(PLAN_THREADS);
+    const bool m = a.mask != nullptr;
+    if (m && seg) hipLaunchKernelGGL((plan_count_kernel<true, true>), g, b, 0, s, a);
+    else if (m) hipLaunchKernelGGL((plan_count_kernel<true, false>), g, b, 0, s, a);
+    else if (seg) hipLaunchKernelGGL((plan_count_kernel<false, true>), g, b, 0, s, a);
+    else hipLaunchKernelGGL((plan_count_kernel<false, false>), g, b, 0, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (m) hipLaunchKernelGGL((plan_scatter_kernel<true>), g, b, 0, s, a);
+    else hipLaunchKernelGGL((plan_scatter_kernel<false>), g, b, 0, s, a);
     return hipGetLastError();
   }
   const bool pk_lds = a.n <= LDS_ROWS;

@@ -57,6 +57,13 @@ FUZZ = [
     ("large_n", lambda r: (r.integers(-1, 50, 70001), 50, r.integers(0, 2, 70001))),
     ("max_slots", lambda r: (r.integers(-1, 1024, 20000), 1024, None)),
     ("zipf_1024", lambda r: (np.minimum(r.zipf(1.3, 9000) - 1, 1023), 1024, r.integers(0, 2, 9000))),
+    # chunk edges of the chunked grouping: one row past a chunk, whole chunks,
+    # and one run spanning several chunks
+    ("chunk_plus_one", lambda r: (r.integers(-1, 4, 1025), 4, r.integers(0, 2, 1025))),
+    ("two_chunks", lambda r: (r.integers(-1, 3, 2048), 3, None)),
+    ("run_across_chunks", lambda r: (np.concatenate([np.full(3000, 2), np.full(100, -1),
+                                                     np.full(2500, 1)]), 4, r.integers(0, 2, 5600))),
+    ("chunked_limit", lambda r: (r.integers(-1, 40, 65536), 40, r.integers(0, 2, 65536))),
 ]
 
 
@@ -103,6 +110,18 @@ def test_plan_segments_edge_cases():
         got = L.Plan(table, seg_offsets=dv(off), seg_adapter=dv(ad), n=n).export()
         assert got["data_flags"] == L.LORA_DATA_BAD_SEGMENTS
         assert got["offsets"].tolist() == [0] * (S + 1) and got["n_runs"] == 0
+    # longer batches (grouped in chunks): empty segments, runs across chunk edges
+    r = np.random.default_rng(5)
+    lens = r.integers(0, 180, 60)
+    n = int(lens.sum())
+    off = np.concatenate([[0], np.cumsum(lens)]).tolist()
+    ad = r.integers(-1, S, 60).tolist()
+    got = L.Plan(table, seg_offsets=dv(off), seg_adapter=dv(ad), n=n).export()
+    compare_plan(got, oracle.canonical_plan(oracle.segments_to_ids(off, ad, n), S))
+    bad = list(off)
+    bad[30] = bad[31] + 1
+    got = L.Plan(table, seg_offsets=dv(bad), seg_adapter=dv(ad), n=n).export()
+    assert got["data_flags"] == L.LORA_DATA_BAD_SEGMENTS and got["n_runs"] == 0
 
 
 def test_plan_check_reports_flags():
