@@ -473,7 +473,7 @@ lora_status lora_shrink(const lora_plan* p, const void* X, lora_dtype x_dtype, i
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e;
   if (x_dtype == LORA_BF16 && t->w_dtype == LORA_BF16)
-    e = lora::launch_shrink_mfma(o, X, ldx, H, ldh, s);
+    e = lora::launch_shrink_mfma(o, X, ldx, H, ldh, 1, 0, s);
   else
     e = lora::launch_shrink_valu(o, X, x_dtype, ldx, t->w_dtype, H, ldh, s);
   if (e != hipSuccess) return hip_fail(e, "shrink launch");
@@ -495,17 +495,19 @@ lora_status lora_expand(const lora_plan* p, const float* H, int64_t ldh, void* Y
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e;
   if (t->w_dtype == LORA_BF16)
-    e = lora::launch_expand_mfma(o, H, ldh, Y, y_dtype, ldy, s);
+    e = lora::launch_expand_mfma(o, H, ldh, 1, 0, Y, y_dtype, ldy, s);
   else
     e = lora::launch_expand_valu(o, H, ldh, t->w_dtype, Y, y_dtype, ldy, s);
   if (e != hipSuccess) return hip_fail(e, "expand launch");
   return ok();
 }
 
+// Apply workspace: the float32 H of every row, once per d-slice of the grouped
+// shrink (the vector path uses one plane).
 size_t lora_apply_workspace_bytes(const lora_plan* p) {
   if (p == nullptr) return 0;
   const int64_t ldh = (std::max(p->r_max, 1) + 7) / 8 * 8;
-  return al256((size_t)std::max(p->n, 1) * ldh * 4);
+  return al256((size_t)std::max(p->n, 1) * ldh * 4) * lora::SHRINK_KS_MAX;
 }
 
 lora_status lora_apply(const lora_plan* p, const void* X, lora_dtype x_dtype, int64_t ldx, void* Y,
@@ -534,8 +536,10 @@ lora_status lora_apply(const lora_plan* p, const void* X, lora_dtype x_dtype, in
       o.count_word = lora::HDR_NRB_LARGE;
       o.first_word = -1;
       o.rb_ub = ub_large(p);
-      e = lora::launch_shrink_mfma(o, X, ldx, H, ldh, s);
-      if (e == hipSuccess) e = lora::launch_expand_mfma(o, H, ldh, Y, y_dtype, ldy, s);
+      const int64_t plane = (int64_t)(al256((size_t)std::max(p->n, 1) * ldh * 4) / 4);
+      e = lora::launch_shrink_mfma(o, X, ldx, H, ldh, lora::SHRINK_KS_MAX, plane, s);
+      if (e == hipSuccess)
+        e = lora::launch_expand_mfma(o, H, ldh, lora::SHRINK_KS_MAX, plane, Y, y_dtype, ldy, s);
       if (e != hipSuccess) return hip_fail(e, "grouped shrink/expand launch");
     }
     o.count_word = lora::HDR_NSMALL;

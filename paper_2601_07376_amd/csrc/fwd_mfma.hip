@@ -27,6 +27,11 @@
 
 namespace lora {
 
+// Target of the stores of padding lanes (rows past the block, columns past the
+// output): never read.  128 bytes per thread of a workgroup.  External
+// linkage, so that the compiler keeps stores whose only target it is.
+__device__ __align__(256) uint4 g_store_sink[256 * 8];
+
 namespace {
 
 struct FwdArgs {
@@ -45,6 +50,8 @@ struct FwdArgs {
   int32_t n_chunks, chunk;
   const SmallRec* srec;     // fused path: small-group records
   int32_t n_rec;            // records the array holds (host bound)
+  int32_t ks_max;           // large groups: most d-slices of the shrink (partial planes)
+  int64_t hp_stride;        // elements between partial H planes
 };
 
 __device__ __forceinline__ void entry_range(const FwdArgs& p, int& first, int& count) {
@@ -238,68 +245,193 @@ __device__ __forceinline__ void shrink_steps(f32x4 (&acc)[MT * NT], const uint16
 }
 
 // ---------------------------------------------------------------------------
-// shrink: H[t, :r] = X[t] A^T over row blocks of up to 64 rows
+// Large groups: row blocks of up to 256 rows.  In both kernels wave w owns
+// rows 64 w .. 64 w + 63 of the block (four 16-row tiles) and the workgroup
+// stages the weight columns of each 32-wide step in LDS once for all four
+// waves, so a block reads its adapter's weights once (not once per wave, and
+// a 256-row block amortises them over four times the rows of a 64-row one).
+// Loads run several steps ahead through register rings; LDS is double
+// buffered with one barrier per step.
 // ---------------------------------------------------------------------------
-template <int NT>
+
+// d-slices of the shrink: enough (block, slice) units to cover the chip once,
+// at most p.ks_max (the workspace holds that many partial planes)
+__device__ __forceinline__ int shrink_splits(const FwdArgs& p, int count) {
+  return max(1, min(p.ks_max, 256 / max(count, 1)));
+}
+
+// slice ks of [0, d) in multiples of 32
+__device__ __forceinline__ void kslice(int d, int nks, int ks, int& b, int& e) {
+  const int w = ((d + nks - 1) / nks + 31) / 32 * 32;
+  b = min(d, ks * w);
+  e = min(d, b + w);
+}
+
+// Pipeline shape shared by both kernels: the k- (or column-) steps of a unit
+// are taken in batches of U steps, double buffered in registers (the loads of
+// batch b + 1 are in flight while batch b feeds the matrix cores) and in LDS
+// (one barrier per batch).  Every load of a batch is issued unconditionally
+// (batches past the end repeat the last one and are never consumed), weight
+// pieces first, and every store is unconditional too (padding lanes write to
+// a sink): memory operations behind branches would make the compiler's wait
+// counts conservative and drain the pipeline.
+//
+// LDS reuse: a wave stages batch b + 2 into a buffer only after the barrier of
+// batch b + 1, which every wave reaches after its reads of batch b.
+
+
+// ---------------------------------------------------------------------------
+// shrink: Hp[ks][t, :r] = X[t, slice ks] A[:, slice ks]^T; with one slice this
+// is H itself.  Work unit = (row block, d-slice).
+// ---------------------------------------------------------------------------
+template <int NT, int U>
 __global__ __launch_bounds__(256) void shrink_kernel(FwdArgs p) {
-  constexpr int U = NT <= 4 ? 2 : 1;
-  __shared__ f32x4 s_red[2 * 4 * NT * 64];
-  const int lane = threadIdx.x & 63, w = wave_id();
+  constexpr int AS = NT * 16;                  // staged A rows (rank padded to 16)
+  constexpr int AP = AS * 4;                   // 16-byte A pieces per step
+  constexpr int APT = (AP + 255) / 256;        // ... per thread
+  constexpr int TS = 32 + 8;                   // LDS stride (bf16) of one staged row
+  __shared__ __align__(16) uint16_t s_a[2][U][AS * TS];
+  const int lane = threadIdx.x & 63, w = wave_id(), tid = threadIdx.x;
+  const int mrow = lane & 15, kg = (lane >> 4) * 8;
   int first, count;
   entry_range(p, first, count);
-  const XcdRange xr = xcd_range(count);
-  for (int e = xr.first; e < xr.end; e += xr.step) {
+  const int nks = shrink_splits(p, count);
+  const XcdRange xr = xcd_range(count * nks);
+  for (int unit = xr.first; unit < xr.end; unit += xr.step) {
+    const int e = unit / nks, ks = unit - e * nks;
     const int4 en = load_entry(p.rb, first + e);
     const int a = en.x, p0 = en.y, rows = en.z;
     const Slot m = load_slot(p.meta, a);
     const int r = m.rank;
     const rsrc_t A = make_rsrc(m.A, (uint32_t)r * (uint32_t)p.d_in * 2u);
-    const int mt_used = (rows + 15) >> 4;
+    int kb, ke;
+    kslice(p.d_in, nks, ks, kb, ke);
+    const int nst = max(1, (ke - kb + 31) / 32);
+    const int nb = (nst + U - 1) / U;
+    const int kend = max(ke, 8);
 
     const uint16_t* xrow[4];
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt) {
-      const int i = mt * 16 + (lane & 15);
+      const int i = 64 * w + 16 * mt + mrow;
       xrow[mt] = p.X + (int64_t)ldg(p.perm + p0 + (i < rows ? i : rows - 1)) * p.ldx;
     }
-    uint32_t arow[NT];
+    // row ids of the accumulator layout (rows 4 (l / 16) + v of each tile),
+    // requested now so that the stores at the end do not wait on them
+    int orow[4][4];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      const int j = nt * 16 + (lane & 15);
-      arow[nt] = (uint32_t)(j < r ? j : r - 1) * (uint32_t)p.d_in;
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int i = 64 * w + 16 * mt + (lane >> 4) * 4 + v;
+        orow[mt][v] = ldg(p.perm + p0 + (i < rows ? i : rows - 1));
+      }
+    // this thread's A pieces: row j (clamped to the rank), columns 8 c .. 8 c + 7
+    // of a step.  With fewer pieces than threads (rank <= 32) several threads
+    // load the same piece and store the same bytes.
+    uint32_t arow[APT];
+    int acol[APT], apos[APT];
+#pragma unroll
+    for (int h = 0; h < APT; ++h) {
+      const int pc = (tid + 256 * h) & (AP - 1);   // (AP is a power of two)
+      const int j = pc >> 2;
+      arow[h] = (uint32_t)(j < r ? j : r - 1) * (uint32_t)p.d_in;
+      acol[h] = (pc & 3) * 8;
+      apos[h] = j * TS + acol[h];
     }
-    f32x4 acc[4 * NT];
+
+    f32x4 acc[4][NT];
 #pragma unroll
-    for (int i = 0; i < 4 * NT; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    shrink_steps<4, NT, U>(acc, xrow, A, arow, w * 32, 128, p.d_in);
-    reduce_waves<4 * NT>(acc, s_red);
-    if (w == 0) {
+    for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt) {
-        if (mt >= mt_used) continue;
+      for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    struct Buf {
+      uint4 a[U][APT];
+      uint4 x[U][4];
+    };
+    auto load = [&](Buf& b, int bt) {
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int i = mt * 16 + (lane >> 4) * 4 + v;
-          if (i >= rows) continue;
-          float* hrow = p.H + (int64_t)ldg(p.perm + p0 + i) * p.ldh;
+      for (int u = 0; u < U; ++u) {
+        const int k0 = kb + 32 * (bt * U + u);
 #pragma unroll
-          for (int nt = 0; nt < NT; ++nt) {
-            const int j = nt * 16 + (lane & 15);
-            if (j < r) stg(hrow + j, acc[mt * NT + nt][v]);
-          }
+        for (int h = 0; h < APT; ++h) {
+          const int ka = k0 + acol[h];
+          b.a[u][h] = bload16(A, (arow[h] + (uint32_t)(ka < kend ? ka : kend - 8)) * 2u);
         }
       }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int k = kb + 32 * (bt * U + u) + kg;
+        const int kk = k < kend ? k : kend - 8;
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) b.x[u][mt] = ldg16(xrow[mt] + kk);
+      }
+    };
+    auto stage = [&](const Buf& b, int buf) {
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int h = 0; h < APT; ++h)
+          *reinterpret_cast<uint4*>(&s_a[buf][u][apos[h]]) = b.a[u][h];
+    };
+    // steps past the slice (k >= ke) are zeroed on the X operand
+    auto compute = [&](const Buf& b, int bt, int buf) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const bool kv = kb + 32 * (bt * U + u) + kg < ke;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const bf16x8 wv =
+              as_bf16x8(*reinterpret_cast<const uint4*>(&s_a[buf][u][(nt * 16 + mrow) * TS + kg]));
+#pragma unroll
+          for (int mt = 0; mt < 4; ++mt)
+            acc[mt][nt] = mfma_16x16x32(sel(kv, as_bf16x8(b.x[u][mt])), wv, acc[mt][nt]);
+        }
+      }
+    };
+    Buf b0, b1;
+    load(b0, 0);
+    __syncthreads();                 // the previous unit's reads of s_a are done
+    // one exit, at the end of a pair of batches (a break between the halves
+    // would give the compiler a path on which b1's loads are still pending
+    // at the top, and a wait for all of them there)
+    for (int bt = 0; bt < nb; bt += 2) {
+      load(b1, min(bt + 1, nb - 1));
+      __builtin_amdgcn_sched_barrier(0);
+      stage(b0, 0);
+      __syncthreads();
+      compute(b0, bt, 0);
+      load(b0, min(bt + 2, nb - 1));
+      __builtin_amdgcn_sched_barrier(0);
+      stage(b1, 1);
+      __syncthreads();
+      if (bt + 1 < nb) compute(b1, bt + 1, 1);
     }
+    mfma_fence();
+    float* H = p.H + (int64_t)ks * p.hp_stride;
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int i = 64 * w + 16 * mt + (lane >> 4) * 4 + v;
+        if (i >= rows) continue;
+        float* hrow = H + (int64_t)orow[mt][v] * p.ldh;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const int j = nt * 16 + mrow;
+          if (j < r) stg(hrow + j, acc[mt][nt][v]);
+        }
+      }
   }
 }
 
 // ---------------------------------------------------------------------------
-// expand: Y[t] += s H[t, :r] B^T.  Work unit = (row block of <= 64 rows, 1024
-// output columns).  The unit's H operands (hi / lo) are loaded once; then each
-// wave streams 32-column slices (columns c0 + 128 s + 32 w), keeping two slices
-// of B and Y in flight ahead of the one feeding the matrix cores.
+// expand: Y[t] += s (sum_ks Hp[ks][t, :r]) B^T.  Work unit = (row block, 1024
+// output columns).  Each wave's H operands (hi / lo) are formed once per unit;
+// the B rows of each 32-column step are staged in LDS for all waves.
 //
-// Slice layout: tile q (0, 1), operand row m, covers column
+// Step layout: tile q (0, 1), operand row m, covers column
 // o_w + 8 (m / 4) + 4 q + (m % 4), so lane l (og = l / 16) holds the 8
 // consecutive columns o_w + 8 og + [0, 8) of one row: one 16-byte load for a
 // bf16 Y, and the wave's load covers 64 contiguous bytes of 16 rows.
@@ -312,7 +444,7 @@ struct Y8 {
 template <bool YBF16>
 __device__ __forceinline__ void y8_load(Y8<YBF16>& f, const void* Yv, int64_t ldy, int t, int o,
                                         int d_out) {
-  o = o < d_out ? o : d_out - 8;            // clamped; such lanes are never stored
+  o = o < d_out ? o : d_out - 8;            // clamped; such lanes store to the sink
   if (YBF16) {
     f.v[0] = ldg16(reinterpret_cast<const uint16_t*>(Yv) + (int64_t)t * ldy + o);
   } else {
@@ -322,11 +454,14 @@ __device__ __forceinline__ void y8_load(Y8<YBF16>& f, const void* Yv, int64_t ld
   }
 }
 
+// y + s * acc, rounded once to the storage type, stored to dst (the row's 8
+// columns, or the sink)
+// y + s * acc for the 8 columns of a lane, rounded once to the storage type:
+// 16 bytes (bf16) or 32 bytes (f32) in out[0..1]
 template <bool YBF16>
-__device__ __forceinline__ void y8_store(const Y8<YBF16>& f, void* Yv, int64_t ldy, int t, int o,
-                                         float s, const f32x4& a0, const f32x4& a1) {
+__device__ __forceinline__ void y8_combine(const Y8<YBF16>& f, float s, const f32x4& a0,
+                                           const f32x4& a1, uint4 (&out)[2]) {
   if (YBF16) {
-    uint16_t* Y = reinterpret_cast<uint16_t*>(Yv) + (int64_t)t * ldy + o;
     const uint32_t w[4] = {f.v[0].x, f.v[0].y, f.v[0].z, f.v[0].w};
     uint32_t o4[4];
 #pragma unroll
@@ -336,155 +471,242 @@ __device__ __forceinline__ void y8_store(const Y8<YBF16>& f, void* Yv, int64_t l
       o4[i] = pack2_bf16(fmaf(s, a[e0], bf16_to_f32(w[i] & 0xffffu)),
                          fmaf(s, a[e0 + 1], bf16_to_f32(w[i] >> 16)));
     }
-    stg16(Y, make_uint4(o4[0], o4[1], o4[2], o4[3]));
+    out[0] = make_uint4(o4[0], o4[1], o4[2], o4[3]);
   } else {
-    float* Y = reinterpret_cast<float*>(Yv) + (int64_t)t * ldy + o;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const uint4 u = f.v[h];
       const f32x4& a = h ? a1 : a0;
-      float4 v;
-      v.x = fmaf(s, a[0], __uint_as_float(u.x));
-      v.y = fmaf(s, a[1], __uint_as_float(u.y));
-      v.z = fmaf(s, a[2], __uint_as_float(u.z));
-      v.w = fmaf(s, a[3], __uint_as_float(u.w));
-      stg_f4(Y + 4 * h, v);
+      out[h] = make_uint4(__float_as_uint(fmaf(s, a[0], __uint_as_float(u.x))),
+                          __float_as_uint(fmaf(s, a[1], __uint_as_float(u.y))),
+                          __float_as_uint(fmaf(s, a[2], __uint_as_float(u.z))),
+                          __float_as_uint(fmaf(s, a[3], __uint_as_float(u.w))));
     }
   }
 }
 
-// TT = row tiles (of 16 rows) per wave: the 4 waves form 4 / TT row groups and
-// TT column groups, so one step of the workgroup covers 64 rows x 32 TT columns.
-// DY = how many steps ahead Y is requested (HBM latency); B (L2) is double
-// buffered one step ahead.
-template <bool YBF16, bool RANK8, int KSM, int TT, int DY>
-__global__ __launch_bounds__(256) void expand_kernel(FwdArgs p) {
-  constexpr int CW = 1024, STEP = 32 * TT, NS = CW / STEP, R = DY + 1;
-  static_assert(R % 2 == 0, "ring length must be even");
-  const int lane = threadIdx.x & 63, w = wave_id();
+// Results leave through LDS.  A store instruction in the matrix-core layout
+// covers 64 bytes of each of 16 rows (half cache lines); one that covers whole
+// 128-byte lines of 8 rows moves read-modify-write traffic markedly faster.
+// So each wave writes its results for 128 bytes of every row (two steps of a
+// bf16 Y, one of an f32 Y) into its own LDS area, then stores them with 8
+// lanes per row.
+template <bool YBF16, bool RANK8, int KSM, int U>
+__global__ __launch_bounds__(256, (KSM == 1 || (YBF16 && KSM == 2 && U == 1)) ? 2 : 1) void expand_kernel(FwdArgs p) {
+  constexpr int CW = 1024;
+  constexpr int BS = KSM * 32, TS = BS + 8;    // staged ranks per column; LDS stride
+  constexpr int BP = 32 * BS / 8;              // 16-byte B pieces per step (rank padded)
+  constexpr int BPT = (BP + 255) / 256;        // ... per thread
+  constexpr int ES = YBF16 ? 2 : 4;            // bytes per Y element
+  constexpr int SP = YBF16 ? 2 : 1;            // steps per 128 bytes of a row
+  constexpr int OS = 128 + 16;                 // bytes per row of a wave's output area
+  __shared__ __align__(16) uint16_t s_b[2][U][32 * TS];
+  __shared__ __align__(16) unsigned char s_o[4][64 * OS];
+  const int lane = threadIdx.x & 63, w = wave_id(), tid = threadIdx.x;
   const int og = lane >> 4, mrow = lane & 15, jg = og * 8;
-  const int rg = w % (4 / TT);     // row group: row tiles rg * TT .. rg * TT + TT - 1
-  const int cg = w / (4 / TT);     // column group: columns cg * 32 .. + 32 of every step
+  unsigned char* const so = s_o[w];
+  uint4* const sink = g_store_sink + 8 * tid;
   int first, count;
   entry_range(p, first, count);
+  const int nks = shrink_splits(p, count);
   const int n_ch = (p.d_out + CW - 1) / CW;
   const XcdRange xr = xcd_range(count * n_ch);
   for (int unit = xr.first; unit < xr.end; unit += xr.step) {
     const int e = unit / n_ch, ch = unit - e * n_ch;
     const int c0 = ch * CW, c1 = min(p.d_out, c0 + CW);
+    const int nst = (c1 - c0 + 31) / 32;
     const int4 en = load_entry(p.rb, first + e);
     const int a = en.x, p0 = en.y, rows = en.z;
-    if (rg * TT * 16 >= rows) continue;           // uniform: no rows for this wave
     const Slot m = load_slot(p.meta, a);
     const int r = m.rank;
     const float s = m.scale;
     const rsrc_t Bw = make_rsrc(m.B, (uint32_t)p.d_out * (uint32_t)r * 2u);
-    int trow[TT];
-    bool rv[TT];
+
+    // rows of the matrix-core layout: tile tt, lane row mrow
+    int trow[4];
+    bool rv[4];
 #pragma unroll
-    for (int tt = 0; tt < TT; ++tt) {
-      const int i = (rg * TT + tt) * 16 + mrow;
+    for (int tt = 0; tt < 4; ++tt) {
+      const int i = 64 * w + 16 * tt + mrow;
       rv[tt] = i < rows;
       trow[tt] = ldg(p.perm + p0 + (i < rows ? i : rows - 1));
     }
-
-    // H operands of the wave's rows (hi / lo), loaded once per unit
-    bf16x8 hh[KSM][TT], hl[KSM][TT];
-    {
-      float4 hraw[KSM][TT][2];
+    // rows of the store layout: instruction i, lane row lane / 8 (padding rows
+    // store to the sink)
+    int srow[8];
 #pragma unroll
-      for (int ks = 0; ks < KSM; ++ks) {
-        const int j = ks * 32 + jg;
-        const int jj = RANK8 ? (j < r ? j : r - 8) : 0;
-#pragma unroll
-        for (int tt = 0; tt < TT; ++tt) {
-          const float* hrow = p.H + (int64_t)trow[tt] * p.ldh;
-          if (RANK8) {
-            hraw[ks][tt][0] = ldg_f4(hrow + jj);
-            hraw[ks][tt][1] = ldg_f4(hrow + jj + 4);
-          } else {
-            float h[8];
-#pragma unroll
-            for (int i = 0; i < 8; ++i) h[i] = (j + i < r) ? ldg(hrow + j + i) : 0.0f;
-            hraw[ks][tt][0] = make_float4(h[0], h[1], h[2], h[3]);
-            hraw[ks][tt][1] = make_float4(h[4], h[5], h[6], h[7]);
-          }
-        }
-      }
-#pragma unroll
-      for (int ks = 0; ks < KSM; ++ks) {
-        const bool jv = ks * 32 + jg < r;
-#pragma unroll
-        for (int tt = 0; tt < TT; ++tt) {
-          const bool k = jv && rv[tt];
-          const float4 a0 = hraw[ks][tt][0], a1 = hraw[ks][tt][1];
-          const float h[8] = {k ? a0.x : 0.f, k ? a0.y : 0.f, k ? a0.z : 0.f, k ? a0.w : 0.f,
-                              k ? a1.x : 0.f, k ? a1.y : 0.f, k ? a1.z : 0.f, k ? a1.w : 0.f};
-          split_hi_lo(h, hh[ks][tt], hl[ks][tt]);
-        }
-      }
+    for (int i = 0; i < 8; ++i) {
+      const int ri = 64 * w + 8 * i + (lane >> 3);
+      srow[i] = ri < rows ? ldg(p.perm + p0 + ri) : -1;
     }
 
-    Y8<YBF16> yb[R][TT];
-    bf16x8 bb[2][KSM][2];
-    auto load_y = [&](Y8<YBF16> (&y)[TT], int st) {
-      const int o = c0 + st * STEP + cg * 32 + 8 * og;
+    // H operands (hi / lo) of the wave's rows: the slices' partial sums added
+    // in slice order, loaded once per unit
+    bf16x8 hh[KSM][4], hl[KSM][4];
 #pragma unroll
-      for (int tt = 0; tt < TT; ++tt) y8_load<YBF16>(y[tt], p.Y, p.ldy, trow[tt], o, p.d_out);
+    for (int ks = 0; ks < KSM; ++ks) {
+      const int j = ks * 32 + jg;
+      const int jj = RANK8 ? (j < r ? j : r - 8) : 0;
+      float4 h[4][2];
+#pragma unroll
+      for (int tt = 0; tt < 4; ++tt) {
+        h[tt][0] = make_float4(0.f, 0.f, 0.f, 0.f);
+        h[tt][1] = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+      for (int sl = 0; sl < nks; ++sl) {
+        const float* Hs = p.H + (int64_t)sl * p.hp_stride;
+#pragma unroll
+        for (int tt = 0; tt < 4; ++tt) {
+          const float* hrow = Hs + (int64_t)trow[tt] * p.ldh;
+          float4 a0, a1;
+          if (RANK8) {
+            a0 = ldg_f4(hrow + jj);
+            a1 = ldg_f4(hrow + jj + 4);
+          } else {
+            float q[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) q[i] = ldg(hrow + (j + i < r ? j + i : r - 1));
+            a0 = make_float4(q[0], q[1], q[2], q[3]);
+            a1 = make_float4(q[4], q[5], q[6], q[7]);
+          }
+          h[tt][0].x += a0.x; h[tt][0].y += a0.y; h[tt][0].z += a0.z; h[tt][0].w += a0.w;
+          h[tt][1].x += a1.x; h[tt][1].y += a1.y; h[tt][1].z += a1.z; h[tt][1].w += a1.w;
+        }
+      }
+#pragma unroll
+      for (int tt = 0; tt < 4; ++tt) {
+        float hv[8] = {h[tt][0].x, h[tt][0].y, h[tt][0].z, h[tt][0].w,
+                       h[tt][1].x, h[tt][1].y, h[tt][1].z, h[tt][1].w};
+#pragma unroll
+        for (int i = 0; i < 8; ++i) hv[i] = (rv[tt] && j + i < r) ? hv[i] : 0.0f;
+        split_hi_lo(hv, hh[ks][tt], hl[ks][tt]);
+      }
+    }
+    vmem_drained();
+
+    // this thread's B pieces: column col of a step, ranks 8 jq .. 8 jq + 7
+    int bcol[BPT], bj[BPT];
+#pragma unroll
+    for (int h = 0; h < BPT; ++h) {
+      const int pc = (tid + 256 * h) & (BP - 1);   // (BP is a power of two)
+      bcol[h] = pc / (BS / 8);
+      bj[h] = (pc - bcol[h] * (BS / 8)) * 8;
+    }
+
+    struct Buf {
+      uint4 b[U][BPT];
+      Y8<YBF16> y[U][4];
     };
-    auto load_b = [&](bf16x8 (&b)[KSM][2], int st) {
-      const int o_w = c0 + st * STEP + cg * 32;
+    auto load = [&](Buf& q, int st0) {
 #pragma unroll
-      for (int q = 0; q < 2; ++q) {
-        int o = o_w + 8 * (mrow >> 2) + 4 * q + (mrow & 3);
-        o = o < p.d_out ? o : p.d_out - 1;
+      for (int u = 0; u < U; ++u) {
+        const int ob = c0 + 32 * min(st0 + u, nst - 1);
 #pragma unroll
-        for (int ks = 0; ks < KSM; ++ks) b[ks][q] = wrow8<RANK8>(Bw, (uint32_t)o * r, ks * 32 + jg, r);
+        for (int h = 0; h < BPT; ++h) {
+          int oc = ob + bcol[h];
+          oc = oc < p.d_out ? oc : p.d_out - 1;
+          q.b[u][h] = __builtin_bit_cast(uint4, wrow8<RANK8>(Bw, (uint32_t)oc * r, bj[h], r));
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int ob = c0 + 32 * min(st0 + u, nst - 1);
+#pragma unroll
+        for (int tt = 0; tt < 4; ++tt)
+          y8_load<YBF16>(q.y[u][tt], p.Y, p.ldy, trow[tt], ob + 8 * og, p.d_out);
       }
     };
-    auto run = [&](const bf16x8 (&b)[KSM][2], const Y8<YBF16> (&y)[TT], int st) {
-      const int o_w = c0 + st * STEP + cg * 32;
-      if (o_w >= c1) return;
-      f32x4 acc[2][TT];
+    auto stage = [&](const Buf& q, int buf) {
 #pragma unroll
-      for (int q = 0; q < 2; ++q)
+      for (int u = 0; u < U; ++u)
 #pragma unroll
-        for (int tt = 0; tt < TT; ++tt) acc[q][tt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int h = 0; h < BPT; ++h)
+          *reinterpret_cast<uint4*>(&s_b[buf][u][bcol[h] * TS + bj[h]]) = q.b[u][h];
+    };
+    // product of step st (batch slot u), added to Y, into the wave's output area
+    auto run = [&](const Buf& q, int u, int st, int buf) {
+      f32x4 acc[2][4];
+#pragma unroll
+      for (int qq = 0; qq < 2; ++qq)
+#pragma unroll
+        for (int tt = 0; tt < 4; ++tt) acc[qq][tt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < KSM; ++ks) {
         const bool jv = ks * 32 + jg < r;
 #pragma unroll
-        for (int q = 0; q < 2; ++q) {
-          const bf16x8 bq = sel(jv, b[ks][q]);
+        for (int qq = 0; qq < 2; ++qq) {
+          const int oc = 8 * (mrow >> 2) + 4 * qq + (mrow & 3);
+          const bf16x8 b = sel(jv, as_bf16x8(*reinterpret_cast<const uint4*>(
+                                       &s_b[buf][u][oc * TS + ks * 32 + jg])));
 #pragma unroll
-          for (int tt = 0; tt < TT; ++tt) {
-            acc[q][tt] = mfma_16x16x32(bq, hh[ks][tt], acc[q][tt]);
-            acc[q][tt] = mfma_16x16x32(bq, hl[ks][tt], acc[q][tt]);
+          for (int tt = 0; tt < 4; ++tt) {
+            acc[qq][tt] = mfma_16x16x32(b, hh[ks][tt], acc[qq][tt]);
+            acc[qq][tt] = mfma_16x16x32(b, hl[ks][tt], acc[qq][tt]);
           }
         }
       }
       mfma_fence();
-      const int o = o_w + 8 * og;
-      if (o < c1) {
+      const int cb = ((st % SP) * 32 + 8 * og) * ES;    // byte column in the area
 #pragma unroll
-        for (int tt = 0; tt < TT; ++tt)
-          if (rv[tt]) y8_store<YBF16>(y[tt], p.Y, p.ldy, trow[tt], o, s, acc[0][tt], acc[1][tt]);
+      for (int tt = 0; tt < 4; ++tt) {
+        uint4 out[2];
+        y8_combine<YBF16>(q.y[u][tt], s, acc[0][tt], acc[1][tt], out);
+        unsigned char* d = so + (16 * tt + mrow) * OS + cb;
+        *reinterpret_cast<uint4*>(d) = out[0];
+        if (!YBF16) *reinterpret_cast<uint4*>(d + 16) = out[1];
       }
     };
-    // Y and B run ahead unconditionally (past the last step they repeat it):
-    // a load behind a branch would drain every outstanding load at the join
+    // the output area's 128 bytes per row, from step st0 on, to Y
+    auto flush = [&](int st0) {
+      asm volatile("" ::: "memory");   // the area's writes above come first
+      const int o = c0 + 32 * st0 + (lane & 7) * (16 / ES);
+      const bool ov = o < c1;
 #pragma unroll
-    for (int d = 0; d < DY; ++d) load_y(yb[d], min(d, NS - 1));
-    load_b(bb[0], 0);
-    for (int st0 = 0; st0 < NS; st0 += R) {
-#pragma unroll
-      for (int u = 0; u < R; ++u) {
-        const int st = st0 + u;
-        if (st >= NS) break;
-        load_y(yb[(u + DY) % R], min(st + DY, NS - 1));
-        load_b(bb[(u + 1) & 1], min(st + 1, NS - 1));
-        run(bb[u & 1], yb[u], st);
+      for (int i = 0; i < 8; ++i) {
+        const uint4 v = *reinterpret_cast<const uint4*>(so + (8 * i + (lane >> 3)) * OS + (lane & 7) * 16);
+        uint4* dst = (ov && srow[i] >= 0)
+                         ? reinterpret_cast<uint4*>(reinterpret_cast<char*>(p.Y) +
+                                                    ((int64_t)srow[i] * p.ldy + o) * ES)
+                         : sink + i;
+        stg16(dst, v);
       }
+      asm volatile("" ::: "memory");   // ... and the next writes come after the reads
+    };
+    // a batch of U steps from st0: products, and a flush after every SP-th step
+    auto batch = [&](const Buf& q, int st0, int buf) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        run(q, u, st0 + u, buf);
+        if ((st0 + u) % SP == SP - 1) flush(st0 + u - (SP - 1));
+      }
+    };
+    // Batches in pairs, double buffered in registers and LDS: the loads of the
+    // next batch are in flight while a batch feeds the matrix cores.  Loads are
+    // unconditional (past the last step they repeat it) and so are stores;
+    // steps past the chunk store to the sink.  One exit, at the end of a pair.
+    Buf b0, b1;
+    load(b0, 0);
+    // as many stores (to the sink) as a pair ends with after its last loads,
+    // so that the loop is entered with the same sequence of memory operations
+    // outstanding as it loops back with, and the compiler's wait counts stay
+    // exact
+    constexpr int TAIL = 8 * (U >= SP ? U / SP : 1);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < TAIL; ++i) stg16(sink + (i & 7), make_uint4(0u, 0u, 0u, (uint32_t)i));
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();                 // the previous unit's reads of s_b are done
+    for (int st = 0; st < nst; st += 2 * U) {
+      load(b1, st + U);
+      __builtin_amdgcn_sched_barrier(0);
+      stage(b0, 0);
+      __syncthreads();
+      batch(b0, st, 0);
+      load(b0, st + 2 * U);
+      __builtin_amdgcn_sched_barrier(0);
+      stage(b1, 1);
+      __syncthreads();
+      batch(b1, st + U, 1);
     }
   }
 }
@@ -658,25 +880,22 @@ int env_int(const char* name, int dflt) {
   return (v != nullptr && *v) ? std::atoi(v) : dflt;
 }
 
-// Expand shapes: (TT, Y prefetch depth).  The default, all four row tiles in
-// every wave (the waves split the columns) with one slice of Y prefetched, measured fastest on the prefill and
-// mixed-rank workloads; LORA_EXPAND_VARIANT selects another for measurements.
+// Steps per batch: two for a bf16 Y up to rank 64 (more bytes in flight per
+// wave), else one (register budget).  LORA_EXPAND_U=1 forces one.
 template <bool YB, bool R8, int KSM>
-hipError_t launch_expand_variant(int grid, const FwdArgs& a, hipStream_t s) {
-  switch (env_int("LORA_EXPAND_VARIANT", 0)) {
-    case 1: return launch(expand_kernel<YB, R8, KSM, 2, 1>, grid, a, s);
-    case 2: return launch(expand_kernel<YB, R8, KSM, 1, 3>, grid, a, s);
-    case 3: return launch(expand_kernel<YB, R8, KSM, 4, 3>, grid, a, s);
-    default: return launch(expand_kernel<YB, R8, KSM, 4, 1>, grid, a, s);
+hipError_t launch_expand_u(int grid, const FwdArgs& a, hipStream_t s) {
+  if constexpr (YB && KSM <= 2) {
+    if (env_int("LORA_EXPAND_U", 1) == 2) return launch(expand_kernel<YB, R8, KSM, 2>, grid, a, s);
   }
+  return launch(expand_kernel<YB, R8, KSM, 1>, grid, a, s);
 }
 
 template <bool YB, bool R8>
 hipError_t launch_expand_ks(const OpLaunch& o, int grid, const FwdArgs& a, hipStream_t s) {
   const int ks = (o.r_max + 31) / 32;
-  if (ks <= 1) return launch_expand_variant<YB, R8, 1>(grid, a, s);
-  if (ks <= 2) return launch_expand_variant<YB, R8, 2>(grid, a, s);
-  return launch_expand_variant<YB, R8, 4>(grid, a, s);
+  if (ks <= 1) return launch_expand_u<YB, R8, 1>(grid, a, s);
+  if (ks <= 2) return launch_expand_u<YB, R8, 2>(grid, a, s);
+  return launch_expand_u<YB, R8, 4>(grid, a, s);
 }
 
 template <bool YB, bool R8>
@@ -692,25 +911,32 @@ hipError_t launch_fused_nt(const OpLaunch& o, int grid, const FwdArgs& a, hipStr
 }  // namespace
 
 hipError_t launch_shrink_mfma(const OpLaunch& o, const void* X, int64_t ldx, float* H,
-                              int64_t ldh, hipStream_t s) {
+                              int64_t ldh, int32_t ks_max, int64_t hp_stride, hipStream_t s) {
   FwdArgs a = base_args(o);
   a.X = reinterpret_cast<const uint16_t*>(X);
   a.ldx = ldx;
   a.H = H;
   a.ldh = ldh;
-  const int grid = round8(std::min(o.rb_ub, 2048));
+  a.ks_max = std::min(std::max(ks_max, 1), SHRINK_KS_MAX);   // the expand sums at most this many planes
+  a.hp_stride = hp_stride;
+  // (row block, d-slice) units: blocks x min(ks_max, 256 / blocks) <= max(blocks, 256)
+  const int grid = round8(std::min<long long>((long long)o.rb_ub * a.ks_max, 2048));
   const int nt = (o.r_max + 15) / 16;
-  if (nt <= 1) return launch(shrink_kernel<1>, grid, a, s);
-  if (nt <= 2) return launch(shrink_kernel<2>, grid, a, s);
-  if (nt <= 4) return launch(shrink_kernel<4>, grid, a, s);
-  return launch(shrink_kernel<8>, grid, a, s);
+  const int u = env_int("LORA_SHRINK_U", 4);
+  if (nt <= 1) return u == 2 ? launch(shrink_kernel<1, 2>, grid, a, s) : u == 1 ? launch(shrink_kernel<1, 1>, grid, a, s) : launch(shrink_kernel<1, 4>, grid, a, s);
+  if (nt <= 2) return u == 2 ? launch(shrink_kernel<2, 2>, grid, a, s) : u == 1 ? launch(shrink_kernel<2, 1>, grid, a, s) : launch(shrink_kernel<2, 4>, grid, a, s);
+  if (nt <= 4) return u == 2 ? launch(shrink_kernel<4, 2>, grid, a, s) : u == 1 ? launch(shrink_kernel<4, 1>, grid, a, s) : launch(shrink_kernel<4, 4>, grid, a, s);
+  return launch(shrink_kernel<8, 1>, grid, a, s);
 }
 
-hipError_t launch_expand_mfma(const OpLaunch& o, const float* H, int64_t ldh, void* Y,
-                              lora_dtype y_dtype, int64_t ldy, hipStream_t s) {
+hipError_t launch_expand_mfma(const OpLaunch& o, const float* H, int64_t ldh, int32_t ks_max,
+                              int64_t hp_stride, void* Y, lora_dtype y_dtype, int64_t ldy,
+                              hipStream_t s) {
   FwdArgs a = base_args(o);
   a.H = const_cast<float*>(H);
   a.ldh = ldh;
+  a.ks_max = std::min(std::max(ks_max, 1), SHRINK_KS_MAX);   // the expand sums at most this many planes
+  a.hp_stride = hp_stride;
   a.Y = Y;
   a.ldy = ldy;
   const long long units = (long long)o.rb_ub * ((o.d_out + 1023) / 1024);

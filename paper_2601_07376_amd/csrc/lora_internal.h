@@ -33,7 +33,8 @@ enum : int {
   HDR_WORDS = 64
 };
 
-constexpr int RB_ROWS = 64;      // rows per large-group row block
+constexpr int RB_ROWS = 256;     // rows per large-group row block
+constexpr int SHRINK_KS_MAX = 4; // most d-slices of the grouped shrink inside lora_apply
 constexpr int SMALL_ROWS = 16;   // rows per small-group entry (one matrix-core column tile)
 constexpr int MRB_ROWS = 64;     // trainable rows per gradient row block
 constexpr int PLAN_THREADS = 1024;
@@ -125,12 +126,16 @@ struct OpLaunch {
   int first_word;               // header word holding the first entry (-1: 0)
 };
 
-// H[t, :r] = X[t] A^T over entries [first, count) (bf16 X and weights, matrix cores)
+// H[t, :r] = X[t] A^T over entries [first, count) (bf16 X and weights, matrix
+// cores).  With ks_max > 1 the kernel may split d_in into up to ks_max slices
+// and write one partial plane per slice, plane k at H + k * hp_stride; the
+// expand given the same (ks_max, hp_stride) and entries sums them.
 hipError_t launch_shrink_mfma(const OpLaunch& o, const void* X, int64_t ldx, float* H,
-                              int64_t ldh, hipStream_t s);
+                              int64_t ldh, int32_t ks_max, int64_t hp_stride, hipStream_t s);
 // Y[t] += s H[t, :r] B^T over entries (bf16 weights, matrix cores, hi/lo split of H)
-hipError_t launch_expand_mfma(const OpLaunch& o, const float* H, int64_t ldh, void* Y,
-                              lora_dtype y_dtype, int64_t ldy, hipStream_t s);
+hipError_t launch_expand_mfma(const OpLaunch& o, const float* H, int64_t ldh, int32_t ks_max,
+                              int64_t hp_stride, void* Y, lora_dtype y_dtype, int64_t ldy,
+                              hipStream_t s);
 // fused small-group kernel: shrink into LDS + expand, entries [first, count)
 hipError_t launch_bgmv_mfma(const OpLaunch& o, const void* X, int64_t ldx, void* Y,
                             lora_dtype y_dtype, int64_t ldy, int32_t n_chunks, hipStream_t s);
