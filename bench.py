@@ -328,13 +328,13 @@ def cpu_baseline(case, seconds):
                        f"plan + float64 residual, {el:.1f} s")
 
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_bgmv.fused_small_kernel.hbm_counters.txt")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_bgmv.lora_apply.hbm_counters.txt")
 
 
 def traffic_for(result):
-    """HBM bytes per launch of the headline kernel from the committed rocprofv3
-    counter summary, if its counters were taken on the current kernel sources;
-    otherwise None."""
+    """HBM bytes per call of the headline op (the sum over its kernels) from the
+    committed rocprofv3 counter summary, if its counters were taken on the
+    current kernel sources; otherwise None."""
     if not os.path.exists(TRAFFIC_FILE):
         return None
     kv = {}
@@ -377,7 +377,8 @@ def main():
     calib = calib_copy() if args.calib_copy else None
     h = results[HEADLINE]
     traffic = traffic_for(h)
-    roof = dict(bound="hbm", kernel="fused_small_kernel (lora_apply, decode)",
+    roof = dict(bound="hbm",
+                kernel="lora_apply on the decode batch (small_shrink_kernel + small_expand_kernel)",
                 achieved=round(h["op_GBps"], 1), peak=HBM_PEAK_GBS, unit="GB/s",
                 frac=round(h["op_hbm_frac"], 4), traffic=traffic,
                 bytes_per_launch=h["op_bytes"], avg_launch_us=round(h["op_us_mean"], 3))

@@ -179,9 +179,12 @@ lora_status lora_shrink(const lora_plan* p, const void* X, lora_dtype x_dtype, i
 lora_status lora_expand(const lora_plan* p, const float* H, int64_t ldh, void* Y,
                         lora_dtype y_dtype, int64_t ldy, void* stream);
 /* lora_apply: shrink and expand in one call, Y[t] += s_a (X[t] A_a^T) B_a^T.
- * Small adapter groups (decode rows) run in one fused kernel that keeps H on
- * chip; larger groups (prefill segments) run a grouped matrix-core shrink and
- * expand through the workspace.  ws: device, lora_apply_workspace_bytes(p). */
+ * Small adapter groups (decode rows) run either a shrink per d-slice plus an
+ * expand, with partial H in the workspace (d_in >= 1024), or one fused kernel
+ * that keeps H on chip; larger groups (prefill segments) run a grouped
+ * matrix-core shrink and expand through the workspace.  ws: device,
+ * lora_apply_workspace_bytes(p) bytes, 16-byte aligned; it may be NULL only
+ * when every group is small (the fused kernel then runs). */
 size_t      lora_apply_workspace_bytes(const lora_plan* p);
 lora_status lora_apply(const lora_plan* p, const void* X, lora_dtype x_dtype, int64_t ldx,
                        void* Y, lora_dtype y_dtype, int64_t ldy, void* ws, size_t ws_bytes,

@@ -503,11 +503,38 @@ lora_status lora_expand(const lora_plan* p, const float* H, int64_t ldh, void* Y
 }
 
 // Apply workspace: the float32 H of every row, once per d-slice of the grouped
-// shrink (the vector path uses one plane).
-size_t lora_apply_workspace_bytes(const lora_plan* p) {
-  if (p == nullptr) return 0;
+// shrink (the vector path uses one plane), then the partial planes of the split
+// small-group path.
+size_t apply_h_bytes(const lora_plan* p) {
   const int64_t ldh = (std::max(p->r_max, 1) + 7) / 8 * 8;
   return al256((size_t)std::max(p->n, 1) * ldh * 4) * lora::SHRINK_KS_MAX;
+}
+size_t apply_split_bytes(const lora_plan* p) {
+  // rank padding of the planes: the kernels' 16-column tile count, 1, 2, 4 or 8
+  const int nt = (std::max(p->r_max, 1) + 15) / 16;
+  const int64_t ldp = 16 * (nt <= 1 ? 1 : nt <= 2 ? 2 : nt <= 4 ? 4 : 8);
+  return al256((size_t)lora::SPLIT_SLICES_MAX * std::max(ub_small(p), 1) * 16 * ldp * 4);
+}
+size_t lora_apply_workspace_bytes(const lora_plan* p) {
+  if (p == nullptr) return 0;
+  return apply_h_bytes(p) + apply_split_bytes(p);
+}
+
+// Small groups take the split path (shrink per d-slice, then expand) unless
+// d_in is short: the fused kernel saves a launch, but each of its P sibling
+// workgroups (column chunks) reads all of A, which dominates once A is large.
+// The split path measured faster on the 4096-wide decode batch and on the
+// skewed mixed batch.  LORA_SMALL_SPLIT=0/1 forces either path.  Four
+// d-slices (of at least 256 columns) measured best on both.
+bool small_split_policy(const lora_plan* p) {
+  const int v = env_int("LORA_SMALL_SPLIT", -1);
+  if (v >= 0) return v != 0;
+  return p->table->d_in >= 1024;
+}
+int32_t small_split_slices(const lora_plan* p) {
+  const int v = env_int("LORA_SPLIT_SLICES", 0);
+  const int sl = v > 0 ? v : std::min(4, p->table->d_in / 256);
+  return std::max(1, std::min(lora::SPLIT_SLICES_MAX, sl));
 }
 
 lora_status lora_apply(const lora_plan* p, const void* X, lora_dtype x_dtype, int64_t ldx, void* Y,
@@ -545,8 +572,17 @@ lora_status lora_apply(const lora_plan* p, const void* X, lora_dtype x_dtype, in
     o.count_word = lora::HDR_NSMALL;
     o.first_word = -1;
     o.rb_ub = ub_small(p);
-    e = lora::launch_bgmv_mfma(o, X, ldx, Y, y_dtype, ldy, small_chunks_policy(t->d_out), s);
-    if (e != hipSuccess) return hip_fail(e, "fused small-group launch");
+    // (the split path needs the workspace; without a usable one the fused
+    // kernel runs)
+    if (ws != nullptr && ws_bytes >= need && aligned(ws, 16) && small_split_policy(p)) {
+      float* part = reinterpret_cast<float*>(static_cast<char*>(ws) + apply_h_bytes(p));
+      e = lora::launch_small_split_mfma(o, X, ldx, Y, y_dtype, ldy, small_chunks_policy(t->d_out),
+                                        small_split_slices(p), part, s);
+      if (e != hipSuccess) return hip_fail(e, "split small-group launch");
+    } else {
+      e = lora::launch_bgmv_mfma(o, X, ldx, Y, y_dtype, ldy, small_chunks_policy(t->d_out), s);
+      if (e != hipSuccess) return hip_fail(e, "fused small-group launch");
+    }
   } else {
     o.count_word = lora::HDR_NRB_TOTAL;
     o.first_word = -1;

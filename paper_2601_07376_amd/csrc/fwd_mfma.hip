@@ -853,6 +853,169 @@ __global__ __launch_bounds__(FW * 64) void fused_small_kernel(FwdArgs p) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Split small-group path, for small groups whose weights are large: the fused
+// kernel's sibling workgroups each re-read the whole of A, which then
+// dominates.  Here the shrink runs per (record, d-slice) and reads A once,
+// writing partial H planes to the workspace; the expand runs per (record,
+// column chunk), sums the planes in slice order and applies B as the fused
+// kernel does.
+//
+// Partial planes: plane sl at p.H + sl * p.hp_stride, record e's 16 x p.ldh
+// floats at e * 16 * p.ldh (rows and rank columns past the record's are
+// don't-care values, never used).
+// ---------------------------------------------------------------------------
+constexpr int SPLIT_SMAX = 8;     // most d-slices of the split shrink
+
+template <int NT, int U>
+__global__ __launch_bounds__(256) void small_shrink_kernel(FwdArgs p) {
+  __shared__ f32x4 s_red[2 * NT * 64];
+  const int lane = threadIdx.x & 63, w = wave_id();
+  const int mrow = lane & 15;
+  const int S = p.ks_max;
+  const int e = (int)blockIdx.x / S, sl = (int)blockIdx.x - e * S;
+  const int er = min(e, p.n_rec - 1);
+  const int4 h0 = *reinterpret_cast<const int4*>(p.srec + er);
+  const int4 h1 = *(reinterpret_cast<const int4*>(p.srec + er) + 1);
+  const int trow = ldg(&p.srec[er].row[mrow]);
+  const int count = p.hdr[p.count_word];
+  if (e >= count) return;
+  const void* Ap = uni_ptr(reinterpret_cast<const void*>(
+      (uint64_t)(uint32_t)h0.x | ((uint64_t)(uint32_t)h0.y << 32)));
+  const int r = uni(h1.y);
+  const rsrc_t A = make_rsrc(Ap, (uint32_t)r * (uint32_t)p.d_in * 2u);
+  int kb, ke;
+  kslice(p.d_in, S, sl, kb, ke);
+
+  f32x4 acc[NT];
+#pragma unroll
+  for (int i = 0; i < NT; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const uint16_t* xrow[1] = {p.X + (int64_t)trow * p.ldx};
+  uint32_t arow[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int j = nt * 16 + mrow;
+    arow[nt] = (uint32_t)(j < r ? j : r - 1) * (uint32_t)p.d_in;
+  }
+  shrink_steps<1, NT, U>(acc, xrow, A, arow, kb + w * 32, 128, ke);
+  reduce_waves<NT>(acc, s_red);
+  if (w == 0) {
+    float* Hp = p.H + (int64_t)sl * p.hp_stride + (int64_t)e * 16 * p.ldh;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) stg(Hp + ((lane >> 4) * 4 + v) * p.ldh + nt * 16 + mrow, acc[nt][v]);
+  }
+}
+
+template <bool YBF16, int NT, bool RANK8>
+__global__ __launch_bounds__(FW * 64) void small_expand_kernel(FwdArgs p) {
+  constexpr int KSM = (NT * 16 + 31) / 32;
+  constexpr int LDH = NT * 16;                // row stride of the partial planes
+  constexpr bool B_AHEAD = KSM <= 2;          // B of every slice requested up front
+  __shared__ __align__(16) float s_p[SPLIT_SMAX * 16 * LDH];
+  const int lane = threadIdx.x & 63, w = wave_id();
+  const int og = lane >> 4, mrow = lane & 15;
+  const int P = p.n_chunks, S = p.ks_max;
+  // siblings (same record, different column chunk) share blockIdx % 8, i.e. one XCD
+  const int slot = (int)(blockIdx.x >> 3);
+  const int e = 8 * (slot / P) + (int)(blockIdx.x & 7);
+  const int pc = slot % P;
+  const int er = min(e, p.n_rec - 1);
+  const int4 h0 = *reinterpret_cast<const int4*>(p.srec + er);
+  const int4 h1 = *(reinterpret_cast<const int4*>(p.srec + er) + 1);
+  const int trow = ldg(&p.srec[er].row[mrow]);
+  const int count = p.hdr[p.count_word];
+  if (e >= count) return;
+  const void* Bp = uni_ptr(reinterpret_cast<const void*>(
+      (uint64_t)(uint32_t)h0.z | ((uint64_t)(uint32_t)h0.w << 32)));
+  const int rows = uni(h1.x), r = uni(h1.y);
+  const float s = __int_as_float(uni(h1.z));
+  const rsrc_t Bw = make_rsrc(Bp, (uint32_t)p.d_out * (uint32_t)r * 2u);
+  const bool rv = mrow < rows;
+  const int c0 = pc * p.chunk;
+  const int c1 = min(p.d_out, c0 + p.chunk);
+
+  // ---- the record's partial planes into LDS, every piece in one round trip
+  {
+    const int n4 = S * 16 * LDH / 4;
+    const float4* src = reinterpret_cast<const float4*>(p.H + (int64_t)e * 16 * LDH);
+    for (int i = threadIdx.x; i < n4; i += FW * 64) {
+      const int pl = i / (16 * LDH / 4), q = i - pl * (16 * LDH / 4);
+      reinterpret_cast<float4*>(s_p)[i] = ldg_f4(reinterpret_cast<const float*>(
+          src + (int64_t)pl * (p.hp_stride / 4) + q));
+    }
+  }
+  // ---- B (ranks up to 64) and Y of this wave's column slices
+  bf16x8 bo_ahead[B_AHEAD ? FSL : 1][B_AHEAD ? KSM : 1][4];
+  if (B_AHEAD) {
+#pragma unroll
+    for (int sl = 0; sl < FSL; ++sl) {
+      const int o_w = c0 + 64 * (w + FW * sl);
+#pragma unroll
+      for (int ks = 0; ks < KSM; ++ks)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int o = out_col(o_w, q, mrow);
+          bo_ahead[B_AHEAD ? sl : 0][B_AHEAD ? ks : 0][q] =
+              wrow8<RANK8>(Bw, (uint32_t)(o < c1 ? o : c1 - 1) * r, ks * 32 + og * 8, r);
+        }
+    }
+  }
+  YFrag<YBF16> yf[FSL];
+#pragma unroll
+  for (int sl = 0; sl < FSL; ++sl)
+    y_load<YBF16>(yf[sl], p.Y, p.ldy, trow, c0 + 64 * (w + FW * sl), og, c1);
+  __syncthreads();
+
+  // ---- H = sum of the planes in slice order, as hi / lo operands
+  bf16x8 hh[KSM], hl[KSM];
+#pragma unroll
+  for (int ks = 0; ks < KSM; ++ks) {
+    float h[8];
+    const int j = ks * 32 + og * 8;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) h[i] = 0.0f;
+    if (j < LDH) {
+      for (int pl = 0; pl < S; ++pl) {
+        const float* row = s_p + (pl * 16 + mrow) * LDH + j;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) h[i] += row[i];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) h[i] = (rv && j + i < r) ? h[i] : 0.0f;
+    split_hi_lo(h, hh[ks], hl[ks]);
+  }
+
+  // ---- expand over this wave's column slices
+#pragma unroll
+  for (int sl = 0; sl < FSL; ++sl) {
+    const int o_w = c0 + 64 * (w + FW * sl);
+    f32x4 acc2[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) acc2[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KSM; ++ks) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        bf16x8 bo;
+        if (B_AHEAD) {
+          bo = bo_ahead[B_AHEAD ? sl : 0][B_AHEAD ? ks : 0][q];
+        } else {
+          const int o = out_col(o_w, q, mrow);
+          bo = wrow8<RANK8>(Bw, (uint32_t)(o < c1 ? o : c1 - 1) * r, ks * 32 + og * 8, r);
+        }
+        bo = sel(ks * 32 + og * 8 < r, bo);
+        acc2[q] = mfma_16x16x32(bo, hh[ks], acc2[q]);
+        acc2[q] = mfma_16x16x32(bo, hl[ks], acc2[q]);
+      }
+    }
+    mfma_fence();
+    if (rv && o_w < c1) y_store<YBF16>(yf[sl], p.Y, p.ldy, trow, o_w, og, c1, s, acc2);
+  }
+}
+
 template <typename K>
 hipError_t launch(K kernel, int grid, const FwdArgs& a, hipStream_t s, int threads = 256) {
   if (grid <= 0) return hipSuccess;
@@ -946,6 +1109,51 @@ hipError_t launch_expand_mfma(const OpLaunch& o, const float* H, int64_t ldh, in
   if (yb) return launch_expand_ks<true, false>(o, grid, a, s);
   if (o.rank8) return launch_expand_ks<false, true>(o, grid, a, s);
   return launch_expand_ks<false, false>(o, grid, a, s);
+}
+
+template <bool YB, bool R8>
+hipError_t launch_small_expand_nt(const OpLaunch& o, int grid, const FwdArgs& a, hipStream_t s) {
+  const int nt = (o.r_max + 15) / 16;
+  constexpr int T = FW * 64;
+  if (nt <= 1) return launch(small_expand_kernel<YB, 1, R8>, grid, a, s, T);
+  if (nt <= 2) return launch(small_expand_kernel<YB, 2, R8>, grid, a, s, T);
+  if (nt <= 4) return launch(small_expand_kernel<YB, 4, R8>, grid, a, s, T);
+  return launch(small_expand_kernel<YB, 8, R8>, grid, a, s, T);
+}
+
+hipError_t launch_small_split_mfma(const OpLaunch& o, const void* X, int64_t ldx, void* Y,
+                                   lora_dtype y_dtype, int64_t ldy, int32_t n_chunks,
+                                   int32_t slices, float* part, hipStream_t s) {
+  FwdArgs a = base_args(o);
+  a.X = reinterpret_cast<const uint16_t*>(X);
+  a.ldx = ldx;
+  a.Y = Y;
+  a.ldy = ldy;
+  a.srec = o.srec;
+  a.n_rec = std::max(o.rb_ub, 1);
+  const int nt = (o.r_max + 15) / 16;
+  const int tiles = nt <= 1 ? 1 : nt <= 2 ? 2 : nt <= 4 ? 4 : 8;
+  a.H = part;
+  a.ldh = tiles * 16;
+  a.ks_max = std::min(std::max(slices, 1), SPLIT_SMAX);
+  a.hp_stride = (int64_t)a.n_rec * 16 * a.ldh;
+  const int g1 = a.n_rec * a.ks_max;
+  hipError_t e;
+  if (tiles == 1) e = launch(small_shrink_kernel<1, 4>, g1, a, s);
+  else if (tiles == 2) e = launch(small_shrink_kernel<2, 4>, g1, a, s);
+  else if (tiles == 4) e = launch(small_shrink_kernel<4, 2>, g1, a, s);
+  else e = launch(small_shrink_kernel<8, 1>, g1, a, s);
+  if (e != hipSuccess) return e;
+  constexpr int CW = 64 * FW * FSL;
+  const int P = std::max({1, n_chunks, (o.d_out + CW - 1) / CW});
+  a.n_chunks = P;
+  a.chunk = ((o.d_out + P - 1) / P + 63) / 64 * 64;
+  const int grid = 8 * P * ((o.rb_ub + 7) / 8);
+  const bool yb = y_dtype == LORA_BF16;
+  if (yb && o.rank8) return launch_small_expand_nt<true, true>(o, grid, a, s);
+  if (yb) return launch_small_expand_nt<true, false>(o, grid, a, s);
+  if (o.rank8) return launch_small_expand_nt<false, true>(o, grid, a, s);
+  return launch_small_expand_nt<false, false>(o, grid, a, s);
 }
 
 hipError_t launch_bgmv_mfma(const OpLaunch& o, const void* X, int64_t ldx, void* Y,

@@ -140,6 +140,15 @@ hipError_t launch_expand_mfma(const OpLaunch& o, const float* H, int64_t ldh, in
 hipError_t launch_bgmv_mfma(const OpLaunch& o, const void* X, int64_t ldx, void* Y,
                             lora_dtype y_dtype, int64_t ldy, int32_t n_chunks, hipStream_t s);
 
+// split small-group path: shrink per (record, d-slice) into partial planes
+// (part: SPLIT_SLICES_MAX x records x 16 x 16 t floats, t = 1, 2, 4 or 8 the
+// rank tiles of r_max), then expand
+// per (record, column chunk)
+constexpr int SPLIT_SLICES_MAX = 8;
+hipError_t launch_small_split_mfma(const OpLaunch& o, const void* X, int64_t ldx, void* Y,
+                                   lora_dtype y_dtype, int64_t ldy, int32_t n_chunks,
+                                   int32_t slices, float* part, hipStream_t s);
+
 // vector-ALU kernels for any mix of f32 / bf16 storage
 hipError_t launch_shrink_valu(const OpLaunch& o, const void* X, lora_dtype x_dtype,
                               int64_t ldx, lora_dtype w_dtype, float* H, int64_t ldh,

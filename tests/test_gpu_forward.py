@@ -151,3 +151,32 @@ def test_fp32_tiny_workload_all_entry_points():
     case = workloads.make_config(1)
     Yo, plan = run_apply(case, segments=True)
     check_forward(case, Yo, effective(case))
+
+
+SMALL_PATH_CASES = ["decode_r16", "decode_hetero", "odd_ranks", "segments_mixed", "rank128"]
+
+
+@pytest.mark.parametrize("path", ["fused", "split1", "split3", "split8"])
+@pytest.mark.parametrize("name", SMALL_PATH_CASES)
+def test_apply_small_group_paths(name, path):
+    """Both small-group paths (the fused kernel, and the split shrink per d-slice
+    + expand with 1, 3 or 8 slices) against the oracle."""
+    kw = next(f[1] for f in FUZZ if f[0] == name)
+    say(f"apply small path {path} {name}")
+    case = workloads.random_case(12, y_dtype="f32", **kw)
+    split = "0" if path == "fused" else "1"
+    slices = None if path == "fused" else path[5:]
+    with env(LORA_SMALL_SPLIT=split, LORA_SPLIT_SLICES=slices):
+        Yo, _ = run_apply(case)
+    check_forward(case, Yo, effective(case))
+
+
+@pytest.mark.parametrize("path", ["fused", "split"])
+@pytest.mark.parametrize("cfg", [2, 4])
+def test_apply_configs_both_small_paths(cfg, path):
+    say(f"apply config {cfg} small path {path}")
+    case = workloads.make_config(cfg, y_dtype="bf16")
+    with env(LORA_SMALL_SPLIT="0" if path == "fused" else "1"):
+        Yo, _ = run_apply(case)
+    rel, mx = check_forward(case, Yo, effective(case))
+    say(f"  relF {rel:.3g} maxabs {mx:.3g}")
