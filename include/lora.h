@@ -131,8 +131,11 @@ void        lora_table_destroy(lora_table* t);
  * nonzero = the row's target token is trainable.  The explicit mask is kept
  * apart from the learning signal (Section 3.3): a trainable row whose dY is zero
  * still counts.  The table, idx, mask and ws must stay valid until every op
- * using the plan has finished.  Errors: NULL, SHAPE (n not in [0,
- * LORA_MAX_ROWS]), ALIGN, WORKSPACE, HIP. */
+ * using the plan has finished.  A plan records the table's slot contents
+ * (weight pointers, ranks, scales) as uploaded when it is built: after
+ * lora_table_set / lora_table_clear + lora_table_upload, build the plan again
+ * before using it.  Errors: NULL, SHAPE (n not in [0, LORA_MAX_ROWS]), ALIGN,
+ * WORKSPACE, HIP. */
 size_t      lora_plan_workspace_bytes(int32_t n, int32_t num_slots);
 lora_status lora_plan_build(const lora_table* t, int32_t n, const int32_t* idx,
                             const uint8_t* mask, void* ws, size_t ws_bytes, void* stream,

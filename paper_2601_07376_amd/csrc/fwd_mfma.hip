@@ -926,6 +926,18 @@ __global__ __launch_bounds__(FW * 64) void small_expand_kernel(FwdArgs p) {
   const int4 h1 = *(reinterpret_cast<const int4*>(p.srec + er) + 1);
   const int trow = ldg(&p.srec[er].row[mrow]);
   const int count = p.hdr[p.count_word];
+  // the record's partial planes depend on e alone: requested in the same
+  // round trip as the record (clamped, unconditional; stored to LDS below)
+  constexpr int PQ = (SPLIT_SMAX * 16 * LDH / 4 + FW * 64 - 1) / (FW * 64);
+  const int n4 = S * 16 * LDH / 4;
+  float4 pv[PQ];
+#pragma unroll
+  for (int u = 0; u < PQ; ++u) {
+    int i = (int)threadIdx.x + u * FW * 64;
+    i = i < n4 ? i : n4 - 1;
+    const int pl = i / (16 * LDH / 4), q = i - pl * (16 * LDH / 4);
+    pv[u] = ldg_f4(p.H + (int64_t)pl * p.hp_stride + (int64_t)er * 16 * LDH + 4 * q);
+  }
   if (e >= count) return;
   const void* Bp = uni_ptr(reinterpret_cast<const void*>(
       (uint64_t)(uint32_t)h0.z | ((uint64_t)(uint32_t)h0.w << 32)));
@@ -936,15 +948,11 @@ __global__ __launch_bounds__(FW * 64) void small_expand_kernel(FwdArgs p) {
   const int c0 = pc * p.chunk;
   const int c1 = min(p.d_out, c0 + p.chunk);
 
-  // ---- the record's partial planes into LDS, every piece in one round trip
-  {
-    const int n4 = S * 16 * LDH / 4;
-    const float4* src = reinterpret_cast<const float4*>(p.H + (int64_t)e * 16 * LDH);
-    for (int i = threadIdx.x; i < n4; i += FW * 64) {
-      const int pl = i / (16 * LDH / 4), q = i - pl * (16 * LDH / 4);
-      reinterpret_cast<float4*>(s_p)[i] = ldg_f4(reinterpret_cast<const float*>(
-          src + (int64_t)pl * (p.hp_stride / 4) + q));
-    }
+  // ---- the partial planes into LDS
+#pragma unroll
+  for (int u = 0; u < PQ; ++u) {
+    const int i = (int)threadIdx.x + u * FW * 64;
+    if (i < n4) reinterpret_cast<float4*>(s_p)[i] = pv[u];
   }
   // ---- B (ranks up to 64) and Y of this wave's column slices
   bf16x8 bo_ahead[B_AHEAD ? FSL : 1][B_AHEAD ? KSM : 1][4];
