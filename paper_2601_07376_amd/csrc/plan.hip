@@ -371,7 +371,7 @@ __global__ __launch_bounds__(PLAN_THREADS) void plan_kernel(PlanLaunch a) {
 constexpr int SEG_STAGE = 4096;   // LDS words for the segment table
 
 // Exclusive scan of N values per thread over the block; total[i] = sum.
-template <int N>
+template <int N, int WV = PLAN_WAVES>
 __device__ __forceinline__ void block_scan_n(int (&v)[N], int (&total)[N],
                                              int (*s_w)[PLAN_WAVES]) {
   const int lane = threadIdx.x & 63, w = wave_id();
@@ -384,15 +384,18 @@ __device__ __forceinline__ void block_scan_n(int (&v)[N], int (&total)[N],
   __syncthreads();
 #pragma unroll
   for (int i = 0; i < N; ++i) {
-    const int c = row_incl_scan(lane < PLAN_WAVES ? s_w[i][lane] : 0);   // lanes 0..15
-    total[i] = lane_value(c, PLAN_WAVES - 1);
+    const int c = row_incl_scan(lane < WV ? s_w[i][lane] : 0);   // lanes 0..WV-1
+    total[i] = lane_value(c, WV - 1);
     v[i] = lane_value(c, w) - lane_value(x[i], 63) + x[i] - v[i];
   }
   __syncthreads();
 }
 
-template <bool MASKED, bool SEG>
-__global__ __launch_bounds__(PLAN_THREADS) void plan_small_kernel(PlanLaunch a) {
+// T threads (T / 64 waves, at most 16); n <= T and num_slots <= T.  The
+// per-(adapter, wave) counters keep a stride of 16 waves.
+template <bool MASKED, bool SEG, int T>
+__global__ __launch_bounds__(T) void plan_small_kernel(PlanLaunch a) {
+  constexpr int WV = T / 64;
   __shared__ int s_rank[LORA_MAX_SLOTS];
   __shared__ unsigned short s_wc[LORA_MAX_SLOTS * PLAN_WAVES];    // [adapter][wave]
   __shared__ unsigned short s_wcm[MASKED ? LORA_MAX_SLOTS * PLAN_WAVES : 1];
@@ -402,7 +405,7 @@ __global__ __launch_bounds__(PLAN_THREADS) void plan_small_kernel(PlanLaunch a) 
   __shared__ int s_moff[MASKED ? LORA_MAX_SLOTS : 1];
   __shared__ int s_sbase[LORA_MAX_SLOTS];
   __shared__ int s_seg[SEG ? SEG_STAGE : 1];
-  __shared__ int s_efirst[PLAN_WAVES], s_elast[PLAN_WAVES];
+  __shared__ int s_efirst[WV], s_elast[WV];
   __shared__ int s_w[7][PLAN_WAVES];
   __shared__ unsigned s_flags;
 
@@ -418,11 +421,11 @@ __global__ __launch_bounds__(PLAN_THREADS) void plan_small_kernel(PlanLaunch a) 
   if (!SEG) {
     if (tid < n) raw = a.idx[tid];
   } else {
-    for (int i = tid; i <= ns; i += PLAN_THREADS) s_seg[i] = a.seg_offsets[i];
-    for (int i = tid; i < ns; i += PLAN_THREADS) s_seg[ns + 1 + i] = a.seg_adapter[i];
+    for (int i = tid; i <= ns; i += T) s_seg[i] = a.seg_offsets[i];
+    for (int i = tid; i < ns; i += T) s_seg[ns + 1 + i] = a.seg_adapter[i];
   }
   if (MASKED && tid < n) mk = a.mask[tid];
-  for (int i = tid; i < S * PLAN_WAVES; i += PLAN_THREADS) {
+  for (int i = tid; i < S * PLAN_WAVES; i += T) {
     s_wc[i] = 0;
     if (MASKED) s_wcm[i] = 0;
   }
@@ -432,7 +435,7 @@ __global__ __launch_bounds__(PLAN_THREADS) void plan_small_kernel(PlanLaunch a) 
   uint32_t flags = 0u;
   if (SEG) {
     bool bad = false;
-    for (int i = tid; i <= ns; i += PLAN_THREADS) {
+    for (int i = tid; i <= ns; i += T) {
       const int o = s_seg[i];
       if (i == 0 && o != 0) bad = true;
       if (i == ns && o != n) bad = true;
@@ -481,7 +484,7 @@ __global__ __launch_bounds__(PLAN_THREADS) void plan_small_kernel(PlanLaunch a) 
   __syncthreads();
 
   // ---- 3. cursors (exclusive prefix over waves) and run boundaries
-  for (int k0 = 0; k0 < S * PLAN_WAVES; k0 += PLAN_THREADS) {
+  for (int k0 = 0; k0 < S * PLAN_WAVES; k0 += T) {
     const int k = k0 + tid;
     const bool act = k < S * PLAN_WAVES;
     const int v = act ? (int)s_wc[k] : 0;
@@ -500,7 +503,7 @@ __global__ __launch_bounds__(PLAN_THREADS) void plan_small_kernel(PlanLaunch a) 
     }
   }
   const int ep = lane_prev(e, w > 0 ? s_elast[w - 1] : -1);
-  const int en = lane_next(e, w + 1 < PLAN_WAVES ? s_efirst[w + 1] : -1);
+  const int en = lane_next(e, w + 1 < WV ? s_efirst[w + 1] : -1);
   const bool st = e >= 0 && ep != e;
   const bool ed = e >= 0 && en != e;
   __syncthreads();
@@ -515,7 +518,7 @@ __global__ __launch_bounds__(PLAN_THREADS) void plan_small_kernel(PlanLaunch a) 
   const int nbm = live ? (mcnt + MRB_ROWS - 1) / MRB_ROWS : 0;
   int v[7] = {cnt, mcnt, nbl, nbs, nbm, st ? 1 : 0, ed ? 1 : 0};
   int tot[7];
-  block_scan_n<7>(v, tot, s_w);
+  block_scan_n<7, WV>(v, tot, s_w);
   const int off = v[0], moff = v[1], pl = v[2], ps = v[3], pm = v[4];
   if (live) {
     d.counts[tid] = cnt;
@@ -889,14 +892,20 @@ hipError_t launch_plan(const PlanLaunch& a, hipStream_t s) {
   const bool seg = a.seg_offsets != nullptr;
   if (a.n <= PLAN_THREADS && (!seg || 2 * a.num_segs + 1 <= SEG_STAGE)) {
     const bool m = a.mask != nullptr;
-    if (m && seg)
-      hipLaunchKernelGGL((plan_small_kernel<true, true>), dim3(1), dim3(PLAN_THREADS), 0, s, a);
-    else if (m)
-      hipLaunchKernelGGL((plan_small_kernel<true, false>), dim3(1), dim3(PLAN_THREADS), 0, s, a);
-    else if (seg)
-      hipLaunchKernelGGL((plan_small_kernel<false, true>), dim3(1), dim3(PLAN_THREADS), 0, s, a);
-    else
-      hipLaunchKernelGGL((plan_small_kernel<false, false>), dim3(1), dim3(PLAN_THREADS), 0, s, a);
+    // a quarter of the threads (fewer waves at every barrier and scan) when
+    // the rows and the slots fit
+    if (a.n <= 256 && a.num_slots <= 256) {
+      if (m && seg) hipLaunchKernelGGL((plan_small_kernel<true, true, 256>), dim3(1), dim3(256), 0, s, a);
+      else if (m) hipLaunchKernelGGL((plan_small_kernel<true, false, 256>), dim3(1), dim3(256), 0, s, a);
+      else if (seg) hipLaunchKernelGGL((plan_small_kernel<false, true, 256>), dim3(1), dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((plan_small_kernel<false, false, 256>), dim3(1), dim3(256), 0, s, a);
+      return hipGetLastError();
+    }
+    constexpr int T = PLAN_THREADS;
+    if (m && seg) hipLaunchKernelGGL((plan_small_kernel<true, true, T>), dim3(1), dim3(T), 0, s, a);
+    else if (m) hipLaunchKernelGGL((plan_small_kernel<true, false, T>), dim3(1), dim3(T), 0, s, a);
+    else if (seg) hipLaunchKernelGGL((plan_small_kernel<false, true, T>), dim3(1), dim3(T), 0, s, a);
+    else hipLaunchKernelGGL((plan_small_kernel<false, false, T>), dim3(1), dim3(T), 0, s, a);
     return hipGetLastError();
   }
   if (a.d.chunks > 0 && (!seg || 2 * a.num_segs + 1 <= SEG_STAGE)) {
