@@ -170,7 +170,10 @@ void        lora_plan_destroy(lora_plan* p);
  * intermediate H = X A_a^T is kept in float32 (split into two bfloat16 terms
  * when it feeds a bfloat16 matrix product); s_a is applied once to the float32
  * accumulator; a bfloat16 Y is rounded to nearest even once, at the store.
- * Rows with id -1 are neither read nor written. */
+ * Rows with id -1 are neither read nor written.  Row-indexed matrices (X, Y,
+ * H, dY, H_saved) are device pointers with leading dimension a multiple of 8
+ * and 16-byte alignment; for a plan with n = 0 they are never touched and may
+ * be NULL.  Errors: NULL, DTYPE, SHAPE, ALIGN, WORKSPACE, HIP. */
 
 /* lora_shrink (gather + shrink): H[t, 0:r_a] = X[t, :] A_a^T (unscaled) for
  * every row t with id a >= 0.  H is float32 [n, ldh], ldh >= max rank over the

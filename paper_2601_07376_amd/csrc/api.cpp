@@ -118,8 +118,10 @@ lora::OpLaunch op_base(const lora_plan* p) {
   return o;
 }
 
+// rows == 0: the matrix is never touched and may be NULL
 lora_status check_matrix(const void* ptr, lora_dtype dt, int64_t ld, int32_t cols,
-                         const char* name) {
+                         const char* name, int32_t rows = 1) {
+  if (ptr == nullptr && rows == 0) return valid_dtype(dt) ? LORA_OK : fail(LORA_ERR_DTYPE, "%s: unknown dtype %d", name, (int)dt);
   if (ptr == nullptr) return fail(LORA_ERR_NULL, "%s is NULL", name);
   if (!valid_dtype(dt)) return fail(LORA_ERR_DTYPE, "%s: unknown dtype %d", name, (int)dt);
   if (ld < cols) return fail(LORA_ERR_SHAPE, "%s: leading dim %lld < %d", name, (long long)ld, cols);
@@ -463,8 +465,8 @@ lora_status lora_shrink(const lora_plan* p, const void* X, lora_dtype x_dtype, i
   lora_status st = check_plan(p);
   if (st != LORA_OK) return st;
   const lora_table* t = p->table;
-  if ((st = check_matrix(X, x_dtype, ldx, t->d_in, "X")) != LORA_OK) return st;
-  if ((st = check_matrix(H, LORA_F32, ldh, std::max(p->r_max, 1), "H")) != LORA_OK) return st;
+  if ((st = check_matrix(X, x_dtype, ldx, t->d_in, "X", p->n)) != LORA_OK) return st;
+  if ((st = check_matrix(H, LORA_F32, ldh, std::max(p->r_max, 1), "H", p->n)) != LORA_OK) return st;
   if (p->n == 0) return ok();
   lora::OpLaunch o = op_base(p);
   o.count_word = lora::HDR_NRB_TOTAL;
@@ -485,8 +487,8 @@ lora_status lora_expand(const lora_plan* p, const float* H, int64_t ldh, void* Y
   lora_status st = check_plan(p);
   if (st != LORA_OK) return st;
   const lora_table* t = p->table;
-  if ((st = check_matrix(H, LORA_F32, ldh, std::max(p->r_max, 1), "H")) != LORA_OK) return st;
-  if ((st = check_matrix(Y, y_dtype, ldy, t->d_out, "Y")) != LORA_OK) return st;
+  if ((st = check_matrix(H, LORA_F32, ldh, std::max(p->r_max, 1), "H", p->n)) != LORA_OK) return st;
+  if ((st = check_matrix(Y, y_dtype, ldy, t->d_out, "Y", p->n)) != LORA_OK) return st;
   if (p->n == 0) return ok();
   lora::OpLaunch o = op_base(p);
   o.count_word = lora::HDR_NRB_TOTAL;
@@ -542,8 +544,8 @@ lora_status lora_apply(const lora_plan* p, const void* X, lora_dtype x_dtype, in
   lora_status st = check_plan(p);
   if (st != LORA_OK) return st;
   const lora_table* t = p->table;
-  if ((st = check_matrix(X, x_dtype, ldx, t->d_in, "X")) != LORA_OK) return st;
-  if ((st = check_matrix(Y, y_dtype, ldy, t->d_out, "Y")) != LORA_OK) return st;
+  if ((st = check_matrix(X, x_dtype, ldx, t->d_in, "X", p->n)) != LORA_OK) return st;
+  if ((st = check_matrix(Y, y_dtype, ldy, t->d_out, "Y", p->n)) != LORA_OK) return st;
   const size_t need = lora_apply_workspace_bytes(p);
   const bool mfma = x_dtype == LORA_BF16 && t->w_dtype == LORA_BF16;
   const bool needs_ws = !mfma || ub_large(p) > 0;
@@ -608,11 +610,11 @@ lora_status lora_grad(const lora_plan* p, const void* X, lora_dtype x_dtype, int
   lora_status st = check_plan(p);
   if (st != LORA_OK) return st;
   const lora_table* t = p->table;
-  if ((st = check_matrix(X, x_dtype, ldx, t->d_in, "X")) != LORA_OK) return st;
-  if ((st = check_matrix(dY, dy_dtype, lddy, t->d_out, "dY")) != LORA_OK) return st;
+  if ((st = check_matrix(X, x_dtype, ldx, t->d_in, "X", p->n)) != LORA_OK) return st;
+  if ((st = check_matrix(dY, dy_dtype, lddy, t->d_out, "dY", p->n)) != LORA_OK) return st;
   if (x_dtype != dy_dtype) return fail(LORA_ERR_DTYPE, "X and dY dtypes differ");
   if (H_saved != nullptr &&
-      (st = check_matrix(H_saved, LORA_F32, ldh, std::max(p->r_max, 1), "H_saved")) != LORA_OK)
+      (st = check_matrix(H_saved, LORA_F32, ldh, std::max(p->r_max, 1), "H_saved", p->n)) != LORA_OK)
     return st;
   for (int32_t a = 0; a < t->num_slots; ++a) {
     const float* pa = dA ? dA[a] : nullptr;

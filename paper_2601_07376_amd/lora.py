@@ -98,7 +98,11 @@ def _stream(stream):
 
 
 def _rowmajor(t, name):
-    if t.dim() != 2 or t.stride(1) != 1:
+    if t.dim() != 2:
+        raise ValueError(f"{name} must be a 2-D tensor")
+    if t.shape[0] == 0:                  # never touched: any valid leading dimension
+        return (t.shape[1] + 7) // 8 * 8
+    if t.stride(1) != 1:
         raise ValueError(f"{name} must be a 2-D tensor with unit column stride")
     return t.stride(0)
 

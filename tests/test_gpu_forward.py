@@ -180,3 +180,67 @@ def test_apply_configs_both_small_paths(cfg, path):
         Yo, _ = run_apply(case)
     rel, mx = check_forward(case, Yo, effective(case))
     say(f"  relF {rel:.3g} maxabs {mx:.3g}")
+
+
+def _permuted(case, perm):
+    """The same batch with its rows reordered: row i of the result is row perm[i]."""
+    import copy
+    c = copy.copy(case)
+    c.idx = case.idx[perm]
+    c.X = case.X[perm]
+    c.Y = case.Y[perm]
+    c.seg_offsets = c.seg_adapter = None
+    if case.mask is not None:
+        c.mask = case.mask[perm]
+    return c
+
+
+@pytest.mark.parametrize("cfg", [2, 4])
+def test_apply_row_permutation_invariance(cfg):
+    """Each row's result depends only on that row (grouping is by adapter
+    identity, Section 3.4): reordering the batch reorders the output rows, bit
+    for bit."""
+    say(f"row permutation invariance, config {cfg}")
+    case = workloads.make_config(cfg, y_dtype="bf16")
+    perm = np.random.default_rng(5).permutation(case.n)
+    y1, _ = run_apply(case)
+    y2, _ = run_apply(_permuted(case, perm))
+    assert y2.tobytes() == y1[perm].tobytes()
+
+
+def test_apply_adapter_isolation():
+    """Changing one adapter's weights changes no row of any other adapter."""
+    say("adapter isolation")
+    case = workloads.make_config(4, y_dtype="bf16")
+    eff = effective(case)
+    counts = np.bincount(eff[eff >= 0], minlength=case.num_slots)
+    b = int(np.argmax(counts))           # the busiest adapter (large-group path)
+    small = int(np.nonzero((counts > 0) & (counts <= 16))[0][0])   # and a small one
+    y1, _ = run_apply(case)
+    import copy
+    c2 = copy.copy(case)
+    rng = np.random.default_rng(9)
+    c2.A = list(case.A)
+    c2.B = list(case.B)
+    for a in (b, small):
+        c2.A[a] = workloads.encode(rng.standard_normal(case.A[a].shape), "bf16")
+        c2.B[a] = workloads.encode(rng.standard_normal(case.B[a].shape), "bf16")
+    y2, _ = run_apply(c2)
+    keep = (eff != b) & (eff != small)
+    assert y2[keep].tobytes() == y1[keep].tobytes()
+    assert y2[eff == b].tobytes() != y1[eff == b].tobytes()
+    check_forward(c2, y2, eff)
+
+
+def test_apply_empty_batch():
+    """n = 0: every entry point returns OK and touches nothing."""
+    say("empty batch")
+    case = workloads.random_case(3, 0, 128, 64, 4, rank_choices=(16,), y_dtype="f32")
+    dev = case_to_device(case, DEV)
+    table = make_table(case, dev)
+    plan = make_plan(case, dev, table, mask=False)
+    L.apply(plan, dev["X"], dev["Y"])
+    H = torch.zeros((0, 16), dtype=torch.float32, device=DEV)
+    L.shrink(plan, dev["X"], H)
+    L.expand(plan, H, dev["Y"])
+    torch.cuda.synchronize()

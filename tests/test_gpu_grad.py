@@ -157,3 +157,26 @@ def test_grad_fp32_vector_path():
                                  x_dtype="f32", w_dtype="f32", want_dy=True, want_y=False)
     dA, dB = run_grad(case)
     check_grads(case, dA, dB, effective(case), case.mask, tol=(1e-5, 1e-4))
+
+
+def test_grad_empty_batch():
+    """n = 0: overwrite mode gives exact zeros for every slot; accumulate mode
+    leaves the buffers as they were."""
+    say("grad empty batch")
+    case = workloads.random_case(7, 0, 128, 96, 3, rank_choices=(8, 16), want_dy=True,
+                                 want_y=False)
+    dev = case_to_device(case, DEV)
+    table = make_table(case, dev)
+    plan = make_plan(case, dev, table, mask=True)
+    t = plan.table
+    dA = [torch.full((r, t.d_in), 7.0, dtype=torch.float32, device=DEV) if r > 0 else None
+          for r in t.ranks]
+    dB = [torch.full((t.d_out, r), 7.0, dtype=torch.float32, device=DEV) if r > 0 else None
+          for r in t.ranks]
+    L.grad(plan, dev["X"], dev["dY"], dA=dA, dB=dB, accumulate=True)
+    torch.cuda.synchronize()
+    assert all(bool(torch.all(x == 7.0)) for x in dA + dB if x is not None)
+    L.grad(plan, dev["X"], dev["dY"], dA=dA, dB=dB, accumulate=False)
+    torch.cuda.synchronize()
+    assert all(bool(torch.all(x == 0.0)) and not bool(torch.signbit(x).any())
+               for x in dA + dB if x is not None)
