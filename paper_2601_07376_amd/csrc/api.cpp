@@ -222,16 +222,15 @@ int32_t small_max_policy(int32_t n) {
   return n <= 1024 ? INT32_MAX : SMALL_ROWS;
 }
 
-// Gradient workspace: fp32 partial planes (two per d-slice), the summed bf16
-// hi / lo planes, and B^T of every slot.
-GradLayout grad_layout(int32_t mrb_ub, int32_t r_max, int32_t num_slots, int32_t d_out) {
+// Gradient workspace: fp32 partial planes (two per d-slice) and the summed bf16
+// hi / lo planes.
+GradLayout grad_layout(int32_t mrb_ub, int32_t r_max) {
   GradLayout G{};
   const size_t r_pad = (size_t)(std::max(r_max, 1) + 15) / 16 * 16;
   const size_t p_stride = (size_t)mrb_ub * MRB_ROWS;
   size_t o = 0;
   G.partial = o; o += al256(2 * GRAD_SPLITS_MAX * r_pad * p_stride * 4);
   G.fin = o;     o += al256(2 * 2 * r_pad * p_stride * 2);
-  G.bt = o;      o += al256((size_t)num_slots * r_pad * (size_t)d_out * 2);
   G.total = o;
   return G;
 }
@@ -600,7 +599,7 @@ lora_status lora_apply(const lora_plan* p, const void* X, lora_dtype x_dtype, in
 
 size_t lora_grad_workspace_bytes(const lora_plan* p) {
   if (p == nullptr) return 0;
-  return lora::grad_layout(ub_mrb(p), p->r_max, p->table->num_slots, p->table->d_out).total;
+  return lora::grad_layout(ub_mrb(p), p->r_max).total;
 }
 
 lora_status lora_grad(const lora_plan* p, const void* X, lora_dtype x_dtype, int64_t ldx,
@@ -649,11 +648,10 @@ lora_status lora_grad(const lora_plan* p, const void* X, lora_dtype x_dtype, int
   g.dA = dA;
   g.dB = dB;
   g.accumulate = accumulate;
-  const lora::GradLayout GL = lora::grad_layout(ub_mrb(p), p->r_max, t->num_slots, t->d_out);
+  const lora::GradLayout GL = lora::grad_layout(ub_mrb(p), p->r_max);
   char* wsb = static_cast<char*>(ws);
   g.hg = reinterpret_cast<float*>(wsb + GL.partial);
   g.fin = reinterpret_cast<uint16_t*>(wsb + GL.fin);
-  g.bt = reinterpret_cast<uint16_t*>(wsb + GL.bt);
   g.k_splits = mfma ? grad_splits_policy(t->d_in, t->d_out) : 1;
   g.p_stride = ub_mrb(p) * lora::MRB_ROWS;
   g.r_pad = (std::max(p->r_max, 1) + 15) / 16 * 16;

@@ -5,12 +5,11 @@
 //
 //   H = X_m A_a^T,  G = dY_m B_a,  dB_a = s_a dY_m^T H,  dA_a = s_a G^T X_m.
 //
-// Matrix-core path, four launches:
-//  0. B_a^T of every live slot into the workspace, so that G reads its second
-//     operand with d_out contiguous, as H reads A_a with d_in contiguous.
+// Matrix-core path, three launches:
 //  1. per trainable row block (<= 64 rows) and d-slice: partial H and G over
 //     the slice, written transposed into fp32 "planes" [j][column], where row i
-//     of block e sits in column 64 e + i.
+//     of block e sits in column 64 e + i.  G's second operand is gathered from
+//     B_a as stored ([d_out][r], eight 2-byte loads per lane and k-step).
 //  2. the slice planes summed in slice order and split into bf16 hi + lo.
 //  3. per adapter and 128-wide column tile of dB or dA: a fixed-order
 //     reduction over the adapter's trainable rows, 32 rows per step; the row
@@ -51,7 +50,6 @@ struct GradArgs {
   int32_t p_stride;
   int32_t r_pad;
   uint16_t* fin;            // summed planes, bf16: [which][hi, lo][j][column]
-  uint16_t* bt;             // B_a^T per slot: [slot][r_pad][d_out]
 };
 
 __device__ __forceinline__ uint16_t* fin_plane(const GradArgs& g, int which, int hl) {
@@ -111,43 +109,6 @@ __device__ __forceinline__ void reduce_waves(f32x4 (&acc)[N], f32x4* s_red) {
   }
 }
 
-// ---------------------------------------------------------------------------
-// stage 0: B_a^T of every live slot, 64 rows of B per tile, through LDS
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void bt_kernel(GradArgs g) {
-  __shared__ uint16_t s_b[64][LORA_MAX_RANK + 2];
-  const int tid = threadIdx.x;
-  const int tpo = (g.d_out + 63) / 64;
-  for (int tile = blockIdx.x; tile < g.num_slots * tpo; tile += gridDim.x) {
-    const int a = tile / tpo, o0 = (tile - a * tpo) * 64;
-    const Slot m = load_slot(g.meta, a);
-    const int r = m.rank;
-    if (r <= 0) continue;
-    const rsrc_t Bw = make_rsrc(m.B, (uint32_t)g.d_out * (uint32_t)r * 2u);
-    const int orows = min(64, g.d_out - o0);     // a multiple of 8
-    __syncthreads();
-    // B[o0 .. o0 + orows) is one contiguous run of orows * r elements
-    for (int i = tid; i < orows * r / 8; i += 256) {
-      const uint4 u = bload16(Bw, ((uint32_t)o0 * r + 8u * i) * 2u);
-      const uint32_t wv[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        const int e = 8 * i + q, o = e / r, j = e - o * r;
-        s_b[o][j] = (uint16_t)(wv[q >> 1] >> (16 * (q & 1)));
-      }
-    }
-    __syncthreads();
-    uint16_t* bt = g.bt + (int64_t)a * g.r_pad * g.d_out + o0;
-    for (int i = tid; i < r * (orows / 8); i += 256) {
-      const int j = i / (orows / 8), o8 = (i - j * (orows / 8)) * 8;
-      uint32_t b[8];
-#pragma unroll
-      for (int q = 0; q < 8; ++q) b[q] = s_b[o8 + q][j];
-      stg16(bt + (int64_t)j * g.d_out + o8,
-            make_uint4(b[0] | (b[1] << 16), b[2] | (b[3] << 16), b[4] | (b[5] << 16), b[6] | (b[7] << 16)));
-    }
-  }
-}
 
 // ---------------------------------------------------------------------------
 // stage 1 (matrix cores): partial H and G for one (row block, slice).  Both are
@@ -165,15 +126,19 @@ __device__ __forceinline__ void rows_times_w2(f32x4 (&acc_h)[MT * NT], f32x4 (&a
                                               const uint16_t* (&xr)[MT], rsrc_t W1,
                                               const uint32_t (&wr1)[NT], int k1b, int k1e,
                                               const uint16_t* (&yr)[MT], rsrc_t W2,
-                                              const uint32_t (&wr2)[NT], int k2b, int k2e) {
+                                              const uint32_t (&wr2)[NT], int k2b, int k2e,
+                                              int r2) {
   const int kg = ((threadIdx.x & 63) >> 4) * 8 + wave_id() * 32;
   struct Buf {
     bf16x8 x[U][MT];
     bf16x8 w[U][NT];
     bool kv[U];
   };
+  // gather = false: W is [rows][K] (K contiguous), wr[nt] the row offset;
+  // gather = true:  W is [K][r] (B_a as stored), wr[nt] the column, and the
+  //                 eight K values of a lane are eight 2-byte loads r apart
   auto load = [&](Buf& b, const uint16_t* (&rr)[MT], rsrc_t W, const uint32_t (&wr)[NT], int kb,
-                  int ke) {
+                  int ke, bool gather) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int k = kb + u * 128 + kg;
@@ -182,7 +147,17 @@ __device__ __forceinline__ void rows_times_w2(f32x4 (&acc_h)[MT * NT], f32x4 (&a
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) b.x[u][mt] = as_bf16x8(ldg16(rr[mt] + kk));
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) b.w[u][nt] = as_bf16x8(bload16(W, (wr[nt] + (uint32_t)kk) * 2u));
+      for (int nt = 0; nt < NT; ++nt) {
+        if (!gather) {
+          b.w[u][nt] = as_bf16x8(bload16(W, (wr[nt] + (uint32_t)kk) * 2u));
+        } else {
+          uint32_t e[8];
+#pragma unroll
+          for (int i = 0; i < 8; ++i)
+            e[i] = bload_u16(W, ((uint32_t)(kk + i) * (uint32_t)r2 + wr[nt]) * 2u);
+          b.w[u][nt] = pack_bf16x8(e);
+        }
+      }
     }
   };
   auto compute = [&](const Buf& b, f32x4 (&acc)[MT * NT]) {
@@ -201,8 +176,8 @@ __device__ __forceinline__ void rows_times_w2(f32x4 (&acc_h)[MT * NT], f32x4 (&a
   const int rounds = max(n1, n2);
   for (int i = 0; i < rounds; ++i) {
     Buf bh, bg;
-    load(bh, xr, W1, wr1, k1b + i * U * 128, max(k1e, 8));
-    load(bg, yr, W2, wr2, k2b + i * U * 128, max(k2e, 8));
+    load(bh, xr, W1, wr1, k1b + i * U * 128, max(k1e, 8), false);
+    load(bg, yr, W2, wr2, k2b + i * U * 128, max(k2e, 8), true);
     // keep the whole round's loads ahead of its arithmetic (the scheduler
     // would otherwise interleave them to save registers, and wait on each)
     __builtin_amdgcn_sched_barrier(0);
@@ -231,8 +206,7 @@ __global__ __launch_bounds__(256) void hg_kernel(GradArgs g) {
     const Slot m = load_slot(g.meta, a);
     const int r = m.rank;
     const rsrc_t Aw = make_rsrc(m.A, (uint32_t)r * (uint32_t)g.d_in * 2u);
-    const rsrc_t Btw = make_rsrc(g.bt + (int64_t)a * g.r_pad * g.d_out,
-                                 (uint32_t)r * (uint32_t)g.d_out * 2u);
+    const rsrc_t Bw = make_rsrc(m.B, (uint32_t)g.d_out * (uint32_t)r * 2u);
     const uint16_t* xrow[MT];
     const uint16_t* yrow[MT];
 #pragma unroll
@@ -247,7 +221,7 @@ __global__ __launch_bounds__(256) void hg_kernel(GradArgs g) {
     for (int nt = 0; nt < NT; ++nt) {
       const int j = nt * 16 + (lane & 15);
       arow[nt] = (uint32_t)(j < r ? j : r - 1) * (uint32_t)g.d_in;
-      brow[nt] = (uint32_t)(j < r ? j : r - 1) * (uint32_t)g.d_out;
+      brow[nt] = (uint32_t)(j < r ? j : r - 1);
     }
     // acc[0 .. MT NT) : H tiles (mt, nt); acc[MT NT .. 2 MT NT) : G tiles
     f32x4 acc[N];
@@ -260,7 +234,7 @@ __global__ __launch_bounds__(256) void hg_kernel(GradArgs g) {
       slice(g.d_in, nks, ks, kb, ke);
       slice(g.d_out, nks, ks, ob, oe);
       if (g.H_saved != nullptr) ke = kb;          // H comes from the caller
-      rows_times_w2<MT, NT, U>(acc_h, acc_g, xrow, Aw, arow, kb, ke, yrow, Btw, brow, ob, oe);
+      rows_times_w2<MT, NT, U>(acc_h, acc_g, xrow, Aw, arow, kb, ke, yrow, Bw, brow, ob, oe, r);
     }
     vmem_drained();
     reduce_waves<N, CH>(acc, s_red);
@@ -623,7 +597,6 @@ GradArgs make_args(const GradLaunch& l) {
   g.p_stride = l.p_stride;
   g.r_pad = l.r_pad;
   g.fin = l.fin;
-  g.bt = l.bt;
   return g;
 }
 
@@ -645,11 +618,7 @@ bool set_group(const GradLaunch& l, GradArgs& g, int base) {
 
 template <int NT>
 hipError_t launch_nt(const GradLaunch& l, const GradArgs& g, hipStream_t s) {
-  const int tpo = (l.o.d_out + 63) / 64;
-  const int grid0 = std::min(l.o.num_slots * tpo, 8192);
-  hipLaunchKernelGGL(bt_kernel, dim3(grid0), dim3(256), 0, s, g);
-  hipError_t err = hipGetLastError();
-  if (err != hipSuccess) return err;
+  hipError_t err;
   const int grid1 = round8(std::min<long long>((long long)l.o.rb_ub * l.k_splits, 4096));
   hipLaunchKernelGGL((hg_kernel<NT>), dim3(grid1), dim3(256), 0, s, g);
   if ((err = hipGetLastError()) != hipSuccess) return err;

@@ -179,14 +179,13 @@ struct GradLaunch {
   int32_t p_stride;              // row stride (elements) of the H^T / G^T planes
   int32_t r_pad;                 // rank padding of the planes
   uint16_t* fin;                 // workspace: summed planes, bf16 hi / lo
-  uint16_t* bt;                  // workspace: B_a^T per slot [num_slots][r_pad][d_out]
 };
 
 // Byte offsets of the gradient workspace parts.
 struct GradLayout {
-  size_t partial, fin, bt, total;
+  size_t partial, fin, total;
 };
-GradLayout grad_layout(int32_t mrb_ub, int32_t r_max, int32_t num_slots, int32_t d_out);
+GradLayout grad_layout(int32_t mrb_ub, int32_t r_max);
 hipError_t launch_grad_mfma(const GradLaunch& g, hipStream_t s);
 hipError_t launch_grad_valu(const GradLaunch& g, lora_dtype x_dtype, lora_dtype w_dtype,
                             hipStream_t s);
