@@ -52,6 +52,7 @@ struct FwdArgs {
   int32_t n_rec;            // records the array holds (host bound)
   int32_t ks_max;           // large groups: most d-slices of the shrink (partial planes)
   int64_t hp_stride;        // elements between partial H planes
+  int32_t cw;               // expand column chunk (0: chosen from the block count)
 };
 
 __device__ __forceinline__ void entry_range(const FwdArgs& p, int& first, int& count) {
@@ -493,7 +494,6 @@ __device__ __forceinline__ void y8_combine(const Y8<YBF16>& f, float s, const f3
 // lanes per row.
 template <bool YBF16, bool RANK8, int KSM, int U>
 __global__ __launch_bounds__(256, (KSM == 1 || (YBF16 && KSM == 2 && U == 1)) ? 2 : 1) void expand_kernel(FwdArgs p) {
-  constexpr int CW = 1024;
   constexpr int BS = KSM * 32, TS = BS + 8;    // staged ranks per column; LDS stride
   constexpr int BP = 32 * BS / 8;              // 16-byte B pieces per step (rank padded)
   constexpr int BPT = (BP + 255) / 256;        // ... per thread
@@ -509,6 +509,9 @@ __global__ __launch_bounds__(256, (KSM == 1 || (YBF16 && KSM == 2 && U == 1)) ? 
   int first, count;
   entry_range(p, first, count);
   const int nks = shrink_splits(p, count);
+  // column chunk of a unit (finer chunks, tried for batches with few row
+  // blocks, measured slower: each unit repeats the H prologue)
+  const int CW = p.cw > 0 ? p.cw : 1024;
   const int n_ch = (p.d_out + CW - 1) / CW;
   const XcdRange xr = xcd_range(count * n_ch);
   for (int unit = xr.first; unit < xr.end; unit += xr.step) {
@@ -541,42 +544,72 @@ __global__ __launch_bounds__(256, (KSM == 1 || (YBF16 && KSM == 2 && U == 1)) ? 
     }
 
     // H operands (hi / lo) of the wave's rows: the slices' partial sums added
-    // in slice order, loaded once per unit
+    // in slice order, loaded once per unit (one round trip per plane: every
+    // rank step and row tile of a plane requested together).
+    float4 h[KSM][4][2];
+#pragma unroll
+    for (int ks = 0; ks < KSM; ++ks)
+#pragma unroll
+      for (int tt = 0; tt < 4; ++tt) {
+        h[ks][tt][0] = make_float4(0.f, 0.f, 0.f, 0.f);
+        h[ks][tt][1] = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    if constexpr (RANK8) {
+      for (int sl = 0; sl < nks; ++sl) {
+        const float* Hs = p.H + (int64_t)sl * p.hp_stride;
+        float4 q[KSM][4][2];
+#pragma unroll
+        for (int ks = 0; ks < KSM; ++ks) {
+          const int j = ks * 32 + jg;
+          const int jj = j < r ? j : r - 8;
+#pragma unroll
+          for (int tt = 0; tt < 4; ++tt) {
+            const float* hrow = Hs + (int64_t)trow[tt] * p.ldh;
+            q[ks][tt][0] = ldg_f4(hrow + jj);
+            q[ks][tt][1] = ldg_f4(hrow + jj + 4);
+          }
+        }
+#pragma unroll
+        for (int ks = 0; ks < KSM; ++ks)
+#pragma unroll
+          for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+            for (int c = 0; c < 2; ++c) {
+              float4& d = h[ks][tt][c];
+              const float4 x = q[ks][tt][c];
+              d.x += x.x; d.y += x.y; d.z += x.z; d.w += x.w;
+            }
+      }
+    } else {
+      // ranks not a multiple of 8: element loads, one rank step at a time
+      // (fewer registers in flight)
+#pragma unroll
+      for (int ks = 0; ks < KSM; ++ks) {
+        const int j = ks * 32 + jg;
+        for (int sl = 0; sl < nks; ++sl) {
+          const float* Hs = p.H + (int64_t)sl * p.hp_stride;
+#pragma unroll
+          for (int tt = 0; tt < 4; ++tt) {
+            const float* hrow = Hs + (int64_t)trow[tt] * p.ldh;
+            float e[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) e[i] = ldg(hrow + (j + i < r ? j + i : r - 1));
+            float4& d0 = h[ks][tt][0];
+            float4& d1 = h[ks][tt][1];
+            d0.x += e[0]; d0.y += e[1]; d0.z += e[2]; d0.w += e[3];
+            d1.x += e[4]; d1.y += e[5]; d1.z += e[6]; d1.w += e[7];
+          }
+        }
+      }
+    }
     bf16x8 hh[KSM][4], hl[KSM][4];
 #pragma unroll
     for (int ks = 0; ks < KSM; ++ks) {
       const int j = ks * 32 + jg;
-      const int jj = RANK8 ? (j < r ? j : r - 8) : 0;
-      float4 h[4][2];
 #pragma unroll
       for (int tt = 0; tt < 4; ++tt) {
-        h[tt][0] = make_float4(0.f, 0.f, 0.f, 0.f);
-        h[tt][1] = make_float4(0.f, 0.f, 0.f, 0.f);
-      }
-      for (int sl = 0; sl < nks; ++sl) {
-        const float* Hs = p.H + (int64_t)sl * p.hp_stride;
-#pragma unroll
-        for (int tt = 0; tt < 4; ++tt) {
-          const float* hrow = Hs + (int64_t)trow[tt] * p.ldh;
-          float4 a0, a1;
-          if (RANK8) {
-            a0 = ldg_f4(hrow + jj);
-            a1 = ldg_f4(hrow + jj + 4);
-          } else {
-            float q[8];
-#pragma unroll
-            for (int i = 0; i < 8; ++i) q[i] = ldg(hrow + (j + i < r ? j + i : r - 1));
-            a0 = make_float4(q[0], q[1], q[2], q[3]);
-            a1 = make_float4(q[4], q[5], q[6], q[7]);
-          }
-          h[tt][0].x += a0.x; h[tt][0].y += a0.y; h[tt][0].z += a0.z; h[tt][0].w += a0.w;
-          h[tt][1].x += a1.x; h[tt][1].y += a1.y; h[tt][1].z += a1.z; h[tt][1].w += a1.w;
-        }
-      }
-#pragma unroll
-      for (int tt = 0; tt < 4; ++tt) {
-        float hv[8] = {h[tt][0].x, h[tt][0].y, h[tt][0].z, h[tt][0].w,
-                       h[tt][1].x, h[tt][1].y, h[tt][1].z, h[tt][1].w};
+        float hv[8] = {h[ks][tt][0].x, h[ks][tt][0].y, h[ks][tt][0].z, h[ks][tt][0].w,
+                       h[ks][tt][1].x, h[ks][tt][1].y, h[ks][tt][1].z, h[ks][tt][1].w};
 #pragma unroll
         for (int i = 0; i < 8; ++i) hv[i] = (rv[tt] && j + i < r) ? hv[i] : 0.0f;
         split_hi_lo(hv, hh[ks][tt], hl[ks][tt]);
@@ -1110,7 +1143,11 @@ hipError_t launch_expand_mfma(const OpLaunch& o, const float* H, int64_t ldh, in
   a.hp_stride = hp_stride;
   a.Y = Y;
   a.ldy = ldy;
-  const long long units = (long long)o.rb_ub * ((o.d_out + 1023) / 1024);
+  // (row block, 1024-column chunk) units; LORA_EXPAND_CW sets another chunk
+  // width (whole pairs of 32-column steps) for measurements
+  const int cw = env_int("LORA_EXPAND_CW", 0);
+  a.cw = cw > 0 ? std::max(64, cw / 64 * 64) : 1024;
+  const long long units = (long long)o.rb_ub * ((o.d_out + a.cw - 1) / a.cw);
   const int grid = round8(std::min<long long>(units, 4096));
   const bool yb = y_dtype == LORA_BF16;
   if (yb && o.rank8) return launch_expand_ks<true, true>(o, grid, a, s);
