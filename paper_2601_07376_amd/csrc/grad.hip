@@ -320,8 +320,7 @@ __device__ __forceinline__ void dadb_tile(const GradArgs& g, int sl, int c0, uin
                                           uint16_t (*s_p)[2 * NT * 16 * DT_TS], int* s_rows) {
   constexpr int CT = dt_ct(NT), TS = DT_TS, PSEG = 2 * NT * 16 * 4;   // 16-byte plane pieces per step
   constexpr int PPT = (PSEG + 255) / 256;                               // per thread
-  constexpr int AHEAD = NT <= 2 ? 4 : 2;                                // steps in flight
-  constexpr int R = AHEAD + 1;                                          // register ring
+  constexpr int UB = NT <= 2 ? 2 : 1;                                   // steps per batch
   constexpr int CSN = CT / 8, I4 = CT / 64;     // loader column segments; 16-column tiles per wave
   const int lane = threadIdx.x & 63, w = wave_id(), tid = threadIdx.x;
   // loader: columns 8 cs .., rows 4 tq ..; with 128-column tiles the upper
@@ -357,31 +356,36 @@ __device__ __forceinline__ void dadb_tile(const GradArgs& g, int sl, int c0, uin
     }
     __syncthreads();
 
-    uint4 tr[R][4], pr[R][PPT];
-    // raw loads of step cc into ring slot q (clamped addresses; masked at the LDS write)
-    auto load = [&](int q, int cc) {
+    struct Step {
+      uint4 t[4];
+      uint4 p[PPT];
+    };
+    // raw loads of step cc (clamped to the window's last step; steps past it
+    // are staged as zero rows)
+    auto load = [&](Step& q, int cc) {
+      cc = min(cc, wch - 1);
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        tr[q][i] = ldg16(src + (int64_t)s_rows[cc * 32 + tq * 4 + i] * ld + lcol);
+        q.t[i] = ldg16(src + (int64_t)s_rows[cc * 32 + tq * 4 + i] * ld + lcol);
       const int col0 = blk0 * MRB_ROWS + (w0 + cc) * 32;
 #pragma unroll
       for (int h = 0; h < PPT; ++h) {
         const int sgm = (tid + 256 * h) & (PSEG - 1);
         const int hl = sgm / (NT * 64), rem = sgm - hl * (NT * 64);
         const int j = rem >> 2, part = (rem & 3) * 8;
-        pr[q][h] = ldg16((hl ? fin1 : fin0) + (int64_t)j * g.p_stride + col0 + part);
+        q.p[h] = ldg16((hl ? fin1 : fin0) + (int64_t)j * g.p_stride + col0 + part);
       }
     };
-    auto stage = [&](int q, int cc, int buf) {
+    auto stage = [&](const Step& q, int cc, int buf) {
       const int rows_left = mc - (w0 + cc) * 32;
       uint32_t v[4][4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const bool ok = lcol_ok && tq * 4 + i < rows_left;
-        v[i][0] = ok ? tr[q][i].x : 0u;
-        v[i][1] = ok ? tr[q][i].y : 0u;
-        v[i][2] = ok ? tr[q][i].z : 0u;
-        v[i][3] = ok ? tr[q][i].w : 0u;
+        v[i][0] = ok ? q.t[i].x : 0u;
+        v[i][1] = ok ? q.t[i].y : 0u;
+        v[i][2] = ok ? q.t[i].z : 0u;
+        v[i][3] = ok ? q.t[i].w : 0u;
       }
       // 4 rows x 8 columns -> 8 columns x 4 rows (bf16 pairs through byte permutes)
 #pragma unroll
@@ -402,7 +406,7 @@ __device__ __forceinline__ void dadb_tile(const GradArgs& g, int sl, int c0, uin
         const int sgm = (tid + 256 * h) & (PSEG - 1);
         const int hl = sgm / (NT * 64), rem = sgm - hl * (NT * 64);
         const int j = rem >> 2, part = (rem & 3) * 8;
-        *reinterpret_cast<uint4*>(&s_p[buf][(hl * NT * 16 + j) * TS + part]) = pr[q][h];
+        *reinterpret_cast<uint4*>(&s_p[buf][(hl * NT * 16 + j) * TS + part]) = q.p[h];
       }
     };
     auto mma = [&](int buf) {
@@ -428,20 +432,33 @@ __device__ __forceinline__ void dadb_tile(const GradArgs& g, int sl, int c0, uin
         }
       }
     };
-    // loads run AHEAD steps ahead, unconditionally (past the last step they
-    // repeat it): a load behind a branch would drain the whole pipeline
+    // Batches of UB steps, double buffered in registers (the next batch's loads
+    // are in flight while a batch is staged and multiplied); one exit, at the
+    // end of a pair of batches, and no memory operation behind a branch, so
+    // the compiler's wait counts stay exact.  LDS buffer cc & 1: a step is
+    // staged only after the barrier of the step before, which every wave
+    // passes after its products of the step before that.
+    Step b0[UB], b1[UB];
 #pragma unroll
-    for (int q = 0; q < AHEAD; ++q) load(q, min(q, wch - 1));
-    for (int cc0 = 0; cc0 < wch; cc0 += R) {
+    for (int u = 0; u < UB; ++u) load(b0[u], u);
+    for (int cc = 0; cc < wch; cc += 2 * UB) {
 #pragma unroll
-      for (int u = 0; u < R; ++u) {
-        const int cc = cc0 + u;
-        if (cc >= wch) break;
-        load((u + AHEAD) % R, min(cc + AHEAD, wch - 1));
-        __builtin_amdgcn_sched_barrier(0);     // requests stay ahead of the staging
-        stage(u, cc, cc & 1);
+      for (int u = 0; u < UB; ++u) load(b1[u], cc + UB + u);
+      __builtin_amdgcn_sched_barrier(0);       // requests stay ahead of the staging
+#pragma unroll
+      for (int u = 0; u < UB; ++u) {
+        stage(b0[u], cc + u, (cc + u) & 1);
         __syncthreads();
-        mma(cc & 1);
+        mma((cc + u) & 1);
+      }
+#pragma unroll
+      for (int u = 0; u < UB; ++u) load(b0[u], cc + 2 * UB + u);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int u = 0; u < UB; ++u) {
+        stage(b1[u], cc + UB + u, (cc + UB + u) & 1);
+        __syncthreads();
+        mma((cc + UB + u) & 1);
       }
     }
   }
