@@ -80,10 +80,9 @@ int32_t small_chunks_policy(int32_t d_out) {
 // there are enough row blocks to fill the chip).
 int32_t grad_splits_policy(int32_t d_in, int32_t d_out) {
   const int v = env_int("LORA_GRAD_SPLITS", 0);
-  if (v > 0) return std::min(v, 8);
-  return std::max(1, std::min(8, (std::min(d_in, d_out) + 511) / 512));   // slices of >= 512
+  if (v > 0) return std::min(v, lora::GRAD_SPLITS_MAX);
+  return std::max(1, std::min(lora::GRAD_SPLITS_MAX, (std::min(d_in, d_out) + 511) / 512));   // slices of >= 512
 }
-constexpr int32_t GRAD_SPLITS_MAX = 8;
 
 // host upper bounds of the entry lists
 int32_t ub_large(const lora_plan* p) {

@@ -11,10 +11,10 @@
 //     of block e sits in column 64 e + i.  G's second operand is gathered from
 //     B_a as stored ([d_out][r], eight 2-byte loads per lane and k-step).
 //  2. the slice planes summed in slice order and split into bf16 hi + lo.
-//  3. per adapter and 128-wide column tile of dB or dA: a fixed-order
-//     reduction over the adapter's trainable rows, 32 rows per step; the row
-//     tile is transposed through LDS and meets the hi / lo planes on the
-//     matrix cores.
+//  3. per adapter and 256-wide column tile of dB or dA: a fixed-order
+//     reduction over the adapter's trainable rows, one 64-row block per step;
+//     the row tile is transposed through LDS and meets the hi / lo planes on
+//     the matrix cores.
 // Rows outside T_a^m are never read.  No floating-point atomics anywhere, so
 // the result is the same bytes run to run.
 #include <algorithm>
@@ -121,7 +121,7 @@ __device__ __forceinline__ void reduce_waves(f32x4 (&acc)[N], f32x4* s_red) {
 // clamped address) and then feeds the matrix cores, so the second product's
 // loads overlap the first one's arithmetic and nothing waits behind a branch.
 // Every tile is computed (tiles past the rows or the rank are never stored).
-template <int MT, int NT, int U>
+template <int MT, int NT, int U, bool DB>
 __device__ __forceinline__ void rows_times_w2(f32x4 (&acc_h)[MT * NT], f32x4 (&acc_g)[MT * NT],
                                               const uint16_t* (&xr)[MT], rsrc_t W1,
                                               const uint32_t (&wr1)[NT], int k1b, int k1e,
@@ -132,6 +132,7 @@ __device__ __forceinline__ void rows_times_w2(f32x4 (&acc_h)[MT * NT], f32x4 (&a
   struct Buf {
     bf16x8 x[U][MT];
     bf16x8 w[U][NT];
+    uint32_t e[U][NT][8];   // gathered values, packed only when multiplied
     bool kv[U];
   };
   // gather = false: W is [rows][K] (K contiguous), wr[nt] the row offset;
@@ -151,48 +152,79 @@ __device__ __forceinline__ void rows_times_w2(f32x4 (&acc_h)[MT * NT], f32x4 (&a
         if (!gather) {
           b.w[u][nt] = as_bf16x8(bload16(W, (wr[nt] + (uint32_t)kk) * 2u));
         } else {
-          uint32_t e[8];
 #pragma unroll
           for (int i = 0; i < 8; ++i)
-            e[i] = bload_u16(W, ((uint32_t)(kk + i) * (uint32_t)r2 + wr[nt]) * 2u);
-          b.w[u][nt] = pack_bf16x8(e);
+            b.e[u][nt][i] = bload_u16(W, ((uint32_t)(kk + i) * (uint32_t)r2 + wr[nt]) * 2u);
         }
       }
     }
   };
-  auto compute = [&](const Buf& b, f32x4 (&acc)[MT * NT]) {
+  auto compute = [&](const Buf& b, f32x4 (&acc)[MT * NT], bool gather) {
 #pragma unroll
-    for (int u = 0; u < U; ++u)
+    for (int u = 0; u < U; ++u) {
+      bf16x8 wv[NT];
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) wv[nt] = gather ? pack_bf16x8(b.e[u][nt]) : b.w[u][nt];
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         const bf16x8 xo = sel(b.kv[u], b.x[u][mt]);
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt)
-          acc[mt * NT + nt] = mfma_16x16x32(xo, b.w[u][nt], acc[mt * NT + nt]);
+          acc[mt * NT + nt] = mfma_16x16x32(xo, wv[nt], acc[mt * NT + nt]);
       }
+    }
   };
   const int n1 = max(0, (k1e - k1b + U * 128 - 1) / (U * 128));
   const int n2 = max(0, (k2e - k2b + U * 128 - 1) / (U * 128));
   const int rounds = max(n1, n2);
-  for (int i = 0; i < rounds; ++i) {
-    Buf bh, bg;
-    load(bh, xr, W1, wr1, k1b + i * U * 128, max(k1e, 8), false);
-    load(bg, yr, W2, wr2, k2b + i * U * 128, max(k2e, 8), true);
-    // keep the whole round's loads ahead of its arithmetic (the scheduler
-    // would otherwise interleave them to save registers, and wait on each)
-    __builtin_amdgcn_sched_barrier(0);
-    compute(bh, acc_h);
-    compute(bg, acc_g);
+  const int e1 = max(k1e, 8), e2 = max(k2e, 8);
+  if (DB) {
+    // rounds double buffered in registers: round i + 1 is requested before
+    // round i is multiplied, so the memory stream never pauses for the
+    // arithmetic (rounds past the end read clamped addresses and add zeros);
+    // one exit, at the end of a pair of rounds
+    Buf h0, g0, h1, g1;
+    load(h0, xr, W1, wr1, k1b, e1, false);
+    load(g0, yr, W2, wr2, k2b, e2, true);
+    for (int i = 0; i < rounds; i += 2) {
+      load(h1, xr, W1, wr1, k1b + (i + 1) * U * 128, e1, false);
+      load(g1, yr, W2, wr2, k2b + (i + 1) * U * 128, e2, true);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(h0, acc_h, false);
+      compute(g0, acc_g, true);
+      load(h0, xr, W1, wr1, k1b + (i + 2) * U * 128, e1, false);
+      load(g0, yr, W2, wr2, k2b + (i + 2) * U * 128, e2, true);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(h1, acc_h, false);
+      compute(g1, acc_g, true);
+    }
+  } else {
+    for (int i = 0; i < rounds; ++i) {
+      Buf bh, bg;
+      load(bh, xr, W1, wr1, k1b + i * U * 128, e1, false);
+      load(bg, yr, W2, wr2, k2b + i * U * 128, e2, true);
+      // keep the whole round's loads ahead of its arithmetic (the scheduler
+      // would otherwise interleave them to save registers, and wait on each)
+      __builtin_amdgcn_sched_barrier(0);
+      compute(bh, acc_h, false);
+      compute(bg, acc_g, true);
+    }
   }
   mfma_fence();
 }
 
+#ifndef HG_U
+#define HG_U 1
+#endif
 template <int NT>
 __global__ __launch_bounds__(256) void hg_kernel(GradArgs g) {
   constexpr int MT = MRB_ROWS / 16;                      // row tiles per block
-  constexpr int U = NT <= 2 ? 4 : (NT == 4 ? 2 : 1);     // k-steps per wave and round
+  constexpr int U = HG_U > 0 ? HG_U : 1;                 // k-steps per wave and round
+  constexpr bool DB = NT <= 4;                           // double-buffered rounds
   constexpr int N = 2 * MT * NT, CH = N < 16 ? N : 16;
-  __shared__ f32x4 s_red[2 * CH * 64];
+  constexpr int OS = MRB_ROWS + 1;                       // LDS row stride of the plane tile
+  constexpr int RED = 2 * CH * 64, OUT = (NT * 16 * OS + 3) / 4;
+  __shared__ f32x4 s_red[RED > OUT ? RED : OUT];
   const int lane = threadIdx.x & 63, w = wave_id();
   const int n_blocks = g.hdr[HDR_NMRB];
   const int nks = active_splits(g, n_blocks);
@@ -234,34 +266,45 @@ __global__ __launch_bounds__(256) void hg_kernel(GradArgs g) {
       slice(g.d_in, nks, ks, kb, ke);
       slice(g.d_out, nks, ks, ob, oe);
       if (g.H_saved != nullptr) ke = kb;          // H comes from the caller
-      rows_times_w2<MT, NT, U>(acc_h, acc_g, xrow, Aw, arow, kb, ke, yrow, Bw, brow, ob, oe, r);
+      rows_times_w2<MT, NT, U, DB>(acc_h, acc_g, xrow, Aw, arow, kb, ke, yrow, Bw, brow, ob, oe, r);
     }
     vmem_drained();
     reduce_waves<N, CH>(acc, s_red);
-    if (w == 0) {
-      float* ph = plane(g, 0, ks);
-      float* pg = plane(g, 1, ks);
-      const int col0 = e * MRB_ROWS;
+    // wave 0 holds the totals; each plane's tile [j][64 columns] is staged in
+    // LDS and leaves as whole 256-byte row pieces
+    float* s_o = reinterpret_cast<float*>(s_red);
+    const int col0 = e * MRB_ROWS;
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
+    for (int which = 0; which < 2; ++which) {
+      __syncthreads();
+      if (w == 0) {
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt)
+        for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-          for (int v = 0; v < 4; ++v) {
-            const int i = mt * 16 + (lane >> 4) * 4 + v;
-            const int j = nt * 16 + (lane & 15);
-            if (j >= g.r_pad) continue;
-            const bool in = i < rows;
-            if (g.H_saved == nullptr) ph[(int64_t)j * g.p_stride + col0 + i] = in ? acc[mt * NT + nt][v] : 0.0f;
-            pg[(int64_t)j * g.p_stride + col0 + i] = in ? acc[MT * NT + mt * NT + nt][v] : 0.0f;
-          }
-      if (g.H_saved != nullptr) {
-        for (int q = lane; q < MRB_ROWS * g.r_pad; q += 64) {
-          const int i = q / g.r_pad, j = q - i * g.r_pad;
-          float h = 0.0f;
-          if (ks == 0 && i < rows && j < r) h = g.H_saved[(int64_t)g.m_perm[p0 + i] * g.ldh + j];
-          ph[(int64_t)j * g.p_stride + col0 + i] = h;
+          for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+              const int i = mt * 16 + (lane >> 4) * 4 + v, j = nt * 16 + (lane & 15);
+              s_o[j * OS + i] = i < rows ? acc[which * MT * NT + mt * NT + nt][v] : 0.0f;
+            }
+      }
+      __syncthreads();
+      if (which == 1 || g.H_saved == nullptr) {
+        float* pl = plane(g, which, ks);
+        for (int q = threadIdx.x; q < g.r_pad * (MRB_ROWS / 4); q += 256) {
+          const int j = q / (MRB_ROWS / 4), c4 = (q - j * (MRB_ROWS / 4)) * 4;
+          const float* so = s_o + j * OS + c4;
+          stg_f4(pl + (int64_t)j * g.p_stride + col0 + c4, make_float4(so[0], so[1], so[2], so[3]));
         }
+      }
+    }
+    if (g.H_saved != nullptr && w == 0) {
+      float* ph = plane(g, 0, ks);
+      for (int q = lane; q < MRB_ROWS * g.r_pad; q += 64) {
+        const int i = q / g.r_pad, j = q - i * g.r_pad;
+        float h = 0.0f;
+        if (ks == 0 && i < rows && j < r) h = g.H_saved[(int64_t)g.m_perm[p0 + i] * g.ldh + j];
+        ph[(int64_t)j * g.p_stride + col0 + i] = h;
       }
     }
   }
@@ -281,12 +324,21 @@ __global__ __launch_bounds__(256) void hgsum_kernel(GradArgs g) {
     const int which = (int)(q / per);
     const int64_t u = q - which * per;
     const int j = (int)(u / n8), c = (int)(u - (int64_t)j * n8) * 8;
+    // every slice requested at once (slices past nks read the last one again
+    // and are not added), then summed in slice order
+    float4 x0[GRAD_SPLITS_MAX], x1[GRAD_SPLITS_MAX];
+#pragma unroll
+    for (int ks = 0; ks < GRAD_SPLITS_MAX; ++ks) {
+      const float* p = plane(g, which, min(ks, nks - 1)) + (int64_t)j * g.p_stride + c;
+      x0[ks] = ldg_f4(p);
+      x1[ks] = ldg_f4(p + 4);
+    }
     float h[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (int ks = 0; ks < nks; ++ks) {
-      const float* p = plane(g, which, ks) + (int64_t)j * g.p_stride + c;
-      const float4 x0 = ldg_f4(p), x1 = ldg_f4(p + 4);
-      h[0] += x0.x; h[1] += x0.y; h[2] += x0.z; h[3] += x0.w;
-      h[4] += x1.x; h[5] += x1.y; h[6] += x1.z; h[7] += x1.w;
+#pragma unroll
+    for (int ks = 0; ks < GRAD_SPLITS_MAX; ++ks) {
+      if (ks >= nks) break;
+      h[0] += x0[ks].x; h[1] += x0[ks].y; h[2] += x0[ks].z; h[3] += x0[ks].w;
+      h[4] += x1[ks].x; h[5] += x1[ks].y; h[6] += x1[ks].z; h[7] += x1[ks].w;
     }
     bf16x8 hi, lo;
     split_hi_lo(h, hi, lo);
@@ -297,33 +349,42 @@ __global__ __launch_bounds__(256) void hgsum_kernel(GradArgs g) {
 
 // ---------------------------------------------------------------------------
 // stage 3 (matrix cores): one workgroup per (slot, dB or dA, 256-column tile).
-// Per 32-row step every thread loads four rows x 8 columns of dY (for dB) or
-// X (for dA), transposes them in registers and writes 8 columns x 4 rows into
-// LDS (column-major, 16-byte chunks swizzled by column), next to the step's
-// hi / lo plane columns; loads run several steps ahead and LDS is double
-// buffered with one barrier per step.
+// A step is one 64-row gradient block of the slot: every thread loads eight
+// rows x 8 columns of dY (for dB) or X (for dA), transposes them in registers
+// and writes 8 columns x 8 rows into LDS as 16-byte units, next to the step's
+// hi / lo plane columns; the next step's loads are in flight meanwhile and LDS
+// is double buffered with one barrier per step.
 //   dB[o][j] = s sum_t dY[t][o] H[t][j]:  A operand = dY^T tile, B = H plane
 //   dA[j][k] = s sum_t G[t][j] X[t][k]:   A operand = G plane, B = X^T tile
 // ---------------------------------------------------------------------------
 // tile columns: 256, or 128 for ranks above 64 (register budget)
 constexpr int dt_ct(int NT) { return NT <= 4 ? 256 : 128; }
-constexpr int DT_TS = 32 + 8;         // LDS stride (bf16) of one transposed column
-constexpr int DT_WIN = 512;           // row ids staged per window
+constexpr int DT_ROWS = MRB_ROWS;     // rows per step: one trainable row block
+constexpr int DT_WIN = 1024;          // row ids staged per window
 
-// 16-byte chunk g (rows 8g .. 8g + 7 of a step) of column `col` in the tile
-__device__ __forceinline__ int dt_chunk(int col, int g) { return g ^ ((col >> 3) & 3); }
+// LDS slot of 16-byte unit g (rows 8 g .. 8 g + 7 of a step) of column `col`
+// (a tile column, or a plane row j).  Two columns share each 256-byte line
+// and the units are permuted inside it, so that the 16 lanes of a transposing
+// write (columns 8 apart) and of a matrix-core read (16 consecutive columns)
+// both fall in 16 distinct 16-byte bank groups.
+__device__ __forceinline__ int dt_unit(int col, int g) {
+  const int r = col >> 1;
+  const int f = (r & 7) ^ ((r >> 3) & 3) ^ (((r >> 5) & 1) << 3);
+  return r * 16 + ((((col & 1) << 3) | g) ^ f);
+}
 
 // One (slot, column tile) of dB (IS_B) or dA: the whole reduction over the
 // slot's trainable rows, then the scaled store.
 template <int NT, bool IS_B>
-__device__ __forceinline__ void dadb_tile(const GradArgs& g, int sl, int c0, uint16_t (*s_t)[dt_ct(NT) * DT_TS],
-                                          uint16_t (*s_p)[2 * NT * 16 * DT_TS], int* s_rows) {
-  constexpr int CT = dt_ct(NT), TS = DT_TS, PSEG = 2 * NT * 16 * 4;   // 16-byte plane pieces per step
-  constexpr int PPT = (PSEG + 255) / 256;                               // per thread
-  constexpr int UB = NT <= 2 ? 2 : 1;                                   // steps per batch
+__device__ __forceinline__ void dadb_tile(const GradArgs& g, int sl, int c0, uint16_t (*s_t)[dt_ct(NT) * DT_ROWS],
+                                          uint16_t (*s_p)[2 * NT * 16 * DT_ROWS], int* s_rows) {
+  constexpr int CT = dt_ct(NT);
+  constexpr int PSEG = 2 * NT * 16 * (DT_ROWS / 8);   // 16-byte plane units per step
+  constexpr int PPT = PSEG / 256;                     // per thread
   constexpr int CSN = CT / 8, I4 = CT / 64;     // loader column segments; 16-column tiles per wave
+  static_assert(PSEG % 256 == 0, "plane units per thread");
   const int lane = threadIdx.x & 63, w = wave_id(), tid = threadIdx.x;
-  // loader: columns 8 cs .., rows 4 tq ..; with 128-column tiles the upper
+  // loader: columns 8 cs .., rows 8 tq ..; with 128-column tiles the upper
   // half of the threads repeats the lower half (same values, same addresses)
   const int cs = tid % CSN, tq = (tid / CSN) & 7;
   const int a = g.slot_base + sl;
@@ -346,120 +407,112 @@ __device__ __forceinline__ void dadb_tile(const GradArgs& g, int sl, int c0, uin
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[i][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int nch = (mc + 31) >> 5;
-  for (int w0 = 0; w0 < nch; w0 += DT_WIN / 32) {
-    const int wch = min(DT_WIN / 32, nch - w0);
+  const int nch = (mc + DT_ROWS - 1) / DT_ROWS;
+  for (int w0 = 0; w0 < nch; w0 += DT_WIN / DT_ROWS) {
+    const int wch = min(DT_WIN / DT_ROWS, nch - w0);
     __syncthreads();
     for (int i = tid; i < DT_WIN; i += 256) {
-      const int p = w0 * 32 + i;
+      const int p = w0 * DT_ROWS + i;
       s_rows[i] = g.m_perm[moff + (p < mc ? p : mc - 1)];
     }
     __syncthreads();
 
     struct Step {
-      uint4 t[4];
+      uint4 t[8];
       uint4 p[PPT];
     };
     // raw loads of step cc (clamped to the window's last step; steps past it
-    // are staged as zero rows)
+    // are staged as zero rows).  Step cc is row block blk0 + w0 + cc, so its
+    // plane columns are that block's 64 columns.
     auto load = [&](Step& q, int cc) {
       cc = min(cc, wch - 1);
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        q.t[i] = ldg16(src + (int64_t)s_rows[cc * 32 + tq * 4 + i] * ld + lcol);
-      const int col0 = blk0 * MRB_ROWS + (w0 + cc) * 32;
+      for (int i = 0; i < 8; ++i)
+        q.t[i] = ldg16(src + (int64_t)s_rows[cc * DT_ROWS + tq * 8 + i] * ld + lcol);
+      const int col0 = (blk0 + w0 + cc) * DT_ROWS;
 #pragma unroll
       for (int h = 0; h < PPT; ++h) {
-        const int sgm = (tid + 256 * h) & (PSEG - 1);
-        const int hl = sgm / (NT * 64), rem = sgm - hl * (NT * 64);
-        const int j = rem >> 2, part = (rem & 3) * 8;
-        q.p[h] = ldg16((hl ? fin1 : fin0) + (int64_t)j * g.p_stride + col0 + part);
+        const int u = tid + 256 * h, jr = u >> 3, gg = u & 7;
+        const int hl = jr / (NT * 16), j = jr - hl * (NT * 16);
+        q.p[h] = ldg16((hl ? fin1 : fin0) + (int64_t)j * g.p_stride + col0 + gg * 8);
       }
     };
     auto stage = [&](const Step& q, int cc, int buf) {
-      const int rows_left = mc - (w0 + cc) * 32;
-      uint32_t v[4][4];
+      const int rows_left = mc - (w0 + cc) * DT_ROWS;
+      uint32_t v[8][4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const bool ok = lcol_ok && tq * 4 + i < rows_left;
+      for (int i = 0; i < 8; ++i) {
+        const bool ok = lcol_ok && tq * 8 + i < rows_left;
         v[i][0] = ok ? q.t[i].x : 0u;
         v[i][1] = ok ? q.t[i].y : 0u;
         v[i][2] = ok ? q.t[i].z : 0u;
         v[i][3] = ok ? q.t[i].w : 0u;
       }
-      // 4 rows x 8 columns -> 8 columns x 4 rows (bf16 pairs through byte permutes)
+      // 8 rows x 8 columns -> 8 columns x 8 rows (bf16 pairs through byte permutes)
 #pragma unroll
-      for (int wd = 0; wd < 4; ++wd) {
-        const uint32_t e01 = __builtin_amdgcn_perm(v[1][wd], v[0][wd], 0x05040100u);
-        const uint32_t o01 = __builtin_amdgcn_perm(v[1][wd], v[0][wd], 0x07060302u);
-        const uint32_t e23 = __builtin_amdgcn_perm(v[3][wd], v[2][wd], 0x05040100u);
-        const uint32_t o23 = __builtin_amdgcn_perm(v[3][wd], v[2][wd], 0x07060302u);
-        const int col_e = cs * 8 + 2 * wd, col_o = col_e + 1;
-        const int off = (tq & 1) * 4;
-        *reinterpret_cast<uint2*>(&s_t[buf][col_e * TS + dt_chunk(col_e, tq >> 1) * 8 + off]) =
-            make_uint2(e01, e23);
-        *reinterpret_cast<uint2*>(&s_t[buf][col_o * TS + dt_chunk(col_o, tq >> 1) * 8 + off]) =
-            make_uint2(o01, o23);
+      for (int c = 0; c < 8; ++c) {
+        const uint32_t sel = (c & 1) ? 0x07060302u : 0x05040100u;
+        uint4 o;
+        o.x = __builtin_amdgcn_perm(v[1][c >> 1], v[0][c >> 1], sel);
+        o.y = __builtin_amdgcn_perm(v[3][c >> 1], v[2][c >> 1], sel);
+        o.z = __builtin_amdgcn_perm(v[5][c >> 1], v[4][c >> 1], sel);
+        o.w = __builtin_amdgcn_perm(v[7][c >> 1], v[6][c >> 1], sel);
+        *reinterpret_cast<uint4*>(&s_t[buf][dt_unit(cs * 8 + c, tq) * 8]) = o;
       }
 #pragma unroll
       for (int h = 0; h < PPT; ++h) {
-        const int sgm = (tid + 256 * h) & (PSEG - 1);
-        const int hl = sgm / (NT * 64), rem = sgm - hl * (NT * 64);
-        const int j = rem >> 2, part = (rem & 3) * 8;
-        *reinterpret_cast<uint4*>(&s_p[buf][(hl * NT * 16 + j) * TS + part]) = q.p[h];
+        const int u = tid + 256 * h;
+        *reinterpret_cast<uint4*>(&s_p[buf][dt_unit(u >> 3, u & 7) * 8]) = q.p[h];
       }
     };
     auto mma = [&](int buf) {
       const int gq = lane >> 4, n = lane & 15;
 #pragma unroll
-      for (int i4 = 0; i4 < I4; ++i4) {
-        const int col = w * (16 * I4) + i4 * 16 + n;
-        const bf16x8 tv = as_bf16x8(
-            *reinterpret_cast<const uint4*>(&s_t[buf][col * TS + dt_chunk(col, gq) * 8]));
+      for (int kc = 0; kc < DT_ROWS / 32; ++kc) {
+        const int gu = kc * 4 + gq;
+        bf16x8 hi[NT], lo[NT];
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
-          const bf16x8 hi = as_bf16x8(
-              *reinterpret_cast<const uint4*>(&s_p[buf][(nt * 16 + n) * TS + gq * 8]));
-          const bf16x8 lo = as_bf16x8(
-              *reinterpret_cast<const uint4*>(&s_p[buf][((NT + nt) * 16 + n) * TS + gq * 8]));
-          if (IS_B) {
-            acc[i4][nt] = mfma_16x16x32(tv, hi, acc[i4][nt]);
-            acc[i4][nt] = mfma_16x16x32(tv, lo, acc[i4][nt]);
-          } else {
-            acc[i4][nt] = mfma_16x16x32(hi, tv, acc[i4][nt]);
-            acc[i4][nt] = mfma_16x16x32(lo, tv, acc[i4][nt]);
+          hi[nt] = as_bf16x8(*reinterpret_cast<const uint4*>(&s_p[buf][dt_unit(nt * 16 + n, gu) * 8]));
+          lo[nt] = as_bf16x8(
+              *reinterpret_cast<const uint4*>(&s_p[buf][dt_unit((NT + nt) * 16 + n, gu) * 8]));
+        }
+#pragma unroll
+        for (int i4 = 0; i4 < I4; ++i4) {
+          const int col = w * (16 * I4) + i4 * 16 + n;
+          const bf16x8 tv = as_bf16x8(*reinterpret_cast<const uint4*>(&s_t[buf][dt_unit(col, gu) * 8]));
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt) {
+            if (IS_B) {
+              acc[i4][nt] = mfma_16x16x32(tv, hi[nt], acc[i4][nt]);
+              acc[i4][nt] = mfma_16x16x32(tv, lo[nt], acc[i4][nt]);
+            } else {
+              acc[i4][nt] = mfma_16x16x32(hi[nt], tv, acc[i4][nt]);
+              acc[i4][nt] = mfma_16x16x32(lo[nt], tv, acc[i4][nt]);
+            }
           }
         }
       }
     };
-    // Batches of UB steps, double buffered in registers (the next batch's loads
-    // are in flight while a batch is staged and multiplied); one exit, at the
-    // end of a pair of batches, and no memory operation behind a branch, so
-    // the compiler's wait counts stay exact.  LDS buffer cc & 1: a step is
-    // staged only after the barrier of the step before, which every wave
-    // passes after its products of the step before that.
-    Step b0[UB], b1[UB];
-#pragma unroll
-    for (int u = 0; u < UB; ++u) load(b0[u], u);
-    for (int cc = 0; cc < wch; cc += 2 * UB) {
-#pragma unroll
-      for (int u = 0; u < UB; ++u) load(b1[u], cc + UB + u);
+    // Steps double buffered in registers (the next step's loads are in flight
+    // while a step is staged and multiplied); one exit, at the end of a pair
+    // of steps, and no memory operation behind a branch, so the compiler's
+    // wait counts stay exact.  LDS buffer cc & 1: a step is staged only after
+    // the barrier of the step before, which every wave passes after its
+    // products of the step before that.
+    Step b0, b1;
+    load(b0, 0);
+    for (int cc = 0; cc < wch; cc += 2) {
+      load(b1, cc + 1);
       __builtin_amdgcn_sched_barrier(0);       // requests stay ahead of the staging
-#pragma unroll
-      for (int u = 0; u < UB; ++u) {
-        stage(b0[u], cc + u, (cc + u) & 1);
-        __syncthreads();
-        mma((cc + u) & 1);
-      }
-#pragma unroll
-      for (int u = 0; u < UB; ++u) load(b0[u], cc + 2 * UB + u);
+      stage(b0, cc, 0);
+      __syncthreads();
+      mma(0);
+      load(b0, cc + 2);
       __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int u = 0; u < UB; ++u) {
-        stage(b1[u], cc + UB + u, (cc + UB + u) & 1);
-        __syncthreads();
-        mma((cc + UB + u) & 1);
-      }
+      stage(b1, cc + 1, 1);
+      __syncthreads();
+      mma(1);
     }
   }
 
@@ -492,8 +545,8 @@ __device__ __forceinline__ void dadb_tile(const GradArgs& g, int sl, int c0, uin
 template <int NT>
 __global__ __launch_bounds__(256) void dadb_kernel(GradArgs g) {
   constexpr int CT = dt_ct(NT);
-  __shared__ __align__(16) uint16_t s_t[2][CT * DT_TS];
-  __shared__ __align__(16) uint16_t s_p[2][2 * NT * 16 * DT_TS];     // [hl][j][t]
+  __shared__ __align__(16) uint16_t s_t[2][CT * DT_ROWS];
+  __shared__ __align__(16) uint16_t s_p[2][2 * NT * 16 * DT_ROWS];   // [hl][j] columns
   __shared__ int s_rows[DT_WIN];
   const int nbB = (g.d_out + CT - 1) / CT, nbA = (g.d_in + CT - 1) / CT, nbt = nbB + nbA;
   const XcdRange xr = xcd_range(g.slot_count * nbt);

@@ -159,6 +159,7 @@ hipError_t launch_expand_valu(const OpLaunch& o, const float* H, int64_t ldh,
 
 // gradient path
 constexpr int GRAD_SLOT_GROUP = 64;   // output pointers passed per launch
+constexpr int GRAD_SPLITS_MAX = 8;    // most d-slices (partial planes) of the first stage
 struct GradLaunch {
   OpLaunch o;                    // o.rb / o.rb_ub describe the trainable row blocks
   const int32_t* m_perm;
