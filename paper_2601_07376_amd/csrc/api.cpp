@@ -88,8 +88,17 @@ int32_t grad_splits_policy(int32_t d_in, int32_t d_out) {
 int32_t ub_large(const lora_plan* p) {
   if (p->small_max == INT32_MAX) return 0;
   const int32_t S = p->table->num_slots, n = p->n;
+  return n / lora::RB_FINE + std::min(S, n / (p->small_max + 1)) + 1;   // either block size
+}
+// ... of a plan that chose RB_ROWS blocks, and of one that chose RB_FINE blocks
+// (it does so only below FINE_BELOW coarse blocks, and a group's fine blocks
+// are at most four times its coarse ones)
+int32_t ub_coarse(const lora_plan* p) {
+  if (p->small_max == INT32_MAX) return 0;
+  const int32_t S = p->table->num_slots, n = p->n;
   return n / lora::RB_ROWS + std::min(S, n / (p->small_max + 1)) + 1;
 }
+int32_t ub_fine(const lora_plan* p) { return std::min(ub_large(p), 4 * lora::FINE_BELOW); }
 int32_t ub_small(const lora_plan* p) {
   const int32_t S = p->table->num_slots, n = p->n;
   const int64_t all = n / lora::SMALL_ROWS + std::min(S, n) + 1;
@@ -470,6 +479,8 @@ lora_status lora_shrink(const lora_plan* p, const void* X, lora_dtype x_dtype, i
   o.count_word = lora::HDR_NRB_TOTAL;
   o.first_word = -1;
   o.rb_ub = ub_large(p) + ub_small(p);
+  o.coarse_ub = ub_coarse(p) + ub_small(p);
+  o.fine_ub = ub_fine(p) + ub_small(p);
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e;
   if (x_dtype == LORA_BF16 && t->w_dtype == LORA_BF16)
@@ -492,6 +503,8 @@ lora_status lora_expand(const lora_plan* p, const float* H, int64_t ldh, void* Y
   o.count_word = lora::HDR_NRB_TOTAL;
   o.first_word = -1;
   o.rb_ub = ub_large(p) + ub_small(p);
+  o.coarse_ub = ub_coarse(p) + ub_small(p);
+  o.fine_ub = ub_fine(p) + ub_small(p);
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e;
   if (t->w_dtype == LORA_BF16)
@@ -563,6 +576,8 @@ lora_status lora_apply(const lora_plan* p, const void* X, lora_dtype x_dtype, in
       o.count_word = lora::HDR_NRB_LARGE;
       o.first_word = -1;
       o.rb_ub = ub_large(p);
+      o.coarse_ub = ub_coarse(p);
+      o.fine_ub = ub_fine(p);
       const int64_t plane = (int64_t)(al256((size_t)std::max(p->n, 1) * ldh * 4) / 4);
       e = lora::launch_shrink_mfma(o, X, ldx, H, ldh, lora::SHRINK_KS_MAX, plane, s);
       if (e == hipSuccess)

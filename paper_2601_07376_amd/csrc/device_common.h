@@ -235,4 +235,40 @@ __device__ __forceinline__ XcdRange xcd_range(int total) {
   return r;
 }
 
+// Sum the four waves' accumulators in a fixed order, ((w0 + w2) + (w1 + w3)),
+// leaving the total in wave 0; CH accumulators at a time through s_red
+// (2 x CH x 64 f32x4).
+template <int N, int CH>
+__device__ __forceinline__ void reduce_waves(f32x4 (&acc)[N], f32x4* s_red) {
+  const int lane = threadIdx.x & 63, w = wave_id();
+#pragma unroll
+  for (int c0 = 0; c0 < N; c0 += CH) {
+    constexpr int C = CH;
+    __syncthreads();
+    if (w >= 2) {
+#pragma unroll
+      for (int i = 0; i < C; ++i)
+        if (c0 + i < N) s_red[((w - 2) * C + i) * 64 + lane] = acc[c0 + i];
+    }
+    __syncthreads();
+    if (w < 2) {
+#pragma unroll
+      for (int i = 0; i < C; ++i)
+        if (c0 + i < N) acc[c0 + i] += s_red[(w * C + i) * 64 + lane];
+    }
+    __syncthreads();
+    if (w == 1) {
+#pragma unroll
+      for (int i = 0; i < C; ++i)
+        if (c0 + i < N) s_red[i * 64 + lane] = acc[c0 + i];
+    }
+    __syncthreads();
+    if (w == 0) {
+#pragma unroll
+      for (int i = 0; i < C; ++i)
+        if (c0 + i < N) acc[c0 + i] += s_red[i * 64 + lane];
+    }
+  }
+}
+
 }  // namespace lora

@@ -152,33 +152,6 @@ __device__ __forceinline__ void y_store(const YFrag<YBF16>& f, void* Yv, int64_t
   }
 }
 
-// Sum the four waves' accumulators in a fixed order, ((w0 + w2) + (w1 + w3)),
-// leaving the total in wave 0.  s_red holds 2 x N x 64 f32x4.
-template <int N>
-__device__ __forceinline__ void reduce_waves(f32x4 (&acc)[N], f32x4* s_red) {
-  const int lane = threadIdx.x & 63, w = wave_id();
-  __syncthreads();
-  if (w >= 2) {
-#pragma unroll
-    for (int i = 0; i < N; ++i) s_red[((w - 2) * N + i) * 64 + lane] = acc[i];
-  }
-  __syncthreads();
-  if (w < 2) {
-#pragma unroll
-    for (int i = 0; i < N; ++i) acc[i] += s_red[(w * N + i) * 64 + lane];
-  }
-  __syncthreads();
-  if (w == 1) {
-#pragma unroll
-    for (int i = 0; i < N; ++i) s_red[i * 64 + lane] = acc[i];
-  }
-  __syncthreads();
-  if (w == 0) {
-#pragma unroll
-    for (int i = 0; i < N; ++i) acc[i] += s_red[i * 64 + lane];
-  }
-}
-
 // acc[mt * NT + nt] += X[rows of mt] A[rows of nt]^T over this wave's k-steps
 // k0 = kstart + i * kstride (k0 < kend).  xr[mt] points at a real X row and
 // ar[nt] is the element offset of a real A row; padding lanes use a clamped row,
@@ -294,6 +267,7 @@ __global__ __launch_bounds__(256) void shrink_kernel(FwdArgs p) {
   __shared__ __align__(16) uint16_t s_a[2][U][AS * TS];
   const int lane = threadIdx.x & 63, w = wave_id(), tid = threadIdx.x;
   const int mrow = lane & 15, kg = (lane >> 4) * 8;
+  if (p.hdr[HDR_RB_ROWS] == RB_FINE) return;     // the fine kernel's batch
   int first, count;
   entry_range(p, first, count);
   const int nks = shrink_splits(p, count);
@@ -506,6 +480,7 @@ __global__ __launch_bounds__(256, (KSM == 1 || (YBF16 && KSM == 2 && U == 1)) ? 
   const int og = lane >> 4, mrow = lane & 15, jg = og * 8;
   unsigned char* const so = s_o[w];
   uint4* const sink = g_store_sink + 8 * tid;
+  if (p.hdr[HDR_RB_ROWS] == RB_FINE) return;     // the fine kernel's batch
   int first, count;
   entry_range(p, first, count);
   const int nks = shrink_splits(p, count);
@@ -745,6 +720,313 @@ __global__ __launch_bounds__(256, (KSM == 1 || (YBF16 && KSM == 2 && U == 1)) ? 
 }
 
 // ---------------------------------------------------------------------------
+// Large groups in 64-row blocks.  Batches whose large groups are few or short
+// give too few 256-row blocks to fill the chip, and a 256-row block that holds
+// a short group spends most of its work on padding rows.  Here the four waves
+// of a workgroup share the block's 64 rows: the shrink splits the d-slice's
+// k-steps over the waves (partial sums meet in LDS in a fixed order), the
+// expand splits the unit's columns over the waves (H formed once per unit in
+// LDS, each wave loading the B rows of its own columns, no barrier in the
+// column loop).
+// ---------------------------------------------------------------------------
+template <int NT>
+__global__ __launch_bounds__(256) void shrink_fine_kernel(FwdArgs p) {
+  constexpr int N = 4 * NT, CH = N < 16 ? N : 16;
+  __shared__ f32x4 s_red[2 * CH * 64];
+  const int lane = threadIdx.x & 63, w = wave_id();
+  const int mrow = lane & 15, kg = (lane >> 4) * 8;
+  if (p.hdr[HDR_RB_ROWS] != RB_FINE) return;     // the coarse kernel's batch
+  int first, count;
+  entry_range(p, first, count);
+  const int nks = shrink_splits(p, count);
+  const XcdRange xr = xcd_range(count * nks);
+  for (int unit = xr.first; unit < xr.end; unit += xr.step) {
+    const int e = unit / nks, ks = unit - e * nks;
+    const int4 en = load_entry(p.rb, first + e);
+    const int a = en.x, p0 = en.y, rows = en.z;
+    const Slot m = load_slot(p.meta, a);
+    const int r = m.rank;
+    const rsrc_t A = make_rsrc(m.A, (uint32_t)r * (uint32_t)p.d_in * 2u);
+    int kb, ke;
+    kslice(p.d_in, nks, ks, kb, ke);
+    const int kend = max(ke, 8);
+    const int nst = max(1, (ke - kb + 31) / 32);
+    const int rounds = (nst + 3) / 4;            // k-steps per wave: w, w + 4, ...
+
+    const uint16_t* xrow[4];
+    int orow[4][4];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) {
+      const int i = 16 * mt + mrow;
+      xrow[mt] = p.X + (int64_t)ldg(p.perm + p0 + (i < rows ? i : rows - 1)) * p.ldx;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int io = 16 * mt + (lane >> 4) * 4 + v;
+        orow[mt][v] = ldg(p.perm + p0 + (io < rows ? io : rows - 1));
+      }
+    }
+    uint32_t arow[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const int j = nt * 16 + mrow;
+      arow[nt] = (uint32_t)(j < r ? j : r - 1) * (uint32_t)p.d_in;
+    }
+    f32x4 acc[N];
+#pragma unroll
+    for (int i = 0; i < N; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    struct Buf {
+      bf16x8 x[4];
+      bf16x8 a[NT];
+      bool kv;
+    };
+    auto load = [&](Buf& b, int i) {
+      const int k = kb + 32 * (w + 4 * i) + kg;
+      b.kv = k < ke;
+      const int kk = k < kend ? k : kend - 8;
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) b.a[nt] = as_bf16x8(bload16(A, (arow[nt] + (uint32_t)kk) * 2u));
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) b.x[mt] = as_bf16x8(ldg16(xrow[mt] + kk));
+    };
+    auto compute = [&](const Buf& b) {
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) {
+        const bf16x8 xo = sel(b.kv, b.x[mt]);
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) acc[mt * NT + nt] = mfma_16x16x32(xo, b.a[nt], acc[mt * NT + nt]);
+      }
+    };
+    // rounds double buffered in registers; one exit, at the end of a pair
+    // (rounds past the end read clamped addresses and add zeros)
+    Buf b0, b1;
+    load(b0, 0);
+    for (int i = 0; i < rounds; i += 2) {
+      load(b1, i + 1);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(b0);
+      load(b0, i + 2);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(b1);
+    }
+    mfma_fence();
+    vmem_drained();
+    reduce_waves<N, CH>(acc, s_red);
+    if (w == 0) {
+      float* H = p.H + (int64_t)ks * p.hp_stride;
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int i = 16 * mt + (lane >> 4) * 4 + v;
+          if (i >= rows) continue;
+          float* hrow = H + (int64_t)orow[mt][v] * p.ldh;
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt) {
+            const int j = nt * 16 + mrow;
+            if (j < r) stg(hrow + j, acc[mt * NT + nt][v]);
+          }
+        }
+    }
+  }
+}
+
+template <bool YBF16, bool RANK8, int KSM, int U>
+__global__ __launch_bounds__(256, KSM == 1 ? 2 : 1) void expand_fine_kernel(FwdArgs p) {
+  constexpr int HS = KSM * 32, HT = HS + 4;    // H columns (rank padded); LDS stride
+  constexpr int ES = YBF16 ? 2 : 4;            // bytes per Y element
+  constexpr int SP = YBF16 ? 2 : 1;            // steps per 128 bytes of a row
+  constexpr int OS = 128 + 16;                 // bytes per row of a wave's output area
+  constexpr int HQ = 2 * KSM;                  // float4 of a row per thread and plane
+  __shared__ __align__(16) float s_h[64 * HT];
+  __shared__ __align__(16) unsigned char s_o[4][64 * OS];
+  const int lane = threadIdx.x & 63, w = wave_id(), tid = threadIdx.x;
+  const int og = lane >> 4, mrow = lane & 15, jg = og * 8;
+  unsigned char* const so = s_o[w];
+  uint4* const sink = g_store_sink + 8 * tid;
+  if (p.hdr[HDR_RB_ROWS] != RB_FINE) return;     // the coarse kernel's batch
+  int first, count;
+  entry_range(p, first, count);
+  const int nks = shrink_splits(p, count);
+  const int CW = p.cw > 0 ? p.cw : 1024;
+  const int QW = CW / 4;                       // columns per wave
+  const int n_ch = (p.d_out + CW - 1) / CW;
+  const XcdRange xr = xcd_range(count * n_ch);
+  for (int unit = xr.first; unit < xr.end; unit += xr.step) {
+    const int e = unit / n_ch, ch = unit - e * n_ch;
+    const int c0 = ch * CW, c1 = min(p.d_out, c0 + CW);
+    const int4 en = load_entry(p.rb, first + e);
+    const int a = en.x, p0 = en.y, rows = en.z;
+    const Slot m = load_slot(p.meta, a);
+    const int r = m.rank;
+    const float s = m.scale;
+    const rsrc_t Bw = make_rsrc(m.B, (uint32_t)p.d_out * (uint32_t)r * 2u);
+    // this wave's columns
+    const int cw0 = min(c0 + w * QW, c1), cw1 = min(c1, cw0 + QW);
+    const int nst = (cw1 - cw0 + 31) / 32;
+
+    int trow[4];
+#pragma unroll
+    for (int tt = 0; tt < 4; ++tt) {
+      const int i = 16 * tt + mrow;
+      trow[tt] = ldg(p.perm + p0 + (i < rows ? i : rows - 1));
+    }
+    int srow[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int ri = 8 * i + (lane >> 3);
+      srow[i] = ri < rows ? ldg(p.perm + p0 + ri) : -1;
+    }
+
+    // H of the block's rows: thread -> row tid / 4, float4 quarter tid % 4 of
+    // the rank columns; the slices' planes requested in one round trip and
+    // added in slice order (rows past the block and ranks past r are zero)
+    {
+      const int hr = tid >> 2, hq = tid & 3;
+      const int hrow = ldg(p.perm + p0 + (hr < rows ? hr : rows - 1));
+      float4 q[SHRINK_KS_MAX][HQ];
+#pragma unroll
+      for (int sl = 0; sl < SHRINK_KS_MAX; ++sl) {
+        const float* Hs = p.H + (int64_t)min(sl, nks - 1) * p.hp_stride + (int64_t)hrow * p.ldh;
+#pragma unroll
+        for (int c = 0; c < HQ; ++c) {
+          const int j = 4 * (hq + 4 * c);
+          if (RANK8) {
+            q[sl][c] = ldg_f4(Hs + (j < r ? j : r - 4));
+          } else {
+            q[sl][c] = make_float4(ldg(Hs + min(j, r - 1)), ldg(Hs + min(j + 1, r - 1)),
+                                   ldg(Hs + min(j + 2, r - 1)), ldg(Hs + min(j + 3, r - 1)));
+          }
+        }
+      }
+      __syncthreads();                 // the previous unit's reads of s_h are done
+#pragma unroll
+      for (int c = 0; c < HQ; ++c) {
+        const int j = 4 * (hq + 4 * c);
+        float4 h = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int sl = 0; sl < SHRINK_KS_MAX; ++sl) {
+          if (sl >= nks) break;
+          h.x += q[sl][c].x; h.y += q[sl][c].y; h.z += q[sl][c].z; h.w += q[sl][c].w;
+        }
+        const bool ok = hr < rows;
+        h.x = (ok && j < r) ? h.x : 0.f;
+        h.y = (ok && j + 1 < r) ? h.y : 0.f;
+        h.z = (ok && j + 2 < r) ? h.z : 0.f;
+        h.w = (ok && j + 3 < r) ? h.w : 0.f;
+        *reinterpret_cast<float4*>(&s_h[hr * HT + j]) = h;
+      }
+      __syncthreads();
+    }
+    bf16x8 hh[KSM][4], hl[KSM][4];
+#pragma unroll
+    for (int ks = 0; ks < KSM; ++ks)
+#pragma unroll
+      for (int tt = 0; tt < 4; ++tt) {
+        const float* hp = &s_h[(16 * tt + mrow) * HT + ks * 32 + jg];
+        const float4 x0 = *reinterpret_cast<const float4*>(hp);
+        const float4 x1 = *reinterpret_cast<const float4*>(hp + 4);
+        const float hv[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+        split_hi_lo(hv, hh[ks][tt], hl[ks][tt]);
+      }
+    vmem_drained();
+
+    struct Buf {
+      bf16x8 b[U][KSM][2];
+      Y8<YBF16> y[U][4];
+    };
+    auto load = [&](Buf& q, int st0) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int ob = cw0 + 32 * max(0, min(st0 + u, nst - 1));
+#pragma unroll
+        for (int ks = 0; ks < KSM; ++ks)
+#pragma unroll
+          for (int qq = 0; qq < 2; ++qq) {
+            int oc = ob + 8 * (mrow >> 2) + 4 * qq + (mrow & 3);
+            oc = oc < p.d_out ? oc : p.d_out - 1;
+            q.b[u][ks][qq] = wrow8<RANK8>(Bw, (uint32_t)oc * r, ks * 32 + jg, r);
+          }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int ob = cw0 + 32 * max(0, min(st0 + u, nst - 1));
+#pragma unroll
+        for (int tt = 0; tt < 4; ++tt)
+          y8_load<YBF16>(q.y[u][tt], p.Y, p.ldy, trow[tt], ob + 8 * og, p.d_out);
+      }
+    };
+    auto run = [&](const Buf& q, int u, int st) {
+      f32x4 acc[2][4];
+#pragma unroll
+      for (int qq = 0; qq < 2; ++qq)
+#pragma unroll
+        for (int tt = 0; tt < 4; ++tt) acc[qq][tt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KSM; ++ks) {
+        const bool jv = ks * 32 + jg < r;
+#pragma unroll
+        for (int qq = 0; qq < 2; ++qq) {
+          const bf16x8 b = sel(jv, q.b[u][ks][qq]);
+#pragma unroll
+          for (int tt = 0; tt < 4; ++tt) {
+            acc[qq][tt] = mfma_16x16x32(b, hh[ks][tt], acc[qq][tt]);
+            acc[qq][tt] = mfma_16x16x32(b, hl[ks][tt], acc[qq][tt]);
+          }
+        }
+      }
+      mfma_fence();
+      const int cb = ((st % SP) * 32 + 8 * og) * ES;
+#pragma unroll
+      for (int tt = 0; tt < 4; ++tt) {
+        uint4 out[2];
+        y8_combine<YBF16>(q.y[u][tt], s, acc[0][tt], acc[1][tt], out);
+        unsigned char* d = so + (16 * tt + mrow) * OS + cb;
+        *reinterpret_cast<uint4*>(d) = out[0];
+        if (!YBF16) *reinterpret_cast<uint4*>(d + 16) = out[1];
+      }
+    };
+    auto flush = [&](int st0) {
+      asm volatile("" ::: "memory");
+      const int o = cw0 + 32 * st0 + (lane & 7) * (16 / ES);
+      const bool ov = o < cw1;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const uint4 v = *reinterpret_cast<const uint4*>(so + (8 * i + (lane >> 3)) * OS + (lane & 7) * 16);
+        uint4* dst = (ov && srow[i] >= 0)
+                         ? reinterpret_cast<uint4*>(reinterpret_cast<char*>(p.Y) +
+                                                    ((int64_t)srow[i] * p.ldy + o) * ES)
+                         : sink + i;
+        stg16(dst, v);
+      }
+      asm volatile("" ::: "memory");
+    };
+    auto batch = [&](const Buf& q, int st0) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        run(q, u, st0 + u);
+        if ((st0 + u) % SP == SP - 1) flush(st0 + u - (SP - 1));
+      }
+    };
+    Buf b0, b1;
+    load(b0, 0);
+    constexpr int TAIL = 8 * (U >= SP ? U / SP : 1);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < TAIL; ++i) stg16(sink + (i & 7), make_uint4(0u, 0u, 0u, (uint32_t)i));
+    __builtin_amdgcn_sched_barrier(0);
+    for (int st = 0; st < nst; st += 2 * U) {
+      load(b1, st + U);
+      __builtin_amdgcn_sched_barrier(0);
+      batch(b0, st);
+      load(b0, st + 2 * U);
+      __builtin_amdgcn_sched_barrier(0);
+      batch(b1, st + U);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // fused small-group kernel: one small-group record (<= 16 rows of one adapter)
 // per workgroup, and a chunk of at most 64 * FW * FSL output columns.
 //
@@ -931,7 +1213,7 @@ __global__ __launch_bounds__(256) void small_shrink_kernel(FwdArgs p) {
     arow[nt] = (uint32_t)(j < r ? j : r - 1) * (uint32_t)p.d_in;
   }
   shrink_steps<1, NT, U>(acc, xrow, A, arow, kb + w * 32, 128, ke);
-  reduce_waves<NT>(acc, s_red);
+  reduce_waves<NT, NT>(acc, s_red);
   if (w == 0) {
     float* Hp = p.H + (int64_t)sl * p.hp_stride + (int64_t)e * 16 * p.ldh;
 #pragma unroll
@@ -1095,8 +1377,13 @@ hipError_t launch_expand_u(int grid, const FwdArgs& a, hipStream_t s) {
 }
 
 template <bool YB, bool R8>
-hipError_t launch_expand_ks(const OpLaunch& o, int grid, const FwdArgs& a, hipStream_t s) {
+hipError_t launch_expand_ks(const OpLaunch& o, int grid, int gridf, const FwdArgs& a, hipStream_t s) {
   const int ks = (o.r_max + 31) / 32;
+  // both block sizes, as in the shrink
+  hipError_t err = ks <= 1   ? launch(expand_fine_kernel<YB, R8, 1, YB ? 2 : 1>, gridf, a, s)
+                   : ks <= 2 ? launch(expand_fine_kernel<YB, R8, 2, YB ? 2 : 1>, gridf, a, s)
+                             : launch(expand_fine_kernel<YB, R8, 4, 1>, gridf, a, s);
+  if (err != hipSuccess) return err;
   if (ks <= 1) return launch_expand_u<YB, R8, 1>(grid, a, s);
   if (ks <= 2) return launch_expand_u<YB, R8, 2>(grid, a, s);
   return launch_expand_u<YB, R8, 4>(grid, a, s);
@@ -1124,8 +1411,16 @@ hipError_t launch_shrink_mfma(const OpLaunch& o, const void* X, int64_t ldx, flo
   a.ks_max = std::min(std::max(ks_max, 1), SHRINK_KS_MAX);   // the expand sums at most this many planes
   a.hp_stride = hp_stride;
   // (row block, d-slice) units: blocks x min(ks_max, 256 / blocks) <= max(blocks, 256)
-  const int grid = round8(std::min<long long>((long long)o.rb_ub * a.ks_max, 2048));
+  const int grid = round8(std::min<long long>((long long)o.coarse_ub * a.ks_max, 2048));
+  const int gridf = round8(std::min<long long>((long long)o.fine_ub * a.ks_max, 2048));
   const int nt = (o.r_max + 15) / 16;
+  // the plan picks the block size on the device: both kernels are launched and
+  // the one for the other size returns at once
+  hipError_t err = nt <= 1   ? launch(shrink_fine_kernel<1>, gridf, a, s)
+                   : nt <= 2 ? launch(shrink_fine_kernel<2>, gridf, a, s)
+                   : nt <= 4 ? launch(shrink_fine_kernel<4>, gridf, a, s)
+                             : launch(shrink_fine_kernel<8>, gridf, a, s);
+  if (err != hipSuccess) return err;
   const int u = env_int("LORA_SHRINK_U", 4);
   if (nt <= 1) return u == 2 ? launch(shrink_kernel<1, 2>, grid, a, s) : u == 1 ? launch(shrink_kernel<1, 1>, grid, a, s) : launch(shrink_kernel<1, 4>, grid, a, s);
   if (nt <= 2) return u == 2 ? launch(shrink_kernel<2, 2>, grid, a, s) : u == 1 ? launch(shrink_kernel<2, 1>, grid, a, s) : launch(shrink_kernel<2, 4>, grid, a, s);
@@ -1147,13 +1442,14 @@ hipError_t launch_expand_mfma(const OpLaunch& o, const float* H, int64_t ldh, in
   // width (whole pairs of 32-column steps) for measurements
   const int cw = env_int("LORA_EXPAND_CW", 0);
   a.cw = cw > 0 ? std::max(64, cw / 64 * 64) : 1024;
-  const long long units = (long long)o.rb_ub * ((o.d_out + a.cw - 1) / a.cw);
-  const int grid = round8(std::min<long long>(units, 4096));
+  const long long n_ch = (o.d_out + a.cw - 1) / a.cw;
+  const int grid = round8(std::min<long long>((long long)o.coarse_ub * n_ch, 4096));
+  const int gridf = round8(std::min<long long>((long long)o.fine_ub * n_ch, 4096));
   const bool yb = y_dtype == LORA_BF16;
-  if (yb && o.rank8) return launch_expand_ks<true, true>(o, grid, a, s);
-  if (yb) return launch_expand_ks<true, false>(o, grid, a, s);
-  if (o.rank8) return launch_expand_ks<false, true>(o, grid, a, s);
-  return launch_expand_ks<false, false>(o, grid, a, s);
+  if (yb && o.rank8) return launch_expand_ks<true, true>(o, grid, gridf, a, s);
+  if (yb) return launch_expand_ks<true, false>(o, grid, gridf, a, s);
+  if (o.rank8) return launch_expand_ks<false, true>(o, grid, gridf, a, s);
+  return launch_expand_ks<false, false>(o, grid, gridf, a, s);
 }
 
 template <bool YB, bool R8>

@@ -30,10 +30,13 @@ enum : int {
   HDR_NRB_TOTAL = 5,  // all entries: large-group blocks, then small-group entries
   HDR_NMRB = 6,       // trainable row-block entries (gradient path)
   HDR_NSMALL = 7,     // small-group records (fused path); equals NRB_TOTAL - NRB_LARGE
+  HDR_RB_ROWS = 8,    // rows per large-group block of this plan: RB_ROWS or RB_FINE
   HDR_WORDS = 64
 };
 
 constexpr int RB_ROWS = 256;     // rows per large-group row block
+constexpr int RB_FINE = 64;      // ... when the batch has fewer than FINE_BELOW such blocks
+constexpr int FINE_BELOW = 48;
 constexpr int SHRINK_KS_MAX = 4; // most d-slices of the grouped shrink inside lora_apply
 constexpr int SMALL_ROWS = 16;   // rows per small-group entry (one matrix-core column tile)
 constexpr int MRB_ROWS = 64;     // trainable rows per gradient row block
@@ -122,6 +125,7 @@ struct OpLaunch {
   int32_t r_max;
   bool rank8;                   // every live rank is a multiple of 8
   int32_t rb_ub;                // host upper bound of the entry count
+  int32_t coarse_ub, fine_ub;   // ... when the plan chose RB_ROWS / RB_FINE blocks (grouped kernels)
   int count_word;               // header word holding the entry count
   int first_word;               // header word holding the first entry (-1: 0)
 };

@@ -304,19 +304,27 @@ __global__ __launch_bounds__(PLAN_THREADS) void plan_kernel(PlanLaunch a) {
                                    m_n_act, unused);
   }
 
-  // ---- entry lists.  Large groups: blocks of RB_ROWS rows; small groups:
-  // entries of at most SMALL_ROWS rows, placed after every large-group block.
+  // ---- entry lists.  Large groups: blocks of RB_ROWS rows (RB_FINE rows when
+  // the batch has fewer than FINE_BELOW coarse blocks); small groups: entries
+  // of at most SMALL_ROWS rows, placed after every large-group block.
   const bool live = tid < S;
   const bool small = live && cnt > 0 && cnt <= a.small_max;
-  const int nbl = (live && cnt > a.small_max) ? (cnt + RB_ROWS - 1) / RB_ROWS : 0;
+  const bool large = live && cnt > a.small_max;
+  const int nbc = large ? (cnt + RB_ROWS - 1) / RB_ROWS : 0;
+  const int nbf = large ? (cnt + RB_FINE - 1) / RB_FINE : 0;
   const int nbs = small ? (cnt + SMALL_ROWS - 1) / SMALL_ROWS : 0;
   const int nbm = live ? (mcnt + MRB_ROWS - 1) / MRB_ROWS : 0;
-  int tot_l, tot_s, tot_m;
-  const int pl = block_excl_scan(nbl, s_wsum, tot_l);
+  int tot_c, tot_f, tot_s, tot_m;
+  const int pc = block_excl_scan(nbc, s_wsum, tot_c);
+  const int pf = block_excl_scan(nbf, s_wsum, tot_f);
   const int ps = block_excl_scan(nbs, s_wsum, tot_s);
   const int pm = block_excl_scan(nbm, s_wsum, tot_m);
+  // block size of the whole batch: fine blocks when coarse ones are too few
+  const bool fine = tot_c < FINE_BELOW;
+  const int rbr = fine ? RB_FINE : RB_ROWS, nbl = fine ? nbf : nbc, pl = fine ? pf : pc;
+  const int tot_l = fine ? tot_f : tot_c;
   for (int i = 0; i < nbl; ++i)
-    a.d.rb[pl + i] = make_int4(tid, off + i * RB_ROWS, min(RB_ROWS, cnt - i * RB_ROWS), 0);
+    a.d.rb[pl + i] = make_int4(tid, off + i * rbr, min(rbr, cnt - i * rbr), 0);
   for (int i = 0; i < nbs; ++i) {
     const int rows = min(SMALL_ROWS, cnt - i * SMALL_ROWS);
     a.d.rb[tot_l + ps + i] = make_int4(tid, off + i * SMALL_ROWS, rows, 1);
@@ -349,6 +357,7 @@ __global__ __launch_bounds__(PLAN_THREADS) void plan_kernel(PlanLaunch a) {
     h[HDR_MNACT] = m_n_act;
     h[HDR_NRB_LARGE] = tot_l;
     h[HDR_NRB_TOTAL] = tot_l + tot_s;
+    h[HDR_RB_ROWS] = rbr;
     h[HDR_NMRB] = tot_m;
     h[HDR_NSMALL] = tot_s;
   }
@@ -406,7 +415,7 @@ __global__ __launch_bounds__(T) void plan_small_kernel(PlanLaunch a) {
   __shared__ int s_sbase[LORA_MAX_SLOTS];
   __shared__ int s_seg[SEG ? SEG_STAGE : 1];
   __shared__ int s_efirst[WV], s_elast[WV];
-  __shared__ int s_w[7][PLAN_WAVES];
+  __shared__ int s_w[8][PLAN_WAVES];
   __shared__ unsigned s_flags;
 
   const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
@@ -513,13 +522,19 @@ __global__ __launch_bounds__(T) void plan_small_kernel(PlanLaunch a) {
   const int cnt = live ? s_cnt[tid] : 0;
   const int mcnt = MASKED ? (live ? s_mcnt[tid] : 0) : cnt;
   const bool small = live && cnt > 0 && cnt <= a.small_max;
-  const int nbl = (live && cnt > a.small_max) ? (cnt + RB_ROWS - 1) / RB_ROWS : 0;
+  const bool large = live && cnt > a.small_max;
+  const int nbc = large ? (cnt + RB_ROWS - 1) / RB_ROWS : 0;
+  const int nbf = large ? (cnt + RB_FINE - 1) / RB_FINE : 0;
   const int nbs = small ? (cnt + SMALL_ROWS - 1) / SMALL_ROWS : 0;
   const int nbm = live ? (mcnt + MRB_ROWS - 1) / MRB_ROWS : 0;
-  int v[7] = {cnt, mcnt, nbl, nbs, nbm, st ? 1 : 0, ed ? 1 : 0};
-  int tot[7];
-  block_scan_n<7, WV>(v, tot, s_w);
-  const int off = v[0], moff = v[1], pl = v[2], ps = v[3], pm = v[4];
+  int v[8] = {cnt, mcnt, nbc, nbs, nbm, st ? 1 : 0, ed ? 1 : 0, nbf};
+  int tot[8];
+  block_scan_n<8, WV>(v, tot, s_w);
+  const int off = v[0], moff = v[1], ps = v[3], pm = v[4];
+  // block size of the whole batch: fine blocks when coarse ones are too few
+  const bool fine = tot[2] < FINE_BELOW;
+  const int rbr = fine ? RB_FINE : RB_ROWS, nbl = fine ? nbf : nbc, pl = fine ? v[7] : v[2];
+  const int tot_l = fine ? tot[7] : tot[2];
   if (live) {
     d.counts[tid] = cnt;
     d.offsets[tid] = off;
@@ -530,10 +545,10 @@ __global__ __launch_bounds__(T) void plan_small_kernel(PlanLaunch a) {
     if (MASKED) s_moff[tid] = moff;
     s_sbase[tid] = small ? ps : -1;
     for (int i = 0; i < nbl; ++i)
-      d.rb[pl + i] = make_int4(tid, off + i * RB_ROWS, min(RB_ROWS, cnt - i * RB_ROWS), 0);
+      d.rb[pl + i] = make_int4(tid, off + i * rbr, min(rbr, cnt - i * rbr), 0);
     for (int i = 0; i < nbs; ++i) {
       const int rows = min(SMALL_ROWS, cnt - i * SMALL_ROWS);
-      d.rb[tot[2] + ps + i] = make_int4(tid, off + i * SMALL_ROWS, rows, 1);
+      d.rb[tot_l + ps + i] = make_int4(tid, off + i * SMALL_ROWS, rows, 1);
       SmallRec* r = d.srec + ps + i;
       r->A = my.A;
       r->B = my.B;
@@ -588,8 +603,9 @@ __global__ __launch_bounds__(T) void plan_small_kernel(PlanLaunch a) {
     h[HDR_NACT] = tot[0];
     h[HDR_NRUNS] = tot[5];
     h[HDR_MNACT] = tot[1];
-    h[HDR_NRB_LARGE] = tot[2];
-    h[HDR_NRB_TOTAL] = tot[2] + tot[3];
+    h[HDR_NRB_LARGE] = tot_l;
+    h[HDR_NRB_TOTAL] = tot_l + tot[3];
+    h[HDR_RB_ROWS] = rbr;
     h[HDR_NMRB] = tot[4];
     h[HDR_NSMALL] = tot[3];
   }
@@ -739,7 +755,7 @@ __global__ __launch_bounds__(PLAN_THREADS) void plan_scatter_kernel(PlanLaunch a
   __shared__ int s_off[LORA_MAX_SLOTS];
   __shared__ int s_cnt[LORA_MAX_SLOTS];
   __shared__ int s_sbase[LORA_MAX_SLOTS];
-  __shared__ int s_w[7][PLAN_WAVES];
+  __shared__ int s_w[8][PLAN_WAVES];
   __shared__ int s_misc[4];
 
   const int tid = threadIdx.x;
@@ -798,13 +814,19 @@ __global__ __launch_bounds__(PLAN_THREADS) void plan_scatter_kernel(PlanLaunch a
 
   const bool live = tid < S;
   const bool small = live && cnt > 0 && cnt <= a.small_max;
-  const int nbl = (live && cnt > a.small_max) ? (cnt + RB_ROWS - 1) / RB_ROWS : 0;
+  const bool large = live && cnt > a.small_max;
+  const int nbc = large ? (cnt + RB_ROWS - 1) / RB_ROWS : 0;
+  const int nbf = large ? (cnt + RB_FINE - 1) / RB_FINE : 0;
   const int nbs = small ? (cnt + SMALL_ROWS - 1) / SMALL_ROWS : 0;
   const int nbm = live ? (mcnt + MRB_ROWS - 1) / MRB_ROWS : 0;
-  int v[7] = {cnt, mcnt, nbl, nbs, nbm, st ? 1 : 0, ed ? 1 : 0};
-  int tot[7];
-  block_scan_n<7>(v, tot, s_w);            // (barriers inside: s_misc is visible after it)
-  const int off = v[0], moff = v[1], pl = v[2], ps = v[3], pm = v[4];
+  int v[8] = {cnt, mcnt, nbc, nbs, nbm, st ? 1 : 0, ed ? 1 : 0, nbf};
+  int tot[8];
+  block_scan_n<8>(v, tot, s_w);            // (barriers inside: s_misc is visible after it)
+  const int off = v[0], moff = v[1], ps = v[3], pm = v[4];
+  // block size of the whole batch: fine blocks when coarse ones are too few
+  const bool fine = tot[2] < FINE_BELOW;
+  const int rbr = fine ? RB_FINE : RB_ROWS, nbl = fine ? nbf : nbc, pl = fine ? v[7] : v[2];
+  const int tot_l = fine ? tot[7] : tot[2];
   if (live) {
     s_base[tid] = off + pre;
     if (MASKED) s_mbase[tid] = moff + mpre;
@@ -821,10 +843,10 @@ __global__ __launch_bounds__(PLAN_THREADS) void plan_scatter_kernel(PlanLaunch a
       d.m_offsets[tid] = moff;
       d.m_blk[tid] = pm;
       for (int i = 0; i < nbl; ++i)
-        d.rb[pl + i] = make_int4(tid, off + i * RB_ROWS, min(RB_ROWS, cnt - i * RB_ROWS), 0);
+        d.rb[pl + i] = make_int4(tid, off + i * rbr, min(rbr, cnt - i * rbr), 0);
       for (int i = 0; i < nbs; ++i) {
         const int rows = min(SMALL_ROWS, cnt - i * SMALL_ROWS);
-        d.rb[tot[2] + ps + i] = make_int4(tid, off + i * SMALL_ROWS, rows, 1);
+        d.rb[tot_l + ps + i] = make_int4(tid, off + i * SMALL_ROWS, rows, 1);
         SmallRec* r = d.srec + ps + i;
         r->A = my.A;
         r->B = my.B;
@@ -844,8 +866,9 @@ __global__ __launch_bounds__(PLAN_THREADS) void plan_scatter_kernel(PlanLaunch a
       h[HDR_NACT] = tot[0];
       h[HDR_NRUNS] = s_misc[1];
       h[HDR_MNACT] = tot[1];
-      h[HDR_NRB_LARGE] = tot[2];
-      h[HDR_NRB_TOTAL] = tot[2] + tot[3];
+      h[HDR_NRB_LARGE] = tot_l;
+      h[HDR_NRB_TOTAL] = tot_l + tot[3];
+      h[HDR_RB_ROWS] = rbr;
       h[HDR_NMRB] = tot[4];
       h[HDR_NSMALL] = tot[3];
     }

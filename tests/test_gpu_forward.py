@@ -244,3 +244,63 @@ def test_apply_empty_batch():
     L.shrink(plan, dev["X"], H)
     L.expand(plan, H, dev["Y"])
     torch.cuda.synchronize()
+
+
+def _grouped_case(seed, sizes, pad_none, ranks, d_in=256, d_out=136, y_dtype="f32"):
+    """A batch whose adapter groups have exactly the given sizes (rows shuffled),
+    plus pad_none rows without an adapter."""
+    S = len(sizes)
+    case = workloads.random_case(seed, n=sum(sizes) + pad_none, d_in=d_in, d_out=d_out,
+                                 num_slots=S, ranks=ranks, frac_none=0.0, y_dtype=y_dtype)
+    idx = np.concatenate([np.full(c, a, np.int32) for a, c in enumerate(sizes)] +
+                         [np.full(pad_none, -1, np.int32)])
+    case.idx = np.random.default_rng(seed).permutation(idx).astype(np.int32)
+    return case
+
+
+def _coarse_blocks(case):
+    """Large-group blocks of 256 rows the plan counts (groups above 16 rows when
+    n > 1024)."""
+    eff = effective(case)
+    cnt = np.bincount(eff[eff >= 0], minlength=case.num_slots)
+    small_max = 16 if case.n > 1024 else np.iinfo(np.int32).max
+    return int(sum((c + 255) // 256 for c in cnt if c > small_max))
+
+
+BLOCK_MODE_CASES = {
+    # 47 coarse blocks: the batch takes 64-row blocks
+    "fine_47": (dict(sizes=[17] * 47, pad_none=400, ranks=[8, 16, 32, 64, 128] * 9 + [16, 8]), False),
+    # 48: 256-row blocks
+    "coarse_48": (dict(sizes=[17] * 48, pad_none=400, ranks=[8, 16, 32, 64, 128] * 9 + [16, 8, 24]), True),
+    # ragged fine blocks: 1, 63, 64, 65, 255, 256, 257 rows and a long group
+    "fine_ragged": (dict(sizes=[257, 256, 255, 65, 64, 63, 1000, 17, 3, 1],
+                         pad_none=200, ranks=[64, 32, 16, 8, 48, 128, 40, 24, 16, 8]), False),
+    # long groups: many 256-row blocks with ragged ends
+    "coarse_long": (dict(sizes=[2900, 3100, 1, 2500, 3333, 1800], pad_none=500,
+                         ranks=[64, 16, 8, 32, 128, 40]), True),
+}
+
+
+@pytest.mark.parametrize("ydt", ["f32", "bf16"])
+@pytest.mark.parametrize("name", list(BLOCK_MODE_CASES))
+def test_apply_large_block_sizes(name, ydt):
+    """The plan cuts large groups into 256-row blocks, or into 64-row blocks when
+    that gives fewer than 48 of them; both grouped kernel pairs against the
+    oracle, on each side of the threshold and with ragged group ends."""
+    kw, coarse = BLOCK_MODE_CASES[name]
+    case = _grouped_case(31, y_dtype=ydt, **kw)
+    nb = _coarse_blocks(case)
+    assert (nb >= 48) == coarse, nb
+    say(f"apply block mode {name} ({nb} coarse blocks) y={ydt}")
+    Yo, _ = run_apply(case)
+    rel, mx = check_forward(case, Yo, effective(case))
+    say(f"  relF {rel:.3g} maxabs {mx:.3g}")
+    # the standalone shrink and expand take the same kernels
+    dev = case_to_device(case, DEV)
+    table = make_table(case, dev)
+    plan = make_plan(case, dev, table, mask=False)
+    H = L.shrink(plan, dev["X"])
+    Y = dev["Y"].clone()
+    L.expand(plan, H, Y)
+    torch.cuda.synchronize()
+    check_forward(case, from_torch(Y), effective(case))
