@@ -1,7 +1,7 @@
 // Forward kernels on the vector ALU for any mix of float32 / bfloat16 storage
 // (Section 3.4, LoRA layer equation).  Every dot product is a sequential
 // float32 fused multiply-add chain in index order, one thread per output, so
-// the result does not depend on the launch shape.
+// the result does not depend on the launch shape; the operands come from LDS.
 #include <algorithm>
 
 #include "device_common.h"
@@ -32,54 +32,160 @@ struct ValuArgs {
   int64_t ldy;
 };
 
-// H[t, j] = sum_k X[t, k] A[j, k]; one workgroup per entry, one thread per (row, j).
-template <bool XB, bool WB>
+// Work unit: an entry's rows in groups of VG; each group's operands are staged
+// in LDS (the next chunk's loads in flight while a chunk is used), so the
+// per-thread chains read LDS, not memory.
+constexpr int VG = 16;                 // rows per unit
+constexpr int VGROUPS = RB_ROWS / VG;  // most row groups of an entry
+
+// H[t, j] = sum_k X[t, k] A[j, k] for ranks up to RM, k staged in chunks of
+// VK (fewer, longer chunks for small ranks).  Thread pairs (row, j) = tid + 256 m.
+template <bool XB, bool WB, int RM>
 __global__ __launch_bounds__(256) void shrink_valu_kernel(ValuArgs p) {
+  constexpr int VK = RM <= 32 ? 256 : 64;
+  constexpr int PM = VG * RM / 256;                     // pairs per thread
+  constexpr int XL = VG * VK / 256;                     // X values per thread and chunk
+  constexpr int AL = RM * VK / 256;                     // A values per thread and chunk
+  constexpr int KS = VK + 4;                            // LDS row stride (16-byte rows)
+  __shared__ __align__(16) float s_x[VG][KS];
+  __shared__ __align__(16) float s_a[RM][KS];
+  const int tid = threadIdx.x;
   const int first = p.first_word >= 0 ? p.hdr[p.first_word] : 0;
   const int count = p.hdr[p.count_word] - first;
-  for (int e = blockIdx.x; e < count; e += gridDim.x) {
+  for (int tile = blockIdx.x; tile < count * VGROUPS; tile += gridDim.x) {
+    const int e = tile / VGROUPS, g = tile - e * VGROUPS;
     const int4 en = load_entry(p.rb, first + e);
-    const int a = en.x, p0 = en.y, rows = en.z;
+    const int a = en.x, rows = min(VG, en.z - g * VG), p0 = en.y + g * VG;
+    if (rows <= 0) continue;
     const Slot m = load_slot(p.meta, a);
     const int r = m.rank;
-    for (int q = threadIdx.x; q < rows * r; q += blockDim.x) {
-      const int i = q / r, j = q - i * r;
-      const int t = p.perm[p0 + i];
-      const int64_t xo = (int64_t)t * p.ldx, ao = (int64_t)j * p.d_in;
-      float acc = 0.0f;
-      for (int k = 0; k < p.d_in; ++k) acc = fmaf(ld<XB>(p.X, xo + k), ld<WB>(m.A, ao + k), acc);
-      p.H[(int64_t)t * p.ldh + j] = acc;
+    int xt[XL];
+#pragma unroll
+    for (int u = 0; u < XL; ++u) {
+      const int i = (tid + 256 * u) / VK;
+      xt[u] = p.perm[p0 + (i < rows ? i : rows - 1)];
+    }
+    float xv[XL], av[AL];
+    auto fetch = [&](int k0) {
+#pragma unroll
+      for (int u = 0; u < XL; ++u) {
+        const int k = k0 + (tid + 256 * u) % VK;
+        xv[u] = k < p.d_in ? ld<XB>(p.X, (int64_t)xt[u] * p.ldx + k) : 0.0f;
+      }
+#pragma unroll
+      for (int u = 0; u < AL; ++u) {
+        const int q = tid + 256 * u, j = q / VK, k = k0 + q % VK;
+        av[u] = (j < r && k < p.d_in) ? ld<WB>(m.A, (int64_t)j * p.d_in + k) : 0.0f;
+      }
+    };
+    float acc[PM];
+#pragma unroll
+    for (int i = 0; i < PM; ++i) acc[i] = 0.0f;
+    fetch(0);
+    for (int k0 = 0; k0 < p.d_in; k0 += VK) {
+      __syncthreads();                 // the previous chunk's reads are done
+#pragma unroll
+      for (int u = 0; u < XL; ++u) s_x[(tid + 256 * u) / VK][(tid + 256 * u) % VK] = xv[u];
+#pragma unroll
+      for (int u = 0; u < AL; ++u) s_a[(tid + 256 * u) / VK][(tid + 256 * u) % VK] = av[u];
+      __syncthreads();
+      if (k0 + VK < p.d_in) fetch(k0 + VK);
+      const int kn = min(VK, p.d_in - k0);
+#pragma unroll
+      for (int mm = 0; mm < PM; ++mm) {
+        const int q = tid + 256 * mm, i = q / max(r, 1), j = q - i * max(r, 1);
+        if (r == 0 || i >= rows) continue;
+        // kn is a multiple of 8 (so is every dimension)
+        float c = acc[mm];
+#pragma unroll 8
+        for (int kk = 0; kk < kn; kk += 4) {
+          const float4 x4 = *reinterpret_cast<const float4*>(&s_x[i][kk]);
+          const float4 a4 = *reinterpret_cast<const float4*>(&s_a[j][kk]);
+          c = fmaf(x4.x, a4.x, c);
+          c = fmaf(x4.y, a4.y, c);
+          c = fmaf(x4.z, a4.z, c);
+          c = fmaf(x4.w, a4.w, c);
+        }
+        acc[mm] = c;
+      }
+    }
+#pragma unroll
+    for (int mm = 0; mm < PM; ++mm) {
+      const int q = tid + 256 * mm, i = q / max(r, 1), j = q - i * max(r, 1);
+      if (r == 0 || i >= rows) continue;
+      p.H[(int64_t)p.perm[p0 + i] * p.ldh + j] = acc[mm];
     }
   }
 }
 
-// Y[t, o] += s * sum_j H[t, j] B[o, j]; workgroup per (entry, 256 columns).
+// Y[t, o] += s * sum_j H[t, j] B[o, j]; unit = (entry, 256 columns, row group),
+// thread = column, the group's H rows staged in LDS.
 template <bool WB, bool YB>
 __global__ __launch_bounds__(256) void expand_valu_kernel(ValuArgs p) {
+  constexpr int HL = VG * LORA_MAX_RANK / 256;          // H values per thread
+  constexpr int JB = 32;                                // B values per thread in flight
+  __shared__ float s_h[VG][LORA_MAX_RANK];
+  const int tid = threadIdx.x;
   const int first = p.first_word >= 0 ? p.hdr[p.first_word] : 0;
   const int count = p.hdr[p.count_word] - first;
   const int n_ot = (p.d_out + 255) / 256;
-  for (int tile = blockIdx.x; tile < count * n_ot; tile += gridDim.x) {
-    const int e = tile / n_ot, o = (tile - e * n_ot) * 256 + (int)threadIdx.x;
-    if (o >= p.d_out) continue;
+  for (int tile = blockIdx.x; tile < count * n_ot * VGROUPS; tile += gridDim.x) {
+    const int g = tile % VGROUPS, eo = tile / VGROUPS;
+    const int e = eo / n_ot, o = (eo - e * n_ot) * 256 + tid;
     const int4 en = load_entry(p.rb, first + e);
-    const int a = en.x, p0 = en.y, rows = en.z;
+    const int a = en.x, rows = min(VG, en.z - g * VG), p0 = en.y + g * VG;
+    if (rows <= 0) continue;
     const Slot m = load_slot(p.meta, a);
     const int r = m.rank;
     const float s = m.scale;
-    for (int i = 0; i < rows; ++i) {
-      const int t = p.perm[p0 + i];
-      const float* h = p.H + (int64_t)t * p.ldh;
-      float acc = 0.0f;
-      for (int j = 0; j < r; ++j) acc = fmaf(h[j], ld<WB>(m.B, (int64_t)o * r + j), acc);
-      const int64_t yo = (int64_t)t * p.ldy + o;
-      if (YB) {
-        uint16_t* Y = reinterpret_cast<uint16_t*>(p.Y);
-        Y[yo] = (uint16_t)f32_to_bf16_rne(fmaf(s, acc, bf16_to_f32(Y[yo])));
-      } else {
-        float* Y = reinterpret_cast<float*>(p.Y);
-        Y[yo] = fmaf(s, acc, Y[yo]);
+    // B (first JB ranks) and Y of this thread's column are requested together
+    // with H, so the unit costs one round trip after the slot
+    const bool ov = o < p.d_out;
+    const int oc = ov ? o : p.d_out - 1;
+    int yt[VG];
+    float yv[VG];
+#pragma unroll
+    for (int i = 0; i < VG; ++i) {
+      yt[i] = p.perm[p0 + (i < rows ? i : rows - 1)];
+      const int64_t yo = (int64_t)yt[i] * p.ldy + oc;
+      yv[i] = YB ? bf16_to_f32(reinterpret_cast<const uint16_t*>(p.Y)[yo])
+                 : reinterpret_cast<const float*>(p.Y)[yo];
+    }
+    float b[JB];
+    auto fetch_b = [&](int j0) {
+#pragma unroll
+      for (int jj = 0; jj < JB; ++jj)
+        b[jj] = j0 + jj < r ? ld<WB>(m.B, (int64_t)oc * r + j0 + jj) : 0.0f;
+    };
+    fetch_b(0);
+    __syncthreads();                   // the previous unit's reads of s_h are done
+#pragma unroll
+    for (int u = 0; u < HL; ++u) {
+      const int q = tid + 256 * u, i = q / LORA_MAX_RANK, j = q % LORA_MAX_RANK;
+      s_h[i][j] = (i < rows && j < r) ? p.H[(int64_t)p.perm[p0 + i] * p.ldh + j] : 0.0f;
+    }
+    __syncthreads();
+    float acc[VG];
+#pragma unroll
+    for (int i = 0; i < VG; ++i) acc[i] = 0.0f;
+    for (int j0 = 0; j0 < r; j0 += JB) {
+      if (j0 > 0) fetch_b(j0);
+      const int jn = min(JB, r - j0);
+#pragma unroll
+      for (int jj = 0; jj < JB; ++jj) {
+        if (jj >= jn) break;
+#pragma unroll
+        for (int i = 0; i < VG; ++i) acc[i] = fmaf(s_h[i][j0 + jj], b[jj], acc[i]);
       }
+    }
+    if (!ov) continue;
+#pragma unroll
+    for (int i = 0; i < VG; ++i) {
+      if (i >= rows) break;
+      const int64_t yo = (int64_t)yt[i] * p.ldy + o;
+      const float y = fmaf(s, acc[i], yv[i]);
+      if (YB) reinterpret_cast<uint16_t*>(p.Y)[yo] = (uint16_t)f32_to_bf16_rne(y);
+      else reinterpret_cast<float*>(p.Y)[yo] = y;
     }
   }
 }
@@ -107,12 +213,20 @@ hipError_t launch_shrink_valu(const OpLaunch& o, const void* X, lora_dtype x_dty
   a.ldx = ldx;
   a.H = H;
   a.ldh = ldh;
-  const int grid = std::max(1, std::min(o.rb_ub, 4096));
+  const int grid = (int)std::max<long long>(1, std::min<long long>((long long)o.rb_ub * VGROUPS, 4096));
   const bool xb = x_dtype == LORA_BF16, wb = w_dtype == LORA_BF16;
-  if (xb && wb) hipLaunchKernelGGL((shrink_valu_kernel<true, true>), dim3(grid), dim3(256), 0, s, a);
-  else if (xb) hipLaunchKernelGGL((shrink_valu_kernel<true, false>), dim3(grid), dim3(256), 0, s, a);
-  else if (wb) hipLaunchKernelGGL((shrink_valu_kernel<false, true>), dim3(grid), dim3(256), 0, s, a);
-  else hipLaunchKernelGGL((shrink_valu_kernel<false, false>), dim3(grid), dim3(256), 0, s, a);
+  if (o.r_max <= 32) {
+    if (xb && wb) hipLaunchKernelGGL((shrink_valu_kernel<true, true, 32>), dim3(grid), dim3(256), 0, s, a);
+    else if (xb) hipLaunchKernelGGL((shrink_valu_kernel<true, false, 32>), dim3(grid), dim3(256), 0, s, a);
+    else if (wb) hipLaunchKernelGGL((shrink_valu_kernel<false, true, 32>), dim3(grid), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((shrink_valu_kernel<false, false, 32>), dim3(grid), dim3(256), 0, s, a);
+  } else {
+    constexpr int R = LORA_MAX_RANK;
+    if (xb && wb) hipLaunchKernelGGL((shrink_valu_kernel<true, true, R>), dim3(grid), dim3(256), 0, s, a);
+    else if (xb) hipLaunchKernelGGL((shrink_valu_kernel<true, false, R>), dim3(grid), dim3(256), 0, s, a);
+    else if (wb) hipLaunchKernelGGL((shrink_valu_kernel<false, true, R>), dim3(grid), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((shrink_valu_kernel<false, false, R>), dim3(grid), dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 
@@ -124,7 +238,7 @@ hipError_t launch_expand_valu(const OpLaunch& o, const float* H, int64_t ldh,
   a.ldh = ldh;
   a.Y = Y;
   a.ldy = ldy;
-  const long long tiles = (long long)o.rb_ub * ((o.d_out + 255) / 256);
+  const long long tiles = (long long)o.rb_ub * ((o.d_out + 255) / 256) * VGROUPS;
   const int grid = (int)std::max<long long>(1, std::min<long long>(tiles, 8192));
   const bool wb = w_dtype == LORA_BF16, yb = y_dtype == LORA_BF16;
   if (wb && yb) hipLaunchKernelGGL((expand_valu_kernel<true, true>), dim3(grid), dim3(256), 0, s, a);
