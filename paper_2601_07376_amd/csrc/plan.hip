@@ -493,7 +493,25 @@ __global__ __launch_bounds__(T) void plan_small_kernel(PlanLaunch a) {
   __syncthreads();
 
   // ---- 3. cursors (exclusive prefix over waves) and run boundaries
-  for (int k0 = 0; k0 < S * PLAN_WAVES; k0 += T) {
+  if constexpr (WV <= 4) {
+    // few waves: one thread per adapter walks its WV counters
+    if (tid < S) {
+      int c = 0, cm = 0;
+#pragma unroll
+      for (int ww = 0; ww < WV; ++ww) {
+        const int x = s_wc[tid * PLAN_WAVES + ww];
+        s_wc[tid * PLAN_WAVES + ww] = (unsigned short)c;
+        c += x;
+        if (MASKED) {
+          const int xm = s_wcm[tid * PLAN_WAVES + ww];
+          s_wcm[tid * PLAN_WAVES + ww] = (unsigned short)cm;
+          cm += xm;
+        }
+      }
+      s_cnt[tid] = c;
+      if (MASKED) s_mcnt[tid] = cm;
+    }
+  } else for (int k0 = 0; k0 < S * PLAN_WAVES; k0 += T) {
     const int k = k0 + tid;
     const bool act = k < S * PLAN_WAVES;
     const int v = act ? (int)s_wc[k] : 0;
@@ -527,9 +545,22 @@ __global__ __launch_bounds__(T) void plan_small_kernel(PlanLaunch a) {
   const int nbf = large ? (cnt + RB_FINE - 1) / RB_FINE : 0;
   const int nbs = small ? (cnt + SMALL_ROWS - 1) / SMALL_ROWS : 0;
   const int nbm = live ? (mcnt + MRB_ROWS - 1) / MRB_ROWS : 0;
-  int v[8] = {cnt, mcnt, nbc, nbs, nbm, st ? 1 : 0, ed ? 1 : 0, nbf};
-  int tot[8];
-  block_scan_n<8, WV>(v, tot, s_w);
+  // eight scans as four: pairs packed in 16-bit halves (every total is at
+  // most n <= 1024, so nothing carries into the upper half)
+  int pv[4] = {cnt | (mcnt << 16), nbc | (nbs << 16), nbm | (nbf << 16),
+               (st ? 1 : 0) | ((ed ? 1 : 0) << 16)};
+  int ptot[4];
+  block_scan_n<4, WV>(pv, ptot, s_w);
+  int v[8], tot[8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int lo = i == 0 ? 0 : i == 1 ? 2 : i == 2 ? 4 : 5;
+    const int hi = i == 0 ? 1 : i == 1 ? 3 : i == 2 ? 7 : 6;
+    v[lo] = pv[i] & 0xffff;
+    v[hi] = (int)((unsigned)pv[i] >> 16);
+    tot[lo] = ptot[i] & 0xffff;
+    tot[hi] = (int)((unsigned)ptot[i] >> 16);
+  }
   const int off = v[0], moff = v[1], ps = v[3], pm = v[4];
   // block size of the whole batch: fine blocks when coarse ones are too few
   const bool fine = tot[2] < FINE_BELOW;
