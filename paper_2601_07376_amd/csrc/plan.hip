@@ -413,6 +413,7 @@ __global__ __launch_bounds__(T) void plan_small_kernel(PlanLaunch a) {
   __shared__ int s_off[LORA_MAX_SLOTS];
   __shared__ int s_moff[MASKED ? LORA_MAX_SLOTS : 1];
   __shared__ int s_sbase[LORA_MAX_SLOTS];
+  __shared__ int s_last[LORA_MAX_SLOTS];      // each group's last row
   __shared__ int s_seg[SEG ? SEG_STAGE : 1];
   __shared__ int s_efirst[WV], s_elast[WV];
   __shared__ int s_w[8][PLAN_WAVES];
@@ -438,7 +439,10 @@ __global__ __launch_bounds__(T) void plan_small_kernel(PlanLaunch a) {
     s_wc[i] = 0;
     if (MASKED) s_wcm[i] = 0;
   }
-  if (tid < S) s_rank[tid] = my.rank;
+  if (tid < S) {
+    s_rank[tid] = my.rank;
+    s_last[tid] = -1;
+  }
   __syncthreads();
 
   uint32_t flags = 0u;
@@ -482,6 +486,7 @@ __global__ __launch_bounds__(T) void plan_small_kernel(PlanLaunch a) {
   const uint64_t peers = match_peers(e + 1, nbits);
   const int rank_in = __popcll(peers & lt);
   if (e >= 0 && rank_in == 0) s_wc[e * PLAN_WAVES + w] = (unsigned short)__popcll(peers);
+  if (e >= 0 && rank_in == __popcll(peers) - 1) atomicMax(&s_last[e], tid);
   int mrank_in = 0;
   if (MASKED) {
     const uint64_t mpeers = match_peers(em + 1, nbits);
@@ -580,13 +585,21 @@ __global__ __launch_bounds__(T) void plan_small_kernel(PlanLaunch a) {
     for (int i = 0; i < nbs; ++i) {
       const int rows = min(SMALL_ROWS, cnt - i * SMALL_ROWS);
       d.rb[tot_l + ps + i] = make_int4(tid, off + i * SMALL_ROWS, rows, 1);
-      SmallRec* r = d.srec + ps + i;
-      r->A = my.A;
-      r->B = my.B;
-      r->rows = rows;
-      r->rank = my.rank;
-      r->scale = my.scale;
-      r->adapter = tid;
+      // the record's first 32 bytes as two 16-byte stores
+      int4* r4 = reinterpret_cast<int4*>(d.srec + ps + i);
+      const uint64_t pa = reinterpret_cast<uint64_t>(my.A), pb = reinterpret_cast<uint64_t>(my.B);
+      r4[0] = make_int4((int)(uint32_t)pa, (int)(uint32_t)(pa >> 32), (int)(uint32_t)pb,
+                        (int)(uint32_t)(pb >> 32));
+      r4[1] = make_int4(rows, my.rank, __float_as_int(my.scale), tid);
+    }
+    if (nbs > 0) {
+      // padding slots of the group's last record repeat its last row (the
+      // scatter below writes the real slots)
+      const int lr = s_last[tid];
+      int* rr = d.srec[ps + nbs - 1].row;
+      int j = cnt - (nbs - 1) * SMALL_ROWS;
+      for (; j < SMALL_ROWS && (j & 3) != 0; ++j) rr[j] = lr;
+      for (; j < SMALL_ROWS; j += 4) *reinterpret_cast<int4*>(rr + j) = make_int4(lr, lr, lr, lr);
     }
     for (int i = 0; i < nbm; ++i)
       d.mrb[pm + i] = make_int4(tid, moff + i * MRB_ROWS, min(MRB_ROWS, mcnt - i * MRB_ROWS), 0);
@@ -615,8 +628,6 @@ __global__ __launch_bounds__(T) void plan_small_kernel(PlanLaunch a) {
       SmallRec* r = d.srec + q;
       const int j = rel % SMALL_ROWS;
       r->row[j] = tid;
-      if (rel == s_cnt[e] - 1)
-        for (int jj = j + 1; jj < SMALL_ROWS; ++jj) r->row[jj] = tid;
     }
   }
   if (MASKED && em >= 0) {
