@@ -808,6 +808,11 @@ __global__ __launch_bounds__(256) void shrink_fine_kernel(FwdArgs p) {
       load(b0, i + 2);
       __builtin_amdgcn_sched_barrier(0);
       compute(b1);
+      // wait states on the back edge between the last product and the loop
+      // head, where the compiler may read an accumulator register
+      __builtin_amdgcn_sched_barrier(0);
+      asm volatile("s_nop 7");
+      __builtin_amdgcn_sched_barrier(0);
     }
     mfma_fence();
     vmem_drained();

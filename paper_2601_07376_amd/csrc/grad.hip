@@ -160,6 +160,11 @@ __device__ __forceinline__ void rows_times_w2(f32x4 (&acc_h)[MT * NT], f32x4 (&a
       __builtin_amdgcn_sched_barrier(0);
       compute(h1, acc_h, false);
       compute(g1, acc_g, true);
+      // wait states on the back edge between the last product and the loop
+      // head, where the compiler may read an accumulator register
+      __builtin_amdgcn_sched_barrier(0);
+      asm volatile("s_nop 7");
+      __builtin_amdgcn_sched_barrier(0);
     }
   } else {
     for (int i = 0; i < rounds; ++i) {
