@@ -52,6 +52,12 @@ FUZZ = [
     ("empty", lambda r: (np.zeros(0, np.int64), 3, None)),
     ("one_row", lambda r: (np.array([2]), 3, np.array([1]))),
     ("ragged_65", lambda r: (r.integers(-1, 9, 65), 9, r.integers(0, 2, 65))),
+    # edges of the 256-thread grouping (n <= 256 and slots <= 256) and of the
+    # 1024-thread one
+    ("t256_full", lambda r: (r.integers(-1, 256, 256), 256, r.integers(0, 2, 256))),
+    ("t256_slots_past", lambda r: (r.integers(-1, 300, 200), 300, r.integers(0, 2, 200))),
+    ("t256_rows_past", lambda r: (r.integers(-1, 64, 257), 64, r.integers(0, 2, 257))),
+    ("t1024_full", lambda r: (r.integers(-1, 1024, 1024), 1024, r.integers(0, 2, 1024))),
     ("long_runs", lambda r: (np.repeat(r.integers(-1, 12, 400), 37)[:13001], 12,
                              r.integers(0, 2, 13001))),
     ("large_n", lambda r: (r.integers(-1, 50, 70001), 50, r.integers(0, 2, 70001))),
