@@ -6,15 +6,16 @@ with the HIP library (no kernels, headers, helpers or constants).
 
 Parity pins (tests/test_oracle_pins.py): hand-derived worked examples in
 tests/golden/, scalar brute force on tiny inputs, exact linearity of the
-masked loss in A and in B (pins the backward), closed forms for permutation /
-diagonal / rank-1 adapters, integer-valued exactness, and planted-mistake
-checks that each pin rejects.  No function here is "parity unpinned".
+masked loss in A, in B and in X (pins the backward and the input gradient),
+closed forms for permutation / diagonal / rank-1 adapters, integer-valued
+exactness, and planted-mistake checks that each pin rejects.  No function here is "parity unpinned".
 """
 from .lora_oracle import (effective_ids, canonical_plan, plan_bruteforce,
                           segments_to_ids, shrink, expand, apply, delta_rows,
-                          apply_bruteforce, grad, grad_bruteforce, masked_loss,
-                          rel_fro, max_abs)
+                          apply_bruteforce, grad, grad_bruteforce, grad_x,
+                          grad_x_bruteforce, masked_loss, rel_fro, max_abs)
 
 __all__ = ["effective_ids", "canonical_plan", "plan_bruteforce", "segments_to_ids",
            "shrink", "expand", "apply", "delta_rows", "apply_bruteforce", "grad",
-           "grad_bruteforce", "masked_loss", "rel_fro", "max_abs"]
+           "grad_bruteforce", "grad_x", "grad_x_bruteforce", "masked_loss", "rel_fro",
+           "max_abs"]

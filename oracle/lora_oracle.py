@@ -20,6 +20,9 @@ widening bfloat16 or binary32 to float64 is exact):
   write the backward; it is the chain rule on the LoRA equation:
   with H = X_m A_a^T and G = dY_m B_a,  dB_a = s_a dY_m^T H  and
   dA_a = s_a G^T X_m.
+* ``grad_x`` -- the input gradient through the same residual over the same
+  masked rows, dX_t += s_a (dY_t B_a) A_a (the chain rule on the LoRA equation
+  with respect to x; rows outside T_a^m are left as they are).
 * ``*_bruteforce`` -- scalar Python loops over the same definitions, used only
   as an independent pin on tiny inputs.
 
@@ -315,11 +318,47 @@ def grad_bruteforce(eff, mask, X, dY, A, B, scale):
     return dA, dB
 
 
+def grad_x(eff, mask, dY, A, B, scale, dX):
+    """dX_out = dX + s_a (dY_t B_a) A_a for every row t in T_a^m = {t : eff[t] = a
+    and mask[t] != 0}; every other row of dX is returned unchanged (bit-identical).
+    dY is [n, d_out], dX [n, d_in]; returns a new float64 array.
+    """
+    out = np.array(dX, dtype=np.float64, copy=True)
+    for a in range(len(A)):
+        if A[a] is None:
+            continue
+        sel = eff == a
+        if mask is not None:
+            sel = sel & (np.asarray(mask) != 0)
+        rows = np.nonzero(sel)[0]
+        if rows.size == 0:
+            continue
+        out[rows] = out[rows] + float(scale[a]) * ((dY[rows] @ B[a]) @ A[a])
+    return out
+
+
+def grad_x_bruteforce(eff, mask, dY, A, B, scale, dX):
+    """Scalar loops for the input gradient (tiny inputs only)."""
+    n, d_out = dY.shape
+    out = [[float(v) for v in row] for row in np.asarray(dX, np.float64)]
+    for t in range(n):
+        a = int(eff[t])
+        if a < 0 or A[a] is None or (mask is not None and mask[t] == 0):
+            continue
+        r, d_in = A[a].shape
+        s = float(scale[a])
+        g = [sum(float(dY[t][o]) * float(B[a][o][j]) for o in range(d_out)) for j in range(r)]
+        for k in range(d_in):
+            out[t][k] = out[t][k] + s * sum(g[j] * float(A[a][j][k]) for j in range(r))
+    return np.array(out)
+
+
 def masked_loss(eff, mask, X, dY, A, B, scale):
     """L = sum over masked rows t with an adapter of <dY_t, Delta_t>.
 
-    L is linear in each A_a (B fixed) and in each B_a (A fixed), and its partial
-    derivatives are exactly dA_a and dB_a; the tests use this to pin ``grad``.
+    L is linear in each A_a (B fixed), in each B_a (A fixed) and in X, and its
+    partial derivatives are exactly dA_a, dB_a and dX; the tests use this to pin
+    ``grad`` and ``grad_x``.
     """
     total = 0.0
     for a in range(len(A)):

@@ -236,10 +236,58 @@ def check_grad_mask_exact(impl):
     return True
 
 
+def check_grad_x_linearity(impl):
+    """L(X + eps E) - L(X) = eps <dX, E> exactly up to f64 rounding: the masked
+    loss is linear in X, and it is evaluated by the forward oracle."""
+    for seed in range(4):
+        c, eff, X, A, B, Y, dY = _tiny_case(400 + seed, n=17, mask_p=0.6)
+        dX = impl.grad_x(eff, c.mask, dY, A, B, c.scales, np.zeros_like(X))
+        L0 = oracle.masked_loss(eff, c.mask, X, dY, A, B, c.scales)
+        E = np.random.default_rng(seed).standard_normal(X.shape)
+        eps = 0.29
+        L1 = oracle.masked_loss(eff, c.mask, X + eps * E, dY, A, B, c.scales)
+        pred = eps * float(np.sum(dX * E))
+        if abs((L1 - L0) - pred) > 1e-10 * max(1.0, abs(pred), abs(L0)):
+            return False
+    return True
+
+
+def check_grad_x_bruteforce(impl):
+    for seed in range(3):
+        c, eff, X, A, B, Y, dY = _tiny_case(500 + seed, n=11, d_in=5, d_out=4, mask_p=0.5)
+        dX0 = np.random.default_rng(seed).standard_normal(X.shape)
+        got = impl.grad_x(eff, c.mask, dY, A, B, c.scales, dX0)
+        ref = oracle.grad_x_bruteforce(eff, c.mask, dY, A, B, c.scales, dX0)
+        if not np.allclose(got, ref, rtol=1e-12, atol=1e-12):
+            return False
+    return True
+
+
+def check_grad_x_dense_and_untouched(impl):
+    """One adapter, no mask: dX + s dY (B A) by numpy in the other association.
+    Rows with id -1 or mask 0 come back bit-identical, whatever their dY holds."""
+    c, eff, X, A, B, Y, dY = _tiny_case(600, n=9, S=1, frac_none=0.0, mask_p=0.5)
+    dX0 = np.random.default_rng(1).standard_normal(X.shape)
+    got = impl.grad_x(eff, None, dY, A, B, c.scales, dX0)
+    ref = dX0 + float(c.scales[0]) * (dY @ (B[0] @ A[0]))
+    if not np.allclose(got, ref, rtol=1e-12, atol=1e-12):
+        return False
+    c, eff, X, A, B, Y, dY = _tiny_case(601, n=19, mask_p=0.5, frac_none=0.3)
+    out = (c.mask == 0) | (eff < 0)
+    dYj = dY.copy()
+    junk = np.array([np.nan, np.inf, -np.inf, 1e30])
+    dYj[out] = junk[np.arange(dYj[out].size) % 4].reshape(dYj[out].shape)
+    dX0 = np.random.default_rng(2).standard_normal(X.shape)
+    got = impl.grad_x(eff, c.mask, dYj, A, B, c.scales, dX0)
+    clean = impl.grad_x(eff, c.mask, np.where(out[:, None], 0.0, dY), A, B, c.scales, dX0)
+    return got[out].tobytes() == dX0[out].tobytes() and got.tobytes() == clean.tobytes()
+
+
 ALL_CHECKS = [check_plan_golden, check_plan_bruteforce, check_forward_golden,
               check_forward_bruteforce, check_forward_closed_form,
               check_forward_integer_exact, check_grad_golden, check_grad_linearity,
-              check_grad_bruteforce, check_grad_mask_exact]
+              check_grad_bruteforce, check_grad_mask_exact, check_grad_x_linearity,
+              check_grad_x_bruteforce, check_grad_x_dense_and_untouched]
 
 
 # ----------------------------------------------------------------------------
@@ -334,7 +382,8 @@ def test_explicit_mask_not_inferred_from_zero_dy():
 
 def _mutant(**overrides):
     ns = types.SimpleNamespace(canonical_plan=oracle.canonical_plan, apply=oracle.apply,
-                               grad=oracle.grad, masked_loss=oracle.masked_loss)
+                               grad=oracle.grad, grad_x=oracle.grad_x,
+                               masked_loss=oracle.masked_loss)
     for k, v in overrides.items():
         setattr(ns, k, v)
     return ns
@@ -396,6 +445,33 @@ def _grad_mask_multiplied(eff, mask, X, dY, A, B, scale, H_saved=None):
     return oracle.grad(eff, None, X * m, dY * m, A, B, scale)
 
 
+def _grad_x_mask_ignored(eff, mask, dY, A, B, scale, dX):
+    return oracle.grad_x(eff, None, dY, A, B, scale, dX)
+
+
+def _grad_x_no_scale(eff, mask, dY, A, B, scale, dX):
+    return oracle.grad_x(eff, mask, dY, A, B, np.ones_like(scale), dX)
+
+
+def _grad_x_sign(eff, mask, dY, A, B, scale, dX):
+    return 2 * np.asarray(dX, np.float64) - oracle.grad_x(eff, mask, dY, A, B, scale, dX)
+
+
+def _grad_x_overwrites(eff, mask, dY, A, B, scale, dX):
+    # the delta stored instead of added
+    d = oracle.grad_x(eff, mask, dY, A, B, scale, np.zeros_like(dX))
+    sel = np.any(d != 0, axis=1)
+    out = np.array(dX, dtype=np.float64, copy=True)
+    out[sel] = d[sel]
+    return out
+
+
+def _grad_x_wrong_weight(eff, mask, dY, A, B, scale, dX):
+    # A reversed along d_in (a transposed or mis-indexed operand)
+    return oracle.grad_x(eff, mask, dY, [a[:, ::-1] if a is not None else None for a in A], B,
+                         scale, dX)
+
+
 def _plan_unstable(idx, num_slots, mask=None, ranks=None):
     p = oracle.canonical_plan(idx, num_slots, mask=mask, ranks=ranks)
     p = dict(p)
@@ -433,6 +509,11 @@ MUTANTS = {
     "grad_sign": _mutant(grad=_grad_sign),
     "grad_no_scale": _mutant(grad=_grad_no_scale),
     "grad_mask_multiplied": _mutant(grad=_grad_mask_multiplied),
+    "grad_x_mask_ignored": _mutant(grad_x=_grad_x_mask_ignored),
+    "grad_x_no_scale": _mutant(grad_x=_grad_x_no_scale),
+    "grad_x_sign": _mutant(grad_x=_grad_x_sign),
+    "grad_x_overwrites": _mutant(grad_x=_grad_x_overwrites),
+    "grad_x_wrong_weight": _mutant(grad_x=_grad_x_wrong_weight),
     "plan_unstable": _mutant(canonical_plan=_plan_unstable),
     "plan_inclusive_offsets": _mutant(canonical_plan=_plan_inclusive_offsets),
     "plan_mask_ignored": _mutant(canonical_plan=_plan_mask_ignored),
