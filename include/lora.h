@@ -215,6 +215,21 @@ lora_status lora_grad(const lora_plan* p, const void* X, lora_dtype x_dtype, int
                       int64_t ldh, float* const* dA, float* const* dB, int32_t accumulate,
                       void* ws, size_t ws_bytes, void* stream);
 
+/* Input gradient through the adapter residual (the chain rule on the LoRA
+ * layer equation of Section 3.4 with respect to x; same masked rows T_a^m as
+ * lora_grad, Sections 3.3 and 3.5):
+ *     dX[t] += s_a (dY[t] B_a) A_a      for every t in T_a^m,
+ * every other row of dX untouched (rows with mask 0 or id -1 are never read).
+ * dY: device [n, lddy] bfloat16 (the table's weights must be bfloat16 too);
+ * dX: device [n, lddx] float32 or bfloat16, updated in place (one rounding
+ * per element for bfloat16).  ws: lora_grad_x_workspace_bytes(p) bytes,
+ * 16-byte aligned.  Errors: LORA_ERR_DTYPE for other dtypes, and the common
+ * argument errors.  Asynchronous on stream. */
+size_t      lora_grad_x_workspace_bytes(const lora_plan* p);
+lora_status lora_grad_x(const lora_plan* p, const void* dY, lora_dtype dy_dtype, int64_t lddy,
+                        void* dX, lora_dtype dx_dtype, int64_t lddx, void* ws, size_t ws_bytes,
+                        void* stream);
+
 #ifdef __cplusplus
 }
 #endif

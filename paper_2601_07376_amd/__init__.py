@@ -1,15 +1,15 @@
 """Mixed-adapter LoRA layer for AMD Instinct MI355X (gfx950).
 
 Python face of liblora_mi355x.so (include/lora.h): ``Table`` (adapter table),
-``Plan`` (row grouping by adapter id), ``shrink``, ``expand``, ``apply`` and
-``grad``.  Torch supplies device memory and streams; the computation runs in
+``Plan`` (row grouping by adapter id), ``shrink``, ``expand``, ``apply``,
+``grad`` and ``grad_x``.  Torch supplies device memory and streams; the computation runs in
 the library's HIP kernels.  Nothing here falls back to another implementation:
 if the library is not built, every call raises.
 """
 from .lora import (LORA_BF16, LORA_DATA_BAD_ID, LORA_DATA_BAD_SEGMENTS, LORA_DATA_EMPTY_SLOT,
                    LORA_F32, LIB_PATH, LoraError, Plan, Table, apply, apply_workspace, expand,
-                   grad, grad_workspace, lib, shrink)
+                   grad, grad_workspace, grad_x, grad_x_workspace, lib, shrink)
 
-__all__ = ["Table", "Plan", "shrink", "expand", "apply", "grad", "apply_workspace",
-           "grad_workspace", "lib", "LoraError", "LORA_F32", "LORA_BF16", "LORA_DATA_BAD_ID",
+__all__ = ["Table", "Plan", "shrink", "expand", "apply", "grad", "grad_x", "apply_workspace",
+           "grad_workspace", "grad_x_workspace", "lib", "LoraError", "LORA_F32", "LORA_BF16", "LORA_DATA_BAD_ID",
            "LORA_DATA_EMPTY_SLOT", "LORA_DATA_BAD_SEGMENTS", "LIB_PATH"]

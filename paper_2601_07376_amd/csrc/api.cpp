@@ -677,4 +677,44 @@ lora_status lora_grad(const lora_plan* p, const void* X, lora_dtype x_dtype, int
   return ok();
 }
 
+// ---- input gradient ----------------------------------------------------------
+
+size_t lora_grad_x_workspace_bytes(const lora_plan* p) {
+  if (p == nullptr) return 0;
+  return apply_h_bytes(p);   // SHRINK_KS_MAX fp32 planes [n, pad8(r_max)]
+}
+
+lora_status lora_grad_x(const lora_plan* p, const void* dY, lora_dtype dy_dtype, int64_t lddy,
+                        void* dX, lora_dtype dx_dtype, int64_t lddx, void* ws, size_t ws_bytes,
+                        void* stream) {
+  lora_status st = check_plan(p);
+  if (st != LORA_OK) return st;
+  const lora_table* t = p->table;
+  if ((st = check_matrix(dY, dy_dtype, lddy, t->d_out, "dY", p->n)) != LORA_OK) return st;
+  if ((st = check_matrix(dX, dx_dtype, lddx, t->d_in, "dX", p->n)) != LORA_OK) return st;
+  if (dy_dtype != LORA_BF16 || t->w_dtype != LORA_BF16)
+    return fail(LORA_ERR_DTYPE, "input gradient needs bfloat16 dY and weights");
+  const size_t need = lora_grad_x_workspace_bytes(p);
+  if (ws == nullptr) return fail(LORA_ERR_NULL, "input-gradient workspace is NULL");
+  if (!aligned(ws, 16)) return fail(LORA_ERR_ALIGN, "input-gradient workspace not 16-byte aligned");
+  if (ws_bytes < need)
+    return fail(LORA_ERR_WORKSPACE, "input-gradient workspace %zu bytes < %zu", ws_bytes, need);
+  if (p->n == 0) return ok();
+  lora::OpLaunch o = op_base(p);
+  o.d_in = t->d_out;                 // the shrink reads dY rows
+  o.d_out = t->d_in;                 // the expand writes dX rows
+  o.rb = p->d.mrb;
+  o.perm = p->d.m_perm;
+  o.count_word = lora::HDR_NMRB;
+  o.first_word = -1;
+  o.rb_ub = ub_mrb(p);
+  o.fine_ub = ub_mrb(p);
+  const int64_t ldh = (std::max(p->r_max, 1) + 7) / 8 * 8;
+  const int64_t plane = (int64_t)(al256((size_t)std::max(p->n, 1) * ldh * 4) / 4);
+  hipError_t e = lora::launch_grad_x_mfma(o, dY, lddy, static_cast<float*>(ws), ldh, plane, dX,
+                                          dx_dtype, lddx, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "input-gradient launch");
+  return ok();
+}
+
 }  // extern "C"

@@ -53,6 +53,7 @@ struct FwdArgs {
   int32_t ks_max;           // large groups: most d-slices of the shrink (partial planes)
   int64_t hp_stride;        // elements between partial H planes
   int32_t cw;               // expand column chunk (0: chosen from the block count)
+  int32_t force_fine;       // run the 64-row kernels whatever the plan chose (input gradient)
 };
 
 __device__ __forceinline__ void entry_range(const FwdArgs& p, int& first, int& count) {
@@ -729,13 +730,15 @@ __global__ __launch_bounds__(256, (KSM == 1 || (YBF16 && KSM == 2 && U == 1)) ? 
 // LDS, each wave loading the B rows of its own columns, no barrier in the
 // column loop).
 // ---------------------------------------------------------------------------
-template <int NT>
+// WT (input gradient): the weight is B_a as stored, [K][r] with K = p.d_in,
+// gathered (eight 2-byte loads per lane and k-step, packed when multiplied).
+template <int NT, bool WT>
 __global__ __launch_bounds__(256) void shrink_fine_kernel(FwdArgs p) {
   constexpr int N = 4 * NT, CH = N < 16 ? N : 16;
   __shared__ f32x4 s_red[2 * CH * 64];
   const int lane = threadIdx.x & 63, w = wave_id();
   const int mrow = lane & 15, kg = (lane >> 4) * 8;
-  if (p.hdr[HDR_RB_ROWS] != RB_FINE) return;     // the coarse kernel's batch
+  if (!p.force_fine && p.hdr[HDR_RB_ROWS] != RB_FINE) return;   // the coarse kernel's batch
   int first, count;
   entry_range(p, first, count);
   const int nks = shrink_splits(p, count);
@@ -746,7 +749,7 @@ __global__ __launch_bounds__(256) void shrink_fine_kernel(FwdArgs p) {
     const int a = en.x, p0 = en.y, rows = en.z;
     const Slot m = load_slot(p.meta, a);
     const int r = m.rank;
-    const rsrc_t A = make_rsrc(m.A, (uint32_t)r * (uint32_t)p.d_in * 2u);
+    const rsrc_t A = make_rsrc(WT ? m.B : m.A, (uint32_t)r * (uint32_t)p.d_in * 2u);
     int kb, ke;
     kslice(p.d_in, nks, ks, kb, ke);
     const int kend = max(ke, 8);
@@ -769,7 +772,7 @@ __global__ __launch_bounds__(256) void shrink_fine_kernel(FwdArgs p) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const int j = nt * 16 + mrow;
-      arow[nt] = (uint32_t)(j < r ? j : r - 1) * (uint32_t)p.d_in;
+      arow[nt] = WT ? (uint32_t)(j < r ? j : r - 1) : (uint32_t)(j < r ? j : r - 1) * (uint32_t)p.d_in;
     }
     f32x4 acc[N];
 #pragma unroll
@@ -777,7 +780,8 @@ __global__ __launch_bounds__(256) void shrink_fine_kernel(FwdArgs p) {
 
     struct Buf {
       bf16x8 x[4];
-      bf16x8 a[NT];
+      bf16x8 a[WT ? 1 : NT];
+      uint32_t e[WT ? NT : 1][8];
       bool kv;
     };
     auto load = [&](Buf& b, int i) {
@@ -785,16 +789,27 @@ __global__ __launch_bounds__(256) void shrink_fine_kernel(FwdArgs p) {
       b.kv = k < ke;
       const int kk = k < kend ? k : kend - 8;
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) b.a[nt] = as_bf16x8(bload16(A, (arow[nt] + (uint32_t)kk) * 2u));
+      for (int nt = 0; nt < NT; ++nt) {
+        if (!WT) {
+          b.a[WT ? 0 : nt] = as_bf16x8(bload16(A, (arow[nt] + (uint32_t)kk) * 2u));
+        } else {
+#pragma unroll
+          for (int q = 0; q < 8; ++q)
+            b.e[WT ? nt : 0][q] = bload_u16(A, ((uint32_t)(kk + q) * (uint32_t)r + arow[nt]) * 2u);
+        }
+      }
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt) b.x[mt] = as_bf16x8(ldg16(xrow[mt] + kk));
     };
     auto compute = [&](const Buf& b) {
+      bf16x8 av[NT];
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) av[nt] = WT ? pack_bf16x8(b.e[WT ? nt : 0]) : b.a[WT ? 0 : nt];
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt) {
         const bf16x8 xo = sel(b.kv, b.x[mt]);
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) acc[mt * NT + nt] = mfma_16x16x32(xo, b.a[nt], acc[mt * NT + nt]);
+        for (int nt = 0; nt < NT; ++nt) acc[mt * NT + nt] = mfma_16x16x32(xo, av[nt], acc[mt * NT + nt]);
       }
     };
     // rounds double buffered in registers; one exit, at the end of a pair
@@ -836,7 +851,9 @@ __global__ __launch_bounds__(256) void shrink_fine_kernel(FwdArgs p) {
   }
 }
 
-template <bool YBF16, bool RANK8, int KSM, int U>
+// WT (input gradient): the weight is A_a as stored, [r][p.d_out], gathered
+// (eight 2-byte loads per operand, packed when multiplied).
+template <bool YBF16, bool RANK8, int KSM, int U, bool WT>
 __global__ __launch_bounds__(256, KSM == 1 ? 2 : 1) void expand_fine_kernel(FwdArgs p) {
   constexpr int HS = KSM * 32, HT = HS + 4;    // H columns (rank padded); LDS stride
   constexpr int ES = YBF16 ? 2 : 4;            // bytes per Y element
@@ -849,7 +866,7 @@ __global__ __launch_bounds__(256, KSM == 1 ? 2 : 1) void expand_fine_kernel(FwdA
   const int og = lane >> 4, mrow = lane & 15, jg = og * 8;
   unsigned char* const so = s_o[w];
   uint4* const sink = g_store_sink + 8 * tid;
-  if (p.hdr[HDR_RB_ROWS] != RB_FINE) return;     // the coarse kernel's batch
+  if (!p.force_fine && p.hdr[HDR_RB_ROWS] != RB_FINE) return;   // the coarse kernel's batch
   int first, count;
   entry_range(p, first, count);
   const int nks = shrink_splits(p, count);
@@ -865,7 +882,7 @@ __global__ __launch_bounds__(256, KSM == 1 ? 2 : 1) void expand_fine_kernel(FwdA
     const Slot m = load_slot(p.meta, a);
     const int r = m.rank;
     const float s = m.scale;
-    const rsrc_t Bw = make_rsrc(m.B, (uint32_t)p.d_out * (uint32_t)r * 2u);
+    const rsrc_t Bw = make_rsrc(WT ? m.A : m.B, (uint32_t)p.d_out * (uint32_t)r * 2u);
     // this wave's columns
     const int cw0 = min(c0 + w * QW, c1), cw1 = min(c1, cw0 + QW);
     const int nst = (cw1 - cw0 + 31) / 32;
@@ -937,7 +954,8 @@ __global__ __launch_bounds__(256, KSM == 1 ? 2 : 1) void expand_fine_kernel(FwdA
     vmem_drained();
 
     struct Buf {
-      bf16x8 b[U][KSM][2];
+      bf16x8 b[WT ? 1 : U][KSM][2];
+      uint32_t e[WT ? U : 1][KSM][2][8];     // gathered weights (WT)
       Y8<YBF16> y[U][4];
     };
     auto load = [&](Buf& q, int st0) {
@@ -950,7 +968,16 @@ __global__ __launch_bounds__(256, KSM == 1 ? 2 : 1) void expand_fine_kernel(FwdA
           for (int qq = 0; qq < 2; ++qq) {
             int oc = ob + 8 * (mrow >> 2) + 4 * qq + (mrow & 3);
             oc = oc < p.d_out ? oc : p.d_out - 1;
-            q.b[u][ks][qq] = wrow8<RANK8>(Bw, (uint32_t)oc * r, ks * 32 + jg, r);
+            if (!WT) {
+              q.b[WT ? 0 : u][ks][qq] = wrow8<RANK8>(Bw, (uint32_t)oc * r, ks * 32 + jg, r);
+            } else {
+#pragma unroll
+              for (int i = 0; i < 8; ++i) {
+                const int j = ks * 32 + jg + i;
+                q.e[WT ? u : 0][ks][qq][i] =
+                    bload_u16(Bw, ((uint32_t)(j < r ? j : r - 1) * (uint32_t)p.d_out + (uint32_t)oc) * 2u);
+              }
+            }
           }
       }
 #pragma unroll
@@ -972,7 +999,16 @@ __global__ __launch_bounds__(256, KSM == 1 ? 2 : 1) void expand_fine_kernel(FwdA
         const bool jv = ks * 32 + jg < r;
 #pragma unroll
         for (int qq = 0; qq < 2; ++qq) {
-          const bf16x8 b = sel(jv, q.b[u][ks][qq]);
+          bf16x8 b;
+          if (!WT) {
+            b = q.b[WT ? 0 : u][ks][qq];
+          } else {
+            uint32_t ev[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) ev[i] = ks * 32 + jg + i < r ? q.e[WT ? u : 0][ks][qq][i] : 0u;
+            b = pack_bf16x8(ev);
+          }
+          b = sel(jv, b);
 #pragma unroll
           for (int tt = 0; tt < 4; ++tt) {
             acc[qq][tt] = mfma_16x16x32(b, hh[ks][tt], acc[qq][tt]);
@@ -1385,9 +1421,9 @@ template <bool YB, bool R8>
 hipError_t launch_expand_ks(const OpLaunch& o, int grid, int gridf, const FwdArgs& a, hipStream_t s) {
   const int ks = (o.r_max + 31) / 32;
   // both block sizes, as in the shrink
-  hipError_t err = ks <= 1   ? launch(expand_fine_kernel<YB, R8, 1, YB ? 2 : 1>, gridf, a, s)
-                   : ks <= 2 ? launch(expand_fine_kernel<YB, R8, 2, YB ? 2 : 1>, gridf, a, s)
-                             : launch(expand_fine_kernel<YB, R8, 4, 1>, gridf, a, s);
+  hipError_t err = ks <= 1   ? launch(expand_fine_kernel<YB, R8, 1, YB ? 2 : 1, false>, gridf, a, s)
+                   : ks <= 2 ? launch(expand_fine_kernel<YB, R8, 2, YB ? 2 : 1, false>, gridf, a, s)
+                             : launch(expand_fine_kernel<YB, R8, 4, 1, false>, gridf, a, s);
   if (err != hipSuccess) return err;
   if (ks <= 1) return launch_expand_u<YB, R8, 1>(grid, a, s);
   if (ks <= 2) return launch_expand_u<YB, R8, 2>(grid, a, s);
@@ -1421,16 +1457,53 @@ hipError_t launch_shrink_mfma(const OpLaunch& o, const void* X, int64_t ldx, flo
   const int nt = (o.r_max + 15) / 16;
   // the plan picks the block size on the device: both kernels are launched and
   // the one for the other size returns at once
-  hipError_t err = nt <= 1   ? launch(shrink_fine_kernel<1>, gridf, a, s)
-                   : nt <= 2 ? launch(shrink_fine_kernel<2>, gridf, a, s)
-                   : nt <= 4 ? launch(shrink_fine_kernel<4>, gridf, a, s)
-                             : launch(shrink_fine_kernel<8>, gridf, a, s);
+  hipError_t err = nt <= 1   ? launch(shrink_fine_kernel<1, false>, gridf, a, s)
+                   : nt <= 2 ? launch(shrink_fine_kernel<2, false>, gridf, a, s)
+                   : nt <= 4 ? launch(shrink_fine_kernel<4, false>, gridf, a, s)
+                             : launch(shrink_fine_kernel<8, false>, gridf, a, s);
   if (err != hipSuccess) return err;
   const int u = env_int("LORA_SHRINK_U", 4);
   if (nt <= 1) return u == 2 ? launch(shrink_kernel<1, 2>, grid, a, s) : u == 1 ? launch(shrink_kernel<1, 1>, grid, a, s) : launch(shrink_kernel<1, 4>, grid, a, s);
   if (nt <= 2) return u == 2 ? launch(shrink_kernel<2, 2>, grid, a, s) : u == 1 ? launch(shrink_kernel<2, 1>, grid, a, s) : launch(shrink_kernel<2, 4>, grid, a, s);
   if (nt <= 4) return u == 2 ? launch(shrink_kernel<4, 2>, grid, a, s) : u == 1 ? launch(shrink_kernel<4, 1>, grid, a, s) : launch(shrink_kernel<4, 4>, grid, a, s);
   return launch(shrink_kernel<8, 1>, grid, a, s);
+}
+
+// Input gradient over the plan's masked 64-row blocks (o.rb, o.perm and
+// o.count_word describe them; o.d_in is the width of dY, o.d_out that of dX):
+// G = dY B_a into d-sliced planes, then dX += s_a G A_a, both weights read as
+// stored through gathers.
+hipError_t launch_grad_x_mfma(const OpLaunch& o, const void* dY, int64_t lddy, float* H, int64_t ldh,
+                              int64_t hp_stride, void* dX, lora_dtype dx_dtype, int64_t lddx,
+                              hipStream_t s) {
+  FwdArgs a = base_args(o);
+  a.X = reinterpret_cast<const uint16_t*>(dY);
+  a.ldx = lddy;
+  a.H = H;
+  a.ldh = ldh;
+  a.ks_max = SHRINK_KS_MAX;
+  a.hp_stride = hp_stride;
+  a.force_fine = 1;
+  const int nt = (o.r_max + 15) / 16;
+  const int grid1 = round8(std::min<long long>((long long)o.fine_ub * a.ks_max, 2048));
+  hipError_t err = nt <= 1   ? launch(shrink_fine_kernel<1, true>, grid1, a, s)
+                   : nt <= 2 ? launch(shrink_fine_kernel<2, true>, grid1, a, s)
+                   : nt <= 4 ? launch(shrink_fine_kernel<4, true>, grid1, a, s)
+                             : launch(shrink_fine_kernel<8, true>, grid1, a, s);
+  if (err != hipSuccess) return err;
+  a.Y = dX;
+  a.ldy = lddx;
+  a.cw = 1024;
+  const int grid2 = round8(std::min<long long>((long long)o.fine_ub * ((o.d_out + 1023) / 1024), 4096));
+  const int ks = (o.r_max + 31) / 32;
+  const bool yb = dx_dtype == LORA_BF16;
+#define GX(YB, R8)                                                                           \
+  (ks <= 1   ? launch(expand_fine_kernel<YB, R8, 1, 1, true>, grid2, a, s)                  \
+   : ks <= 2 ? launch(expand_fine_kernel<YB, R8, 2, 1, true>, grid2, a, s)                  \
+             : launch(expand_fine_kernel<YB, R8, 4, 1, true>, grid2, a, s))
+  if (yb) return o.rank8 ? GX(true, true) : GX(true, false);
+  return o.rank8 ? GX(false, true) : GX(false, false);
+#undef GX
 }
 
 hipError_t launch_expand_mfma(const OpLaunch& o, const float* H, int64_t ldh, int32_t ks_max,

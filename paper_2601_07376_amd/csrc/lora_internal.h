@@ -140,6 +140,11 @@ hipError_t launch_shrink_mfma(const OpLaunch& o, const void* X, int64_t ldx, flo
 hipError_t launch_expand_mfma(const OpLaunch& o, const float* H, int64_t ldh, int32_t ks_max,
                               int64_t hp_stride, void* Y, lora_dtype y_dtype, int64_t ldy,
                               hipStream_t s);
+// input gradient dX += s G A_a with G = dY B_a, over the entries o describes
+// (the plan's masked blocks); H holds SHRINK_KS_MAX partial planes
+hipError_t launch_grad_x_mfma(const OpLaunch& o, const void* dY, int64_t lddy, float* H, int64_t ldh,
+                              int64_t hp_stride, void* dX, lora_dtype dx_dtype, int64_t lddx,
+                              hipStream_t s);
 // fused small-group kernel: shrink into LDS + expand, entries [first, count)
 hipError_t launch_bgmv_mfma(const OpLaunch& o, const void* X, int64_t ldx, void* Y,
                             lora_dtype y_dtype, int64_t ldy, int32_t n_chunks, hipStream_t s);

@@ -47,6 +47,8 @@ SIGNATURES = {
     "lora_grad_workspace_bytes": (_sz, [_vp]),
     "lora_grad": (_i32, [_vp, _vp, _i32, _i64, _vp, _i32, _i64, _vp, _i64, _vp, _vp, _i32,
                          _vp, _sz, _vp]),
+    "lora_grad_x_workspace_bytes": (_sz, [_vp]),
+    "lora_grad_x": (_i32, [_vp, _vp, _i32, _i64, _vp, _i32, _i64, _vp, _sz, _vp]),
 }
 
 _lib = None
@@ -271,3 +273,17 @@ def grad(plan, X, dY, dA=None, dB=None, H_saved=None, accumulate=False, ws=None,
                            _dtype(dY), _rowmajor(dY, "dY"), _ptr(H_saved), ldh, pa, pb,
                            1 if accumulate else 0, _ptr(ws), ws.numel(), _stream(stream)))
     return dA, dB
+
+
+def grad_x_workspace(plan):
+    return torch.empty(max(lib().lora_grad_x_workspace_bytes(plan.handle), 16), dtype=torch.uint8,
+                       device=plan.table.device)
+
+
+def grad_x(plan, dY, dX, ws=None, stream=None):
+    """dX[t] += s_a (dY[t] B_a) A_a in place over the plan's masked rows."""
+    if ws is None:
+        ws = grad_x_workspace(plan)
+    _check(lib().lora_grad_x(plan.handle, _ptr(dY), _dtype(dY), _rowmajor(dY, "dY"), _ptr(dX),
+                             _dtype(dX), _rowmajor(dX, "dX"), _ptr(ws), ws.numel(), _stream(stream)))
+    return dX
