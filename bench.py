@@ -6,7 +6,8 @@ grouping (plan) followed by the forward residual (lora_apply), or, for the
 masked-backward workload, the plan followed by lora_grad.  The headline line is
 the decode workload (256 single-token rows over 64 rank-16 adapters, hidden
 4096 -> 4096, bf16): tokens/s of whole steps.  The other four workloads are
-measured the same way and reported under "extra".
+measured the same way and reported under "extra"; for the masked-backward
+workload the input gradient (lora_grad_x, over the same plan) is also timed alone.
 
 Measurement protocol
   * inputs are resident in HBM before timing; each workload keeps R copies of its
@@ -157,6 +158,8 @@ class Rig:
                                                    for t in d["dA"]])
                 d["pB"] = (ctypes.c_void_p * S)(*[t.data_ptr() if t is not None else None
                                                    for t in d["dB"]])
+                d["dX"] = torch.zeros(n, case.d_in, dtype=torch.float32, device="cuda")
+                d["gx_ws"] = L.grad_x_workspace(probe)
             del probe
             self.sets.append(d)
         torch.cuda.synchronize()
@@ -198,6 +201,16 @@ class Rig:
             st = lib.lora_grad(h, X.data_ptr(), xdt, X.stride(0), dY.data_ptr(), xdt,
                                dY.stride(0), None, 0, d["pA"], d["pB"], 0,
                                d["op_ws"].data_ptr(), d["op_ws"].numel(), stream)
+        assert st == 0, lib.lora_last_error()
+
+    def run_grad_x(self, d, h):
+        """Enqueue the input gradient dX += s dY B A over the masked rows for one copy."""
+        lib = self.L.lib()
+        stream = ctypes.c_void_p(self.torch.cuda.current_stream().cuda_stream)
+        dY, dX = d["dY"], d["dX"]
+        st = lib.lora_grad_x(h, dY.data_ptr(), 1 if self.case.x_dtype == "bf16" else 0,
+                             dY.stride(0), dX.data_ptr(), 0, dX.stride(0),
+                             d["gx_ws"].data_ptr(), d["gx_ws"].numel(), stream)
         assert st == 0, lib.lora_last_error()
 
     def step(self, i):
@@ -263,6 +276,9 @@ def run_workload(cfg, steps, warmup, rate):
     torch.cuda.synchronize()
     nc = len(rig.sets)
     op_mean = timed(lambda i: rig.run_op(rig.sets[i % nc], handles[i % nc]), steps) * 1e3
+    gx_us = None
+    if case.mask is not None and case.x_dtype == "bf16":
+        gx_us = timed(lambda i: rig.run_grad_x(rig.sets[i % nc], handles[i % nc]), steps) * 1e3
     for h in handles:
         L.lib().lora_plan_destroy(h)
     plan_us = timed(lambda i: L.lib().lora_plan_destroy(rig.build_plan(rig.sets[i % nc])),
@@ -282,6 +298,22 @@ def run_workload(cfg, steps, warmup, rate):
     r["mfma_frac_ceiling"] = min(1.0, (counts["flops"] / counts["op_bytes"]) * HBM_PEAK_GBS
                                  / 1e3 / peak_f)
     r["step_GBps"] = ws_bytes / (ms_step * 1e-3) / 1e9
+    if gx_us is not None:
+        # input gradient: dY rows read, f32 dX rows read and written, both
+        # factors of every touched adapter read once
+        n_m = counts["n_masked"]
+        ranks = case.ranks.astype(np.int64)
+        m = (case.idx >= 0) & (case.mask != 0)
+        touched = np.unique(case.idx[m])
+        gx_bytes = (n_m * (case.d_out * 2 + case.d_in * 8)
+                    + int(np.sum(ranks[touched]) * (case.d_in + case.d_out) * 2))
+        gx_flops = int(np.sum(2 * ranks[case.idx[m]] * (case.d_in + case.d_out)))
+        r["grad_x"] = dict(op="lora_grad_x", us_mean=gx_us, bytes=gx_bytes, flops=gx_flops,
+                           GBps=gx_bytes / (gx_us * 1e-6) / 1e9,
+                           hbm_frac=gx_bytes / (gx_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
+                           TFLOPs=gx_flops / (gx_us * 1e-6) / 1e12)
+        log(f"[bench]   lora_grad_x: {gx_us:.2f} us, {r['grad_x']['GBps']:.0f} GB/s = "
+            f"{100 * r['grad_x']['hbm_frac']:.1f}% HBM")
     log(f"[bench]   plan {plan_us:.2f} us; {r['op']}: {op_mean:.2f} us, "
         f"{r['op_GBps']:.0f} GB/s = {100 * r['op_hbm_frac']:.1f}% HBM, "
         f"{r['op_TFLOPs']:.1f} TFLOP/s; step {ms_step * 1e3:.2f} us, "

@@ -870,7 +870,14 @@ __global__ __launch_bounds__(256, KSM == 1 ? 2 : 1) void expand_fine_kernel(FwdA
   int first, count;
   entry_range(p, first, count);
   const int nks = shrink_splits(p, count);
-  const int CW = p.cw > 0 ? p.cw : 1024;
+  // column chunk: the input gradient's (force_fine) is p.cw; a forward
+  // batch's comes from the block count, so that the (block, chunk) units about
+  // fill the workgroups the chip holds at once (two per CU up to rank 32, else
+  // one), in whole 128-byte groups, four waves' worth at a time
+  const int ngr_all = (p.d_out + 32 * SP - 1) / (32 * SP);
+  const int n_want = max(1, min((KSM == 1 ? 512 : 256) / max(count, 1), ngr_all / 4));
+  const int CW = p.force_fine ? (p.cw > 0 ? p.cw : 1024)
+                              : (ngr_all + 4 * n_want - 1) / (4 * n_want) * 4 * (32 * SP);
   const int QW = CW / 4;                       // columns per wave
   const int n_ch = (p.d_out + CW - 1) / CW;
   const XcdRange xr = xcd_range(count * n_ch);
@@ -1516,8 +1523,10 @@ hipError_t launch_expand_mfma(const OpLaunch& o, const float* H, int64_t ldh, in
   a.hp_stride = hp_stride;
   a.Y = Y;
   a.ldy = ldy;
-  // (row block, 1024-column chunk) units; LORA_EXPAND_CW sets another chunk
-  // width (whole pairs of 32-column steps) for measurements
+  // (row block, 1024-column chunk) units of the 256-row kernel (the 64-row
+  // kernel picks its own chunk from the block count and loops over its units);
+  // LORA_EXPAND_CW sets another chunk width (whole pairs of 32-column steps)
+  // of the 256-row kernel for measurements
   const int cw = env_int("LORA_EXPAND_CW", 0);
   a.cw = cw > 0 ? std::max(64, cw / 64 * 64) : 1024;
   const long long n_ch = (o.d_out + a.cw - 1) / a.cw;

@@ -148,6 +148,34 @@ def test_grad_x_masked_rows_never_read():
     assert _bits(junk).tobytes() == _bits(clean).tobytes()
 
 
+def test_grad_x_table_reupload():
+    """The input gradient follows the table as last uploaded: empty slots
+    between live ones, then a re-upload with other ranks, weights and scales
+    on the same table object, each checked against the oracle."""
+    say("grad_x table re-upload")
+    kw = dict(mask_p=0.5, want_dy=True, want_y=False, layout="segments", seg_len=(1, 120))
+    c1 = workloads.random_case(37, 800, 200, 136, 6, ranks=[16, 0, 64, 8, 0, 33], **kw)
+    dev1 = case_to_device(c1, DEV)
+    table = make_table(c1, dev1)
+    dx0 = _dx0(c1, seed=5)
+    dX = dx0.to(DEV).clone()
+    L.grad_x(make_plan(c1, dev1, table), dev1["dY"], dX)
+    torch.cuda.synchronize()
+    check_grad_x(c1, dx0, dX.cpu())
+    c2 = workloads.random_case(38, 800, 200, 136, 6, ranks=[128, 24, 0, 8, 40, 0], **kw)
+    dev2 = case_to_device(c2, DEV)
+    for a in range(c2.num_slots):
+        if c2.ranks[a] > 0:
+            table.set(a, dev2["A"][a], dev2["B"][a], float(c2.scales[a]))
+        else:
+            table.clear(a)
+    table.upload()
+    dX = dx0.to(DEV).clone()
+    L.grad_x(make_plan(c2, dev2, table), dev2["dY"], dX)
+    torch.cuda.synchronize()
+    check_grad_x(c2, dx0, dX.cpu())
+
+
 def test_grad_x_empty_batch_and_dtype_errors():
     case = workloads.random_case(35, 0, 64, 64, 3, rank_choices=(8,), mask_p=0.5, want_dy=True,
                                  want_y=False)
