@@ -23,6 +23,13 @@ widening bfloat16 or binary32 to float64 is exact):
 * ``grad_x`` -- the input gradient through the same residual over the same
   masked rows, dX_t += s_a (dY_t B_a) A_a (the chain rule on the LoRA equation
   with respect to x; rows outside T_a^m are left as they are).
+* ``adamw`` -- one optimizer step of one adapter tensor's own state (the
+  paper keeps gradients, optimizer moments and step counters local to the
+  owning policy and issues the optimizer step per policy, Section 3.5; it
+  names no optimizer, and the update is the published AdamW: Adam's moment
+  estimates with bias correction (Kingma and Ba) and weight decay decoupled
+  from the gradient (Loshchilov and Hutter), with the learning rate scaling
+  both the Adam step and the decay).
 * ``*_bruteforce`` -- scalar Python loops over the same definitions, used only
   as an independent pin on tiny inputs.
 
@@ -378,6 +385,35 @@ def masked_loss(eff, mask, X, dY, A, B, scale):
 # ----------------------------------------------------------------------------
 # comparison metrics
 # ----------------------------------------------------------------------------
+
+# ----------------------------------------------------------------------------
+# adapter-local optimizer step
+# ----------------------------------------------------------------------------
+
+def adamw(p, m, v, g, step, lr, beta1, beta2, eps, weight_decay):
+    """AdamW step number ``step`` (t >= 1) of one tensor, elementwise in float64.
+
+    With the tensor's own moments m, v and step count t:
+        m_t = beta1 m + (1 - beta1) g
+        v_t = beta2 v + (1 - beta2) g^2
+        mhat = m_t / (1 - beta1^t),   vhat = v_t / (1 - beta2^t)
+        p_t = p - lr (mhat / (sqrt(vhat) + eps) + weight_decay p)
+    The decay term uses the value before the step (decoupled weight decay: it
+    never enters the moments).  Returns (p_t, m_t, v_t); the inputs are not
+    modified."""
+    if step < 1:
+        raise ValueError("AdamW step numbers start at 1")
+    p = np.asarray(p, np.float64)
+    m = np.asarray(m, np.float64)
+    v = np.asarray(v, np.float64)
+    g = np.asarray(g, np.float64)
+    m_t = beta1 * m + (1.0 - beta1) * g
+    v_t = beta2 * v + (1.0 - beta2) * g * g
+    mhat = m_t / (1.0 - beta1 ** step)
+    vhat = v_t / (1.0 - beta2 ** step)
+    p_t = p - lr * (mhat / (np.sqrt(vhat) + eps) + weight_decay * p)
+    return p_t, m_t, v_t
+
 
 def rel_fro(out, ref):
     """||out - ref||_F / ||ref||_F (0 when both are zero)."""

@@ -283,11 +283,72 @@ def check_grad_x_dense_and_untouched(impl):
     return got[out].tobytes() == dX0[out].tobytes() and got.tobytes() == clean.tobytes()
 
 
+ADAMW_SETS = [  # (lr, beta1, beta2, eps, weight_decay)
+    (1e-3, 0.9, 0.999, 1e-8, 0.01),
+    (3e-2, 0.8, 0.95, 1e-3, 0.1),
+    (1e-2, 0.0, 0.5, 1e-6, 0.0),
+    (5e-4, 0.95, 0.9999, 1e-8, 1.0),
+]
+
+
+def check_adamw_torch(impl):
+    """Six steps against torch.optim.AdamW in float64 (an independent
+    implementation of the published algorithm), the state carried across steps."""
+    import torch
+    for k, (lr, b1, b2, eps, wd) in enumerate(ADAMW_SETS):
+        rng = np.random.default_rng(700 + k)
+        p0 = rng.standard_normal(37) * 0.3
+        tp = torch.nn.Parameter(torch.from_numpy(p0.copy()))
+        opt = torch.optim.AdamW([tp], lr=lr, betas=(b1, b2), eps=eps, weight_decay=wd)
+        p, m, v = p0.copy(), np.zeros(37), np.zeros(37)
+        for t in range(1, 7):
+            g = rng.standard_normal(37) * (0.1 if t % 2 else 2.0)
+            g[::5] = 0.0
+            tp.grad = torch.from_numpy(g.copy())
+            opt.step()
+            p, m, v = impl.adamw(p, m, v, g, t, lr, b1, b2, eps, wd)
+            if not np.allclose(p, tp.detach().numpy(), rtol=1e-12, atol=1e-15):
+                return False
+            st = opt.state[tp]
+            if not (np.allclose(m, st["exp_avg"].numpy(), rtol=1e-12, atol=1e-300) and
+                    np.allclose(v, st["exp_avg_sq"].numpy(), rtol=1e-12, atol=1e-300)):
+                return False
+    return True
+
+
+def check_adamw_closed_forms(impl):
+    """From zero moments: the first step is p - lr (g / (|g| + eps) + wd p); a
+    zero gradient only decays, p (1 - lr wd)^t; a constant gradient with no
+    decay moves every step by lr g / (|g| + eps) (the bias corrections make
+    mhat = g and vhat = g^2 at every t)."""
+    rng = np.random.default_rng(800)
+    p0 = rng.standard_normal(50)
+    g = rng.standard_normal(50)
+    g[3] = 0.0
+    z = np.zeros(50)
+    for lr, b1, b2, eps, wd in ADAMW_SETS:
+        p1, m1, v1 = impl.adamw(p0, z, z, g, 1, lr, b1, b2, eps, wd)
+        if not np.allclose(p1, p0 - lr * (g / (np.abs(g) + eps) + wd * p0), rtol=1e-12, atol=1e-15):
+            return False
+        p, m, v = p0, z, z
+        for t in range(1, 6):
+            p, m, v = impl.adamw(p, m, v, z, t, lr, b1, b2, eps, wd)
+        if not np.allclose(p, p0 * (1.0 - lr * wd) ** 5, rtol=1e-12, atol=1e-15):
+            return False
+        p, m, v = p0, z, z
+        for t in range(1, 8):
+            p, m, v = impl.adamw(p, m, v, g, t, lr, b1, b2, eps, 0.0)
+        if not np.allclose(p, p0 - 7 * lr * g / (np.abs(g) + eps), rtol=1e-10, atol=1e-13):
+            return False
+    return True
+
+
 ALL_CHECKS = [check_plan_golden, check_plan_bruteforce, check_forward_golden,
               check_forward_bruteforce, check_forward_closed_form,
               check_forward_integer_exact, check_grad_golden, check_grad_linearity,
               check_grad_bruteforce, check_grad_mask_exact, check_grad_x_linearity,
-              check_grad_x_bruteforce, check_grad_x_dense_and_untouched]
+              check_grad_x_bruteforce, check_grad_x_dense_and_untouched, check_adamw_torch,
+              check_adamw_closed_forms]
 
 
 # ----------------------------------------------------------------------------
@@ -383,7 +444,7 @@ def test_explicit_mask_not_inferred_from_zero_dy():
 def _mutant(**overrides):
     ns = types.SimpleNamespace(canonical_plan=oracle.canonical_plan, apply=oracle.apply,
                                grad=oracle.grad, grad_x=oracle.grad_x,
-                               masked_loss=oracle.masked_loss)
+                               masked_loss=oracle.masked_loss, adamw=oracle.adamw)
     for k, v in overrides.items():
         setattr(ns, k, v)
     return ns
@@ -472,6 +533,39 @@ def _grad_x_wrong_weight(eff, mask, dY, A, B, scale, dX):
                          scale, dX)
 
 
+def _adamw_coupled_decay(p, m, v, g, step, lr, b1, b2, eps, wd):
+    # L2 added to the gradient (Adam with L2), not decoupled
+    return oracle.adamw(p, m, v, np.asarray(g) + wd * np.asarray(p), step, lr, b1, b2, eps, 0.0)
+
+
+def _adamw_no_bias_correction(p, m, v, g, step, lr, b1, b2, eps, wd):
+    p = np.asarray(p, np.float64)
+    m_t = b1 * np.asarray(m) + (1 - b1) * np.asarray(g)
+    v_t = b2 * np.asarray(v) + (1 - b2) * np.asarray(g) ** 2
+    return p - lr * (m_t / (np.sqrt(v_t) + eps) + wd * p), m_t, v_t
+
+
+def _adamw_eps_inside_sqrt(p, m, v, g, step, lr, b1, b2, eps, wd):
+    p = np.asarray(p, np.float64)
+    m_t = b1 * np.asarray(m) + (1 - b1) * np.asarray(g)
+    v_t = b2 * np.asarray(v) + (1 - b2) * np.asarray(g) ** 2
+    mh, vh = m_t / (1 - b1 ** step), v_t / (1 - b2 ** step)
+    return p - lr * (mh / np.sqrt(vh + eps) + wd * p), m_t, v_t
+
+
+def _adamw_beta1_in_v(p, m, v, g, step, lr, b1, b2, eps, wd):
+    return oracle.adamw(p, m, v, g, step, lr, b1, b1, eps, wd)
+
+
+def _adamw_step_off_by_one(p, m, v, g, step, lr, b1, b2, eps, wd):
+    return oracle.adamw(p, m, v, g, step + 1, lr, b1, b2, eps, wd)
+
+
+def _adamw_decay_after_step(p, m, v, g, step, lr, b1, b2, eps, wd):
+    p_t, m_t, v_t = oracle.adamw(p, m, v, g, step, lr, b1, b2, eps, 0.0)
+    return p_t * (1 - lr * wd), m_t, v_t
+
+
 def _plan_unstable(idx, num_slots, mask=None, ranks=None):
     p = oracle.canonical_plan(idx, num_slots, mask=mask, ranks=ranks)
     p = dict(p)
@@ -514,6 +608,12 @@ MUTANTS = {
     "grad_x_sign": _mutant(grad_x=_grad_x_sign),
     "grad_x_overwrites": _mutant(grad_x=_grad_x_overwrites),
     "grad_x_wrong_weight": _mutant(grad_x=_grad_x_wrong_weight),
+    "adamw_coupled_decay": _mutant(adamw=_adamw_coupled_decay),
+    "adamw_no_bias_correction": _mutant(adamw=_adamw_no_bias_correction),
+    "adamw_eps_inside_sqrt": _mutant(adamw=_adamw_eps_inside_sqrt),
+    "adamw_beta1_in_v": _mutant(adamw=_adamw_beta1_in_v),
+    "adamw_step_off_by_one": _mutant(adamw=_adamw_step_off_by_one),
+    "adamw_decay_after_step": _mutant(adamw=_adamw_decay_after_step),
     "plan_unstable": _mutant(canonical_plan=_plan_unstable),
     "plan_inclusive_offsets": _mutant(canonical_plan=_plan_inclusive_offsets),
     "plan_mask_ignored": _mutant(canonical_plan=_plan_mask_ignored),
