@@ -7,7 +7,8 @@ masked-backward workload, the plan followed by lora_grad.  The headline line is
 the decode workload (256 single-token rows over 64 rank-16 adapters, hidden
 4096 -> 4096, bf16): tokens/s of whole steps.  The other four workloads are
 measured the same way and reported under "extra"; for the masked-backward
-workload the input gradient (lora_grad_x, over the same plan) is also timed alone.
+workload the input gradient (lora_grad_x, over the same plan) and the AdamW step
+over its adapters' tensors (lora_adamw_step) are also timed alone.
 
 Measurement protocol
   * inputs are resident in HBM before timing; each workload keeps R copies of its
@@ -149,9 +150,9 @@ class Rig:
                 d["op_ws"] = L.apply_workspace(probe)
             else:
                 d["op_ws"] = L.grad_workspace(probe)
-                d["dA"] = [torch.empty(int(r_), case.d_in, dtype=torch.float32, device="cuda")
+                d["dA"] = [torch.zeros(int(r_), case.d_in, dtype=torch.float32, device="cuda")
                            if r_ > 0 else None for r_ in case.ranks]
-                d["dB"] = [torch.empty(case.d_out, int(r_), dtype=torch.float32, device="cuda")
+                d["dB"] = [torch.zeros(case.d_out, int(r_), dtype=torch.float32, device="cuda")
                            if r_ > 0 else None for r_ in case.ranks]
                 S = case.num_slots
                 d["pA"] = (ctypes.c_void_p * S)(*[t.data_ptr() if t is not None else None
@@ -160,6 +161,23 @@ class Rig:
                                                    for t in d["dB"]])
                 d["dX"] = torch.zeros(n, case.d_in, dtype=torch.float32, device="cuda")
                 d["gx_ws"] = L.grad_x_workspace(probe)
+                # optimizer state of every adapter tensor: fp32 master, moments,
+                # the gradient buffers above, and the table's bf16 weights as the
+                # rounded copy
+                keep, recs = [], []
+                for a in range(case.num_slots):
+                    if case.ranks[a] <= 0:
+                        continue
+                    for w, g in ((d["A"][a], d["dA"][a]), (d["B"][a], d["dB"][a])):
+                        pm = w.float().reshape(-1).clone()
+                        mm, vv = torch.zeros_like(pm), torch.zeros_like(pm)
+                        keep += [pm, mm, vv]
+                        recs.append(L.AdamWTensor(pm.data_ptr(), mm.data_ptr(), vv.data_ptr(),
+                                                  g.data_ptr(), w.data_ptr(), pm.numel(), 10,
+                                                  1e-4, 0.9, 0.999, 1e-8, 0.01))
+                d["adam_keep"] = keep
+                d["adam_recs"] = (L.AdamWTensor * len(recs))(*recs)
+                d["adam_elems"] = sum(int(r.n) for r in recs)
             del probe
             self.sets.append(d)
         torch.cuda.synchronize()
@@ -211,6 +229,14 @@ class Rig:
         st = lib.lora_grad_x(h, dY.data_ptr(), 1 if self.case.x_dtype == "bf16" else 0,
                              dY.stride(0), dX.data_ptr(), 0, dX.stride(0),
                              d["gx_ws"].data_ptr(), d["gx_ws"].numel(), stream)
+        assert st == 0, lib.lora_last_error()
+
+    def run_adamw(self, d):
+        """Enqueue one AdamW step over every adapter tensor of one copy."""
+        lib = self.L.lib()
+        stream = ctypes.c_void_p(self.torch.cuda.current_stream().cuda_stream)
+        st = lib.lora_adamw_step(ctypes.cast(d["adam_recs"], ctypes.c_void_p),
+                                 len(d["adam_recs"]), stream)
         assert st == 0, lib.lora_last_error()
 
     def step(self, i):
@@ -276,9 +302,11 @@ def run_workload(cfg, steps, warmup, rate):
     torch.cuda.synchronize()
     nc = len(rig.sets)
     op_mean = timed(lambda i: rig.run_op(rig.sets[i % nc], handles[i % nc]), steps) * 1e3
-    gx_us = None
+    gx_us = adam_us = None
     if case.mask is not None and case.x_dtype == "bf16":
         gx_us = timed(lambda i: rig.run_grad_x(rig.sets[i % nc], handles[i % nc]), steps) * 1e3
+    if case.mask is not None:
+        adam_us = timed(lambda i: rig.run_adamw(rig.sets[i % nc]), steps) * 1e3
     for h in handles:
         L.lib().lora_plan_destroy(h)
     plan_us = timed(lambda i: L.lib().lora_plan_destroy(rig.build_plan(rig.sets[i % nc])),
@@ -314,6 +342,15 @@ def run_workload(cfg, steps, warmup, rate):
                            TFLOPs=gx_flops / (gx_us * 1e-6) / 1e12)
         log(f"[bench]   lora_grad_x: {gx_us:.2f} us, {r['grad_x']['GBps']:.0f} GB/s = "
             f"{100 * r['grad_x']['hbm_frac']:.1f}% HBM")
+    if adam_us is not None:
+        # per element: p, m, v, g read (16 bytes), p, m, v written (12), bf16 copy (2)
+        el = rig.sets[0]["adam_elems"]
+        ab = 30 * el
+        r["adamw"] = dict(op="lora_adamw_step", us_mean=adam_us, tensors=len(rig.sets[0]["adam_recs"]),
+                          elements=el, bytes=ab, GBps=ab / (adam_us * 1e-6) / 1e9,
+                          hbm_frac=ab / (adam_us * 1e-6) / 1e9 / HBM_PEAK_GBS)
+        log(f"[bench]   lora_adamw_step ({r['adamw']['tensors']} tensors, {el} elements): "
+            f"{adam_us:.2f} us, {r['adamw']['GBps']:.0f} GB/s = {100 * r['adamw']['hbm_frac']:.1f}% HBM")
     log(f"[bench]   plan {plan_us:.2f} us; {r['op']}: {op_mean:.2f} us, "
         f"{r['op_GBps']:.0f} GB/s = {100 * r['op_hbm_frac']:.1f}% HBM, "
         f"{r['op_TFLOPs']:.1f} TFLOP/s; step {ms_step * 1e3:.2f} us, "

@@ -65,7 +65,8 @@ typedef enum lora_status {
   LORA_ERR_SLOT = 6,        /* slot index outside [0, num_slots) */
   LORA_ERR_DATA = 7,        /* the device flagged bad ids or segments (lora_plan_check) */
   LORA_ERR_WORKSPACE = 8,   /* workspace too small */
-  LORA_ERR_HIP = 9          /* a HIP runtime call failed */
+  LORA_ERR_HIP = 9,         /* a HIP runtime call failed */
+  LORA_ERR_VALUE = 10       /* a hyperparameter or step number is out of range */
 } lora_status;
 
 typedef enum lora_dtype { LORA_F32 = 0, LORA_BF16 = 1 } lora_dtype;
@@ -229,6 +230,46 @@ size_t      lora_grad_x_workspace_bytes(const lora_plan* p);
 lora_status lora_grad_x(const lora_plan* p, const void* dY, lora_dtype dy_dtype, int64_t lddy,
                         void* dX, lora_dtype dx_dtype, int64_t lddx, void* ws, size_t ws_bytes,
                         void* stream);
+
+/* ---- adapter-local optimizer step (Section 3.5: gradients, optimizer
+ *      moments and step counters stay local to the owning policy, and each
+ *      policy issues its own optimizer step) ------------------------------
+ * The paper names no optimizer; the update is the published AdamW (Adam's
+ * bias-corrected moment estimates, weight decay decoupled from the gradient),
+ * elementwise over one tensor's fp32 state, with t = step:
+ *     m <- beta1 m + (1 - beta1) g
+ *     v <- beta2 v + (1 - beta2) g^2
+ *     p <- p - lr (mhat / (sqrt(vhat) + eps) + weight_decay p),
+ *     mhat = m / (1 - beta1^t),  vhat = v / (1 - beta2^t)
+ * (the decay uses p before the step).  Arithmetic is fp32, with the per-step
+ * constants 1 - lr wd, lr / (1 - beta1^t) and 1 / sqrt(1 - beta2^t) formed in
+ * double on the host.  One call updates any number of tensors (e.g. every
+ * dA_a and dB_a of the adapters that stepped, each with its own moments, step
+ * count and hyperparameters) in one launch per 32 tensors. */
+typedef struct lora_adamw_tensor {
+  float* p;             /* device [n] fp32 master values, updated in place */
+  float* m;             /* device [n] first moment, updated in place (zeros before step 1) */
+  float* v;             /* device [n] second moment, updated in place (zeros before step 1) */
+  const float* g;       /* device [n] gradient, e.g. dA_a or dB_a from lora_grad (same layout as p) */
+  void* p_bf16;         /* nullable device [n] bfloat16: receives p after the update, rounded
+                           to nearest even (e.g. the table's A_a or B_a) */
+  int64_t n;            /* elements (0: the tensor is skipped) */
+  int32_t step;         /* t >= 1: this update's number in this tensor's own count */
+  float lr;             /* >= 0 */
+  float beta1, beta2;   /* in [0, 1) */
+  float eps;            /* > 0 */
+  float weight_decay;   /* >= 0 */
+} lora_adamw_tensor;
+
+/* tensors: host array of `count` records (count >= 0), read before return.
+ * p, m, v, g and p_bf16 must be 16-byte aligned; no two of one record's arrays
+ * may overlap, and no array may overlap another record's.  Non-finite
+ * gradients propagate into p, m and v.  Errors: NULL (tensors, or an array of
+ * a record with n > 0), SHAPE (count < 0, n < 0, overlapping arrays, except
+ * gradients shared read-only), ALIGN, VALUE (step < 1,
+ * a hyperparameter out of its range or not finite), HIP.  Nothing is enqueued
+ * unless every record is valid.  Asynchronous on stream. */
+lora_status lora_adamw_step(const lora_adamw_tensor* tensors, int32_t count, void* stream);
 
 #ifdef __cplusplus
 }

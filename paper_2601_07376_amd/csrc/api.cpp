@@ -4,6 +4,8 @@
 
 #include <algorithm>
 #include <climits>
+#include <cstddef>
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
@@ -302,6 +304,7 @@ const char* lora_status_string(lora_status s) {
     case LORA_ERR_DATA: return "device data error (bad ids or segments)";
     case LORA_ERR_WORKSPACE: return "workspace too small";
     case LORA_ERR_HIP: return "HIP runtime error";
+    case LORA_ERR_VALUE: return "hyperparameter or step number out of range";
   }
   return "unknown status";
 }
@@ -714,6 +717,83 @@ lora_status lora_grad_x(const lora_plan* p, const void* dY, lora_dtype dy_dtype,
   hipError_t e = lora::launch_grad_x_mfma(o, dY, lddy, static_cast<float*>(ws), ldh, plane, dX,
                                           dx_dtype, lddx, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "input-gradient launch");
+  return ok();
+}
+
+// ---- adapter-local optimizer step ---------------------------------------------
+
+static_assert(sizeof(lora_adamw_tensor) == 72 && offsetof(lora_adamw_tensor, n) == 40 &&
+                  offsetof(lora_adamw_tensor, step) == 48 &&
+                  offsetof(lora_adamw_tensor, weight_decay) == 68,
+              "lora_adamw_tensor layout");
+
+lora_status lora_adamw_step(const lora_adamw_tensor* tensors, int32_t count, void* stream) {
+  if (count < 0) return fail(LORA_ERR_SHAPE, "tensor count %d < 0", count);
+  if (count == 0) return ok();
+  if (tensors == nullptr) return fail(LORA_ERR_NULL, "tensors is NULL");
+  struct Span {
+    uintptr_t b, e;
+    bool written;
+  };
+  std::vector<Span> spans;
+  std::vector<lora::AdamwLaunch> recs;
+  recs.reserve(count);
+  for (int32_t k = 0; k < count; ++k) {
+    const lora_adamw_tensor& t = tensors[k];
+    if (t.n < 0) return fail(LORA_ERR_SHAPE, "tensor %d: n = %lld < 0", k, (long long)t.n);
+    if (t.step < 1) return fail(LORA_ERR_VALUE, "tensor %d: step %d < 1", k, t.step);
+    const bool hyper_ok = std::isfinite(t.lr) && t.lr >= 0.f && std::isfinite(t.beta1) &&
+                          t.beta1 >= 0.f && t.beta1 < 1.f && std::isfinite(t.beta2) &&
+                          t.beta2 >= 0.f && t.beta2 < 1.f && std::isfinite(t.eps) && t.eps > 0.f &&
+                          std::isfinite(t.weight_decay) && t.weight_decay >= 0.f;
+    if (!hyper_ok)
+      return fail(LORA_ERR_VALUE, "tensor %d: lr %g, betas (%g, %g), eps %g, weight decay %g out of range",
+                  k, t.lr, t.beta1, t.beta2, t.eps, t.weight_decay);
+    if (t.n == 0) continue;
+    if (t.p == nullptr || t.m == nullptr || t.v == nullptr || t.g == nullptr)
+      return fail(LORA_ERR_NULL, "tensor %d: p, m, v or g is NULL", k);
+    if (!aligned(t.p, 16) || !aligned(t.m, 16) || !aligned(t.v, 16) || !aligned(t.g, 16) ||
+        !aligned(t.p_bf16, 16))
+      return fail(LORA_ERR_ALIGN, "tensor %d: an array is not 16-byte aligned", k);
+    const uintptr_t f = (uintptr_t)t.n * 4u;
+    spans.push_back({(uintptr_t)t.p, (uintptr_t)t.p + f, true});
+    spans.push_back({(uintptr_t)t.m, (uintptr_t)t.m + f, true});
+    spans.push_back({(uintptr_t)t.v, (uintptr_t)t.v + f, true});
+    spans.push_back({(uintptr_t)t.g, (uintptr_t)t.g + f, false});
+    if (t.p_bf16 != nullptr)
+      spans.push_back({(uintptr_t)t.p_bf16, (uintptr_t)t.p_bf16 + (uintptr_t)t.n * 2u, true});
+    lora::AdamwLaunch r{};
+    r.p = t.p;
+    r.m = t.m;
+    r.v = t.v;
+    r.g = t.g;
+    r.p_bf16 = t.p_bf16;
+    r.n = t.n;
+    const double lr = t.lr, b1 = t.beta1, b2 = t.beta2;
+    r.decay = (float)(1.0 - lr * (double)t.weight_decay);
+    r.step_size = (float)(lr / (1.0 - std::pow(b1, (double)t.step)));
+    r.inv_sqrt_bc2 = (float)(1.0 / std::sqrt(1.0 - std::pow(b2, (double)t.step)));
+    r.eps = t.eps;
+    r.beta1 = t.beta1;
+    r.omb1 = (float)(1.0 - b1);
+    r.beta2 = t.beta2;
+    r.omb2 = (float)(1.0 - b2);
+    recs.push_back(r);
+  }
+  // a written array may overlap nothing; read-only gradients may be shared
+  std::sort(spans.begin(), spans.end(), [](const Span& x, const Span& y) { return x.b < y.b; });
+  uintptr_t end_all = 0, end_w = 0;
+  for (const Span& sp : spans) {
+    if (sp.b < (sp.written ? end_all : end_w))
+      return fail(LORA_ERR_SHAPE, "optimizer arrays overlap");
+    end_all = std::max(end_all, sp.e);
+    if (sp.written) end_w = std::max(end_w, sp.e);
+  }
+  for (size_t k0 = 0; k0 < recs.size(); k0 += lora::ADAMW_GROUP) {
+    const int32_t c = (int32_t)std::min<size_t>(lora::ADAMW_GROUP, recs.size() - k0);
+    hipError_t e = lora::launch_adamw(recs.data() + k0, c, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "optimizer launch");
+  }
   return ok();
 }
 

@@ -200,4 +200,21 @@ hipError_t launch_grad_mfma(const GradLaunch& g, hipStream_t s);
 hipError_t launch_grad_valu(const GradLaunch& g, lora_dtype x_dtype, lora_dtype w_dtype,
                             hipStream_t s);
 
+// adapter-local optimizer step: one launch per group of up to ADAMW_GROUP
+// tensors, each with the per-step constants the host derives in double
+constexpr int ADAMW_GROUP = 32;
+struct AdamwLaunch {
+  float* p;
+  float* m;
+  float* v;
+  const float* g;
+  void* p_bf16;          // nullable
+  int64_t n;
+  float decay;           // 1 - lr wd
+  float step_size;       // lr / (1 - beta1^t)
+  float inv_sqrt_bc2;    // 1 / sqrt(1 - beta2^t)
+  float eps, beta1, omb1, beta2, omb2;
+};
+hipError_t launch_adamw(const AdamwLaunch* t, int32_t count, hipStream_t s);
+
 }  // namespace lora

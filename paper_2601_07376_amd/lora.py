@@ -49,6 +49,7 @@ SIGNATURES = {
                          _vp, _sz, _vp]),
     "lora_grad_x_workspace_bytes": (_sz, [_vp]),
     "lora_grad_x": (_i32, [_vp, _vp, _i32, _i64, _vp, _i32, _i64, _vp, _sz, _vp]),
+    "lora_adamw_step": (_i32, [_vp, _i32, _vp]),
 }
 
 _lib = None
@@ -287,3 +288,37 @@ def grad_x(plan, dY, dX, ws=None, stream=None):
     _check(lib().lora_grad_x(plan.handle, _ptr(dY), _dtype(dY), _rowmajor(dY, "dY"), _ptr(dX),
                              _dtype(dX), _rowmajor(dX, "dX"), _ptr(ws), ws.numel(), _stream(stream)))
     return dX
+
+
+class AdamWTensor(ctypes.Structure):
+    """lora_adamw_tensor (include/lora.h)."""
+    _fields_ = [("p", ctypes.c_void_p), ("m", ctypes.c_void_p), ("v", ctypes.c_void_p),
+                ("g", ctypes.c_void_p), ("p_bf16", ctypes.c_void_p), ("n", ctypes.c_int64),
+                ("step", ctypes.c_int32), ("lr", ctypes.c_float), ("beta1", ctypes.c_float),
+                ("beta2", ctypes.c_float), ("eps", ctypes.c_float),
+                ("weight_decay", ctypes.c_float)]
+
+
+def adamw_step(params, stream=None):
+    """One AdamW step over a group of tensors, each with its own state.
+
+    params: sequence of dicts with float32 device tensors ``p``, ``m``, ``v``,
+    ``g`` of one size, optional ``p_bf16`` (bfloat16, same size; receives the
+    rounded update), and ``step``, ``lr``, ``beta1``, ``beta2``, ``eps``,
+    ``weight_decay``.  Tensors are passed as flat arrays, so they must be
+    contiguous."""
+    recs = (AdamWTensor * max(len(params), 1))()
+    for i, q in enumerate(params):
+        n = q["p"].numel()
+        for k in ("p", "m", "v", "g"):
+            t = q[k]
+            if t.dtype != torch.float32 or not t.is_contiguous() or t.numel() != n:
+                raise ValueError(f"params[{i}].{k}: contiguous float32 of {n} elements expected")
+        pb = q.get("p_bf16")
+        if pb is not None and (pb.dtype != torch.bfloat16 or not pb.is_contiguous() or pb.numel() != n):
+            raise ValueError(f"params[{i}].p_bf16: contiguous bfloat16 of {n} elements expected")
+        recs[i] = AdamWTensor(q["p"].data_ptr(), q["m"].data_ptr(), q["v"].data_ptr(),
+                              q["g"].data_ptr(), pb.data_ptr() if pb is not None else None, n,
+                              int(q["step"]), float(q["lr"]), float(q["beta1"]),
+                              float(q["beta2"]), float(q["eps"]), float(q["weight_decay"]))
+    _check(lib().lora_adamw_step(ctypes.cast(recs, ctypes.c_void_p), len(params), _stream(stream)))

@@ -37,7 +37,7 @@ def test_every_declared_symbol_is_exported_and_bound():
 def test_version_and_strings():
     L = lora.lib()
     assert L.lora_abi_version() == 1
-    for s in range(10):
+    for s in range(11):
         assert L.lora_status_string(s)
     assert L.lora_status_string(99) == b"unknown status"
 
@@ -123,3 +123,40 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(lora, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError, match="missing"):
         lora.lib()
+
+
+def _adam(**kw):
+    base = dict(p=FAKE, m=FAKE + 0x1000, v=FAKE + 0x2000, g=FAKE + 0x3000, p_bf16=FAKE + 0x4000,
+                n=256, step=1, lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.01)
+    base.update(kw)
+    return lora.AdamWTensor(**base)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(step=0), 10), (dict(lr=-1.0), 10), (dict(lr=float("nan")), 10), (dict(beta1=1.0), 10),
+    (dict(beta2=-0.1), 10), (dict(eps=0.0), 10), (dict(weight_decay=float("inf")), 10),
+    (dict(n=-1), 2), (dict(p=0), 1), (dict(g=0), 1), (dict(m=FAKE_ODD), 4),
+    (dict(p_bf16=FAKE + 0x4008), 4),
+    (dict(m=FAKE + 0x200), 2),                 # m overlaps p (n = 256 floats = 1 KiB)
+    (dict(p_bf16=FAKE + 0x3100), 2),           # the bf16 copy overlaps the gradient
+])
+def test_adamw_rejects(kw, status):
+    """Host validation only: every record is rejected before anything is enqueued."""
+    L = lora.lib()
+    recs = (lora.AdamWTensor * 1)(_adam(**kw))
+    assert L.lora_adamw_step(ctypes.cast(recs, ctypes.c_void_p), 1, None) == status
+    assert L.lora_last_error()
+
+
+def test_adamw_count_and_cross_record_overlap():
+    L = lora.lib()
+    recs = (lora.AdamWTensor * 2)(_adam(), _adam(p=FAKE + 0x10000, m=FAKE + 0x11000,
+                                                 v=FAKE + 0x12000, g=FAKE + 0x13000,
+                                                 p_bf16=FAKE + 0x2100))   # into record 0's v
+    assert L.lora_adamw_step(ctypes.cast(recs, ctypes.c_void_p), 2, None) == 2
+    assert L.lora_adamw_step(ctypes.cast(recs, ctypes.c_void_p), -1, None) == 2
+    assert L.lora_adamw_step(None, 1, None) == 1
+    assert L.lora_adamw_step(None, 0, None) == 0        # nothing to do
+    # a zero-size record is skipped (nothing to validate but its hyperparameters)
+    empty = (lora.AdamWTensor * 1)(_adam(n=0, p=0, m=0, v=0, g=0, p_bf16=0))
+    assert L.lora_adamw_step(ctypes.cast(empty, ctypes.c_void_p), 1, None) == 0
