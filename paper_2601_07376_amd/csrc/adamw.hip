@@ -20,7 +20,8 @@ namespace {
 
 constexpr int AD_THREADS = 256;
 constexpr int AD_VEC = 4;                               // elements per vector access
-constexpr int AD_CHUNK = AD_THREADS * AD_VEC * 2;       // elements per unit: two vectors per thread
+constexpr int AD_NV = 1;                                // vectors per thread and unit (1, 2 and 4 measured: 1 fastest)
+constexpr int AD_CHUNK = AD_THREADS * AD_VEC * AD_NV;   // elements per unit
 
 struct AdamRec {
   float* p;
@@ -68,28 +69,33 @@ __global__ __launch_bounds__(AD_THREADS) void adamw_kernel(AdamArgs a) {
     while (k + 1 < a.count && a.first_chunk[k + 1] <= u) ++k;   // uniform: the unit's record
     const AdamRec& R = a.r[k];
     const int64_t base = (int64_t)(u - a.first_chunk[k]) * AD_CHUNK;
-    const int64_t e0 = base + (int64_t)threadIdx.x * AD_VEC;
-    const int64_t e1 = e0 + AD_THREADS * AD_VEC;
-    if (e1 + AD_VEC <= R.n) {
-      // both vectors inside: all loads first, then the arithmetic and stores
-      Elem4 x0, x1;
-      x0.p = ldg_f4(R.p + e0); x1.p = ldg_f4(R.p + e1);
-      x0.m = ldg_f4(R.m + e0); x1.m = ldg_f4(R.m + e1);
-      x0.v = ldg_f4(R.v + e0); x1.v = ldg_f4(R.v + e1);
-      x0.g = ldg_f4(R.g + e0); x1.g = ldg_f4(R.g + e1);
-      adam4(R, x0);
-      adam4(R, x1);
-      stg_f4(R.p + e0, x0.p); stg_f4(R.p + e1, x1.p);
-      stg_f4(R.m + e0, x0.m); stg_f4(R.m + e1, x1.m);
-      stg_f4(R.v + e0, x0.v); stg_f4(R.v + e1, x1.v);
-      if (R.pb != nullptr) {
-        *reinterpret_cast<uint2*>(R.pb + e0) = make_uint2(pack2_bf16(x0.p.x, x0.p.y), pack2_bf16(x0.p.z, x0.p.w));
-        *reinterpret_cast<uint2*>(R.pb + e1) = make_uint2(pack2_bf16(x1.p.x, x1.p.y), pack2_bf16(x1.p.z, x1.p.w));
+    int64_t e[AD_NV];   // this thread's vectors, each AD_THREADS vectors apart
+#pragma unroll
+    for (int j = 0; j < AD_NV; ++j) e[j] = base + (int64_t)(j * AD_THREADS + threadIdx.x) * AD_VEC;
+    if (e[AD_NV - 1] + AD_VEC <= R.n) {
+      // every vector inside: all loads first, then the arithmetic and stores
+      Elem4 x[AD_NV];
+#pragma unroll
+      for (int j = 0; j < AD_NV; ++j) {
+        x[j].p = ldg_f4(R.p + e[j]);
+        x[j].m = ldg_f4(R.m + e[j]);
+        x[j].v = ldg_f4(R.v + e[j]);
+        x[j].g = ldg_f4(R.g + e[j]);
+      }
+#pragma unroll
+      for (int j = 0; j < AD_NV; ++j) {
+        adam4(R, x[j]);
+        stg_f4(R.p + e[j], x[j].p);
+        stg_f4(R.m + e[j], x[j].m);
+        stg_f4(R.v + e[j], x[j].v);
+        if (R.pb != nullptr)
+          *reinterpret_cast<uint2*>(R.pb + e[j]) =
+              make_uint2(pack2_bf16(x[j].p.x, x[j].p.y), pack2_bf16(x[j].p.z, x[j].p.w));
       }
     } else {
       // the record's last unit: element by element up to n
-      for (int h = 0; h < 2; ++h) {
-        const int64_t eb = h ? e1 : e0;
+      for (int h = 0; h < AD_NV; ++h) {
+        const int64_t eb = e[h];
         for (int i = 0; i < AD_VEC; ++i) {
           const int64_t e = eb + i;
           if (e >= R.n) break;
