@@ -30,6 +30,14 @@ widening bfloat16 or binary32 to float64 is exact):
   estimates with bias correction (Kingma and Ba) and weight decay decoupled
   from the gradient (Loshchilov and Hutter), with the learning rate scaling
   both the Adam step and the decay).
+* ``token_loss`` -- the masked token-level objectives that produce the
+  gradient at the logits, summed over target positions: cross-entropy with
+  SFT weights w_t, and the importance-sampling and PPO-style policy-gradient
+  losses with the action mask m_t, rollout log-probabilities, advantages and
+  optional correction weights on the same target axis (Section 3.3, the SFT
+  and RL data path; Section 3.5, "Forward/backward path", for the objectives).
+  The paper names the objectives without writing them; the forms are the
+  standard ones (see the function).
 * ``*_bruteforce`` -- scalar Python loops over the same definitions, used only
   as an independent pin on tiny inputs.
 
@@ -413,6 +421,70 @@ def adamw(p, m, v, g, step, lr, beta1, beta2, eps, weight_decay):
     vhat = v_t / (1.0 - beta2 ** step)
     p_t = p - lr * (mhat / (np.sqrt(vhat) + eps) + weight_decay * p)
     return p_t, m_t, v_t
+
+
+# ----------------------------------------------------------------------------
+# masked token-level losses -> gradient at the logits
+# ----------------------------------------------------------------------------
+
+LOSS_CE, LOSS_IS, LOSS_PPO = 0, 1, 2
+
+
+def token_loss(kind, logits, target, weight=None, mask=None, old_logp=None, adv=None,
+               corr=None, clip_lo=0.2, clip_hi=0.2):
+    """Per-token loss L_t, log-probability logp_t and dL_t/dz_t for logits z [n, V].
+
+    logp_t = z_t[y_t] - log sum_v exp(z_t[v])
+    CE  (kind 0): L_t = -w_t logp_t                                  (row active when w_t != 0)
+    IS  (kind 1): L_t = -m_t c_t A_t rho_t,  rho_t = exp(logp_t - l_old_t)
+    PPO (kind 2): L_t = -m_t c_t min(rho_t A_t, clip(rho_t, 1 - clip_lo, 1 + clip_hi) A_t)
+    (for IS / PPO a row is active when m_t != 0; mask None = every row; c_t = 1
+    when corr is None.)  With g_t = -dL_t/dlogp_t the gradient is
+    dL_t/dz_t = g_t (softmax(z_t) - onehot(y_t)); for PPO, g_t = m_t c_t A_t rho_t
+    where the unclipped term is the minimum (ties included), else 0.
+    Inactive rows: L_t = 0, logp_t = 0, a zero gradient row; their logits are
+    never read.  Returns (L [n], logp [n], dz [n, V]) in float64."""
+    z = np.asarray(logits, np.float64)
+    n, V = z.shape
+    y = np.asarray(target, np.int64)
+    if kind == LOSS_CE:
+        act = np.asarray(weight, np.float64) != 0
+    else:
+        act = np.ones(n, bool) if mask is None else (np.asarray(mask) != 0)
+    L = np.zeros(n)
+    lp = np.zeros(n)
+    dz = np.zeros((n, V))
+    for t in np.nonzero(act)[0]:
+        zt = z[t]
+        mx = np.max(zt)
+        e = np.exp(zt - mx)
+        s = np.sum(e)
+        logp = zt[y[t]] - (mx + np.log(s))
+        soft = e / s
+        if kind == LOSS_CE:
+            w = float(weight[t])
+            L[t] = -w * logp
+            g = w
+        else:
+            c = 1.0 if corr is None else float(corr[t])
+            A = float(adv[t])
+            rho = np.exp(logp - float(old_logp[t]))
+            if kind == LOSS_IS:
+                L[t] = -c * A * rho
+                g = c * A * rho
+            else:
+                unclipped = rho * A
+                clipped = min(max(rho, 1.0 - clip_lo), 1.0 + clip_hi) * A
+                if unclipped <= clipped:
+                    L[t] = -c * unclipped
+                    g = c * A * rho
+                else:
+                    L[t] = -c * clipped
+                    g = 0.0
+        lp[t] = logp
+        dz[t] = g * soft
+        dz[t, y[t]] -= g
+    return L, lp, dz
 
 
 def rel_fro(out, ref):

@@ -343,12 +343,113 @@ def check_adamw_closed_forms(impl):
     return True
 
 
+def _loss_case(seed, n=9, V=13, kind=0):
+    rng = np.random.default_rng(seed)
+    z = rng.standard_normal((n, V)) * 2.0
+    z[1] += 800.0                           # large logits: exp overflows unless shifted
+    z[2, 3] = -700.0
+    y = rng.integers(0, V, n)
+    w = rng.uniform(0.5, 2.0, n)
+    w[[0, 4]] = 0.0
+    mask = (rng.random(n) < 0.7).astype(np.uint8)
+    mask[1] = 1
+    adv = rng.standard_normal(n)
+    corr = rng.uniform(0.5, 1.5, n)
+    old = rng.standard_normal(n) - 2.0
+    return z, y, w, mask, old, adv, corr
+
+
+def check_loss_ce_torch(impl):
+    """Cross-entropy, its log-probabilities and gradient against torch in float64
+    (reduction 'none', weighted sum differentiated by autograd)."""
+    import torch
+    import torch.nn.functional as F
+    for seed in range(3):
+        z, y, w, *_ = _loss_case(900 + seed)
+        L, lp, dz = impl.token_loss(oracle.LOSS_CE, z, y, weight=w)
+        tz = torch.tensor(z, requires_grad=True)
+        ce = F.cross_entropy(tz, torch.tensor(y), reduction="none")
+        (torch.tensor(w) * ce).sum().backward()
+        act = w != 0
+        if not (np.allclose(L, w * ce.detach().numpy(), rtol=1e-12, atol=1e-12) and
+                np.allclose(lp[act], -ce.detach().numpy()[act], rtol=1e-12, atol=1e-12) and
+                np.all(lp[~act] == 0) and
+                np.allclose(dz, tz.grad.numpy(), rtol=1e-10, atol=1e-14)):
+            return False
+    return True
+
+
+def check_loss_finite_differences(impl):
+    """dz against central differences of the summed loss, every kind (rows kept
+    away from the PPO clip edges, where the loss has a kink)."""
+    h = 1e-6
+    for kind in (oracle.LOSS_CE, oracle.LOSS_IS, oracle.LOSS_PPO):
+        z, y, w, mask, old, adv, corr = _loss_case(950 + kind, n=5, V=6)
+        z[1] -= 800.0
+        _, lp0, _ = oracle.token_loss(oracle.LOSS_CE, z, y, weight=np.ones(5))
+        rho = np.array([0.5, 0.95, 1.05, 1.6, 0.7])
+        old = lp0 - np.log(rho)
+        kw = dict(weight=w, mask=mask, old_logp=old, adv=adv, corr=corr, clip_lo=0.2, clip_hi=0.25)
+        _, _, dz = impl.token_loss(kind, z, y, **kw)
+        num = np.zeros_like(z)
+        for t in range(z.shape[0]):
+            for v in range(z.shape[1]):
+                zp, zm = z.copy(), z.copy()
+                zp[t, v] += h
+                zm[t, v] -= h
+                num[t, v] = (impl.token_loss(kind, zp, y, **kw)[0].sum() -
+                             impl.token_loss(kind, zm, y, **kw)[0].sum()) / (2 * h)
+        if not np.allclose(dz, num, rtol=1e-6, atol=1e-8):
+            return False
+    return True
+
+
+def check_loss_closed_forms(impl):
+    """Equal logits give logp = -log V; at rho = 1 the IS loss is -m c A; PPO at
+    chosen ratios: clipped above / below (loss at the clip bound, no gradient)
+    and unclipped (loss and gradient of the ratio term); inactive rows with NaN
+    logits give zero loss, zero logp and a zero gradient row."""
+    V = 11
+    z = np.full((6, V), 0.37)
+    y = np.array([0, 3, 5, 7, 10, 2])
+    _, lp, _ = impl.token_loss(oracle.LOSS_CE, z, y, weight=np.ones(6))
+    if not np.allclose(lp, -np.log(V), rtol=0, atol=1e-14):
+        return False
+    rng = np.random.default_rng(990)
+    z = rng.standard_normal((6, V))
+    _, lp, _ = impl.token_loss(oracle.LOSS_CE, z, y, weight=np.ones(6))
+    soft = np.exp(z - z.max(1, keepdims=True))
+    soft /= soft.sum(1, keepdims=True)
+    onehot = np.eye(V)[y]
+    c = np.array([1.0, 0.5, 2.0, 1.5, 0.8, 1.0])
+    A = np.array([0.7, -1.3, 0.9, -0.4, 1.1, 0.6])
+    m = np.array([1, 1, 1, 1, 1, 0], np.uint8)
+    L, _, dz = impl.token_loss(oracle.LOSS_IS, z, y, mask=m, old_logp=lp, adv=A, corr=c)
+    g = m * c * A
+    if not (np.allclose(L, -g, rtol=1e-12, atol=1e-15) and
+            np.allclose(dz, g[:, None] * (soft - onehot), rtol=1e-10, atol=1e-15)):
+        return False
+    #            A>0 rho>1+hi   A<0 rho<1-lo   A>0 rho<1-lo   A<0 rho>1+hi   inside  masked
+    rho = np.array([1.5, 0.5, 0.5, 1.5, 1.1, 1.0])
+    A = np.array([0.8, -0.6, 0.9, -0.7, 0.5, 0.3])
+    zz = z.copy()
+    zz[5] = np.nan
+    L, lpp, dz = impl.token_loss(oracle.LOSS_PPO, zz, y, mask=m, old_logp=lp - np.log(rho), adv=A,
+                                 corr=c, clip_lo=0.2, clip_hi=0.2)
+    want_L = -c * np.array([1.2 * 0.8, 0.8 * -0.6, 0.5 * 0.9, 1.5 * -0.7, 1.1 * 0.5, 0.0])
+    want_g = c * A * rho * np.array([0, 0, 1, 1, 1, 0])
+    return bool(np.allclose(L, want_L, rtol=1e-12, atol=1e-15) and
+                np.allclose(dz[:5], want_g[:5, None] * (soft[:5] - onehot[:5]), rtol=1e-10, atol=1e-15)
+                and np.all(dz[5] == 0) and lpp[5] == 0 and L[5] == 0)
+
+
 ALL_CHECKS = [check_plan_golden, check_plan_bruteforce, check_forward_golden,
               check_forward_bruteforce, check_forward_closed_form,
               check_forward_integer_exact, check_grad_golden, check_grad_linearity,
               check_grad_bruteforce, check_grad_mask_exact, check_grad_x_linearity,
               check_grad_x_bruteforce, check_grad_x_dense_and_untouched, check_adamw_torch,
-              check_adamw_closed_forms]
+              check_adamw_closed_forms, check_loss_ce_torch, check_loss_finite_differences,
+              check_loss_closed_forms]
 
 
 # ----------------------------------------------------------------------------
@@ -444,7 +545,8 @@ def test_explicit_mask_not_inferred_from_zero_dy():
 def _mutant(**overrides):
     ns = types.SimpleNamespace(canonical_plan=oracle.canonical_plan, apply=oracle.apply,
                                grad=oracle.grad, grad_x=oracle.grad_x,
-                               masked_loss=oracle.masked_loss, adamw=oracle.adamw)
+                               masked_loss=oracle.masked_loss, adamw=oracle.adamw,
+                               token_loss=oracle.token_loss)
     for k, v in overrides.items():
         setattr(ns, k, v)
     return ns
@@ -566,6 +668,42 @@ def _adamw_decay_after_step(p, m, v, g, step, lr, b1, b2, eps, wd):
     return p_t * (1 - lr * wd), m_t, v_t
 
 
+def _loss_variant(change):
+    """The token loss with one planted mistake (the definition retyped with a switch)."""
+    def f(kind, logits, target, weight=None, mask=None, old_logp=None, adv=None, corr=None,
+          clip_lo=0.2, clip_hi=0.2):
+        z = np.asarray(logits, np.float64)
+        n, V = z.shape
+        if kind == oracle.LOSS_CE:
+            act = np.asarray(weight) != 0
+        else:
+            act = np.ones(n, bool) if (mask is None or change == "mask_ignored") else np.asarray(mask) != 0
+        L, lp, dz = np.zeros(n), np.zeros(n), np.zeros((n, V))
+        for t in np.nonzero(act)[0]:
+            mx = 0.0 if change == "no_shift" else np.max(z[t])
+            e = np.exp(z[t] - mx)
+            logp = z[t, target[t]] - (mx + np.log(e.sum()))
+            soft = e / e.sum()
+            if kind == oracle.LOSS_CE:
+                L[t], g = -weight[t] * logp, weight[t]
+            else:
+                c = 1.0 if (corr is None or change == "corr_ignored") else corr[t]
+                rho = np.exp((old_logp[t] - logp) if change == "ratio_inverted" else (logp - old_logp[t]))
+                A = adv[t]
+                un, cl = rho * A, min(max(rho, 1 - clip_lo), 1 + clip_hi) * A
+                pick = max if change == "ppo_max" else min
+                if kind == oracle.LOSS_IS or pick(un, cl) == un:
+                    L[t], g = -c * un, c * A * rho
+                else:
+                    L[t], g = -c * cl, 0.0
+            lp[t] = logp
+            dz[t] = (-g if change == "grad_sign" else g) * soft
+            if change != "no_onehot":
+                dz[t, target[t]] -= (-g if change == "grad_sign" else g)
+        return L, lp, dz
+    return f
+
+
 def _plan_unstable(idx, num_slots, mask=None, ranks=None):
     p = oracle.canonical_plan(idx, num_slots, mask=mask, ranks=ranks)
     p = dict(p)
@@ -614,6 +752,13 @@ MUTANTS = {
     "adamw_beta1_in_v": _mutant(adamw=_adamw_beta1_in_v),
     "adamw_step_off_by_one": _mutant(adamw=_adamw_step_off_by_one),
     "adamw_decay_after_step": _mutant(adamw=_adamw_decay_after_step),
+    "loss_no_shift": _mutant(token_loss=_loss_variant("no_shift")),
+    "loss_grad_sign": _mutant(token_loss=_loss_variant("grad_sign")),
+    "loss_no_onehot": _mutant(token_loss=_loss_variant("no_onehot")),
+    "loss_ppo_max": _mutant(token_loss=_loss_variant("ppo_max")),
+    "loss_ratio_inverted": _mutant(token_loss=_loss_variant("ratio_inverted")),
+    "loss_mask_ignored": _mutant(token_loss=_loss_variant("mask_ignored")),
+    "loss_corr_ignored": _mutant(token_loss=_loss_variant("corr_ignored")),
     "plan_unstable": _mutant(canonical_plan=_plan_unstable),
     "plan_inclusive_offsets": _mutant(canonical_plan=_plan_inclusive_offsets),
     "plan_mask_ignored": _mutant(canonical_plan=_plan_mask_ignored),
