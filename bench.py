@@ -7,8 +7,9 @@ masked-backward workload, the plan followed by lora_grad.  The headline line is
 the decode workload (256 single-token rows over 64 rank-16 adapters, hidden
 4096 -> 4096, bf16): tokens/s of whole steps.  The other four workloads are
 measured the same way and reported under "extra"; for the masked-backward
-workload the input gradient (lora_grad_x, over the same plan) and the AdamW step
-over its adapters' tensors (lora_adamw_step) are also timed alone.
+workload the input gradient (lora_grad_x, over the same plan), the AdamW step
+over its adapters' tensors (lora_adamw_step) and the PPO-style token loss over
+logits [n, 32768] with its action mask (lora_token_loss) are also timed alone.
 
 Measurement protocol
   * inputs are resident in HBM before timing; each workload keeps R copies of its
@@ -247,6 +248,44 @@ class Rig:
         self.L.lib().lora_plan_destroy(h)   # host object only; enqueued work keeps its arguments
 
 
+LOSS_VOCAB = 32768
+
+
+def token_loss_leg(case, timed, steps):
+    """The PPO-style token loss on logits [n, LOSS_VOCAB] (bf16 in and out) with
+    the batch's action mask: the active rows' logits are read once (rows up to
+    32768 stay in registers) and every gradient row is written."""
+    import torch
+    import paper_2601_07376_amd as L
+    n, V = case.n, LOSS_VOCAB
+    g = torch.Generator(device="cuda").manual_seed(5)
+    z = (torch.randn(n, V, device="cuda", generator=g) * 2.0).to(torch.bfloat16)
+    dz = torch.empty_like(z)
+    target = torch.randint(0, V, (n,), device="cuda", generator=g, dtype=torch.int32)
+    mask = torch.from_numpy(np.asarray(case.mask, np.uint8)).cuda()
+    old = torch.randn(n, device="cuda", generator=g) - 10.0
+    adv = torch.randn(n, device="cuda", generator=g)
+    loss = torch.empty(n, device="cuda")
+    logp = torch.empty(n, device="cuda")
+    lib = L.lib()
+    args = [2, n, V, z.data_ptr(), 1, V, target.data_ptr(), None, mask.data_ptr(), old.data_ptr(),
+            adv.data_ptr(), None, 0.2, 0.2, loss.data_ptr(), logp.data_ptr(), dz.data_ptr(), 1, V]
+
+    def enqueue(i):
+        st = lib.lora_token_loss(*args, ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+        assert st == 0, lib.lora_last_error()
+    for i in range(3):
+        enqueue(i)
+    us = timed(enqueue, max(20, steps // 4)) * 1e3
+    act = int(np.count_nonzero(case.mask))
+    nbytes = act * V * 2 + n * V * 2 + n * 4 * 6      # active logits read, gradient written, per-row vectors
+    del z, dz
+    torch.cuda.empty_cache()
+    return dict(op="lora_token_loss", kind="ppo", rows=n, active_rows=act, vocab=V, us_mean=us,
+                bytes=nbytes, GBps=nbytes / (us * 1e-6) / 1e9,
+                hbm_frac=nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS)
+
+
 def sleep_rate(torch):
     """GPU sleep-kernel cycles per millisecond (for the start gate)."""
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -307,6 +346,7 @@ def run_workload(cfg, steps, warmup, rate):
         gx_us = timed(lambda i: rig.run_grad_x(rig.sets[i % nc], handles[i % nc]), steps) * 1e3
     if case.mask is not None:
         adam_us = timed(lambda i: rig.run_adamw(rig.sets[i % nc]), steps) * 1e3
+    loss_r = token_loss_leg(case, timed, steps) if case.mask is not None else None
     for h in handles:
         L.lib().lora_plan_destroy(h)
     plan_us = timed(lambda i: L.lib().lora_plan_destroy(rig.build_plan(rig.sets[i % nc])),
@@ -326,6 +366,11 @@ def run_workload(cfg, steps, warmup, rate):
     r["mfma_frac_ceiling"] = min(1.0, (counts["flops"] / counts["op_bytes"]) * HBM_PEAK_GBS
                                  / 1e3 / peak_f)
     r["step_GBps"] = ws_bytes / (ms_step * 1e-3) / 1e9
+    if loss_r is not None:
+        r["token_loss"] = loss_r
+        log(f"[bench]   lora_token_loss (PPO, {loss_r['rows']} rows, {loss_r['active_rows']} active, "
+            f"vocab {loss_r['vocab']}): {loss_r['us_mean']:.2f} us, {loss_r['GBps']:.0f} GB/s = "
+            f"{100 * loss_r['hbm_frac']:.1f}% HBM")
     if gx_us is not None:
         # input gradient: dY rows read, f32 dX rows read and written, both
         # factors of every touched adapter read once

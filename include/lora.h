@@ -271,6 +271,45 @@ typedef struct lora_adamw_tensor {
  * unless every record is valid.  Asynchronous on stream. */
 lora_status lora_adamw_step(const lora_adamw_tensor* tensors, int32_t count, void* stream);
 
+/* ---- masked token-level losses -> gradient at the logits (Section 3.3: SFT
+ *      weights w_t on the target-token axis; for RL the explicit action mask
+ *      m_t, rollout log-probabilities l_old, advantages A_t and optional
+ *      correction weights c_t on the same axis; Section 3.5, "Forward/backward
+ *      path": cross-entropy, importance-sampling and PPO-style objectives) -----
+ * The paper names the objectives; their forms here are the standard ones,
+ * summed over positions (advantages arrive already normalised by the response
+ * length, as the paper's data path sends them).  For row t with logits z_t:
+ *     logp_t = z_t[y_t] - log sum_v exp(z_t[v])
+ *     LORA_LOSS_CE:  L_t = -w_t logp_t                          (row active iff w_t != 0)
+ *     LORA_LOSS_IS:  L_t = -m_t c_t A_t rho_t,  rho_t = exp(logp_t - l_old_t)
+ *     LORA_LOSS_PPO: L_t = -m_t c_t min(rho_t A_t, clip(rho_t, 1 - clip_lo, 1 + clip_hi) A_t)
+ *                    (IS / PPO rows active iff m_t != 0; mask NULL = every row)
+ *     dlogits_t = dL_t / dz_t = g_t (softmax(z_t) - onehot(y_t)),  g_t = -dL_t / dlogp_t
+ *     (PPO: g_t = m_t c_t A_t rho_t where the unclipped term is the minimum,
+ *     ties included, else 0).
+ * Inactive rows: their logits are never read, loss = logp = 0, and their
+ * gradient row is written as zeros.  An active row whose target is outside
+ * [0, vocab) gets NaN loss, logp and gradient row.
+ * logits: device [n, ldz] float32 or bfloat16 (ldz >= vocab, a multiple of 8,
+ * 16-byte aligned; the padding of each row up to the next multiple of 8 is
+ * read, never used).  target: device int32 [n].  weight: device float32 [n]
+ * (CE only, required).  mask: device uint8 [n] (IS / PPO, nullable).
+ * old_logp, adv: device float32 [n] (IS / PPO, required).  corr: device float32
+ * [n] (IS / PPO, nullable = 1).  clip_lo, clip_hi >= 0 (PPO).
+ * loss: device float32 [n] (required); logp: device float32 [n] (nullable).
+ * dlogits: device [n, ldd] float32 or bfloat16, written for columns < vocab of
+ * every row; it must not overlap logits.  Errors: NULL, SHAPE (n or vocab out
+ * of range), DTYPE, ALIGN, VALUE (unknown kind, negative or non-finite clip).
+ * Asynchronous on stream. */
+typedef enum lora_loss_kind { LORA_LOSS_CE = 0, LORA_LOSS_IS = 1, LORA_LOSS_PPO = 2 } lora_loss_kind;
+#define LORA_MAX_VOCAB (1 << 24)
+lora_status lora_token_loss(lora_loss_kind kind, int32_t n, int32_t vocab, const void* logits,
+                            lora_dtype logits_dtype, int64_t ldz, const int32_t* target,
+                            const float* weight, const uint8_t* mask, const float* old_logp,
+                            const float* adv, const float* corr, float clip_lo, float clip_hi,
+                            float* loss, float* logp, void* dlogits, lora_dtype dlogits_dtype,
+                            int64_t ldd, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

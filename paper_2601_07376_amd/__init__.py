@@ -2,15 +2,16 @@
 
 Python face of liblora_mi355x.so (include/lora.h): ``Table`` (adapter table),
 ``Plan`` (row grouping by adapter id), ``shrink``, ``expand``, ``apply``,
-``grad``, ``grad_x`` and ``adamw_step``.  Torch supplies device memory and streams; the computation runs in
+``grad``, ``grad_x``, ``adamw_step`` and ``token_loss``.  Torch supplies device memory and streams; the computation runs in
 the library's HIP kernels.  Nothing here falls back to another implementation:
 if the library is not built, every call raises.
 """
-from .lora import (AdamWTensor, LORA_BF16, LORA_DATA_BAD_ID, LORA_DATA_BAD_SEGMENTS, LORA_DATA_EMPTY_SLOT,
+from .lora import (AdamWTensor, LOSS_CE, LOSS_IS, LOSS_PPO, LORA_BF16, LORA_DATA_BAD_ID, LORA_DATA_BAD_SEGMENTS, LORA_DATA_EMPTY_SLOT,
                    LORA_F32, LIB_PATH, LoraError, Plan, Table, apply, apply_workspace, expand,
-                   adamw_step, grad, grad_workspace, grad_x, grad_x_workspace, lib, shrink)
+                   adamw_step, grad, grad_workspace, grad_x, grad_x_workspace, lib, shrink,
+                   token_loss)
 
 __all__ = ["Table", "Plan", "shrink", "expand", "apply", "grad", "grad_x", "adamw_step",
-           "AdamWTensor", "apply_workspace",
+           "AdamWTensor", "token_loss", "LOSS_CE", "LOSS_IS", "LOSS_PPO", "apply_workspace",
            "grad_workspace", "grad_x_workspace", "lib", "LoraError", "LORA_F32", "LORA_BF16", "LORA_DATA_BAD_ID",
            "LORA_DATA_EMPTY_SLOT", "LORA_DATA_BAD_SEGMENTS", "LIB_PATH"]

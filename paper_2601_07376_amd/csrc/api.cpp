@@ -797,4 +797,54 @@ lora_status lora_adamw_step(const lora_adamw_tensor* tensors, int32_t count, voi
   return ok();
 }
 
+// ---- masked token-level losses ------------------------------------------------
+
+lora_status lora_token_loss(lora_loss_kind kind, int32_t n, int32_t vocab, const void* logits,
+                            lora_dtype logits_dtype, int64_t ldz, const int32_t* target,
+                            const float* weight, const uint8_t* mask, const float* old_logp,
+                            const float* adv, const float* corr, float clip_lo, float clip_hi,
+                            float* loss, float* logp, void* dlogits, lora_dtype dlogits_dtype,
+                            int64_t ldd, void* stream) {
+  if (kind != LORA_LOSS_CE && kind != LORA_LOSS_IS && kind != LORA_LOSS_PPO)
+    return fail(LORA_ERR_VALUE, "unknown loss kind %d", (int)kind);
+  if (n < 0 || n > LORA_MAX_ROWS) return fail(LORA_ERR_SHAPE, "n = %d out of range", n);
+  if (vocab < 1 || vocab > LORA_MAX_VOCAB) return fail(LORA_ERR_SHAPE, "vocab = %d out of range", vocab);
+  if (!(std::isfinite(clip_lo) && clip_lo >= 0.f && std::isfinite(clip_hi) && clip_hi >= 0.f))
+    return fail(LORA_ERR_VALUE, "clip range (%g, %g) out of range", clip_lo, clip_hi);
+  lora_status st;
+  if ((st = check_matrix(logits, logits_dtype, ldz, vocab, "logits", n)) != LORA_OK) return st;
+  if ((st = check_matrix(dlogits, dlogits_dtype, ldd, vocab, "dlogits", n)) != LORA_OK) return st;
+  if (n == 0) return ok();
+  if (target == nullptr || loss == nullptr) return fail(LORA_ERR_NULL, "target or loss is NULL");
+  if (kind == LORA_LOSS_CE && weight == nullptr) return fail(LORA_ERR_NULL, "cross-entropy needs weight");
+  if (kind != LORA_LOSS_CE && (old_logp == nullptr || adv == nullptr))
+    return fail(LORA_ERR_NULL, "policy-gradient losses need old_logp and adv");
+  const uintptr_t zb = (uintptr_t)logits, ze = zb + (uintptr_t)n * (uintptr_t)ldz * dsize(logits_dtype);
+  const uintptr_t db = (uintptr_t)dlogits, de = db + (uintptr_t)n * (uintptr_t)ldd * dsize(dlogits_dtype);
+  if (zb < de && db < ze) return fail(LORA_ERR_SHAPE, "dlogits overlaps logits");
+  lora::LossLaunch l{};
+  l.kind = (int32_t)kind;
+  l.n = n;
+  l.vocab = vocab;
+  l.logits = logits;
+  l.logits_bf16 = logits_dtype == LORA_BF16;
+  l.ldz = ldz;
+  l.target = target;
+  l.weight = weight;
+  l.mask = mask;
+  l.old_logp = old_logp;
+  l.adv = adv;
+  l.corr = corr;
+  l.clip_lo = clip_lo;
+  l.clip_hi = clip_hi;
+  l.loss = loss;
+  l.logp = logp;
+  l.dlogits = dlogits;
+  l.dlogits_bf16 = dlogits_dtype == LORA_BF16;
+  l.ldd = ldd;
+  hipError_t e = lora::launch_token_loss(l, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "token-loss launch");
+  return ok();
+}
+
 }  // extern "C"

@@ -217,4 +217,25 @@ struct AdamwLaunch {
 };
 hipError_t launch_adamw(const AdamwLaunch* t, int32_t count, hipStream_t s);
 
+// masked token-level loss and its gradient at the logits, one workgroup per row
+struct LossLaunch {
+  int32_t kind, n, vocab;
+  const void* logits;
+  bool logits_bf16;
+  int64_t ldz;
+  const int32_t* target;
+  const float* weight;
+  const uint8_t* mask;
+  const float* old_logp;
+  const float* adv;
+  const float* corr;
+  float clip_lo, clip_hi;
+  float* loss;
+  float* logp;
+  void* dlogits;
+  bool dlogits_bf16;
+  int64_t ldd;
+};
+hipError_t launch_token_loss(const LossLaunch& l, hipStream_t s);
+
 }  // namespace lora

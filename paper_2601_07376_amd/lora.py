@@ -50,6 +50,8 @@ SIGNATURES = {
     "lora_grad_x_workspace_bytes": (_sz, [_vp]),
     "lora_grad_x": (_i32, [_vp, _vp, _i32, _i64, _vp, _i32, _i64, _vp, _sz, _vp]),
     "lora_adamw_step": (_i32, [_vp, _i32, _vp]),
+    "lora_token_loss": (_i32, [_i32, _i32, _i32, _vp, _i32, _i64, _vp, _vp, _vp, _vp, _vp, _vp,
+                               ctypes.c_float, ctypes.c_float, _vp, _vp, _vp, _i32, _i64, _vp]),
 }
 
 _lib = None
@@ -322,3 +324,19 @@ def adamw_step(params, stream=None):
                               int(q["step"]), float(q["lr"]), float(q["beta1"]),
                               float(q["beta2"]), float(q["eps"]), float(q["weight_decay"]))
     _check(lib().lora_adamw_step(ctypes.cast(recs, ctypes.c_void_p), len(params), _stream(stream)))
+
+
+LOSS_CE, LOSS_IS, LOSS_PPO = 0, 1, 2
+
+
+def token_loss(kind, logits, target, dlogits, loss, logp=None, weight=None, mask=None,
+               old_logp=None, adv=None, corr=None, clip_lo=0.2, clip_hi=0.2, stream=None):
+    """Masked token-level loss (kind LOSS_CE / LOSS_IS / LOSS_PPO): per-token
+    ``loss`` and ``logp`` and the gradient ``dlogits`` = dL/dlogits, in place."""
+    n, vocab = logits.shape
+    _check(lib().lora_token_loss(int(kind), n, vocab, _ptr(logits), _dtype(logits),
+                                 _rowmajor(logits, "logits"), _ptr(target), _ptr(weight), _ptr(mask),
+                                 _ptr(old_logp), _ptr(adv), _ptr(corr), float(clip_lo),
+                                 float(clip_hi), _ptr(loss), _ptr(logp), _ptr(dlogits),
+                                 _dtype(dlogits), _rowmajor(dlogits, "dlogits"), _stream(stream)))
+    return loss, logp, dlogits

@@ -160,3 +160,29 @@ def test_adamw_count_and_cross_record_overlap():
     # a zero-size record is skipped (nothing to validate but its hyperparameters)
     empty = (lora.AdamWTensor * 1)(_adam(n=0, p=0, m=0, v=0, g=0, p_bf16=0))
     assert L.lora_adamw_step(ctypes.cast(empty, ctypes.c_void_p), 1, None) == 0
+
+
+def _loss_call(kind=0, n=4, vocab=64, z=FAKE, ldz=64, target=FAKE + 0x8000, weight=FAKE + 0x9000,
+               old=FAKE + 0xa000, adv=FAKE + 0xb000, clip_lo=0.2, loss=FAKE + 0xc000,
+               dz=FAKE + 0x20000, ldd=64):
+    L = lora.lib()
+    v = lambda x: ctypes.c_void_p(x) if x else None
+    return L.lora_token_loss(kind, n, vocab, v(z), lora.LORA_BF16, ldz, v(target), v(weight), None,
+                             v(old), v(adv), None, clip_lo, 0.2, v(loss), None, v(dz),
+                             lora.LORA_F32, ldd, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(kind=7), 10), (dict(n=-1), 2), (dict(vocab=0), 2), (dict(clip_lo=-0.5), 10),
+    (dict(clip_lo=float("nan")), 10), (dict(z=FAKE_ODD), 4), (dict(ldz=60), 2), (dict(ldd=68), 4),
+    (dict(z=0), 1), (dict(target=0), 1), (dict(loss=0), 1), (dict(weight=0), 1),
+    (dict(kind=2, adv=0), 1), (dict(dz=FAKE + 0x100), 2),      # dlogits overlaps logits
+])
+def test_token_loss_rejects(kw, status):
+    """Host validation only: every call here is rejected before anything is enqueued."""
+    assert _loss_call(**kw) == status
+    assert lora.lib().lora_last_error()
+
+
+def test_token_loss_empty_batch():
+    assert _loss_call(n=0, target=0, loss=0, weight=0) == 0
