@@ -10,6 +10,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -288,6 +289,59 @@ PlanLayout plan_layout(int32_t n, int32_t S) {
 
 }  // namespace lora
 
+namespace {
+
+// A second stream per device (default priority) for the small-group path of
+// a mixed batch, which runs beside the grouped path: the two write disjoint
+// rows of Y and disjoint parts of the workspace.  Created at the first call
+// that can use it outside stream capture; the fork and join are events, so a
+// captured call records both streams into the caller's graph.  One mutex
+// orders the host-side fork sequences of concurrent callers.
+struct AuxStream {
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+};
+constexpr int AUX_DEVICES = 64;
+std::mutex g_aux_mutex;
+AuxStream g_aux[AUX_DEVICES];
+
+// the device's second stream, or nullptr (forking off, creation refused
+// during capture, or a creation failure: the caller then runs one stream)
+AuxStream* aux_stream(hipStream_t caller) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= AUX_DEVICES) return nullptr;
+  AuxStream& a = g_aux[dev];
+  if (a.s != nullptr) return &a;
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(caller, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) return nullptr;
+  hipStream_t s = nullptr;
+  hipEvent_t f = nullptr, j = nullptr;
+  if (hipStreamCreateWithFlags(&s, hipStreamNonBlocking) != hipSuccess) return nullptr;
+  if (hipEventCreateWithFlags(&f, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&j, hipEventDisableTiming) != hipSuccess) {
+    if (f != nullptr) (void)hipEventDestroy(f);
+    (void)hipStreamDestroy(s);
+    return nullptr;
+  }
+  a.s = s;
+  a.fork = f;
+  a.join = j;
+  return &a;
+}
+
+// Whether a grouped batch forks its small-group path.  The fork and join cost
+// about 10 us of queue latency, so they pay only when both paths have work;
+// the host cannot see the grouping (it is built on the device), so it expects
+// small groups when the batch has fewer than 4 x SMALL_ROWS rows per table
+// slot.  LORA_APPLY_FORK=0 / 2 forces it off / on.
+bool fork_policy(const lora_plan* p) {
+  const int v = env_int("LORA_APPLY_FORK", 1);
+  if (v == 0 || v == 2) return v == 2;
+  return (int64_t)p->n < (int64_t)4 * lora::SMALL_ROWS * p->table->num_slots;
+}
+
+}  // namespace
+
 extern "C" {
 
 int32_t lora_abi_version(void) { return LORA_ABI_VERSION; }
@@ -553,6 +607,7 @@ int32_t small_split_slices(const lora_plan* p) {
   return std::max(1, std::min(lora::SPLIT_SLICES_MAX, sl));
 }
 
+
 lora_status lora_apply(const lora_plan* p, const void* X, lora_dtype x_dtype, int64_t ldx, void* Y,
                        lora_dtype y_dtype, int64_t ldy, void* ws, size_t ws_bytes, void* stream) {
   lora_status st = check_plan(p);
@@ -575,6 +630,41 @@ lora_status lora_apply(const lora_plan* p, const void* X, lora_dtype x_dtype, in
   lora::OpLaunch o = op_base(p);
   hipError_t e = hipSuccess;
   if (mfma) {
+    // a mixed batch: the small-group path on the second stream, forked from
+    // and joined back into the caller's
+    std::unique_lock<std::mutex> lk(g_aux_mutex, std::defer_lock);
+    AuxStream* aux = nullptr;
+    hipStream_t s_small = s;
+    if (ub_large(p) > 0 && fork_policy(p)) {
+      lk.lock();
+      aux = aux_stream(s);
+      if (aux != nullptr) {
+        if ((e = hipEventRecord(aux->fork, s)) != hipSuccess) return hip_fail(e, "fork record");
+        if ((e = hipStreamWaitEvent(aux->s, aux->fork, 0)) != hipSuccess) return hip_fail(e, "fork wait");
+        s_small = aux->s;
+      } else {
+        lk.unlock();
+      }
+    }
+    {
+      lora::OpLaunch os = o;
+      os.count_word = lora::HDR_NSMALL;
+      os.first_word = -1;
+      os.rb_ub = ub_small(p);
+      // (the split path needs the workspace; without a usable one the fused
+      // kernel runs)
+      if (ws != nullptr && ws_bytes >= need && aligned(ws, 16) && small_split_policy(p)) {
+        float* part = reinterpret_cast<float*>(static_cast<char*>(ws) + apply_h_bytes(p));
+        e = lora::launch_small_split_mfma(os, X, ldx, Y, y_dtype, ldy, small_chunks_policy(t->d_out),
+                                          small_split_slices(p), part, s_small);
+        if (e != hipSuccess) return hip_fail(e, "split small-group launch");
+      } else {
+        e = lora::launch_bgmv_mfma(os, X, ldx, Y, y_dtype, ldy, small_chunks_policy(t->d_out), s_small);
+        if (e != hipSuccess) return hip_fail(e, "fused small-group launch");
+      }
+    }
+    if (aux != nullptr && (e = hipEventRecord(aux->join, aux->s)) != hipSuccess)
+      return hip_fail(e, "join record");
     if (ub_large(p) > 0) {
       o.count_word = lora::HDR_NRB_LARGE;
       o.first_word = -1;
@@ -587,20 +677,8 @@ lora_status lora_apply(const lora_plan* p, const void* X, lora_dtype x_dtype, in
         e = lora::launch_expand_mfma(o, H, ldh, lora::SHRINK_KS_MAX, plane, Y, y_dtype, ldy, s);
       if (e != hipSuccess) return hip_fail(e, "grouped shrink/expand launch");
     }
-    o.count_word = lora::HDR_NSMALL;
-    o.first_word = -1;
-    o.rb_ub = ub_small(p);
-    // (the split path needs the workspace; without a usable one the fused
-    // kernel runs)
-    if (ws != nullptr && ws_bytes >= need && aligned(ws, 16) && small_split_policy(p)) {
-      float* part = reinterpret_cast<float*>(static_cast<char*>(ws) + apply_h_bytes(p));
-      e = lora::launch_small_split_mfma(o, X, ldx, Y, y_dtype, ldy, small_chunks_policy(t->d_out),
-                                        small_split_slices(p), part, s);
-      if (e != hipSuccess) return hip_fail(e, "split small-group launch");
-    } else {
-      e = lora::launch_bgmv_mfma(o, X, ldx, Y, y_dtype, ldy, small_chunks_policy(t->d_out), s);
-      if (e != hipSuccess) return hip_fail(e, "fused small-group launch");
-    }
+    if (aux != nullptr && (e = hipStreamWaitEvent(s, aux->join, 0)) != hipSuccess)
+      return hip_fail(e, "join wait");
   } else {
     o.count_word = lora::HDR_NRB_TOTAL;
     o.first_word = -1;
