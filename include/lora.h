@@ -191,7 +191,12 @@ lora_status lora_expand(const lora_plan* p, const float* H, int64_t ldh, void* Y
  * that keeps H on chip; larger groups (prefill segments) run a grouped
  * matrix-core shrink and expand through the workspace.  ws: device,
  * lora_apply_workspace_bytes(p) bytes, 16-byte aligned; it may be NULL only
- * when every group is small (the fused kernel then runs). */
+ * when every group is small (the fused kernel then runs).  A batch with fewer
+ * than 64 rows per table slot that has large groups runs its small-group
+ * kernels on a library-owned second stream of the current device, forked from
+ * and joined back into `stream` with events (so later work on `stream` and a
+ * graph captured from it see the whole update); concurrent calls on one
+ * device take a host mutex around that sequence. */
 size_t      lora_apply_workspace_bytes(const lora_plan* p);
 lora_status lora_apply(const lora_plan* p, const void* X, lora_dtype x_dtype, int64_t ldx,
                        void* Y, lora_dtype y_dtype, int64_t ldy, void* ws, size_t ws_bytes,
