@@ -308,25 +308,33 @@ AuxStream g_aux[AUX_DEVICES];
 // the device's second stream, or nullptr (forking off, creation refused
 // during capture, or a creation failure: the caller then runs one stream)
 AuxStream* aux_stream(hipStream_t caller) {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= AUX_DEVICES) return nullptr;
+  // the caller's stream decides the device (the null stream: the current one)
+  int cur = 0, dev = 0;
+  if (hipGetDevice(&cur) != hipSuccess) return nullptr;
+  dev = cur;
+  if (caller != nullptr && hipStreamGetDevice(caller, &dev) != hipSuccess) return nullptr;
+  if (dev < 0 || dev >= AUX_DEVICES) return nullptr;
   AuxStream& a = g_aux[dev];
   if (a.s != nullptr) return &a;
   hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
   if (hipStreamIsCapturing(caller, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) return nullptr;
+  if (dev != cur && hipSetDevice(dev) != hipSuccess) return nullptr;
   hipStream_t s = nullptr;
   hipEvent_t f = nullptr, j = nullptr;
-  if (hipStreamCreateWithFlags(&s, hipStreamNonBlocking) != hipSuccess) return nullptr;
-  if (hipEventCreateWithFlags(&f, hipEventDisableTiming) != hipSuccess ||
-      hipEventCreateWithFlags(&j, hipEventDisableTiming) != hipSuccess) {
+  bool made = hipStreamCreateWithFlags(&s, hipStreamNonBlocking) == hipSuccess;
+  made = made && hipEventCreateWithFlags(&f, hipEventDisableTiming) == hipSuccess;
+  made = made && hipEventCreateWithFlags(&j, hipEventDisableTiming) == hipSuccess;
+  if (!made) {
+    if (j != nullptr) (void)hipEventDestroy(j);
     if (f != nullptr) (void)hipEventDestroy(f);
-    (void)hipStreamDestroy(s);
-    return nullptr;
+    if (s != nullptr) (void)hipStreamDestroy(s);
+  } else {
+    a.s = s;
+    a.fork = f;
+    a.join = j;
   }
-  a.s = s;
-  a.fork = f;
-  a.join = j;
-  return &a;
+  if (dev != cur) (void)hipSetDevice(cur);
+  return made ? &a : nullptr;
 }
 
 // Whether a grouped batch forks its small-group path.  The fork and join cost
