@@ -7,6 +7,9 @@
 //   IS:  L_t = -m_t c_t A_t rho_t,  rho_t = exp(logp_t - l_old_t)
 //   PPO: L_t = -m_t c_t min(rho_t A_t, clip(rho_t, 1 - lo, 1 + hi) A_t)
 //   dL_t/dz_t = g_t (softmax(z_t) - onehot(y_t)),  g_t = -dL_t/dlogp_t
+// The per-element exponentials (arguments <= 0) use the hardware exp2 path,
+// __expf: its extra relative error, about |z - lse| 2^-24, is below the
+// log-sum-exp's own summation error; per-row values use expf.
 // One workgroup per row.  A row of up to LS_NV vectors per thread stays in
 // registers between the two passes (one read of the logits); longer rows are
 // read twice.  Inactive rows (w_t = 0, or m_t = 0) are not read: their loss and
@@ -136,7 +139,7 @@ __global__ __launch_bounds__(LS_THREADS) void token_loss_kernel(LossArgs a) {
       float cs = 0.f;
 #pragma unroll
       for (int i = 0; i < E; ++i)
-        if (q * E + i < V) cs += expf(reg[k].at(i) - cm);
+        if (q * E + i < V) cs += __expf(reg[k].at(i) - cm);
       lse_combine(m, s, cm, cs);
     }
   }
@@ -208,7 +211,7 @@ __global__ __launch_bounds__(LS_THREADS) void token_loss_kernel(LossArgs a) {
       float d[E];
 #pragma unroll
       for (int i = 0; i < E; ++i) {
-        const float p = expf(reg[k].at(i) - lse);
+        const float p = __expf(reg[k].at(i) - lse);
         d[i] = v0 + i == y ? fmaf(g, p, -g) : g * p;
       }
       if (v0 + E <= V) {
