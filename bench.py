@@ -7,7 +7,8 @@ masked-backward workload, the plan followed by lora_grad.  The headline line is
 the decode workload (256 single-token rows over 64 rank-16 adapters, hidden
 4096 -> 4096, bf16): tokens/s of whole steps.  The other four workloads are
 measured the same way and reported under "extra"; for the masked-backward
-workload the input gradient (lora_grad_x, over the same plan), the AdamW step
+workload the input gradient (lora_grad_x, over the same plan), both gradients in
+one call (lora_backward), the AdamW step
 over its adapters' tensors (lora_adamw_step) and the PPO-style token loss over
 logits [n, 32768] with its action mask (lora_token_loss) are also timed alone.
 
@@ -162,6 +163,7 @@ class Rig:
                                                    for t in d["dB"]])
                 d["dX"] = torch.zeros(n, case.d_in, dtype=torch.float32, device="cuda")
                 d["gx_ws"] = L.grad_x_workspace(probe)
+                d["bw_ws"] = L.backward_workspace(probe)
                 # optimizer state of every adapter tensor: fp32 master, moments,
                 # the gradient buffers above, and the table's bf16 weights as the
                 # rounded copy
@@ -230,6 +232,16 @@ class Rig:
         st = lib.lora_grad_x(h, dY.data_ptr(), 1 if self.case.x_dtype == "bf16" else 0,
                              dY.stride(0), dX.data_ptr(), 0, dX.stride(0),
                              d["gx_ws"].data_ptr(), d["gx_ws"].numel(), stream)
+        assert st == 0, lib.lora_last_error()
+
+    def run_backward(self, d, h):
+        """Enqueue lora_backward (adapter gradients and input gradient) for one copy."""
+        lib = self.L.lib()
+        stream = ctypes.c_void_p(self.torch.cuda.current_stream().cuda_stream)
+        X, dY, dX = d["X"], d["dY"], d["dX"]
+        st = lib.lora_backward(h, X.data_ptr(), 1, X.stride(0), dY.data_ptr(), 1, dY.stride(0), None, 0,
+                               d["pA"], d["pB"], 0, dX.data_ptr(), 0, dX.stride(0),
+                               d["bw_ws"].data_ptr(), d["bw_ws"].numel(), stream)
         assert st == 0, lib.lora_last_error()
 
     def run_adamw(self, d):
@@ -341,9 +353,10 @@ def run_workload(cfg, steps, warmup, rate):
     torch.cuda.synchronize()
     nc = len(rig.sets)
     op_mean = timed(lambda i: rig.run_op(rig.sets[i % nc], handles[i % nc]), steps) * 1e3
-    gx_us = adam_us = None
+    gx_us = adam_us = bw_us = None
     if case.mask is not None and case.x_dtype == "bf16":
         gx_us = timed(lambda i: rig.run_grad_x(rig.sets[i % nc], handles[i % nc]), steps) * 1e3
+        bw_us = timed(lambda i: rig.run_backward(rig.sets[i % nc], handles[i % nc]), steps) * 1e3
     if case.mask is not None:
         adam_us = timed(lambda i: rig.run_adamw(rig.sets[i % nc]), steps) * 1e3
     loss_r = token_loss_leg(case, timed, steps) if case.mask is not None else None
@@ -387,6 +400,14 @@ def run_workload(cfg, steps, warmup, rate):
                            TFLOPs=gx_flops / (gx_us * 1e-6) / 1e12)
         log(f"[bench]   lora_grad_x: {gx_us:.2f} us, {r['grad_x']['GBps']:.0f} GB/s = "
             f"{100 * r['grad_x']['hbm_frac']:.1f}% HBM")
+    if bw_us is not None:
+        bb = counts["op_bytes"] + r["grad_x"]["bytes"]
+        r["backward"] = dict(op="lora_backward", us_mean=bw_us, bytes=bb,
+                             GBps=bb / (bw_us * 1e-6) / 1e9,
+                             hbm_frac=bb / (bw_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
+                             separate_us=op_mean + gx_us)
+        log(f"[bench]   lora_backward (grad + grad_x): {bw_us:.2f} us against "
+            f"{op_mean + gx_us:.2f} us as two calls")
     if adam_us is not None:
         # per element: p, m, v, g read (16 bytes), p, m, v written (12), bf16 copy (2)
         el = rig.sets[0]["adam_elems"]

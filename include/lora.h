@@ -236,6 +236,22 @@ lora_status lora_grad_x(const lora_plan* p, const void* dY, lora_dtype dy_dtype,
                         void* dX, lora_dtype dx_dtype, int64_t lddx, void* ws, size_t ws_bytes,
                         void* stream);
 
+/* Both gradients of one backward step in one call: lora_grad's dA_a / dB_a
+ * and lora_grad_x's dX, with exactly their results (same kernels, same
+ * arguments and semantics as the two calls).  The input gradient runs on a
+ * library-owned second stream of the stream's device, forked from and joined
+ * back into `stream` with events, beside the adapter gradients; both read the
+ * plan and dY as they are when the call is made.  ws:
+ * lora_backward_workspace_bytes(p) bytes, 16-byte aligned.  Needs bfloat16 dY
+ * and weights (the input gradient's matrix-core path).  Errors: those of the
+ * two calls, all checked before anything is enqueued. */
+size_t      lora_backward_workspace_bytes(const lora_plan* p);
+lora_status lora_backward(const lora_plan* p, const void* X, lora_dtype x_dtype, int64_t ldx,
+                          const void* dY, lora_dtype dy_dtype, int64_t lddy, const float* H_saved,
+                          int64_t ldh, float* const* dA, float* const* dB, int32_t accumulate,
+                          void* dX, lora_dtype dx_dtype, int64_t lddx, void* ws, size_t ws_bytes,
+                          void* stream);
+
 /* ---- adapter-local optimizer step (Section 3.5: gradients, optimizer
  *      moments and step counters stay local to the owning policy, and each
  *      policy issues its own optimizer step) ------------------------------

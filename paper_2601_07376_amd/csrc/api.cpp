@@ -806,6 +806,55 @@ lora_status lora_grad_x(const lora_plan* p, const void* dY, lora_dtype dy_dtype,
   return ok();
 }
 
+// ---- combined backward -----------------------------------------------------------
+
+size_t lora_backward_workspace_bytes(const lora_plan* p) {
+  if (p == nullptr) return 0;
+  return al256(lora_grad_workspace_bytes(p)) + lora_grad_x_workspace_bytes(p);
+}
+
+lora_status lora_backward(const lora_plan* p, const void* X, lora_dtype x_dtype, int64_t ldx,
+                          const void* dY, lora_dtype dy_dtype, int64_t lddy, const float* H_saved,
+                          int64_t ldh, float* const* dA, float* const* dB, int32_t accumulate,
+                          void* dX, lora_dtype dx_dtype, int64_t lddx, void* ws, size_t ws_bytes,
+                          void* stream) {
+  lora_status st = check_plan(p);
+  if (st != LORA_OK) return st;
+  const lora_table* t = p->table;
+  // the input gradient's own checks first: once the adapter gradients are
+  // enqueued, nothing may fail before the input gradient is
+  if ((st = check_matrix(dY, dy_dtype, lddy, t->d_out, "dY", p->n)) != LORA_OK) return st;
+  if ((st = check_matrix(dX, dx_dtype, lddx, t->d_in, "dX", p->n)) != LORA_OK) return st;
+  if (dy_dtype != LORA_BF16 || t->w_dtype != LORA_BF16)
+    return fail(LORA_ERR_DTYPE, "the input gradient needs bfloat16 dY and weights");
+  const size_t need = lora_backward_workspace_bytes(p);
+  if (ws == nullptr) return fail(LORA_ERR_NULL, "backward workspace is NULL");
+  if (!aligned(ws, 16)) return fail(LORA_ERR_ALIGN, "backward workspace not 16-byte aligned");
+  if (ws_bytes < need) return fail(LORA_ERR_WORKSPACE, "backward workspace %zu bytes < %zu", ws_bytes, need);
+  const size_t off = al256(lora_grad_workspace_bytes(p));
+  char* wsb = static_cast<char*>(ws);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  // the input gradient on the second stream beside the adapter gradients:
+  // both read the plan and dY as they are when the call is made, and write
+  // disjoint outputs and workspace parts
+  std::unique_lock<std::mutex> lk(g_aux_mutex);
+  AuxStream* aux = p->n > 0 ? aux_stream(s) : nullptr;
+  hipError_t e;
+  if (aux != nullptr && (e = hipEventRecord(aux->fork, s)) != hipSuccess) return hip_fail(e, "fork record");
+  st = lora_grad(p, X, x_dtype, ldx, dY, dy_dtype, lddy, H_saved, ldh, dA, dB, accumulate, wsb, off,
+                 stream);
+  if (st != LORA_OK) return st;
+  if (aux == nullptr) {
+    lk.unlock();
+    return lora_grad_x(p, dY, dy_dtype, lddy, dX, dx_dtype, lddx, wsb + off, ws_bytes - off, stream);
+  }
+  if ((e = hipStreamWaitEvent(aux->s, aux->fork, 0)) != hipSuccess) return hip_fail(e, "fork wait");
+  st = lora_grad_x(p, dY, dy_dtype, lddy, dX, dx_dtype, lddx, wsb + off, ws_bytes - off, aux->s);
+  if ((e = hipEventRecord(aux->join, aux->s)) != hipSuccess) return hip_fail(e, "join record");
+  if ((e = hipStreamWaitEvent(s, aux->join, 0)) != hipSuccess) return hip_fail(e, "join wait");
+  return st;
+}
+
 // ---- adapter-local optimizer step ---------------------------------------------
 
 static_assert(sizeof(lora_adamw_tensor) == 72 && offsetof(lora_adamw_tensor, n) == 40 &&

@@ -50,6 +50,9 @@ SIGNATURES = {
     "lora_grad_x_workspace_bytes": (_sz, [_vp]),
     "lora_grad_x": (_i32, [_vp, _vp, _i32, _i64, _vp, _i32, _i64, _vp, _sz, _vp]),
     "lora_adamw_step": (_i32, [_vp, _i32, _vp]),
+    "lora_backward_workspace_bytes": (_sz, [_vp]),
+    "lora_backward": (_i32, [_vp, _vp, _i32, _i64, _vp, _i32, _i64, _vp, _i64, _vp, _vp, _i32, _vp,
+                             _i32, _i64, _vp, _sz, _vp]),
     "lora_token_loss": (_i32, [_i32, _i32, _i32, _vp, _i32, _i64, _vp, _vp, _vp, _vp, _vp, _vp,
                                ctypes.c_float, ctypes.c_float, _vp, _vp, _vp, _i32, _i64, _vp]),
 }
@@ -290,6 +293,34 @@ def grad_x(plan, dY, dX, ws=None, stream=None):
     _check(lib().lora_grad_x(plan.handle, _ptr(dY), _dtype(dY), _rowmajor(dY, "dY"), _ptr(dX),
                              _dtype(dX), _rowmajor(dX, "dX"), _ptr(ws), ws.numel(), _stream(stream)))
     return dX
+
+
+def backward_workspace(plan):
+    return torch.empty(max(lib().lora_backward_workspace_bytes(plan.handle), 16), dtype=torch.uint8,
+                       device=plan.table.device)
+
+
+def backward(plan, X, dY, dX, dA=None, dB=None, H_saved=None, accumulate=False, ws=None,
+             stream=None):
+    """grad and grad_x of one backward step in one call (the input gradient
+    beside the adapter gradients); returns (dA, dB, dX)."""
+    t = plan.table
+    if dA is None:
+        dA = [torch.empty(r, t.d_in, dtype=torch.float32, device=X.device) if r > 0 else None
+              for r in t.ranks]
+    if dB is None:
+        dB = [torch.empty(t.d_out, r, dtype=torch.float32, device=X.device) if r > 0 else None
+              for r in t.ranks]
+    if ws is None:
+        ws = backward_workspace(plan)
+    pa = (ctypes.c_void_p * t.num_slots)(*[g.data_ptr() if g is not None else None for g in dA])
+    pb = (ctypes.c_void_p * t.num_slots)(*[g.data_ptr() if g is not None else None for g in dB])
+    ldh = _rowmajor(H_saved, "H_saved") if H_saved is not None else 0
+    _check(lib().lora_backward(plan.handle, _ptr(X), _dtype(X), _rowmajor(X, "X"), _ptr(dY),
+                               _dtype(dY), _rowmajor(dY, "dY"), _ptr(H_saved), ldh, pa, pb,
+                               1 if accumulate else 0, _ptr(dX), _dtype(dX), _rowmajor(dX, "dX"),
+                               _ptr(ws), ws.numel(), _stream(stream)))
+    return dA, dB, dX
 
 
 class AdamWTensor(ctypes.Structure):
