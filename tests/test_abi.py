@@ -186,3 +186,12 @@ def test_token_loss_rejects(kw, status):
 
 def test_token_loss_empty_batch():
     assert _loss_call(n=0, target=0, loss=0, weight=0) == 0
+
+
+def test_backward_rejects_null_plan():
+    L = lora.lib()
+    assert L.lora_backward_workspace_bytes(None) == 0
+    st = L.lora_backward(None, ctypes.c_void_p(FAKE), lora.LORA_BF16, 64, ctypes.c_void_p(FAKE),
+                         lora.LORA_BF16, 64, None, 0, None, None, 0, ctypes.c_void_p(FAKE),
+                         lora.LORA_F32, 64, ctypes.c_void_p(FAKE), 1 << 20, None)
+    assert st == 1 and L.lora_last_error()
