@@ -38,16 +38,31 @@ def check_plan_golden(impl):
     return p["n_runs"] == int(g["n_runs"][0]) and p["error"] == bool(g["error"][0])
 
 
+def check_plan_empty_slot_golden(impl):
+    """Rows naming an empty slot (rank 0) carry no adapter and raise the flag."""
+    g = load_golden("plan_empty_slot_example.txt")
+    p = impl.canonical_plan(g["idx"].astype(np.int64), int(g["num_slots"][0]),
+                            mask=g["mask"].astype(np.uint8), ranks=g["ranks"].astype(np.int64))
+    for k in ("counts", "offsets", "perm", "run_start", "run_len", "run_adapter",
+              "m_counts", "m_offsets", "m_perm", "eff"):
+        if not np.array_equal(np.asarray(p[k]), g[k].astype(np.int64)):
+            return False
+    return p["n_runs"] == int(g["n_runs"][0]) and p["error"] == bool(g["error"][0])
+
+
 def _plan_fuzz_cases():
+    """(idx, S, mask, ranks): ranks hold zeros (empty slots) in half the cases."""
     rng = np.random.default_rng(1234)
     cases = [
-        (np.full(37, -1), 5, None),
-        (np.zeros(50, np.int64), 1, None),
-        (np.arange(40) % 7, 7, rng.integers(0, 2, 40)),
-        (np.zeros(0, np.int64), 3, None),
-        (np.array([3, 3, 3, -1, 3, 9, -7, 0]), 4, np.array([1, 0, 1, 1, 1, 1, 1, 0])),
+        (np.full(37, -1), 5, None, None),
+        (np.zeros(50, np.int64), 1, None, None),
+        (np.arange(40) % 7, 7, rng.integers(0, 2, 40), None),
+        (np.zeros(0, np.int64), 3, None, None),
+        (np.array([3, 3, 3, -1, 3, 9, -7, 0]), 4, np.array([1, 0, 1, 1, 1, 1, 1, 0]), None),
+        (np.array([0, 1, 1, 2, 0, 1]), 3, None, np.array([4, 0, 8])),
+        (np.arange(30) % 5, 5, rng.integers(0, 2, 30), np.zeros(5, np.int64)),
     ]
-    for s in range(30):
+    for s in range(40):
         n = int(rng.integers(1, 300))
         S = int(rng.integers(1, 40))
         idx = rng.integers(-2, S + 1, n)
@@ -55,13 +70,18 @@ def _plan_fuzz_cases():
         if seg:
             idx = np.repeat(rng.integers(-1, S, n // 9 + 1), 9)[:n]
         mask = rng.integers(0, 2, n) if rng.random() < 0.6 else None
-        cases.append((idx, S, mask))
+        ranks = None
+        if s % 2 == 0:
+            ranks = rng.integers(1, 65, S)
+            ranks[rng.random(S) < 0.3] = 0
+        cases.append((idx, S, mask, ranks))
     return cases
 
 
 def check_plan_bruteforce(impl):
-    for idx, S, mask in _plan_fuzz_cases():
-        ranks = np.ones(S, np.int64)
+    for idx, S, mask, ranks in _plan_fuzz_cases():
+        if ranks is None:
+            ranks = np.ones(S, np.int64)
         p = impl.canonical_plan(idx, S, mask=mask, ranks=ranks)
         b = oracle.plan_bruteforce(list(idx), S, mask=None if mask is None else list(mask),
                                    ranks=list(ranks))
@@ -443,7 +463,34 @@ def check_loss_closed_forms(impl):
                 and np.all(dz[5] == 0) and lpp[5] == 0 and L[5] == 0)
 
 
-ALL_CHECKS = [check_plan_golden, check_plan_bruteforce, check_forward_golden,
+def check_metrics(impl):
+    """The comparison metrics against hand-computed values: relative Frobenius
+    error ||out - ref||_F / ||ref||_F and the largest absolute difference, with
+    the zero-reference cases and NaN (a NaN output is never within tolerance)."""
+    ref = np.array([[1.0, 2.0], [2.0, 4.0]])            # ||ref||_F = 5
+    out = ref + np.array([[0.0, 3.0], [-4.0, 0.0]])     # ||out - ref||_F = 5
+    if impl.rel_fro(out, ref) != 1.0 or impl.max_abs(out, ref) != 4.0:
+        return False
+    out = ref - np.array([[0.0, 0.0], [0.0, 0.5]])      # ||diff|| = 0.5, of 5
+    if abs(impl.rel_fro(out, ref) - 0.1) > 1e-15 or impl.max_abs(out, ref) != 0.5:
+        return False
+    if impl.rel_fro(2.0 * ref, ref) != 1.0:              # normalised by ref, not out
+        return False
+    z = np.zeros((3, 2))
+    if impl.rel_fro(z, z) != 0.0 or impl.max_abs(z, z) != 0.0:
+        return False
+    if impl.rel_fro(z + 1e-3, z) != float("inf"):
+        return False
+    if impl.max_abs(np.zeros(0), np.zeros(0)) != 0.0:
+        return False
+    bad = ref.copy()
+    bad[0, 1] = np.nan
+    if not (np.isnan(impl.rel_fro(bad, ref)) and np.isnan(impl.max_abs(bad, ref))):
+        return False
+    return True
+
+
+ALL_CHECKS = [check_plan_golden, check_plan_empty_slot_golden, check_metrics, check_plan_bruteforce, check_forward_golden,
               check_forward_bruteforce, check_forward_closed_form,
               check_forward_integer_exact, check_grad_golden, check_grad_linearity,
               check_grad_bruteforce, check_grad_mask_exact, check_grad_x_linearity,
@@ -546,7 +593,8 @@ def _mutant(**overrides):
     ns = types.SimpleNamespace(canonical_plan=oracle.canonical_plan, apply=oracle.apply,
                                grad=oracle.grad, grad_x=oracle.grad_x,
                                masked_loss=oracle.masked_loss, adamw=oracle.adamw,
-                               token_loss=oracle.token_loss)
+                               token_loss=oracle.token_loss, rel_fro=oracle.rel_fro,
+                               max_abs=oracle.max_abs)
     for k, v in overrides.items():
         setattr(ns, k, v)
     return ns
@@ -731,7 +779,42 @@ def _plan_no_validation(idx, num_slots, mask=None, ranks=None):
     return p
 
 
+def _plan_ranks_ignored(idx, num_slots, mask=None, ranks=None):
+    # empty slots treated as live (no flag, their rows grouped)
+    return oracle.canonical_plan(idx, num_slots, mask=mask, ranks=None)
+
+
+def _rel_fro_zero(out, ref):
+    return 0.0
+
+
+def _rel_fro_by_out(out, ref):
+    d = np.linalg.norm(np.asarray(out, np.float64))
+    return float(np.linalg.norm(np.asarray(out, np.float64) - np.asarray(ref, np.float64)) / d) if d else 0.0
+
+
+def _rel_fro_squared(out, ref):
+    r = oracle.rel_fro(out, ref)
+    return r * r
+
+
+def _max_abs_signed(out, ref):
+    d = np.asarray(out, np.float64) - np.asarray(ref, np.float64)
+    return float(np.max(d)) if d.size else 0.0
+
+
+def _max_abs_nan_blind(out, ref):
+    d = np.abs(np.asarray(out, np.float64) - np.asarray(ref, np.float64))
+    return float(np.nanmax(d)) if d.size else 0.0
+
+
 MUTANTS = {
+    "plan_ranks_ignored": _mutant(canonical_plan=_plan_ranks_ignored),
+    "rel_fro_zero": _mutant(rel_fro=_rel_fro_zero),
+    "rel_fro_by_out": _mutant(rel_fro=_rel_fro_by_out),
+    "rel_fro_squared": _mutant(rel_fro=_rel_fro_squared),
+    "max_abs_signed": _mutant(max_abs=_max_abs_signed),
+    "max_abs_nan_blind": _mutant(max_abs=_max_abs_nan_blind),
     "apply_transposed_B": _mutant(apply=_apply_transposed_B),
     "apply_no_scale": _mutant(apply=_apply_no_scale),
     "apply_wrong_rows": _mutant(apply=_apply_wrong_rows),
