@@ -88,10 +88,10 @@ const char* lora_last_error(void);
 /* ---- adapter table (Section 3.4, "Adapter table") -----------------------
  * One table per adapted layer.  A slot holds one pinned adapter version: its
  * rank, scale and layer-local A/B pointers.  The identity / version ->
- * slot mapping and residency belong to the caller.  The paper's rule that a
- * refresh installs a new entry instead of mutating weights used by in-flight
- * generation becomes: a slot referenced by a plan must not be set, cleared or
- * uploaded until every launch using that plan has finished.
+ * slot mapping and residency belong to the caller.  Slot contract (the
+ * paper's refresh rule for the adapter table): new weights go into a free slot,
+ * and a slot that some plan still references is not set, cleared or uploaded
+ * until every launch using that plan has finished.
  *
  * dev_meta: caller device memory of lora_table_device_bytes(num_slots) bytes
  * that receives the slot metadata on lora_table_upload.  It must outlive the
@@ -150,6 +150,30 @@ lora_status lora_plan_build_segments(const lora_table* t, int32_t n, int32_t num
                                      const int32_t* seg_offsets, const int32_t* seg_adapter,
                                      const uint8_t* mask, void* ws, size_t ws_bytes,
                                      void* stream, lora_plan** out);
+/* Path selection (testing and tuning).  Every op picks its kernels from the
+ * plan and the shapes; a policy given to lora_plan_build_policy replaces those
+ * choices for every op run on that plan.  -1 in a field keeps the library's
+ * choice (lora_policy_init sets every field to -1).  No setting changes what is
+ * computed, only which kernels compute it: results agree within each op's
+ * floating-point tolerance, and bit for bit on integer-exact inputs.  The
+ * library reads no environment variables and has no process-wide settings.
+ * Errors: VALUE (a field outside its range), and those of lora_plan_build. */
+typedef struct lora_policy {
+  int32_t small_max;     /* groups of <= small_max rows take the small-group kernels, >= 0
+                            (-1: every group when n <= 1024, else groups of <= 16 rows) */
+  int32_t small_split;   /* small groups: 0 = one fused kernel, 1 = shrink per d-slice + expand
+                            (-1: split when d_in >= 1024) */
+  int32_t split_slices;  /* d-slices of the split small-group shrink, 1..8 (-1: min(4, d_in / 256)) */
+  int32_t small_chunks;  /* output-column chunks per small group, 1..16 (-1: ceil(d_out / 1024)) */
+  int32_t fork;          /* mixed batch in lora_apply: 0 = one stream, 1 = small groups on the
+                            second stream (-1: when n < 64 x num_slots) */
+  int32_t grad_splits;   /* most d-slices of the gradient's first stage, 1..8
+                            (-1: ceil(min(d_in, d_out) / 512)) */
+} lora_policy;
+void        lora_policy_init(lora_policy* q);
+lora_status lora_plan_build_policy(const lora_table* t, int32_t n, const int32_t* idx,
+                                   const uint8_t* mask, const lora_policy* policy, void* ws,
+                                   size_t ws_bytes, void* stream, lora_plan** out);
 /* Copy the plan arrays to host memory (each pointer may be NULL to skip it) and
  * wait for the stream.  Sizes: counts, m_counts [S]; offsets, m_offsets [S+1];
  * perm, m_perm, run_start, run_len, run_adapter [n] (only the first n_act /

@@ -6,7 +6,7 @@ Python face of liblora_mi355x.so (include/lora.h): ``Table`` (adapter table),
 the library's HIP kernels.  Nothing here falls back to another implementation:
 if the library is not built, every call raises.
 """
-from .lora import (AdamWTensor, LOSS_CE, LOSS_IS, LOSS_PPO, LORA_BF16, LORA_DATA_BAD_ID, LORA_DATA_BAD_SEGMENTS, LORA_DATA_EMPTY_SLOT,
+from .lora import (AdamWTensor, Policy, LOSS_CE, LOSS_IS, LOSS_PPO, LORA_BF16, LORA_DATA_BAD_ID, LORA_DATA_BAD_SEGMENTS, LORA_DATA_EMPTY_SLOT,
                    LORA_F32, LIB_PATH, LoraError, Plan, Table, apply, apply_workspace, expand,
                    adamw_step, backward, backward_workspace, grad, grad_workspace, grad_x,
                    grad_x_workspace, lib, shrink, token_loss)

@@ -8,7 +8,6 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
-#include <cstdlib>
 #include <cstring>
 #include <mutex>
 #include <new>
@@ -33,6 +32,7 @@ struct lora_plan {
   int32_t r_max;        // largest live rank when the plan was built
   bool rank8;           // every live rank is a multiple of 8
   int32_t small_max;    // groups of <= small_max rows use the fused small-group kernel
+  lora_policy pol;      // path selection of the ops on this plan (-1 fields: library choice)
 };
 
 namespace {
@@ -66,25 +66,38 @@ bool valid_dtype(lora_dtype d) { return d == LORA_F32 || d == LORA_BF16; }
 
 size_t dsize(lora_dtype d) { return d == LORA_BF16 ? 2 : 4; }
 
-int env_int(const char* name, int dflt) {
-  const char* v = std::getenv(name);
-  if (v == nullptr || *v == 0) return dflt;
-  return std::atoi(v);
-}
-
 // Output-column chunks per small-group entry (sibling workgroups).
-int32_t small_chunks_policy(int32_t d_out) {
-  const int v = env_int("LORA_SMALL_CHUNKS", 0);
-  if (v > 0) return v;
-  return std::max(1, std::min(16, (d_out + 1023) / 1024));
+int32_t small_chunks_policy(const lora_plan* p) {
+  if (p->pol.small_chunks > 0) return p->pol.small_chunks;
+  return std::max(1, std::min(16, (p->table->d_out + 1023) / 1024));
 }
 
 // Most d-slices of the gradient's first stage (the kernel uses fewer when
 // there are enough row blocks to fill the chip).
-int32_t grad_splits_policy(int32_t d_in, int32_t d_out) {
-  const int v = env_int("LORA_GRAD_SPLITS", 0);
-  if (v > 0) return std::min(v, lora::GRAD_SPLITS_MAX);
-  return std::max(1, std::min(lora::GRAD_SPLITS_MAX, (std::min(d_in, d_out) + 511) / 512));   // slices of >= 512
+int32_t grad_splits_policy(const lora_plan* p) {
+  if (p->pol.grad_splits > 0) return std::min(p->pol.grad_splits, lora::GRAD_SPLITS_MAX);
+  const int32_t d = std::min(p->table->d_in, p->table->d_out);
+  return std::max(1, std::min(lora::GRAD_SPLITS_MAX, (d + 511) / 512));   // slices of >= 512
+}
+
+// Each field is -1 (the library's choice) or inside its documented range.
+lora_status check_policy(const lora_policy& q) {
+  const bool ok = q.small_max >= -1 && q.small_split >= -1 && q.small_split <= 1 &&
+                  (q.split_slices == -1 || (q.split_slices >= 1 && q.split_slices <= lora::SPLIT_SLICES_MAX)) &&
+                  (q.small_chunks == -1 || (q.small_chunks >= 1 && q.small_chunks <= 16)) &&
+                  q.fork >= -1 && q.fork <= 1 &&
+                  (q.grad_splits == -1 || (q.grad_splits >= 1 && q.grad_splits <= lora::GRAD_SPLITS_MAX));
+  if (!ok)
+    return fail(LORA_ERR_VALUE, "policy field out of range (small_max %d, small_split %d, split_slices %d, "
+                "small_chunks %d, fork %d, grad_splits %d)", q.small_max, q.small_split, q.split_slices,
+                q.small_chunks, q.fork, q.grad_splits);
+  return LORA_OK;
+}
+
+lora_policy default_policy() {
+  lora_policy q;
+  q.small_max = q.small_split = q.split_slices = q.small_chunks = q.fork = q.grad_splits = -1;
+  return q;
 }
 
 // host upper bounds of the entry lists
@@ -148,11 +161,16 @@ lora_status check_plan(const lora_plan* p) {
 
 lora_status make_plan(const lora_table* t, int32_t n, const int32_t* idx,
                       const int32_t* seg_offsets, const int32_t* seg_adapter, int32_t num_segs,
-                      const uint8_t* mask, void* ws, size_t ws_bytes, hipStream_t stream,
-                      lora_plan** out) {
+                      const uint8_t* mask, const lora_policy* policy, void* ws, size_t ws_bytes,
+                      hipStream_t stream, lora_plan** out) {
   if (out == nullptr) return fail(LORA_ERR_NULL, "out is NULL");
   *out = nullptr;
   if (t == nullptr) return fail(LORA_ERR_NULL, "table is NULL");
+  const lora_policy pol = policy != nullptr ? *policy : default_policy();
+  {
+    const lora_status st = check_policy(pol);
+    if (st != LORA_OK) return st;
+  }
   if (n < 0 || n > LORA_MAX_ROWS) return fail(LORA_ERR_SHAPE, "n = %d outside [0, %d]", n, LORA_MAX_ROWS);
   if (ws == nullptr) return fail(LORA_ERR_NULL, "plan workspace is NULL");
   if (!aligned(ws, 16)) return fail(LORA_ERR_ALIGN, "plan workspace not 16-byte aligned");
@@ -197,7 +215,8 @@ lora_status make_plan(const lora_table* t, int32_t n, const int32_t* idx,
     p->r_max = std::max(p->r_max, s.rank);
     p->rank8 = p->rank8 && (s.rank % 8 == 0);
   }
-  p->small_max = lora::small_max_policy(n);
+  p->pol = pol;
+  p->small_max = pol.small_max >= 0 ? pol.small_max : lora::small_max_policy(n);
 
   lora::PlanLaunch a{};
   a.d = p->d;
@@ -223,15 +242,10 @@ lora_status make_plan(const lora_table* t, int32_t n, const int32_t* idx,
 
 namespace lora {
 
-// Fused small-group policy.  Batches of up to 1024 rows (decode steps) send
-// every adapter group through the fused kernel, so a decode step is a single
-// launch; larger batches send groups of up to 16 rows there and larger groups
-// through the grouped shrink + expand.
-int32_t small_max_policy(int32_t n) {
-  const int v = env_int("LORA_SMALL_MAX", -1);
-  if (v >= 0) return v;
-  return n <= 1024 ? INT32_MAX : SMALL_ROWS;
-}
+// Small-group policy.  Batches of up to 1024 rows (decode steps) send every
+// adapter group through the small-group kernels; larger batches send groups of
+// up to 16 rows there and larger groups through the grouped shrink + expand.
+int32_t small_max_policy(int32_t n) { return n <= 1024 ? INT32_MAX : SMALL_ROWS; }
 
 // Gradient workspace: fp32 partial planes (two per d-slice) and the summed bf16
 // hi / lo planes.
@@ -265,15 +279,9 @@ PlanLayout plan_layout(int32_t n, int32_t S) {
   L.mrb_max = n / MRB_ROWS + std::min(S, n) + 1;
   L.rb = o;          o += al256((size_t)L.rb_max * 16);
   L.mrb = o;         o += al256((size_t)L.mrb_max * 16);
-  {
-    // small-group records: every group may be small, or at most
-    // ceil(small_max / 16) records for each adapter
-    const int32_t sm = small_max_policy(n);
-    int64_t m = L.rb_max;
-    if (sm != INT32_MAX)
-      m = std::min<int64_t>(m, (int64_t)std::min(S, n) * ((sm + SMALL_ROWS - 1) / SMALL_ROWS) + 1);
-    L.srec_max = (int32_t)std::max<int64_t>(m, 1);
-  }
+  // small-group records: every group may be small (whatever the plan's
+  // small-group bound, so the size depends on n and S alone)
+  L.srec_max = std::max(L.rb_max, 1);
   L.srec = o;        o += al256((size_t)L.srec_max * sizeof(SmallRec));
   L.seg_ids = o;     o += al256(nn * 4);
   L.chunks = (n > PLAN_THREADS && n <= PLAN_MULTI_MAX) ? (n + PLAN_THREADS - 1) / PLAN_THREADS : 0;
@@ -305,8 +313,27 @@ constexpr int AUX_DEVICES = 64;
 std::mutex g_aux_mutex;
 AuxStream g_aux[AUX_DEVICES];
 
+// Whether the second stream can join `caller` now.  A stream that joined a
+// capture stays part of it until that capture ends, so the fork is taken only
+// when the second stream is outside every capture (the caller may be capturing:
+// the fork then brings the second stream into the caller's capture), or when
+// both are in the same capture sequence (a later call of the same capture).
+// Otherwise (an eager call while another stream's capture holds the second
+// stream, or two different captures) the call runs on the caller's stream
+// alone.  The host mutex orders these checks with the forks that follow them.
+bool can_fork(hipStream_t caller, hipStream_t aux) {
+  hipStreamCaptureStatus cc = hipStreamCaptureStatusNone, ca = hipStreamCaptureStatusNone;
+  unsigned long long ic = 0, ia = 0;
+  if (hipStreamGetCaptureInfo(caller, &cc, &ic) != hipSuccess) return false;
+  if (hipStreamGetCaptureInfo(aux, &ca, &ia) != hipSuccess) return false;
+  if (cc == hipStreamCaptureStatusInvalidated || ca == hipStreamCaptureStatusInvalidated) return false;
+  if (ca == hipStreamCaptureStatusNone) return true;
+  return cc == hipStreamCaptureStatusActive && ca == hipStreamCaptureStatusActive && ic == ia;
+}
+
 // the device's second stream, or nullptr (forking off, creation refused
-// during capture, or a creation failure: the caller then runs one stream)
+// during capture, the second stream held by another capture, or a creation
+// failure: the caller then runs one stream)
 AuxStream* aux_stream(hipStream_t caller) {
   // the caller's stream decides the device (the null stream: the current one)
   int cur = 0, dev = 0;
@@ -315,7 +342,7 @@ AuxStream* aux_stream(hipStream_t caller) {
   if (caller != nullptr && hipStreamGetDevice(caller, &dev) != hipSuccess) return nullptr;
   if (dev < 0 || dev >= AUX_DEVICES) return nullptr;
   AuxStream& a = g_aux[dev];
-  if (a.s != nullptr) return &a;
+  if (a.s != nullptr) return can_fork(caller, a.s) ? &a : nullptr;
   hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
   if (hipStreamIsCapturing(caller, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) return nullptr;
   if (dev != cur && hipSetDevice(dev) != hipSuccess) return nullptr;
@@ -341,10 +368,9 @@ AuxStream* aux_stream(hipStream_t caller) {
 // about 10 us of queue latency, so they pay only when both paths have work;
 // the host cannot see the grouping (it is built on the device), so it expects
 // small groups when the batch has fewer than 4 x SMALL_ROWS rows per table
-// slot.  LORA_APPLY_FORK=0 / 2 forces it off / on.
+// slot.
 bool fork_policy(const lora_plan* p) {
-  const int v = env_int("LORA_APPLY_FORK", 1);
-  if (v == 0 || v == 2) return v == 2;
+  if (p->pol.fork >= 0) return p->pol.fork == 1;
   return (int64_t)p->n < (int64_t)4 * lora::SMALL_ROWS * p->table->num_slots;
 }
 
@@ -448,7 +474,18 @@ size_t lora_plan_workspace_bytes(int32_t n, int32_t num_slots) {
 
 lora_status lora_plan_build(const lora_table* t, int32_t n, const int32_t* idx, const uint8_t* mask,
                             void* ws, size_t ws_bytes, void* stream, lora_plan** out) {
-  return make_plan(t, n, idx, nullptr, nullptr, 0, mask, ws, ws_bytes,
+  return make_plan(t, n, idx, nullptr, nullptr, 0, mask, nullptr, ws, ws_bytes,
+                   static_cast<hipStream_t>(stream), out);
+}
+
+void lora_policy_init(lora_policy* q) {
+  if (q != nullptr) *q = default_policy();
+}
+
+lora_status lora_plan_build_policy(const lora_table* t, int32_t n, const int32_t* idx,
+                                   const uint8_t* mask, const lora_policy* policy, void* ws,
+                                   size_t ws_bytes, void* stream, lora_plan** out) {
+  return make_plan(t, n, idx, nullptr, nullptr, 0, mask, policy, ws, ws_bytes,
                    static_cast<hipStream_t>(stream), out);
 }
 
@@ -463,7 +500,7 @@ lora_status lora_plan_build_segments(const lora_table* t, int32_t n, int32_t num
   if (num_segs > 0 && seg_adapter == nullptr) return fail(LORA_ERR_NULL, "seg_adapter is NULL");
   if (!aligned(seg_offsets, 4) || (seg_adapter != nullptr && !aligned(seg_adapter, 4)))
     return fail(LORA_ERR_ALIGN, "segment arrays not 4-byte aligned");
-  return make_plan(t, n, nullptr, seg_offsets, seg_adapter, num_segs, mask, ws, ws_bytes,
+  return make_plan(t, n, nullptr, seg_offsets, seg_adapter, num_segs, mask, nullptr, ws, ws_bytes,
                    static_cast<hipStream_t>(stream), out);
 }
 
@@ -602,16 +639,14 @@ size_t lora_apply_workspace_bytes(const lora_plan* p) {
 // d_in is short: the fused kernel saves a launch, but each of its P sibling
 // workgroups (column chunks) reads all of A, which dominates once A is large.
 // The split path measured faster on the 4096-wide decode batch and on the
-// skewed mixed batch.  LORA_SMALL_SPLIT=0/1 forces either path.  Four
-// d-slices (of at least 256 columns) measured best on both.
+// skewed mixed batch.  Four d-slices (of at least 256 columns) measured best
+// on both.
 bool small_split_policy(const lora_plan* p) {
-  const int v = env_int("LORA_SMALL_SPLIT", -1);
-  if (v >= 0) return v != 0;
+  if (p->pol.small_split >= 0) return p->pol.small_split != 0;
   return p->table->d_in >= 1024;
 }
 int32_t small_split_slices(const lora_plan* p) {
-  const int v = env_int("LORA_SPLIT_SLICES", 0);
-  const int sl = v > 0 ? v : std::min(4, p->table->d_in / 256);
+  const int sl = p->pol.split_slices > 0 ? p->pol.split_slices : std::min(4, p->table->d_in / 256);
   return std::max(1, std::min(lora::SPLIT_SLICES_MAX, sl));
 }
 
@@ -663,11 +698,11 @@ lora_status lora_apply(const lora_plan* p, const void* X, lora_dtype x_dtype, in
       // kernel runs)
       if (ws != nullptr && ws_bytes >= need && aligned(ws, 16) && small_split_policy(p)) {
         float* part = reinterpret_cast<float*>(static_cast<char*>(ws) + apply_h_bytes(p));
-        e = lora::launch_small_split_mfma(os, X, ldx, Y, y_dtype, ldy, small_chunks_policy(t->d_out),
+        e = lora::launch_small_split_mfma(os, X, ldx, Y, y_dtype, ldy, small_chunks_policy(p),
                                           small_split_slices(p), part, s_small);
         if (e != hipSuccess) return hip_fail(e, "split small-group launch");
       } else {
-        e = lora::launch_bgmv_mfma(os, X, ldx, Y, y_dtype, ldy, small_chunks_policy(t->d_out), s_small);
+        e = lora::launch_bgmv_mfma(os, X, ldx, Y, y_dtype, ldy, small_chunks_policy(p), s_small);
         if (e != hipSuccess) return hip_fail(e, "fused small-group launch");
       }
     }
@@ -755,7 +790,7 @@ lora_status lora_grad(const lora_plan* p, const void* X, lora_dtype x_dtype, int
   char* wsb = static_cast<char*>(ws);
   g.hg = reinterpret_cast<float*>(wsb + GL.partial);
   g.fin = reinterpret_cast<uint16_t*>(wsb + GL.fin);
-  g.k_splits = mfma ? grad_splits_policy(t->d_in, t->d_out) : 1;
+  g.k_splits = mfma ? grad_splits_policy(p) : 1;
   g.p_stride = ub_mrb(p) * lora::MRB_ROWS;
   g.r_pad = (std::max(p->r_max, 1) + 15) / 16 * 16;
   hipStream_t s = static_cast<hipStream_t>(stream);

@@ -20,7 +20,6 @@
 // K offset 8 * (l / 16); the accumulator lane l holds rows 4 * (l / 16) + v,
 // v = 0..3, of column l % 16.
 #include <algorithm>
-#include <cstdlib>
 
 #include "device_common.h"
 #include "lora_internal.h"
@@ -1409,18 +1408,9 @@ FwdArgs base_args(const OpLaunch& o) {
   return a;
 }
 
-int env_int(const char* name, int dflt) {
-  const char* v = std::getenv(name);
-  return (v != nullptr && *v) ? std::atoi(v) : dflt;
-}
-
-// Steps per batch: two for a bf16 Y up to rank 64 (more bytes in flight per
-// wave), else one (register budget).  LORA_EXPAND_U=1 forces one.
+// One 32-column step per batch (two measured no faster).
 template <bool YB, bool R8, int KSM>
 hipError_t launch_expand_u(int grid, const FwdArgs& a, hipStream_t s) {
-  if constexpr (YB && KSM <= 2) {
-    if (env_int("LORA_EXPAND_U", 1) == 2) return launch(expand_kernel<YB, R8, KSM, 2>, grid, a, s);
-  }
   return launch(expand_kernel<YB, R8, KSM, 1>, grid, a, s);
 }
 
@@ -1469,10 +1459,10 @@ hipError_t launch_shrink_mfma(const OpLaunch& o, const void* X, int64_t ldx, flo
                    : nt <= 4 ? launch(shrink_fine_kernel<4, false>, gridf, a, s)
                              : launch(shrink_fine_kernel<8, false>, gridf, a, s);
   if (err != hipSuccess) return err;
-  const int u = env_int("LORA_SHRINK_U", 4);
-  if (nt <= 1) return u == 2 ? launch(shrink_kernel<1, 2>, grid, a, s) : u == 1 ? launch(shrink_kernel<1, 1>, grid, a, s) : launch(shrink_kernel<1, 4>, grid, a, s);
-  if (nt <= 2) return u == 2 ? launch(shrink_kernel<2, 2>, grid, a, s) : u == 1 ? launch(shrink_kernel<2, 1>, grid, a, s) : launch(shrink_kernel<2, 4>, grid, a, s);
-  if (nt <= 4) return u == 2 ? launch(shrink_kernel<4, 2>, grid, a, s) : u == 1 ? launch(shrink_kernel<4, 1>, grid, a, s) : launch(shrink_kernel<4, 4>, grid, a, s);
+  // four k-steps per batch up to rank 64 (one at rank 128: register budget)
+  if (nt <= 1) return launch(shrink_kernel<1, 4>, grid, a, s);
+  if (nt <= 2) return launch(shrink_kernel<2, 4>, grid, a, s);
+  if (nt <= 4) return launch(shrink_kernel<4, 4>, grid, a, s);
   return launch(shrink_kernel<8, 1>, grid, a, s);
 }
 
@@ -1524,11 +1514,8 @@ hipError_t launch_expand_mfma(const OpLaunch& o, const float* H, int64_t ldh, in
   a.Y = Y;
   a.ldy = ldy;
   // (row block, 1024-column chunk) units of the 256-row kernel (the 64-row
-  // kernel picks its own chunk from the block count and loops over its units);
-  // LORA_EXPAND_CW sets another chunk width (whole pairs of 32-column steps)
-  // of the 256-row kernel for measurements
-  const int cw = env_int("LORA_EXPAND_CW", 0);
-  a.cw = cw > 0 ? std::max(64, cw / 64 * 64) : 1024;
+  // kernel picks its own chunk from the block count and loops over its units)
+  a.cw = 1024;
   const long long n_ch = (o.d_out + a.cw - 1) / a.cw;
   const int grid = round8(std::min<long long>((long long)o.coarse_ub * n_ch, 4096));
   const int gridf = round8(std::min<long long>((long long)o.fine_ub * n_ch, 4096));

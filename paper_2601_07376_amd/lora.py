@@ -37,6 +37,8 @@ SIGNATURES = {
     "lora_plan_workspace_bytes": (_sz, [_i32, _i32]),
     "lora_plan_build": (_i32, [_vp, _i32, _vp, _vp, _vp, _sz, _vp, _pp]),
     "lora_plan_build_segments": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, _vp, _sz, _vp, _pp]),
+    "lora_policy_init": (None, [_vp]),
+    "lora_plan_build_policy": (_i32, [_vp, _i32, _vp, _vp, _vp, _vp, _sz, _vp, _pp]),
     "lora_plan_export": (_i32, [_vp] + [_vp] * 11 + [_vp]),
     "lora_plan_check": (_i32, [_vp, _vp, _vp]),
     "lora_plan_destroy": (None, [_vp]),
@@ -105,6 +107,34 @@ def _stream(stream):
     return ctypes.c_void_p(stream.cuda_stream)
 
 
+def _used_on(stream, *tensors):
+    """Tensors allocated here on torch's current stream but used by kernels on
+    another stream: tell the caching allocator, so that their memory is not
+    handed out again before that stream's work on it has finished."""
+    if stream is None:
+        return
+    if stream.cuda_stream == torch.cuda.current_stream(stream.device).cuda_stream:
+        return
+    for t in tensors:
+        if t is not None:
+            t.record_stream(stream)
+
+
+class Policy(ctypes.Structure):
+    """lora_policy (include/lora.h): path selection for testing and tuning;
+    -1 keeps the library's choice."""
+    _fields_ = [("small_max", ctypes.c_int32), ("small_split", ctypes.c_int32),
+                ("split_slices", ctypes.c_int32), ("small_chunks", ctypes.c_int32),
+                ("fork", ctypes.c_int32), ("grad_splits", ctypes.c_int32)]
+
+    def __init__(self, **kw):
+        super().__init__()
+        lib().lora_policy_init(ctypes.byref(self))
+        for k, v in kw.items():
+            if v is not None:
+                setattr(self, k, int(v))
+
+
 def _rowmajor(t, name):
     if t.dim() != 2:
         raise ValueError(f"{name} must be a 2-D tensor")
@@ -167,7 +197,7 @@ class Plan:
     """Row grouping of one batch (built on the device, no host synchronisation)."""
 
     def __init__(self, table, idx=None, mask=None, seg_offsets=None, seg_adapter=None, n=None,
-                 stream=None):
+                 stream=None, policy=None):
         L = lib()
         self.table = table
         if idx is not None:
@@ -177,9 +207,17 @@ class Plan:
         self.n = int(n)
         self.ws = torch.empty(max(L.lora_plan_workspace_bytes(self.n, table.num_slots), 16),
                               dtype=torch.uint8, device=table.device)
+        _used_on(stream, self.ws)
         self._keep = (idx, mask, seg_offsets, seg_adapter)
         h = ctypes.c_void_p()
-        if idx is not None:
+        if policy is not None and idx is None:
+            raise ValueError("a policy applies to plans built from ids")
+        if idx is not None and policy is not None:
+            pol = policy if isinstance(policy, Policy) else Policy(**policy)
+            _check(L.lora_plan_build_policy(table.handle, self.n, _ptr(idx), _ptr(mask),
+                                            ctypes.byref(pol), _ptr(self.ws), self.ws.numel(),
+                                            _stream(stream), ctypes.byref(h)))
+        elif idx is not None:
             _check(L.lora_plan_build(table.handle, self.n, _ptr(idx), _ptr(mask), _ptr(self.ws),
                                      self.ws.numel(), _stream(stream), ctypes.byref(h)))
         else:
@@ -229,6 +267,7 @@ def shrink(plan, X, H=None, stream=None):
     if H is None:
         r = max(max(plan.table.ranks), 1)
         H = torch.zeros(plan.n, (r + 7) // 8 * 8, dtype=torch.float32, device=X.device)
+        _used_on(stream, H)
     _check(lib().lora_shrink(plan.handle, _ptr(X), _dtype(X), _rowmajor(X, "X"), _ptr(H),
                              _rowmajor(H, "H"), _stream(stream)))
     return H
@@ -250,6 +289,7 @@ def apply(plan, X, Y, ws=None, stream=None):
     """Y[t] += s_a (X[t] A_a^T) B_a^T in place."""
     if ws is None:
         ws = apply_workspace(plan)
+        _used_on(stream, ws)
     _check(lib().lora_apply(plan.handle, _ptr(X), _dtype(X), _rowmajor(X, "X"), _ptr(Y),
                             _dtype(Y), _rowmajor(Y, "Y"), _ptr(ws), ws.numel(), _stream(stream)))
     return Y
@@ -267,11 +307,14 @@ def grad(plan, X, dY, dA=None, dB=None, H_saved=None, accumulate=False, ws=None,
     if dA is None:
         dA = [torch.empty(r, t.d_in, dtype=torch.float32, device=X.device) if r > 0 else None
               for r in t.ranks]
+        _used_on(stream, *dA)
     if dB is None:
         dB = [torch.empty(t.d_out, r, dtype=torch.float32, device=X.device) if r > 0 else None
               for r in t.ranks]
+        _used_on(stream, *dB)
     if ws is None:
         ws = grad_workspace(plan)
+        _used_on(stream, ws)
     pa = (ctypes.c_void_p * t.num_slots)(*[g.data_ptr() if g is not None else None for g in dA])
     pb = (ctypes.c_void_p * t.num_slots)(*[g.data_ptr() if g is not None else None for g in dB])
     ldh = _rowmajor(H_saved, "H_saved") if H_saved is not None else 0
@@ -290,6 +333,7 @@ def grad_x(plan, dY, dX, ws=None, stream=None):
     """dX[t] += s_a (dY[t] B_a) A_a in place over the plan's masked rows."""
     if ws is None:
         ws = grad_x_workspace(plan)
+        _used_on(stream, ws)
     _check(lib().lora_grad_x(plan.handle, _ptr(dY), _dtype(dY), _rowmajor(dY, "dY"), _ptr(dX),
                              _dtype(dX), _rowmajor(dX, "dX"), _ptr(ws), ws.numel(), _stream(stream)))
     return dX
@@ -308,11 +352,14 @@ def backward(plan, X, dY, dX, dA=None, dB=None, H_saved=None, accumulate=False, 
     if dA is None:
         dA = [torch.empty(r, t.d_in, dtype=torch.float32, device=X.device) if r > 0 else None
               for r in t.ranks]
+        _used_on(stream, *dA)
     if dB is None:
         dB = [torch.empty(t.d_out, r, dtype=torch.float32, device=X.device) if r > 0 else None
               for r in t.ranks]
+        _used_on(stream, *dB)
     if ws is None:
         ws = backward_workspace(plan)
+        _used_on(stream, ws)
     pa = (ctypes.c_void_p * t.num_slots)(*[g.data_ptr() if g is not None else None for g in dA])
     pb = (ctypes.c_void_p * t.num_slots)(*[g.data_ptr() if g is not None else None for g in dB])
     ldh = _rowmajor(H_saved, "H_saved") if H_saved is not None else 0

@@ -1,7 +1,5 @@
 """Helpers for the GPU parity tests: run the HIP path through the binding and
 compare with the float64 oracle.  No LoRA arithmetic lives here."""
-import contextlib
-import os
 import sys
 
 import numpy as np
@@ -26,24 +24,6 @@ def say(msg):
     sys.stdout.flush()
 
 
-@contextlib.contextmanager
-def env(**kw):
-    old = {k: os.environ.get(k) for k in kw}
-    try:
-        for k, v in kw.items():
-            if v is None:
-                os.environ.pop(k, None)
-            else:
-                os.environ[k] = str(v)
-        yield
-    finally:
-        for k, v in old.items():
-            if v is None:
-                os.environ.pop(k, None)
-            else:
-                os.environ[k] = v
-
-
 def torch_wdtype(case):
     return torch.bfloat16 if case.w_dtype == "bf16" else torch.float32
 
@@ -57,12 +37,14 @@ def make_table(case, dev):
     return t
 
 
-def make_plan(case, dev, table, segments=False, mask=True):
+def make_plan(case, dev, table, segments=False, mask=True, policy=None):
+    """policy: dict of lora_policy fields (path selection) or None."""
     m = dev["mask"] if mask else None
     if segments:
+        assert policy is None, "path policies apply to plans built from ids"
         return L.Plan(table, seg_offsets=dev["seg_offsets"], seg_adapter=dev["seg_adapter"],
                       n=case.n, mask=m)
-    return L.Plan(table, idx=dev["idx"], mask=m)
+    return L.Plan(table, idx=dev["idx"], mask=m, policy=policy)
 
 
 def compare_plan(got, ref):
@@ -114,10 +96,10 @@ def check_forward(case, Y_out_raw, eff, rows=None, ref_delta=None):
     return rel, mx
 
 
-def run_apply(case, segments=False, ws=None):
+def run_apply(case, segments=False, ws=None, policy=None):
     dev = case_to_device(case, DEV)
     table = make_table(case, dev)
-    plan = make_plan(case, dev, table, segments=segments, mask=False)
+    plan = make_plan(case, dev, table, segments=segments, mask=False, policy=policy)
     Y = dev["Y"].clone()
     L.apply(plan, dev["X"], Y, ws=ws)
     torch.cuda.synchronize()
@@ -130,6 +112,9 @@ def effective(case):
 
 
 def check_grads(case, dA, dB, eff, mask, H_saved=None, tol=(REL_FRO, MAX_ABS)):
+    """dA / dB against the oracle, concatenated over slots and per slot (each
+    slot's dA and dB together): relF and max-abs within the bar.  A slot with
+    no trainable row must hold exact zeros."""
     X, A, B, _, dY = f64_case(case)
     rA, rB = oracle.grad(eff, mask, X, dY, A, B, case.scales, H_saved=H_saved)
     got, ref = [], []
@@ -138,8 +123,14 @@ def check_grads(case, dA, dB, eff, mask, H_saved=None, tol=(REL_FRO, MAX_ABS)):
             continue
         ga = dA[a].detach().cpu().double().numpy()
         gb = dB[a].detach().cpu().double().numpy()
-        got += [ga.ravel(), gb.ravel()]
-        ref += [rA[a].ravel(), rB[a].ravel()]
+        sg = np.concatenate([ga.ravel(), gb.ravel()])
+        sr = np.concatenate([rA[a].ravel(), rB[a].ravel()])
+        srel, smx = oracle.rel_fro(sg, sr), oracle.max_abs(sg, sr)
+        assert srel <= tol[0] and smx <= tol[1], f"slot {a}: grad relF {srel:.3g} maxabs {smx:.3g}"
+        if not np.any(sr):
+            assert not np.any(sg), f"slot {a} has no trainable row but nonzero gradients"
+        got.append(sg)
+        ref.append(sr)
     g = np.concatenate(got)
     r = np.concatenate(ref)
     rel, mx = oracle.rel_fro(g, r), oracle.max_abs(g, r)

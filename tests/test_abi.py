@@ -105,6 +105,47 @@ def test_plan_build_validation():
     L.lora_table_destroy(t)
 
 
+@pytest.mark.parametrize("field,value", [
+    ("small_max", -2), ("small_split", 2), ("split_slices", 0), ("split_slices", 9),
+    ("small_chunks", 17), ("fork", 3), ("grad_splits", 0), ("grad_splits", 9),
+])
+def test_plan_policy_validation(field, value):
+    """A path policy outside its documented range is refused on the host
+    (LORA_ERR_VALUE) before anything is enqueued; the defaults are all -1."""
+    L = lora.lib()
+    st, t = _create(S=8)
+    assert st == 0
+    q = lora.Policy()
+    assert [getattr(q, f) for f, _ in lora.Policy._fields_] == [-1] * len(lora.Policy._fields_)
+    setattr(q, field, value)
+    p = ctypes.c_void_p()
+    need = L.lora_plan_workspace_bytes(100, 8)
+    assert L.lora_plan_build_policy(t, 100, ctypes.c_void_p(FAKE), None, ctypes.byref(q),
+                                    ctypes.c_void_p(FAKE), need, None, ctypes.byref(p)) == 10
+    assert p.value is None
+    assert field.encode() in L.lora_last_error()
+    L.lora_table_destroy(t)
+
+
+def test_plan_workspace_does_not_depend_on_policy():
+    """The plan workspace size is a function of n and num_slots alone."""
+    L = lora.lib()
+    sizes = {n: L.lora_plan_workspace_bytes(n, 33) for n in (0, 1, 100, 1024, 1025, 5000, 70000)}
+    assert all(v > 0 for v in sizes.values())
+    assert sizes[1025] > sizes[1024] and sizes[70000] > sizes[5000]
+
+
+def test_library_reads_no_environment():
+    """No process-wide switches: neither the sources nor the built library
+    call getenv (path selection is per plan, through lora_policy)."""
+    csrc = os.path.join(ROOT, "paper_2601_07376_amd", "csrc")
+    for f in os.listdir(csrc):
+        text = open(os.path.join(csrc, f)).read()
+        assert "getenv" not in text, f"{f} reads the environment"
+    data = open(lora.LIB_PATH, "rb").read()
+    assert b"getenv" not in data
+
+
 def test_ops_reject_null_plan():
     L = lora.lib()
     X = ctypes.c_void_p(FAKE)

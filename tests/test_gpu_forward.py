@@ -11,7 +11,7 @@ import torch
 
 import oracle
 import workloads
-from gpu_helpers import (DEV, check_forward, effective, env, make_plan, make_table, run_apply,
+from gpu_helpers import (DEV, check_forward, effective, make_plan, make_table, run_apply,
                          say)
 from helpers import f64_case
 from workloads.device import case_to_device, from_torch
@@ -33,10 +33,20 @@ def test_apply_config_full(cfg, ydt):
     say(f"  relF {rel:.3g} maxabs {mx:.3g}")
 
 
-@pytest.mark.parametrize("ydt", ["f32", "bf16"])
-def test_apply_config3_sampled_rows(ydt):
-    """Full prefill workload (launch shape of the benchmark); the oracle checks a
-    sample of rows one by one, including every segment's first and last row."""
+def test_apply_config3_every_row():
+    """The full prefill workload (launch shape of the benchmark) in float32 Y,
+    every row against the oracle."""
+    say("apply config 3 y=f32, every row")
+    case = workloads.make_config(3, y_dtype="f32")
+    Yo, _ = run_apply(case, segments=True)
+    rel, mx = check_forward(case, Yo, effective(case))
+    say(f"  relF {rel:.3g} maxabs {mx:.3g}")
+
+
+def test_apply_config3_sampled_rows():
+    """The full prefill workload in bfloat16 Y; the oracle checks a sample of
+    rows one by one, including every segment's first and last row."""
+    ydt = "bf16"
     say(f"apply config 3 y={ydt}")
     case = workloads.make_config(3, y_dtype=ydt)
     Yo, _ = run_apply(case, segments=True)
@@ -73,8 +83,7 @@ def test_apply_fuzz(name, ydt):
     kw, small = next((f[1], f[2]) for f in FUZZ if f[0] == name)
     say(f"apply fuzz {name} y={ydt}")
     case = workloads.random_case(11, y_dtype=ydt, **kw)
-    with env(LORA_SMALL_MAX=small):
-        Yo, _ = run_apply(case)
+    Yo, _ = run_apply(case, policy=None if small is None else dict(small_max=small))
     check_forward(case, Yo, effective(case))
 
 
@@ -86,8 +95,7 @@ def test_apply_integer_exact(small):
     case = workloads.random_case(3, 1100, 256, 136, 7, rank_choices=(8, 16, 40, 64),
                                  layout="segments", seg_len=(1, 90), y_dtype="f32",
                                  int_values=True, scales=[0.25, 0.5, 1, 2, 2, 1, 0.5])
-    with env(LORA_SMALL_MAX=small):
-        Yo, _ = run_apply(case)
+    Yo, _ = run_apply(case, policy=None if small is None else dict(small_max=small))
     X, A, B, Y, _ = f64_case(case)
     ref = oracle.apply(effective(case), X, Y, A, B, case.scales)
     assert np.array_equal(workloads.decode(Yo, "f32"), ref)
@@ -139,6 +147,7 @@ def test_shrink_then_expand(xdt, wdt):
     Href = oracle.shrink(eff, X, A, H=np.full((case.n, 72), 7.0))
     Hg = H.cpu().double().numpy()
     assert oracle.rel_fro(Hg, Href) <= 1e-5
+    assert oracle.max_abs(Hg, Href) <= 1e-3
     assert np.array_equal(Hg[eff < 0], Href[eff < 0])       # untouched rows
     for a in range(case.num_slots):                          # untouched columns
         rows = eff == a
@@ -164,10 +173,9 @@ def test_apply_small_group_paths(name, path):
     kw = next(f[1] for f in FUZZ if f[0] == name)
     say(f"apply small path {path} {name}")
     case = workloads.random_case(12, y_dtype="f32", **kw)
-    split = "0" if path == "fused" else "1"
-    slices = None if path == "fused" else path[5:]
-    with env(LORA_SMALL_SPLIT=split, LORA_SPLIT_SLICES=slices):
-        Yo, _ = run_apply(case)
+    split = 0 if path == "fused" else 1
+    slices = None if path == "fused" else int(path[5:])
+    Yo, _ = run_apply(case, policy=dict(small_split=split, split_slices=slices))
     check_forward(case, Yo, effective(case))
 
 
@@ -176,8 +184,7 @@ def test_apply_small_group_paths(name, path):
 def test_apply_configs_both_small_paths(cfg, path):
     say(f"apply config {cfg} small path {path}")
     case = workloads.make_config(cfg, y_dtype="bf16")
-    with env(LORA_SMALL_SPLIT="0" if path == "fused" else "1"):
-        Yo, _ = run_apply(case)
+    Yo, _ = run_apply(case, policy=dict(small_split=0 if path == "fused" else 1))
     rel, mx = check_forward(case, Yo, effective(case))
     say(f"  relF {rel:.3g} maxabs {mx:.3g}")
 

@@ -5,7 +5,7 @@ import torch
 
 import oracle
 import workloads
-from gpu_helpers import DEV, check_grads, effective, env, make_plan, make_table, say
+from gpu_helpers import DEV, check_grads, effective, make_plan, make_table, say
 from helpers import f64_case
 from workloads.device import case_to_device
 
@@ -14,10 +14,10 @@ import paper_2601_07376_amd as L
 pytestmark = pytest.mark.gpu
 
 
-def run_grad(case, H_saved=None, accumulate=False, init=None, segments=False):
+def run_grad(case, H_saved=None, accumulate=False, init=None, segments=False, policy=None):
     dev = case_to_device(case, DEV)
     table = make_table(case, dev)
-    plan = make_plan(case, dev, table, segments=segments, mask=True)
+    plan = make_plan(case, dev, table, segments=segments, mask=True, policy=policy)
     dA = dB = None
     if init is not None:
         dA = [torch.from_numpy(x).float().to(DEV) if x is not None else None for x in init[0]]
@@ -74,8 +74,7 @@ def test_grad_integer_exact(splits):
                                  layout="segments", seg_len=(1, 120), mask_p=0.5,
                                  want_dy=True, want_y=False, int_values=True,
                                  scales=[0.5, 1, 2, 0.25])
-    with env(LORA_GRAD_SPLITS=splits):
-        dA, dB = run_grad(case)
+    dA, dB = run_grad(case, policy=dict(grad_splits=splits))
     X, A, B, _, dY = f64_case(case)
     rA, rB = oracle.grad(effective(case), case.mask, X, dY, A, B, case.scales)
     for a in range(case.num_slots):

@@ -1,4 +1,6 @@
 """Device row grouping vs the oracle's canonical plan: bit-exact (GPU)."""
+import zlib
+
 import numpy as np
 import pytest
 import torch
@@ -76,7 +78,7 @@ FUZZ = [
 @pytest.mark.parametrize("name", [f[0] for f in FUZZ])
 def test_plan_fuzz(name):
     say(f"plan fuzz {name}")
-    rng = np.random.default_rng(hash(name) % 1000)
+    rng = np.random.default_rng(zlib.crc32(name.encode()))   # stable across processes
     idx, S, mask = dict(FUZZ)[name](rng)
     got, ref = _plan_case(idx, S, mask)
     compare_plan(got, ref)
