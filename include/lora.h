@@ -226,6 +226,25 @@ lora_status lora_apply(const lora_plan* p, const void* X, lora_dtype x_dtype, in
                        void* Y, lora_dtype y_dtype, int64_t ldy, void* ws, size_t ws_bytes,
                        void* stream);
 
+/* lora_apply without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same kernels and the same result as lora_apply, bit
+ * for bit, always on `stream` alone (no second stream).  The workspace is a
+ * fixed array of LORA_NOALLOC_SCRATCH_BYTES in the library's code object, one
+ * per GPU, held until the process ends; its device address is looked up on the
+ * first call on each device.  The call allocates nothing: no hipMalloc,
+ * hipFree or allocating library routine.  Every call on one GPU shares that
+ * GPU's array, so calls that overlap on one GPU (concurrent streams, or
+ * replays of graphs holding this call that overlap) race and give undefined
+ * results; calls ordered on one stream are safe (nothing is carried from one
+ * call to the next: every byte the kernels read is written earlier in the same
+ * call).  Errors: those of lora_apply, and LORA_ERR_WORKSPACE when
+ * lora_apply_workspace_bytes(p) exceeds LORA_NOALLOC_SCRATCH_BYTES (nothing
+ * is enqueued then). */
+#define LORA_NOALLOC_SCRATCH_BYTES (32u << 20)
+lora_status lora_apply_noalloc(const lora_plan* p, const void* X, lora_dtype x_dtype, int64_t ldx,
+                               void* Y, lora_dtype y_dtype, int64_t ldy, void* stream);
+
 /* ---- backward (Sections 3.3 and 3.5: masked, adapter-local gradients) ----
  * For every slot a with dA[a] / dB[a] not NULL, over the rows T_a^m of the
  * plan's mask (mask == NULL at build time: every row of adapter a):

@@ -14,7 +14,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "liblora_mi355x.so")
-SOURCES = ["plan.hip", "fwd_mfma.hip", "fwd_valu.hip", "grad.hip", "adamw.hip", "losses.hip", "api.cpp"]
+SOURCES = ["plan.hip", "fwd_mfma.hip", "fwd_valu.hip", "grad.hip", "adamw.hip", "losses.hip",
+           "noalloc.hip", "api.cpp"]
 ARCH = "gfx950"
 
 # Packed fp32 VALU instructions are disabled for all device code.

@@ -651,8 +651,15 @@ int32_t small_split_slices(const lora_plan* p) {
 }
 
 
-lora_status lora_apply(const lora_plan* p, const void* X, lora_dtype x_dtype, int64_t ldx, void* Y,
-                       lora_dtype y_dtype, int64_t ldy, void* ws, size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// lora_apply with the workspace given; `allow_fork` = false keeps the whole
+// call on the caller's stream (no second stream is created or used).
+lora_status apply_impl(const lora_plan* p, const void* X, lora_dtype x_dtype, int64_t ldx, void* Y,
+                       lora_dtype y_dtype, int64_t ldy, void* ws, size_t ws_bytes, void* stream,
+                       bool allow_fork) {
   lora_status st = check_plan(p);
   if (st != LORA_OK) return st;
   const lora_table* t = p->table;
@@ -678,7 +685,7 @@ lora_status lora_apply(const lora_plan* p, const void* X, lora_dtype x_dtype, in
     std::unique_lock<std::mutex> lk(g_aux_mutex, std::defer_lock);
     AuxStream* aux = nullptr;
     hipStream_t s_small = s;
-    if (ub_large(p) > 0 && fork_policy(p)) {
+    if (allow_fork && ub_large(p) > 0 && fork_policy(p)) {
       lk.lock();
       aux = aux_stream(s);
       if (aux != nullptr) {
@@ -731,6 +738,32 @@ lora_status lora_apply(const lora_plan* p, const void* X, lora_dtype x_dtype, in
     if (e != hipSuccess) return hip_fail(e, "vector-path launch");
   }
   return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+lora_status lora_apply(const lora_plan* p, const void* X, lora_dtype x_dtype, int64_t ldx, void* Y,
+                       lora_dtype y_dtype, int64_t ldy, void* ws, size_t ws_bytes, void* stream) {
+  return apply_impl(p, X, x_dtype, ldx, Y, y_dtype, ldy, ws, ws_bytes, stream, true);
+}
+
+lora_status lora_apply_noalloc(const lora_plan* p, const void* X, lora_dtype x_dtype, int64_t ldx,
+                               void* Y, lora_dtype y_dtype, int64_t ldy, void* stream) {
+  lora_status st = check_plan(p);
+  if (st != LORA_OK) return st;
+  const size_t need = lora_apply_workspace_bytes(p);
+  if (need > (size_t)LORA_NOALLOC_SCRATCH_BYTES)
+    return fail(LORA_ERR_WORKSPACE,
+                "lora_apply_noalloc: this plan needs %zu bytes of scratch, more than the %zu bytes "
+                "the library holds per GPU (use lora_apply with a caller workspace)",
+                need, (size_t)LORA_NOALLOC_SCRATCH_BYTES);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  void* ws = nullptr;
+  const hipError_t e = lora::noalloc_scratch(s, &ws);
+  if (e != hipSuccess) return hip_fail(e, "scratch address");
+  return apply_impl(p, X, x_dtype, ldx, Y, y_dtype, ldy, ws, LORA_NOALLOC_SCRATCH_BYTES, stream, false);
 }
 
 // ---- backward --------------------------------------------------------------

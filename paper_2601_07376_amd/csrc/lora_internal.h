@@ -95,6 +95,10 @@ struct PlanDev {
   int32_t chunks;     //   chunks of PLAN_THREADS rows (0: not chunked)
 };
 
+// Device address of this GPU's fixed scratch array (lora_apply_noalloc),
+// looked up once per device: the device of `stream` (NULL: the current one).
+hipError_t noalloc_scratch(hipStream_t stream, void** out);
+
 // Groups of at most this many rows take the fused small-group path.
 int32_t small_max_policy(int32_t n);
 PlanLayout plan_layout(int32_t n, int32_t num_slots);

@@ -46,6 +46,7 @@ SIGNATURES = {
     "lora_expand": (_i32, [_vp, _vp, _i64, _vp, _i32, _i64, _vp]),
     "lora_apply_workspace_bytes": (_sz, [_vp]),
     "lora_apply": (_i32, [_vp, _vp, _i32, _i64, _vp, _i32, _i64, _vp, _sz, _vp]),
+    "lora_apply_noalloc": (_i32, [_vp, _vp, _i32, _i64, _vp, _i32, _i64, _vp]),
     "lora_grad_workspace_bytes": (_sz, [_vp]),
     "lora_grad": (_i32, [_vp, _vp, _i32, _i64, _vp, _i32, _i64, _vp, _i64, _vp, _vp, _i32,
                          _vp, _sz, _vp]),
@@ -292,6 +293,14 @@ def apply(plan, X, Y, ws=None, stream=None):
         _used_on(stream, ws)
     _check(lib().lora_apply(plan.handle, _ptr(X), _dtype(X), _rowmajor(X, "X"), _ptr(Y),
                             _dtype(Y), _rowmajor(Y, "Y"), _ptr(ws), ws.numel(), _stream(stream)))
+    return Y
+
+
+def apply_noalloc(plan, X, Y, stream=None):
+    """apply() with the library's fixed per-GPU scratch instead of a workspace:
+    allocates nothing (for graph capture and loops that must not allocate)."""
+    _check(lib().lora_apply_noalloc(plan.handle, _ptr(X), _dtype(X), _rowmajor(X, "X"), _ptr(Y),
+                                    _dtype(Y), _rowmajor(Y, "Y"), _stream(stream)))
     return Y
 
 
