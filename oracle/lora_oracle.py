@@ -14,6 +14,9 @@ widening bfloat16 or binary32 to float64 is exact):
 * ``apply`` / ``shrink`` / ``expand`` -- the adapter residual of the LoRA layer
   equation in Section 3.4, y = x W^T + s_a (x A_a^T) B_a^T, evaluated per adapter
   group as Delta_a = s_a (X_a A_a^T) B_a^T and added back to the original rows.
+* ``linear`` -- the whole adapted layer of Section 3.4, the shared base
+  projection x W^T of every row plus the adapter residual of its group (rows
+  with no adapter get the base projection alone).
 * ``grad`` -- the adapter-local gradients dA_a, dB_a of the loss through that
   residual, restricted to rows whose explicit loss mask is nonzero (Section 3.3
   for the mask, Section 3.5 for adapter-local gradients).  The paper does not
@@ -262,6 +265,62 @@ def apply_bruteforce(eff, X, Y, A, B, scale):
                 acc += h[j] * float(B[a][o][j])
             out[t][o] += float(scale[a]) * acc
     return np.array(out)
+
+
+# ----------------------------------------------------------------------------
+# the whole adapted layer: shared base projection plus the adapter residual
+# (Section 3.4, LoRA layer equation)
+# ----------------------------------------------------------------------------
+
+def linear(eff, X, W, A, B, scale):
+    """Y = X W^T + Delta: the base projection of every row (W is [d_out, d_in],
+    the same for all rows), plus s_a (X_a A_a^T) B_a^T on the rows of each
+    adapter group a.  Rows with no adapter get the base projection alone.
+
+    Section 3.4 writes the adapted layer as y = x W^T + s_a (x A_a^T) B_a^T and
+    computes the base term once over all active rows, the residual per group.
+    """
+    out = X @ W.T
+    for a in range(len(A)):
+        if A[a] is None:
+            continue
+        rows = np.nonzero(eff == a)[0]
+        if rows.size == 0:
+            continue
+        out[rows] += float(scale[a]) * ((X[rows] @ A[a].T) @ B[a].T)
+    return out
+
+
+def linear_rows(eff, X, W, A, B, scale, rows):
+    """linear() for the listed rows only (large cases checked on samples)."""
+    rows = np.asarray(rows, dtype=np.int64)
+    out = X[rows] @ W.T
+    for i, t in enumerate(rows):
+        a = int(eff[t])
+        if a >= 0:
+            out[i] += float(scale[a]) * (B[a] @ (A[a] @ X[t]))
+    return out
+
+
+def linear_bruteforce(eff, X, W, A, B, scale):
+    """Scalar loops over the layer equation, row by row (tiny inputs only)."""
+    n, d_in = X.shape
+    d_out = W.shape[0]
+    out = []
+    for t in range(n):
+        row = []
+        a = int(eff[t])
+        h = []
+        if a >= 0:
+            for j in range(A[a].shape[0]):
+                h.append(sum(float(X[t][k]) * float(A[a][j][k]) for k in range(d_in)))
+        for o in range(d_out):
+            y = sum(float(X[t][k]) * float(W[o][k]) for k in range(d_in))
+            if a >= 0:
+                y += float(scale[a]) * sum(h[j] * float(B[a][o][j]) for j in range(len(h)))
+            row.append(y)
+        out.append(row)
+    return np.array(out).reshape(n, d_out)
 
 
 # ----------------------------------------------------------------------------

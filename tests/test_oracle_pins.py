@@ -490,7 +490,83 @@ def check_metrics(impl):
     return True
 
 
-ALL_CHECKS = [check_plan_golden, check_plan_empty_slot_golden, check_metrics, check_plan_bruteforce, check_forward_golden,
+def check_linear_golden(impl):
+    g = load_golden("linear_worked_example.txt")
+    d_in, d_out = int(g["d_in"][0]), int(g["d_out"][0])
+    r = g["rank"].astype(int)
+    X = g["X"].reshape(-1, d_in)
+    W = g["W"].reshape(d_out, d_in)
+    A = [g["A0"].reshape(r[0], d_in), g["A1"].reshape(r[1], d_in)]
+    B = [g["B0"].reshape(d_out, r[0]), g["B1"].reshape(d_out, r[1])]
+    out = impl.linear(g["idx"].astype(np.int64), X, W, A, B, g["scale"])
+    return np.array_equal(out, g["Y_out"].reshape(-1, d_out))
+
+
+def _linear_case(seed, n=11, d_in=7, d_out=5, S=3):
+    c, eff, X, A, B, Y, _ = _tiny_case(seed, n=n, d_in=d_in, d_out=d_out, S=S)
+    W = np.random.default_rng(seed + 500).standard_normal((d_out, d_in))
+    return c, eff, X, W, A, B
+
+
+def check_linear_bruteforce(impl):
+    for seed in range(5):
+        c, eff, X, W, A, B = _linear_case(seed)
+        ref = oracle.linear_bruteforce(eff, X, W, A, B, c.scales)
+        if not np.allclose(impl.linear(eff, X, W, A, B, c.scales), ref, rtol=1e-12, atol=1e-12):
+            return False
+    return True
+
+
+def check_linear_merged_weights(impl):
+    """Each row of adapter a equals x (W + s_a B_a A_a)^T (the adapter merged
+    into the base weight, a different association of the same products); a
+    row with no adapter equals x W^T."""
+    for seed in range(4):
+        c, eff, X, W, A, B = _linear_case(seed + 20, n=17, d_in=9, d_out=6, S=3)
+        out = impl.linear(eff, X, W, A, B, c.scales)
+        for t in range(c.n):
+            a = int(eff[t])
+            Wm = W if a < 0 else W + float(c.scales[a]) * (B[a] @ A[a])
+            if not np.allclose(out[t], Wm @ X[t], rtol=1e-12, atol=1e-12):
+                return False
+    return True
+
+
+def check_linear_zero_base_is_apply(impl):
+    """W = 0 leaves the residual alone: the forward oracle applied to Y = 0."""
+    c, eff, X, W, A, B = _linear_case(41)
+    out = impl.linear(eff, X, np.zeros_like(W), A, B, c.scales)
+    return np.allclose(out, oracle.apply(eff, X, np.zeros((c.n, W.shape[0])), A, B, c.scales),
+                       rtol=1e-13, atol=1e-13)
+
+
+def check_linear_integer_exact(impl):
+    """Integer inputs and power-of-two scales: the result is exact, compared
+    with exact rational arithmetic."""
+    rng = np.random.default_rng(77)
+    n, d_in, d_out, S = 9, 6, 4, 3
+    X = rng.integers(-2, 3, (n, d_in)).astype(np.float64)
+    W = rng.integers(-2, 3, (d_out, d_in)).astype(np.float64)
+    ranks = [2, 1, 3]
+    A = [rng.integers(-2, 3, (r, d_in)).astype(np.float64) for r in ranks]
+    B = [rng.integers(-2, 3, (d_out, r)).astype(np.float64) for r in ranks]
+    scale = np.array([0.5, 2.0, 0.25])
+    eff = np.array([0, -1, 2, 1, 1, -1, 0, 2, 2])
+    out = impl.linear(eff, X, W, A, B, scale)
+    for t in range(n):
+        for o in range(d_out):
+            y = sum(fractions.Fraction(int(X[t, k]) * int(W[o, k])) for k in range(d_in))
+            a = int(eff[t])
+            if a >= 0:
+                h = [sum(int(X[t, k]) * int(A[a][j, k]) for k in range(d_in)) for j in range(ranks[a])]
+                y += fractions.Fraction(scale[a]) * sum(h[j] * int(B[a][o, j]) for j in range(ranks[a]))
+            if fractions.Fraction(out[t, o]) != y:
+                return False
+    return True
+
+
+ALL_CHECKS = [check_linear_golden, check_linear_bruteforce, check_linear_merged_weights,
+              check_linear_zero_base_is_apply, check_linear_integer_exact, check_plan_golden, check_plan_empty_slot_golden, check_metrics, check_plan_bruteforce, check_forward_golden,
               check_forward_bruteforce, check_forward_closed_form,
               check_forward_integer_exact, check_grad_golden, check_grad_linearity,
               check_grad_bruteforce, check_grad_mask_exact, check_grad_x_linearity,
@@ -591,6 +667,7 @@ def test_explicit_mask_not_inferred_from_zero_dy():
 
 def _mutant(**overrides):
     ns = types.SimpleNamespace(canonical_plan=oracle.canonical_plan, apply=oracle.apply,
+                               linear=oracle.linear,
                                grad=oracle.grad, grad_x=oracle.grad_x,
                                masked_loss=oracle.masked_loss, adamw=oracle.adamw,
                                token_loss=oracle.token_loss, rel_fro=oracle.rel_fro,
@@ -808,7 +885,44 @@ def _max_abs_nan_blind(out, ref):
     return float(np.nanmax(d)) if d.size else 0.0
 
 
+def _linear_no_base_on_none(eff, X, W, A, B, scale):
+    out = oracle.linear(eff, X, W, A, B, scale)
+    out[np.asarray(eff) < 0] = 0.0
+    return out
+
+
+def _linear_lora_on_none(eff, X, W, A, B, scale):
+    return oracle.linear(np.where(np.asarray(eff) < 0, 0, eff), X, W, A, B, scale)
+
+
+def _linear_base_reversed(eff, X, W, A, B, scale):
+    # the base weight read with a reversed d_in axis (a mis-indexed operand)
+    return oracle.linear(eff, X, W[:, ::-1], A, B, scale)
+
+
+def _linear_no_scale(eff, X, W, A, B, scale):
+    return oracle.linear(eff, X, W, A, B, np.ones_like(scale))
+
+
+def _linear_base_twice(eff, X, W, A, B, scale):
+    return oracle.linear(eff, X, W, A, B, scale) + X @ W.T
+
+
+def _linear_scale_on_base(eff, X, W, A, B, scale):
+    out = oracle.linear(eff, X, W, A, B, scale)
+    for t in range(X.shape[0]):
+        if eff[t] >= 0:
+            out[t] += (float(scale[eff[t]]) - 1.0) * (W @ X[t])
+    return out
+
+
 MUTANTS = {
+    "linear_no_base_on_none": _mutant(linear=_linear_no_base_on_none),
+    "linear_lora_on_none": _mutant(linear=_linear_lora_on_none),
+    "linear_base_reversed": _mutant(linear=_linear_base_reversed),
+    "linear_no_scale": _mutant(linear=_linear_no_scale),
+    "linear_base_twice": _mutant(linear=_linear_base_twice),
+    "linear_scale_on_base": _mutant(linear=_linear_scale_on_base),
     "plan_ranks_ignored": _mutant(canonical_plan=_plan_ranks_ignored),
     "rel_fro_zero": _mutant(rel_fro=_rel_fro_zero),
     "rel_fro_by_out": _mutant(rel_fro=_rel_fro_by_out),

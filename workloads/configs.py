@@ -217,6 +217,20 @@ def make_config(k, seed=None, y_dtype=None):
     return _MAKERS[k](k - 1 if seed is None else seed, y_dtype=y_dtype)
 
 
+def base_weight(case, seed=None, dtype=None, int_values=False):
+    """The base layer's weight W [d_out, d_in] for a case (the shared
+    projection of the adapted layer): N(0, 1/d_in) so that x W^T has unit
+    variance for unit-variance x, drawn from its own generator (seed defaults
+    to 1000 + the case's seed) so the case's other draws are unchanged.
+    ``int_values`` draws values in {-1, 0, 1}."""
+    seed = 1000 + case.seed if seed is None else seed
+    dtype = dtype or case.w_dtype
+    rng = np.random.Generator(np.random.PCG64(seed))
+    if int_values:
+        return encode(rng.integers(-1, 2, (case.d_out, case.d_in)).astype(np.float64), dtype)
+    return _normal(rng, (case.d_out, case.d_in), 1.0 / np.sqrt(case.d_in), dtype)
+
+
 def random_case(seed, n, d_in, d_out, num_slots, *, ranks=None, rank_choices=(16,),
                 frac_none=0.1, layout="random", seg_len=(1, 64), mask_p=None,
                 x_dtype="bf16", w_dtype="bf16", y_dtype="f32", scales=None,
