@@ -245,6 +245,30 @@ lora_status lora_apply(const lora_plan* p, const void* X, lora_dtype x_dtype, in
 lora_status lora_apply_noalloc(const lora_plan* p, const void* X, lora_dtype x_dtype, int64_t ldx,
                                void* Y, lora_dtype y_dtype, int64_t ldy, void* stream);
 
+/* ---- the whole adapted layer (Section 3.4: LoRA layer equation, with the
+ *      base projection shared by every row and the residual added per group) --
+ *   Y[t, :] = X[t, :] W^T + s_a (X[t, :] A_a^T) B_a^T     for a row with adapter a,
+ *   Y[t, :] = X[t, :] W^T                                  for a row with id -1.
+ * W: device bfloat16 [d_out, ldw >= d_in] row-major (the base layer's weight,
+ * one for every row).  X: bfloat16 [n, ldx].  Y: float32 or bfloat16 [n, ldy],
+ * written (not accumulated; one rounding per element for bfloat16) and not
+ * read; it must not overlap X or W.  The table's adapter weights must be
+ * bfloat16.  Arithmetic: bfloat16 products accumulated in float32; the
+ * residual's H = X A_a^T is kept in float32 and split into two bfloat16 terms
+ * before it meets B_a, with s_a applied to it first.  Two launches: the
+ * grouped shrink (H of every adapter row, into the workspace) and one
+ * matrix-core GEMM whose epilogue adds the residual of each maximal run of
+ * one adapter crossing a 256-row tile (it is built for segment batches:
+ * a tile crossed by many runs, as in a decode batch, pays one rank step per
+ * run).  ws: lora_linear_workspace_bytes(p) bytes, 16-byte aligned.  Errors:
+ * NULL, DTYPE (anything but bfloat16 X, W, weights), SHAPE (ldw < d_in, Y
+ * overlapping X or W), ALIGN, WORKSPACE, HIP. */
+size_t      lora_linear_workspace_bytes(const lora_plan* p);
+lora_status lora_linear(const lora_plan* p, const void* X, lora_dtype x_dtype, int64_t ldx,
+                        const void* W, lora_dtype w_dtype, int64_t ldw, void* Y,
+                        lora_dtype y_dtype, int64_t ldy, void* ws, size_t ws_bytes,
+                        void* stream);
+
 /* ---- backward (Sections 3.3 and 3.5: masked, adapter-local gradients) ----
  * For every slot a with dA[a] / dB[a] not NULL, over the rows T_a^m of the
  * plan's mask (mask == NULL at build time: every row of adapter a):

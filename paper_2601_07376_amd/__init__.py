@@ -9,9 +9,10 @@ if the library is not built, every call raises.
 from .lora import (AdamWTensor, Policy, LOSS_CE, LOSS_IS, LOSS_PPO, LORA_BF16, LORA_DATA_BAD_ID, LORA_DATA_BAD_SEGMENTS, LORA_DATA_EMPTY_SLOT,
                    LORA_F32, LIB_PATH, LoraError, Plan, Table, apply, apply_noalloc, apply_workspace, expand,
                    adamw_step, backward, backward_workspace, grad, grad_workspace, grad_x,
-                   grad_x_workspace, lib, shrink, token_loss)
+                   grad_x_workspace, lib, linear, linear_workspace, shrink, token_loss)
 
-__all__ = ["Table", "Plan", "shrink", "expand", "apply", "apply_noalloc", "grad", "grad_x", "backward",
+__all__ = ["Table", "Plan", "shrink", "expand", "apply", "apply_noalloc", "linear",
+           "linear_workspace", "grad", "grad_x", "backward",
            "backward_workspace", "adamw_step",
            "AdamWTensor", "token_loss", "LOSS_CE", "LOSS_IS", "LOSS_PPO", "apply_workspace",
            "grad_workspace", "grad_x_workspace", "lib", "LoraError", "LORA_F32", "LORA_BF16", "LORA_DATA_BAD_ID",

@@ -766,6 +766,81 @@ lora_status lora_apply_noalloc(const lora_plan* p, const void* X, lora_dtype x_d
   return apply_impl(p, X, x_dtype, ldx, Y, y_dtype, ldy, ws, LORA_NOALLOC_SCRATCH_BYTES, stream, false);
 }
 
+// ---- the whole adapted layer ---------------------------------------------------
+
+// SHRINK_KS_MAX fp32 planes [n, pad8(r_max)], then the packed bf16 s_a H
+// [n, 2 linear_rank_cols(r_max)]
+size_t lora_linear_workspace_bytes(const lora_plan* p) {
+  if (p == nullptr) return 0;
+  return apply_h_bytes(p) +
+         al256((size_t)std::max(p->n, 1) * 2 * lora::linear_rank_cols(p->r_max) * 2);
+}
+
+lora_status lora_linear(const lora_plan* p, const void* X, lora_dtype x_dtype, int64_t ldx,
+                        const void* W, lora_dtype w_dtype, int64_t ldw, void* Y, lora_dtype y_dtype,
+                        int64_t ldy, void* ws, size_t ws_bytes, void* stream) {
+  lora_status st = check_plan(p);
+  if (st != LORA_OK) return st;
+  const lora_table* t = p->table;
+  if ((st = check_matrix(X, x_dtype, ldx, t->d_in, "X", p->n)) != LORA_OK) return st;
+  if ((st = check_matrix(Y, y_dtype, ldy, t->d_out, "Y", p->n)) != LORA_OK) return st;
+  if (W == nullptr) return fail(LORA_ERR_NULL, "W is NULL");
+  if ((st = check_matrix(W, w_dtype, ldw, t->d_in, "W")) != LORA_OK) return st;
+  if (x_dtype != LORA_BF16 || w_dtype != LORA_BF16 || t->w_dtype != LORA_BF16)
+    return fail(LORA_ERR_DTYPE, "lora_linear needs bfloat16 X, W and adapter weights");
+  {
+    // Y must not overlap X or W (it is written while they are read)
+    const uintptr_t yb = (uintptr_t)Y, ye = yb + (uintptr_t)std::max(p->n, 1) * (uintptr_t)ldy * dsize(y_dtype);
+    const uintptr_t xb = (uintptr_t)X, xe = xb + (uintptr_t)std::max(p->n, 1) * (uintptr_t)ldx * 2u;
+    const uintptr_t wb = (uintptr_t)W, we = wb + (uintptr_t)t->d_out * (uintptr_t)ldw * 2u;
+    if (p->n > 0 && ((yb < xe && xb < ye) || (yb < we && wb < ye)))
+      return fail(LORA_ERR_SHAPE, "Y overlaps X or W");
+  }
+  const size_t need = lora_linear_workspace_bytes(p);
+  if (ws == nullptr) return fail(LORA_ERR_NULL, "linear workspace is NULL");
+  if (!aligned(ws, 16)) return fail(LORA_ERR_ALIGN, "linear workspace not 16-byte aligned");
+  if (ws_bytes < need) return fail(LORA_ERR_WORKSPACE, "linear workspace %zu bytes < %zu", ws_bytes, need);
+  if (p->n == 0) return ok();
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t ldh = (std::max(p->r_max, 1) + 7) / 8 * 8;
+  const int64_t plane = (int64_t)(al256((size_t)std::max(p->n, 1) * ldh * 4) / 4);
+  float* H = static_cast<float*>(ws);
+  lora::OpLaunch o = op_base(p);
+  hipError_t e = hipSuccess;
+  if (p->r_max > 0) {
+    // H of every row with an adapter (all entries: large-group blocks and
+    // small-group entries), in SHRINK_KS_MAX partial planes
+    lora::OpLaunch os = o;
+    os.count_word = lora::HDR_NRB_TOTAL;
+    os.first_word = -1;
+    os.rb_ub = ub_large(p) + ub_small(p);
+    os.coarse_ub = ub_coarse(p) + ub_small(p);
+    os.fine_ub = ub_fine(p) + ub_small(p);
+    e = lora::launch_shrink_mfma(os, X, ldx, H, ldh, lora::SHRINK_KS_MAX, plane, s);
+    if (e != hipSuccess) return hip_fail(e, "linear shrink launch");
+  }
+  lora::LinearLaunch l{};
+  l.X = X;
+  l.ldx = ldx;
+  l.W = W;
+  l.ldw = ldw;
+  l.Y = Y;
+  l.ldy = ldy;
+  l.y_bf16 = y_dtype == LORA_BF16;
+  l.run_start = p->d.run_start;
+  l.run_end = p->d.run_end;
+  l.run_adapter = p->d.run_adapter;
+  l.H = H;
+  l.ldh = ldh;
+  l.hp_stride = plane;
+  l.ks_max = lora::SHRINK_KS_MAX;
+  l.Hs = reinterpret_cast<uint16_t*>(static_cast<char*>(ws) + apply_h_bytes(p));
+  o.rb_ub = ub_large(p) + ub_small(p);
+  e = lora::launch_linear_mfma(o, l, s);
+  if (e != hipSuccess) return hip_fail(e, "linear launch");
+  return ok();
+}
+
 // ---- backward --------------------------------------------------------------
 
 size_t lora_grad_workspace_bytes(const lora_plan* p) {

@@ -228,10 +228,8 @@ __device__ __forceinline__ void shrink_steps(f32x4 (&acc)[MT * NT], const uint16
 // buffered with one barrier per step.
 // ---------------------------------------------------------------------------
 
-// d-slices of the shrink: enough (block, slice) units to cover the chip once,
-// at most p.ks_max (the workspace holds that many partial planes)
 __device__ __forceinline__ int shrink_splits(const FwdArgs& p, int count) {
-  return max(1, min(p.ks_max, 256 / max(count, 1)));
+  return shrink_slices(p.ks_max, count);
 }
 
 // slice ks of [0, d) in multiples of 32

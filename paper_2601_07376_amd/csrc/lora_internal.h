@@ -134,6 +134,16 @@ struct OpLaunch {
   int first_word;               // header word holding the first entry (-1: 0)
 };
 
+// d-slices of the grouped shrink over `count` entries: enough (entry, slice)
+// units to cover the chip once, at most ks_max (the workspace holds that many
+// partial planes).  Every reader of the planes uses the same count.
+__host__ __device__ __forceinline__ int shrink_slices(int ks_max, int count) {
+  const int c = count > 1 ? count : 1;
+  const int q = 256 / c;
+  const int k = ks_max < q ? ks_max : q;
+  return k > 1 ? k : 1;
+}
+
 // H[t, :r] = X[t] A^T over entries [first, count) (bf16 X and weights, matrix
 // cores).  With ks_max > 1 the kernel may split d_in into up to ks_max slices
 // and write one partial plane per slice, plane k at H + k * hp_stride; the
@@ -161,6 +171,29 @@ constexpr int SPLIT_SLICES_MAX = 8;
 hipError_t launch_small_split_mfma(const OpLaunch& o, const void* X, int64_t ldx, void* Y,
                                    lora_dtype y_dtype, int64_t ldy, int32_t n_chunks,
                                    int32_t slices, float* part, hipStream_t s);
+
+// the whole adapted layer Y = X W^T + s_a (X A_a^T) B_a^T (bf16 X, W and
+// weights): one GEMM whose epilogue adds the residual of every run crossing a
+// tile, from H = the grouped shrink's ks_max-sliced partial planes
+struct LinearLaunch {
+  const void* X;
+  int64_t ldx;
+  const void* W;
+  int64_t ldw;
+  void* Y;
+  int64_t ldy;
+  bool y_bf16;
+  const int32_t* run_start;
+  const int32_t* run_end;
+  const int32_t* run_adapter;
+  const float* H;
+  int64_t ldh;
+  int64_t hp_stride;
+  int32_t ks_max;
+  uint16_t* Hs;        // [n][2 linear_rank_cols(r_max)] bf16: the packed s_a H (rank multiple of 8)
+};
+int32_t linear_rank_cols(int32_t r_max);
+hipError_t launch_linear_mfma(const OpLaunch& o, const LinearLaunch& l, hipStream_t s);
 
 // vector-ALU kernels for any mix of f32 / bf16 storage
 hipError_t launch_shrink_valu(const OpLaunch& o, const void* X, lora_dtype x_dtype,

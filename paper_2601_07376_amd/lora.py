@@ -47,6 +47,8 @@ SIGNATURES = {
     "lora_apply_workspace_bytes": (_sz, [_vp]),
     "lora_apply": (_i32, [_vp, _vp, _i32, _i64, _vp, _i32, _i64, _vp, _sz, _vp]),
     "lora_apply_noalloc": (_i32, [_vp, _vp, _i32, _i64, _vp, _i32, _i64, _vp]),
+    "lora_linear_workspace_bytes": (_sz, [_vp]),
+    "lora_linear": (_i32, [_vp, _vp, _i32, _i64, _vp, _i32, _i64, _vp, _i32, _i64, _vp, _sz, _vp]),
     "lora_grad_workspace_bytes": (_sz, [_vp]),
     "lora_grad": (_i32, [_vp, _vp, _i32, _i64, _vp, _i32, _i64, _vp, _i64, _vp, _vp, _i32,
                          _vp, _sz, _vp]),
@@ -301,6 +303,22 @@ def apply_noalloc(plan, X, Y, stream=None):
     allocates nothing (for graph capture and loops that must not allocate)."""
     _check(lib().lora_apply_noalloc(plan.handle, _ptr(X), _dtype(X), _rowmajor(X, "X"), _ptr(Y),
                                     _dtype(Y), _rowmajor(Y, "Y"), _stream(stream)))
+    return Y
+
+
+def linear_workspace(plan):
+    return torch.empty(max(lib().lora_linear_workspace_bytes(plan.handle), 16), dtype=torch.uint8,
+                       device=plan.table.device)
+
+
+def linear(plan, X, W, Y, ws=None, stream=None):
+    """Y = X W^T + s_a (X A_a^T) B_a^T (rows with no adapter: X W^T); Y written."""
+    if ws is None:
+        ws = linear_workspace(plan)
+        _used_on(stream, ws)
+    _check(lib().lora_linear(plan.handle, _ptr(X), _dtype(X), _rowmajor(X, "X"), _ptr(W),
+                             _dtype(W), _rowmajor(W, "W"), _ptr(Y), _dtype(Y), _rowmajor(Y, "Y"),
+                             _ptr(ws), ws.numel(), _stream(stream)))
     return Y
 
 
