@@ -262,7 +262,8 @@ lora_status lora_apply_noalloc(const lora_plan* p, const void* X, lora_dtype x_d
  * a tile crossed by many runs, as in a decode batch, pays one rank step per
  * run).  ws: lora_linear_workspace_bytes(p) bytes, 16-byte aligned.  Errors:
  * NULL, DTYPE (anything but bfloat16 X, W, weights), SHAPE (ldw < d_in, Y
- * overlapping X or W), ALIGN, WORKSPACE, HIP. */
+ * overlapping X or W, a leading dimension above 2^21 elements), ALIGN,
+ * WORKSPACE, HIP. */
 size_t      lora_linear_workspace_bytes(const lora_plan* p);
 lora_status lora_linear(const lora_plan* p, const void* X, lora_dtype x_dtype, int64_t ldx,
                         const void* W, lora_dtype w_dtype, int64_t ldw, void* Y,

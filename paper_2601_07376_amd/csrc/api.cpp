@@ -788,6 +788,10 @@ lora_status lora_linear(const lora_plan* p, const void* X, lora_dtype x_dtype, i
   if ((st = check_matrix(W, w_dtype, ldw, t->d_in, "W")) != LORA_OK) return st;
   if (x_dtype != LORA_BF16 || w_dtype != LORA_BF16 || t->w_dtype != LORA_BF16)
     return fail(LORA_ERR_DTYPE, "lora_linear needs bfloat16 X, W and adapter weights");
+  // a 256-row tile of any operand must span less than 2^31 bytes (32-bit offsets)
+  constexpr int64_t LD_MAX = int64_t(1) << 21;
+  if (ldx > LD_MAX || ldw > LD_MAX || ldy > LD_MAX)
+    return fail(LORA_ERR_SHAPE, "lora_linear: leading dimensions above %lld elements", (long long)LD_MAX);
   {
     // Y must not overlap X or W (it is written while they are read)
     const uintptr_t yb = (uintptr_t)Y, ye = yb + (uintptr_t)std::max(p->n, 1) * (uintptr_t)ldy * dsize(y_dtype);

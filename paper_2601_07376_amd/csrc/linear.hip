@@ -33,9 +33,10 @@
 namespace lora {
 
 #ifndef LINEAR_KS
-#define LINEAR_KS 32
-#define LINEAR_NS 4
+#define LINEAR_KS 64
+#define LINEAR_NS 2
 #define LINEAR_NTS 1
+#define LINEAR_DMA 1
 #endif
 
 namespace {
@@ -45,6 +46,9 @@ constexpr int LT_GM = 4;                        // row tiles per group of the ti
 constexpr int LT_SST = 132;                     // row stride (floats) of the store staging
 
 typedef __attribute__((ext_vector_type(16))) float f32x16;
+
+// instruction classes of __builtin_amdgcn_sched_group_barrier
+constexpr int SG_MFMA = 0x008, SG_VMEM = 0x010, SG_DS_READ = 0x100;
 
 struct LinArgs {
   const uint16_t* X;
@@ -128,13 +132,50 @@ __device__ __forceinline__ void lt_dma16(rsrc_t src, uint8_t* lds, uint32_t voff
                                            voff, soff, 0, 0);
 }
 
+// One 16-byte store per lane through a buffer resource (offsets past it are
+// dropped); `nt` marks it non-temporal.
+__device__ __forceinline__ void lt_st16(rsrc_t dst, u32x4 v, uint32_t voff, bool nt) {
+  if (nt) __builtin_amdgcn_raw_buffer_store_b128(v, dst, voff, 0, 2);
+  else __builtin_amdgcn_raw_buffer_store_b128(v, dst, voff, 0, 0);
+}
+
+// One 16-byte load per lane into registers (the staging-through-registers path).
+__device__ __forceinline__ u32x4 lt_ld16(rsrc_t src, uint32_t voff, uint32_t soff) {
+  return __builtin_amdgcn_raw_buffer_load_b128(src, voff, soff, 0);
+}
+
+// Where the loads of one K step go: straight into LDS (DMA), or into the
+// registers R (2 IPW per lane) to be written to LDS one step later.
+template <int KS, bool DMA>
+struct Sink {
+  u32x4 (&R)[2 * Stage<KS>::IPW];
+  __device__ __forceinline__ void put(int k, rsrc_t src, uint8_t* lds, uint32_t voff, uint32_t soff) {
+    if (DMA) lt_dma16(src, lds, voff, soff);
+    else R[k] = lt_ld16(src, voff, soff);
+  }
+};
+
+// Registers of one K step into its LDS slot: load k of wave w sits at bytes
+// (IPW w + k) 1024 + 16 lane of the A tile (k < IPW) or the B tile.
+template <int KS>
+__device__ __forceinline__ void lt_write(const u32x4 (&R)[2 * Stage<KS>::IPW], uint8_t* slot, int w,
+                                         int lane) {
+  using S = Stage<KS>;
+#pragma unroll
+  for (int k = 0; k < 2 * S::IPW; ++k) {
+    uint8_t* d = slot + (k < S::IPW ? 0 : S::OP) + (S::IPW * w + (k % S::IPW)) * 1024 + lane * 16;
+    *reinterpret_cast<u32x4*>(d) = R[k];
+  }
+}
+
 // One operand tile of one K step into LDS, through a buffer resource whose base
 // is the tile's first row and whose size covers its valid rows: offsets past
 // it read zeros (the rows past n or d_out of the last tiles), and chunks past
 // d_in are sent past it (the K tail reads zeros).
-template <int KS>
-__device__ __forceinline__ void lt_stage(const uint16_t* base, uint32_t bytes, const StageMap<KS>& m,
-                                         int k0, int d_in, uint8_t* lds, int w) {
+template <int KS, bool DMA>
+__device__ __forceinline__ void lt_stage(Sink<KS, DMA> sk, int k_base, const uint16_t* base,
+                                         uint32_t bytes, const StageMap<KS>& m, int k0, int d_in,
+                                         uint8_t* lds, int w) {
   using S = Stage<KS>;
   const rsrc_t src = make_rsrc(base, bytes);
   const int left = d_in - k0;          // valid K columns from k0 on
@@ -142,7 +183,8 @@ __device__ __forceinline__ void lt_stage(const uint16_t* base, uint32_t bytes, c
   const uint32_t v1 = 8 * m.chunk[1] < left ? m.off[1] : 0x80000000u;
 #pragma unroll
   for (int i = 0; i < S::IPW; ++i)
-    lt_dma16(src, lds + (S::IPW * w + i) * 1024, (i & 1) ? v1 : v0, (uint32_t)k0 * 2u + (uint32_t)i * m.step);
+    sk.put(k_base + i, src, lds + (S::IPW * w + i) * 1024, (i & 1) ? v1 : v0,
+           (uint32_t)k0 * 2u + (uint32_t)i * m.step);
 }
 
 template <int KS>
@@ -188,10 +230,10 @@ __device__ __forceinline__ void lt_barrier() {
 // step read at rank column (j KS + k') mod rp (hi and lo halves meet the same
 // B_a), zero past r_a.  Rank a multiple of 8, so every 16-byte chunk of a B_a
 // row is aligned and lies wholly inside or outside [0, r_a).
-template <int KS>
-__device__ __forceinline__ void lt_stage_lora(const LinArgs& p, const StageMap<KS>& hm, int r0, int n0,
-                                              int j, int rs, int re, const uint16_t* Ba, int r,
-                                              uint8_t* lds, int w, int lane) {
+template <int KS, bool DMA>
+__device__ __forceinline__ void lt_stage_lora(Sink<KS, DMA> sk, const LinArgs& p, const StageMap<KS>& hm,
+                                              int r0, int n0, int j, int rs, int re, const uint16_t* Ba,
+                                              int r, uint8_t* lds, int w, int lane) {
   using S = Stage<KS>;
   const rsrc_t ha = make_rsrc(p.Hs + (int64_t)r0 * (2 * p.rp),
                               (uint32_t)min(LT_M, p.n - r0) * (uint32_t)(2 * p.rp) * 2u);
@@ -207,13 +249,13 @@ __device__ __forceinline__ void lt_stage_lora(const LinArgs& p, const StageMap<K
   for (int i = 0; i < S::IPW; ++i) {
     const int row = (S::IPW * w + i) * S::RPI + lr;
     const bool in = r0 + row >= rs && r0 + row <= re;
-    lt_dma16(ha, lds + (S::IPW * w + i) * 1024, in ? hm.off[i & 1] : 0x80000000u,
-             (uint32_t)(j * KS) * 2u + (uint32_t)i * hm.step);
+    sk.put(i, ha, lds + (S::IPW * w + i) * 1024, in ? hm.off[i & 1] : 0x80000000u,
+           (uint32_t)(j * KS) * 2u + (uint32_t)i * hm.step);
   }
 #pragma unroll
   for (int i = 0; i < S::IPW; ++i)
-    lt_dma16(bb, lds + S::OP + (S::IPW * w + i) * 1024, bo[i & 1],
-             (uint32_t)((S::IPW * w + i) * S::RPI) * (uint32_t)r * 2u);
+    sk.put(S::IPW + i, bb, lds + S::OP + (S::IPW * w + i) * 1024, bo[i & 1],
+           (uint32_t)((S::IPW * w + i) * S::RPI) * (uint32_t)r * 2u);
 }
 
 // Packs the residual's left operand once per call: for every row t of an
@@ -270,11 +312,14 @@ __device__ __forceinline__ bool lt_tile(const LinArgs& p, int& m, int& nt) {
   return true;
 }
 
-// KS: K columns per step; NS: steps staged in LDS at once (NS - 1 in flight
-// while one is multiplied); NTS: non-temporal stores of Y.
-template <bool YBF16, bool RANK8, int KS, int NS, bool NTS>
+// KS: K columns per step; NS: steps staged in LDS at once; NTS: non-temporal
+// stores of Y; DMA: operands go straight from memory to LDS (NS - 1 steps in
+// flight while one is multiplied), else through registers (NS = 2: one step in
+// LDS being multiplied, the next in LDS, the one after in registers).
+template <bool YBF16, bool RANK8, int KS, int NS, bool NTS, bool DMA>
 __global__ __launch_bounds__(256, 1) void linear_kernel(LinArgs p) {
   using S = Stage<KS>;
+  static_assert(DMA || NS == 2, "register staging keeps two LDS slots");
   // ring of NS steps, each [A | B][256 rows x S::ROW bytes]
   constexpr int BUFB = 2 * S::OP;
   static_assert(NS * BUFB <= 160 * 1024, "LDS");
@@ -332,10 +377,12 @@ __global__ __launch_bounds__(256, 1) void linear_kernel(LinArgs p) {
   const StageMap<KS> hm = lt_map<KS>(2 * p.rp, w, lane);
   int cur_run = -1, rs = 0, re = -1, rr = 8;
   const uint16_t* Ba = p.W;
+  u32x4 R[2 * S::IPW];
+  const Sink<KS, DMA> sk{R};
   auto issue = [&](int st, uint8_t* dst) {
     if (st < nk || st >= T) {
-      lt_stage(xs, xb, xm, st * KS, p.d_in, dst, w);
-      lt_stage(ws, wb, wmap, st * KS, p.d_in, dst + S::OP, w);
+      lt_stage(sk, 0, xs, xb, xm, st * KS, p.d_in, dst, w);
+      lt_stage(sk, S::IPW, ws, wb, wmap, st * KS, p.d_in, dst + S::OP, w);
     } else {
       const int q = st - nk, kr = q / p.spr;
       if (kr != cur_run) {
@@ -346,32 +393,80 @@ __global__ __launch_bounds__(256, 1) void linear_kernel(LinArgs p) {
         Ba = static_cast<const uint16_t*>(sm.B);
         rr = sm.rank;
       }
-      lt_stage_lora<KS>(p, hm, r0, n0, q - kr * p.spr, rs, re, Ba, rr, dst, w, lane);
+      lt_stage_lora(sk, p, hm, r0, n0, q - kr * p.spr, rs, re, Ba, rr, dst, w, lane);
     }
   };
+  if (DMA) {
 #pragma unroll
-  for (int j = 0; j < NS; ++j) issue(j, s_lds + j * BUFB);
-  lt_barrier<(NS - 1) * LPS>();
+    for (int j = 0; j < NS; ++j) issue(j, s_lds + j * BUFB);
+    lt_barrier<(NS - 1) * LPS>();
+  } else {
+    issue(0, s_lds);
+    lt_write<KS>(R, s_lds, w, lane);
+    issue(1, s_lds + BUFB);
+    lt_barrier<LPS>();
+  }
   Frags f0, f1;
   lt_read<KS>(f0, s_lds, s_lds + S::OP, 0, wm, wn, lane);
-  for (int ks = 0; ks < T; ++ks) {
+  // one step: its products, with the loads of step ks + NS (ks + 2 through
+  // the registers) issued at its end through `load`
+  auto step = [&](int ks, auto load) {
     const int slot = ks % NS;
     uint8_t* cur = s_lds + slot * BUFB;
     uint8_t* nxt = s_lds + (slot + 1 == NS ? 0 : slot + 1) * BUFB;
 #pragma unroll
     for (int kk = 0; kk + 1 < S::SUB; ++kk) {
       lt_read<KS>((kk & 1) ? f0 : f1, cur, cur + S::OP, kk + 1, wm, wn, lane);
-      __builtin_amdgcn_sched_barrier(0);
       lt_mma((kk & 1) ? f1 : f0, acc);
+      // one fragment read after each of the first 8 products, so the reads
+      // issue while the matrix core is busy
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(SG_MFMA, 8, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
-    lt_barrier<(NS - 2) * LPS>();
-    issue(ks + NS, cur);
+    if (DMA) {
+      lt_barrier<(NS - 2) * LPS>();
+      load(ks + NS, cur);
+    } else {
+      // step ks + 1 from the registers into the other slot (last read in step
+      // ks - 1, before the previous barrier), then step ks + 2 into the
+      // registers; the barrier waits for the writes, not for those loads
+      lt_write<KS>(R, nxt, w, lane);
+      load(ks + 2, nxt);
+      lt_barrier<LPS>();
+    }
     lt_read<KS>(f0, nxt, nxt + S::OP, 0, wm, wn, lane);
-    __builtin_amdgcn_sched_barrier(0);
     lt_mma(f1, acc);           // the last sub-step (SUB is even: its fragments are in f1)
+    if (DMA) {
+      // the step's loads two per product, then the next step's first reads one
+      // per product: the matrix core stays busy while they issue
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(SG_VMEM, LPS / 8, 0);
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 1, 0);
+      }
+    }
     __builtin_amdgcn_sched_barrier(0);
-  }
+  };
+  // steps whose loads are all of X W^T run without a branch in the loop body;
+  // the rest (the last steps of X W^T and the run steps) take the general loader
+  const int lead = DMA ? NS : 2;
+  const int n_plain = max(0, nk - lead);
+  auto plain = [&](int st, uint8_t* dst) {
+    lt_stage(sk, 0, xs, xb, xm, st * KS, p.d_in, dst, w);
+    lt_stage(sk, S::IPW, ws, wb, wmap, st * KS, p.d_in, dst + S::OP, w);
+  };
+  for (int ks = 0; ks < n_plain; ++ks) step(ks, plain);
+  for (int ks = n_plain; ks < T; ++ks) step(ks, issue);
 
   // ---- ranks not a multiple of 8: + s_a H B_a^T for each run crossing the
   // tile, from the slice planes, after the main loop --------------------------
@@ -438,9 +533,14 @@ __global__ __launch_bounds__(256, 1) void linear_kernel(LinArgs p) {
   // One 32-row block of the wave's 128 x 128 at a time through the wave's own
   // LDS area (32 rows of 128 floats, stride LT_SST), then back as 16-byte
   // vectors of whole rows: each store instruction writes four 256-byte row
-  // pieces (bfloat16) or two 512-byte ones (float32).
+  // pieces (bfloat16) or two 512-byte ones (float32).  The stores go through a
+  // resource covering the tile's valid rows, with columns past d_out sent past
+  // it, so none sits behind a branch.
   lt_barrier<0>();     // the unused loads past the last step have landed; all LDS reads done
   float* st = reinterpret_cast<float*>(s_lds) + w * (32 * LT_SST);
+  constexpr uint32_t ES = YBF16 ? 2u : 4u;
+  const rsrc_t yr = make_rsrc(static_cast<char*>(p.Y) + ((int64_t)r0 * p.ldy + n0) * ES,
+                              (uint32_t)min(LT_M, p.n - r0) * (uint32_t)p.ldy * ES);
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb) {
 #pragma unroll
@@ -448,39 +548,35 @@ __global__ __launch_bounds__(256, 1) void linear_kernel(LinArgs p) {
 #pragma unroll
       for (int v = 0; v < 16; ++v)
         st[(8 * (v >> 2) + 4 * ch + (v & 3)) * LT_SST + nb * 32 + rl] = acc[mb][nb][v];
-    const int row_base = r0 + wm * 128 + mb * 32;
-    const int col_base = n0 + wn * 128;
+    const int row_base = wm * 128 + mb * 32;       // tile-local
     if (YBF16) {
       // lane: row 4 q + lane / 16 of each group of 4 rows, columns 8 (lane % 16) ..
-      const int c8 = (lane & 15) * 8;
+      const int c8 = wn * 128 + (lane & 15) * 8;
+      const bool col_ok = n0 + c8 < p.d_out;
 #pragma unroll
       for (int q = 0; q < 8; ++q) {
         const int rr = 4 * q + (lane >> 4);
-        const float* sp = st + rr * LT_SST + c8;
+        const float* sp = st + rr * LT_SST + (lane & 15) * 8;
         const float4 a0 = *reinterpret_cast<const float4*>(sp);
         const float4 a1 = *reinterpret_cast<const float4*>(sp + 4);
-        const int row = row_base + rr, col = col_base + c8;
-        if (row < p.n && col < p.d_out) {
-          const u32x4 o = {pack2_bf16(a0.x, a0.y), pack2_bf16(a0.z, a0.w),
-                           pack2_bf16(a1.x, a1.y), pack2_bf16(a1.z, a1.w)};
-          u32x4* dst = reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(p.Y) + (int64_t)row * p.ldy + col);
-          if (NTS) __builtin_nontemporal_store(o, dst);
-          else *dst = o;
-        }
+        const u32x4 o = {pack2_bf16(a0.x, a0.y), pack2_bf16(a0.z, a0.w),
+                         pack2_bf16(a1.x, a1.y), pack2_bf16(a1.z, a1.w)};
+        const uint32_t off = col_ok ? ((uint32_t)(row_base + rr) * (uint32_t)p.ldy + (uint32_t)c8) * ES
+                                    : 0x80000000u;
+        lt_st16(yr, o, off, NTS);
       }
     } else {
-      const int c4 = (lane & 31) * 4;
+      const int c4 = wn * 128 + (lane & 31) * 4;
+      const bool col_ok = n0 + c4 < p.d_out;
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
         const int rr = 2 * q + (lane >> 5);
-        const float4 a = *reinterpret_cast<const float4*>(st + rr * LT_SST + c4);
-        const int row = row_base + rr, col = col_base + c4;
-        if (row < p.n && col < p.d_out) {
-          const f32x4 v = {a.x, a.y, a.z, a.w};
-          f32x4* dst = reinterpret_cast<f32x4*>(reinterpret_cast<float*>(p.Y) + (int64_t)row * p.ldy + col);
-          if (NTS) __builtin_nontemporal_store(v, dst);
-          else *dst = v;
-        }
+        const float4 a = *reinterpret_cast<const float4*>(st + rr * LT_SST + (lane & 31) * 4);
+        const u32x4 o = {__float_as_uint(a.x), __float_as_uint(a.y), __float_as_uint(a.z),
+                         __float_as_uint(a.w)};
+        const uint32_t off = col_ok ? ((uint32_t)(row_base + rr) * (uint32_t)p.ldy + (uint32_t)c4) * ES
+                                    : 0x80000000u;
+        lt_st16(yr, o, off, NTS);
       }
     }
   }
@@ -531,11 +627,11 @@ hipError_t launch_linear_mfma(const OpLaunch& o, const LinearLaunch& l, hipStrea
   }
   const bool yb = l.y_bf16;
   constexpr int KS = LINEAR_KS, NS = LINEAR_NS;
-  constexpr bool NTS = LINEAR_NTS;
-  if (yb && o.rank8) hipLaunchKernelGGL((linear_kernel<true, true, KS, NS, NTS>), dim3(grid), dim3(256), 0, s, a);
-  else if (yb) hipLaunchKernelGGL((linear_kernel<true, false, KS, NS, NTS>), dim3(grid), dim3(256), 0, s, a);
-  else if (o.rank8) hipLaunchKernelGGL((linear_kernel<false, true, KS, NS, NTS>), dim3(grid), dim3(256), 0, s, a);
-  else hipLaunchKernelGGL((linear_kernel<false, false, KS, NS, NTS>), dim3(grid), dim3(256), 0, s, a);
+  constexpr bool NTS = LINEAR_NTS, DMA = LINEAR_DMA;
+  if (yb && o.rank8) hipLaunchKernelGGL((linear_kernel<true, true, KS, NS, NTS, DMA>), dim3(grid), dim3(256), 0, s, a);
+  else if (yb) hipLaunchKernelGGL((linear_kernel<true, false, KS, NS, NTS, DMA>), dim3(grid), dim3(256), 0, s, a);
+  else if (o.rank8) hipLaunchKernelGGL((linear_kernel<false, true, KS, NS, NTS, DMA>), dim3(grid), dim3(256), 0, s, a);
+  else hipLaunchKernelGGL((linear_kernel<false, false, KS, NS, NTS, DMA>), dim3(grid), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
