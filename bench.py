@@ -10,7 +10,10 @@ measured the same way and reported under "extra"; for the masked-backward
 workload the input gradient (lora_grad_x, over the same plan), both gradients in
 one call (lora_backward), the AdamW step
 over its adapters' tensors (lora_adamw_step) and the PPO-style token loss over
-logits [n, 32768] with its action mask (lora_token_loss) are also timed alone.
+logits [n, 32768] with its action mask (lora_token_loss) are also timed alone;
+for the prefill workload the whole adapted layer (lora_linear: the base
+projection X W^T plus the residual, one GEMM) is timed too, with torch's own
+X W^T (hipBLASLt) beside it for context.
 
 Measurement protocol
   * inputs are resident in HBM before timing; each workload keeps R copies of its
@@ -22,7 +25,11 @@ Measurement protocol
     host; HIP events on the compute stream bracket the region and each op;
   * achieved bandwidth = algorithmic bytes (each tensor counted once at its
     minimum: touched rows of X and Y, touched adapters' weights, ids) divided by
-    the average op duration; the peak is MI355X's 8 TB/s HBM.
+    the average op duration; the peak is MI355X's 8 TB/s HBM; durations are
+    also reported as the median and p10 / p90 of block averages (8 blocks);
+  * calibration on the same box: a plain 1 GiB device copy (achievable HBM)
+    and a register-only matrix-core loop (achievable bf16 MFMA rate); every
+    fraction is given against both the datasheet peak and the calibrated one.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--configs 1,2,3,4,5]
 """
@@ -60,7 +67,7 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy", action="store_true",
-                    help="also run a plain 1 GiB device copy (counter calibration)")
+                    help="(kept for old command lines: the calibrations always run)")
     return ap.parse_args()
 
 
@@ -298,6 +305,53 @@ def token_loss_leg(case, timed, steps):
                 hbm_frac=nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS)
 
 
+def linear_leg(case, rig, h, timed, steps):
+    """The whole adapted layer on the prefill batch: lora_linear writes
+    Y = X W^T + s_a (X A_a^T) B_a^T (bf16 Y) with W [d_out, d_in] bf16 ~
+    N(0, 1/d_in).  X, W and Y (1.1 GB together) exceed the Infinity Cache, so
+    every call streams them from HBM.  torch.matmul of X W^T alone (hipBLASLt)
+    is timed on the same tensors for context."""
+    import torch
+    import workloads
+    import paper_2601_07376_amd as L
+    d = rig.sets[0]
+    X = d["X"]
+    W = torch.from_numpy(workloads.base_weight(case).view(np.int16)).cuda().view(torch.bfloat16)
+    Y = torch.empty(case.n, case.d_out, dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(max(L.lib().lora_linear_workspace_bytes(h), 16), dtype=torch.uint8, device="cuda")
+    lib = L.lib()
+
+    def enqueue(i):
+        st = lib.lora_linear(h, X.data_ptr(), 1, X.stride(0), W.data_ptr(), 1, W.stride(0),
+                             Y.data_ptr(), 1, Y.stride(0), ws.data_ptr(), ws.numel(),
+                             ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+        assert st == 0, lib.lora_last_error()
+    for i in range(2):
+        enqueue(i)
+    k = max(10, steps // 10)
+    us = timed(enqueue, k, "linear_us") * 1e3
+    Wt = W.t()
+    for i in range(2):
+        torch.matmul(X, Wt, out=Y)
+    t_us = timed(lambda i: torch.matmul(X, Wt, out=Y), k, "torch_xwt_us") * 1e3
+    idx = case.idx
+    act = idx >= 0
+    ranks = case.ranks.astype(np.int64)
+    touched = np.unique(idx[act])
+    base_flops = 2 * case.n * case.d_in * case.d_out
+    lora_flops = int(np.sum(2 * ranks[idx[act]] * (case.d_in + case.d_out)))
+    nbytes = (case.n * case.d_in * 2 + case.d_out * case.d_in * 2 + case.n * case.d_out * 2
+              + int(np.sum(ranks[touched]) * (case.d_in + case.d_out) * 2))
+    fl = base_flops + lora_flops
+    del W, Y, ws
+    torch.cuda.empty_cache()
+    return dict(op="lora_linear", us_mean=us, flops=fl, base_flops=base_flops, lora_flops=lora_flops,
+                bytes=nbytes, TFLOPs=fl / (us * 1e-6) / 1e12,
+                mfma_frac=fl / (us * 1e-6) / 1e12 / BF16_PEAK_TFLOPS,
+                GBps=nbytes / (us * 1e-6) / 1e9, torch_xwt_us=t_us,
+                torch_xwt_TFLOPs=base_flops / (t_us * 1e-6) / 1e12)
+
+
 def sleep_rate(torch):
     """GPU sleep-kernel cycles per millisecond (for the start gate)."""
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -329,41 +383,53 @@ def run_workload(cfg, steps, warmup, rate):
     host_ms = (time.perf_counter() - c0) * 1e3 / max(warmup, 1)
     torch.cuda.synchronize()
 
-    def timed(enqueue, k):
-        """Average GPU time per call of enqueue(i) over k back-to-back calls: the
-        calls are queued behind a GPU-side start gate, so the GPU never waits on
-        the host, and two events on the compute stream bracket them."""
-        es, ee = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    dist = {}
+
+    def timed(enqueue, k, key=None, blocks=8):
+        """Average GPU time (ms) per call of enqueue(i) over k back-to-back calls:
+        the calls are queued behind a GPU-side start gate, so the GPU never waits
+        on the host, and events on the compute stream bracket them; an event
+        after each of `blocks` blocks gives the spread of block averages
+        (median, p10, p90 in us, stored under `key`)."""
+        nb = max(1, min(blocks, k // 8))
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(nb + 1)]
         gate_ms = min(500.0, 2.0 + 2.0 * host_ms * k)
         torch.cuda.synchronize()
         torch.cuda._sleep(int(gate_ms * rate))
-        es.record()
-        for i in range(k):
-            enqueue(i)
-        ee.record()
+        ev[0].record()
+        bounds = [round(j * k / nb) for j in range(nb + 1)]
+        for j in range(nb):
+            for i in range(bounds[j], bounds[j + 1]):
+                enqueue(i)
+            ev[j + 1].record()
         torch.cuda.synchronize()
-        return es.elapsed_time(ee) / k
+        per = [ev[j].elapsed_time(ev[j + 1]) * 1e3 / max(bounds[j + 1] - bounds[j], 1) for j in range(nb)]
+        if key is not None:
+            dist[key] = dict(median=float(np.median(per)), p10=float(np.percentile(per, 10)),
+                             p90=float(np.percentile(per, 90)), blocks=nb)
+        return ev[0].elapsed_time(ev[nb]) / k
 
     # whole steps (plan + op), the measured quantity
     w0 = time.perf_counter()
-    ms_step = timed(rig.step, steps)
+    ms_step = timed(rig.step, steps, "step_us")
     wall_ms = (time.perf_counter() - w0) * 1e3
     # each kernel stage alone, back to back over the same rotating copies
     handles = [rig.build_plan(d) for d in rig.sets]
     torch.cuda.synchronize()
     nc = len(rig.sets)
-    op_mean = timed(lambda i: rig.run_op(rig.sets[i % nc], handles[i % nc]), steps) * 1e3
+    op_mean = timed(lambda i: rig.run_op(rig.sets[i % nc], handles[i % nc]), steps, "op_us") * 1e3
     gx_us = adam_us = bw_us = None
     if case.mask is not None and case.x_dtype == "bf16":
-        gx_us = timed(lambda i: rig.run_grad_x(rig.sets[i % nc], handles[i % nc]), steps) * 1e3
-        bw_us = timed(lambda i: rig.run_backward(rig.sets[i % nc], handles[i % nc]), steps) * 1e3
+        gx_us = timed(lambda i: rig.run_grad_x(rig.sets[i % nc], handles[i % nc]), steps, "grad_x_us") * 1e3
+        bw_us = timed(lambda i: rig.run_backward(rig.sets[i % nc], handles[i % nc]), steps, "backward_us") * 1e3
     if case.mask is not None:
-        adam_us = timed(lambda i: rig.run_adamw(rig.sets[i % nc]), steps) * 1e3
+        adam_us = timed(lambda i: rig.run_adamw(rig.sets[i % nc]), steps, "adamw_us") * 1e3
     loss_r = token_loss_leg(case, timed, steps) if case.mask is not None else None
+    lin_r = linear_leg(case, rig, handles[0], timed, steps) if cfg == 3 else None
     for h in handles:
         L.lib().lora_plan_destroy(h)
     plan_us = timed(lambda i: L.lib().lora_plan_destroy(rig.build_plan(rig.sets[i % nc])),
-                    steps) * 1e3
+                    steps, "plan_us") * 1e3
     r = dict(workload=case.name, config=cfg, copies=copies, steps=steps,
              ms_per_step=ms_step, tokens_per_s=case.n / (ms_step * 1e-3),
              op_us_mean=op_mean, plan_us_mean=plan_us,
@@ -379,6 +445,13 @@ def run_workload(cfg, steps, warmup, rate):
     r["mfma_frac_ceiling"] = min(1.0, (counts["flops"] / counts["op_bytes"]) * HBM_PEAK_GBS
                                  / 1e3 / peak_f)
     r["step_GBps"] = ws_bytes / (ms_step * 1e-3) / 1e9
+    r["timing_spread_us"] = dict(dist)
+    if lin_r is not None:
+        r["linear"] = lin_r
+        log(f"[bench]   lora_linear (X W^T + residual, {case.n} x {case.d_in} -> {case.d_out}): "
+            f"{lin_r['us_mean']:.1f} us, {lin_r['TFLOPs']:.0f} TFLOP/s = "
+            f"{100 * lin_r['mfma_frac']:.1f}% of bf16 peak; torch X W^T alone "
+            f"{lin_r['torch_xwt_us']:.1f} us")
     if loss_r is not None:
         r["token_loss"] = loss_r
         log(f"[bench]   lora_token_loss (PPO, {loss_r['rows']} rows, {loss_r['active_rows']} active, "
@@ -427,45 +500,116 @@ def run_workload(cfg, steps, warmup, rate):
 
 
 def calib_copy():
-    """A plain elementwise copy kernel of known size (read 1 GiB, write 1 GiB): its
-    counter readings scale the FETCH_SIZE / WRITE_SIZE counters to bytes."""
+    """A plain elementwise copy kernel of known size (read 1 GiB, write 1 GiB): the
+    achievable HBM rate on this machine, and the reading that scales the FETCH_SIZE
+    / WRITE_SIZE counters to bytes.  Best of 5."""
     import torch
     a = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
     b = torch.empty_like(a)
     a.fill_(1.0)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    torch.neg(a, out=b)
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1)
-    log(f"[bench] calibration copy (neg) 1 GiB: {ms:.3f} ms = {2 * (1 << 30) / ms / 1e6:.0f} GB/s")
-    return dict(bytes_read=1 << 30, bytes_written=1 << 30, ms=ms)
+    best = None
+    for _ in range(5):
+        e0.record()
+        torch.neg(a, out=b)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        best = ms if best is None else min(best, ms)
+    gbps = 2 * (1 << 30) / best / 1e6
+    log(f"[bench] calibration copy (neg) 1 GiB: {best:.3f} ms = {gbps:.0f} GB/s")
+    del a, b
+    torch.cuda.empty_cache()
+    return dict(bytes_read=1 << 30, bytes_written=1 << 30, ms=best, GBps=gbps)
+
+
+def calib_mfma():
+    """The library's register-only matrix-core loop (lora_calibrate_mfma), one
+    workgroup of 4 waves per CU: the achievable bf16 MFMA rate on this machine
+    (clock under a matrix-core load included).  Best of 3."""
+    import torch
+    import paper_2601_07376_amd as L
+    wgs, iters = 256, 20000
+    out = torch.empty(wgs * 256, dtype=torch.float32, device="cuda")
+    lib = L.lib()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    best = None
+    for _ in range(3):
+        e0.record()
+        st = lib.lora_calibrate_mfma(wgs, iters, out.data_ptr(),
+                                     ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+        assert st == 0, lib.lora_last_error()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        best = ms if best is None else min(best, ms)
+    flops = wgs * 4 * iters * 16 * 32768.0
+    tf = flops / (best * 1e-3) / 1e12
+    log(f"[bench] calibration matrix cores (register-only bf16 loop): {tf:.0f} TFLOP/s")
+    return dict(flops=flops, ms=best, TFLOPs=tf)
+
+
+def _oracle_pass(case):
+    """One pass of the float64 oracle over a whole batch: the plan and the
+    residual (forward workloads) or the masked gradients (backward workload)."""
+    import oracle
+    import workloads
+    dec = workloads.decode
+    X = dec(case.X, case.x_dtype)
+    A = [dec(a, case.w_dtype) if a is not None else None for a in case.A]
+    B = [dec(b, case.w_dtype) if b is not None else None for b in case.B]
+    if case.mask is None:
+        Y = dec(case.Y, case.y_dtype)
+
+        def run():
+            eff, _ = oracle.effective_ids(case.idx, case.num_slots, case.ranks)
+            oracle.canonical_plan(case.idx, case.num_slots, ranks=case.ranks)
+            oracle.apply(eff, X, Y, A, B, case.scales)
+    else:
+        dY = dec(case.dY, case.x_dtype)
+
+        def run():
+            eff, _ = oracle.effective_ids(case.idx, case.num_slots, case.ranks)
+            oracle.canonical_plan(case.idx, case.num_slots, mask=case.mask, ranks=case.ranks)
+            oracle.grad(eff, case.mask, X, dY, A, B, case.scales)
+    return run
+
+
+def _time_passes(run, seconds, min_reps=3):
+    times, t0 = [], time.perf_counter()
+    while len(times) < min_reps or time.perf_counter() - t0 < seconds:
+        a = time.perf_counter()
+        run()
+        times.append(time.perf_counter() - a)
+    return times
 
 
 def cpu_baseline(case, seconds):
-    """The float64 oracle on the host (plan + residual), on the whole headline batch."""
-    import oracle
-    from threadpoolctl import threadpool_info
+    """The float64 oracle on the host (plan + residual) on the whole headline
+    batch, for about `seconds` on every core BLAS uses; tokens/s from the median
+    pass (p10 / p90 beside it).  Then single-thread runs (BLAS limited to one
+    thread) of the tiny, decode and masked-backward workloads, about 2 s each."""
     import workloads
-    X = workloads.decode(case.X, case.x_dtype)
-    Y = workloads.decode(case.Y, case.y_dtype)
-    A = [workloads.decode(a, case.w_dtype) for a in case.A]
-    B = [workloads.decode(b, case.w_dtype) for b in case.B]
-    reps, t0 = 0, time.perf_counter()
-    while True:
-        eff, _ = oracle.effective_ids(case.idx, case.num_slots, case.ranks)
-        oracle.canonical_plan(case.idx, case.num_slots, ranks=case.ranks)
-        oracle.apply(eff, X, Y, A, B, case.scales)
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= seconds:
-            break
-    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
-    return dict(value=case.n * reps / el, unit="tokens/s", cores=int(threads), kind="oracle",
-                sample=f"{reps} passes of the full {case.name} batch ({case.n} rows): "
-                       f"plan + float64 residual, {el:.1f} s")
+    from threadpoolctl import threadpool_info, threadpool_limits
+    blas = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    affinity = len(os.sched_getaffinity(0))
+    times = _time_passes(_oracle_pass(case), seconds)
+    med = float(np.median(times))
+    one = {}
+    with threadpool_limits(limits=1):
+        for c in (1, 2, 5):
+            cs = case if c == HEADLINE else workloads.make_config(c)
+            t = _time_passes(_oracle_pass(cs), 2.0)
+            one[cs.name] = dict(tokens_per_s=cs.n / float(np.median(t)), passes=len(t),
+                                median_s=float(np.median(t)))
+    return dict(value=case.n / med, unit="tokens/s", cores=int(min(blas, affinity)), kind="oracle",
+                sample=f"{len(times)} passes of the full {case.name} batch ({case.n} rows): "
+                       f"plan + float64 residual, {sum(times):.1f} s; median pass",
+                blas_threads=int(blas), affinity_cores=int(affinity),
+                p10_tokens_per_s=case.n / float(np.percentile(times, 90)),
+                p90_tokens_per_s=case.n / float(np.percentile(times, 10)),
+                single_thread=one)
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_bgmv.lora_apply.hbm_counters.txt")
@@ -508,19 +652,26 @@ def main():
     if HEADLINE not in cfgs:
         cfgs = [HEADLINE] + cfgs
     rate = sleep_rate(torch)
+    calib = calib_copy()
+    calib_m = calib_mfma()
     results, head_case = {}, None
     for c in cfgs:
         r, case = run_workload(c, args.steps, args.warmup, rate)
         results[c] = r
         if c == HEADLINE:
             head_case = case
-    calib = calib_copy() if args.calib_copy else None
+    for r in results.values():
+        r["op_hbm_frac_of_copy"] = r["op_GBps"] / calib["GBps"]
+        r["op_mfma_frac_of_calibrated"] = r["op_TFLOPs"] / calib_m["TFLOPs"]
+        if "linear" in r:
+            r["linear"]["mfma_frac_of_calibrated"] = r["linear"]["TFLOPs"] / calib_m["TFLOPs"]
     h = results[HEADLINE]
     traffic = traffic_for(h)
     roof = dict(bound="hbm",
                 kernel="lora_apply on the decode batch (small_shrink_kernel + small_expand_kernel)",
                 achieved=round(h["op_GBps"], 1), peak=HBM_PEAK_GBS, unit="GB/s",
                 frac=round(h["op_hbm_frac"], 4), traffic=traffic,
+                frac_of_copy=round(h["op_hbm_frac_of_copy"], 4), copy_GBps=round(calib["GBps"], 1),
                 bytes_per_launch=h["op_bytes"], avg_launch_us=round(h["op_us_mean"], 3))
     cpu = None
     if not args.no_cpu_baseline:
@@ -545,7 +696,7 @@ def main():
         "roofline": roof,
         "cpu_baseline": cpu,
         "extra": {"workloads": [results[c] for c in cfgs], "calibration_copy": calib,
-                  "source_digest": source_digest()},
+                  "calibration_mfma": calib_m, "source_digest": source_digest()},
     }
     print(json.dumps(line), flush=True)
 

@@ -270,6 +270,15 @@ lora_status lora_linear(const lora_plan* p, const void* X, lora_dtype x_dtype, i
                         lora_dtype y_dtype, int64_t ldy, void* ws, size_t ws_bytes,
                         void* stream);
 
+/* ---- measurement utility (not part of the layer) ---------------------------
+ * A register-only loop of bf16 matrix-core products: `workgroups` x 4 waves,
+ * each running iters x 16 independent v_mfma_f32_32x32x16_bf16 (32768 flops
+ * each), so one call performs workgroups * 4 * iters * 16 * 32768 flops.  Its
+ * timed rate is the achieved matrix-core peak on the device (the benchmark's
+ * calibration).  out: device float [workgroups * 256] (receives the sums, so the
+ * products are not optimised away).  Errors: SHAPE, NULL, HIP. */
+lora_status lora_calibrate_mfma(int32_t workgroups, int32_t iters, float* out, void* stream);
+
 /* ---- backward (Sections 3.3 and 3.5: masked, adapter-local gradients) ----
  * For every slot a with dA[a] / dB[a] not NULL, over the rows T_a^m of the
  * plan's mask (mask == NULL at build time: every row of adapter a):

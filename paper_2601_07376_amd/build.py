@@ -15,7 +15,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "liblora_mi355x.so")
 SOURCES = ["plan.hip", "fwd_mfma.hip", "fwd_valu.hip", "grad.hip", "adamw.hip", "losses.hip",
-           "noalloc.hip", "linear.hip", "api.cpp"]
+           "noalloc.hip", "linear.hip", "calib.hip", "api.cpp"]
 ARCH = "gfx950"
 
 # Packed fp32 VALU instructions are disabled for all device code.

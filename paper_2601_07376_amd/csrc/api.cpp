@@ -766,6 +766,17 @@ lora_status lora_apply_noalloc(const lora_plan* p, const void* X, lora_dtype x_d
   return apply_impl(p, X, x_dtype, ldx, Y, y_dtype, ldy, ws, LORA_NOALLOC_SCRATCH_BYTES, stream, false);
 }
 
+// ---- measurement utility ------------------------------------------------------
+
+lora_status lora_calibrate_mfma(int32_t workgroups, int32_t iters, float* out, void* stream) {
+  if (workgroups < 1 || workgroups > (1 << 16) || iters < 1)
+    return fail(LORA_ERR_SHAPE, "workgroups %d / iters %d out of range", workgroups, iters);
+  if (out == nullptr) return fail(LORA_ERR_NULL, "out is NULL");
+  const hipError_t e = lora::launch_calib_mfma(workgroups, iters, out, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "calibration launch");
+  return ok();
+}
+
 // ---- the whole adapted layer ---------------------------------------------------
 
 // SHRINK_KS_MAX fp32 planes [n, pad8(r_max)], then the packed bf16 s_a H

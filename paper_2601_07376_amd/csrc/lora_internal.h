@@ -193,6 +193,10 @@ struct LinearLaunch {
   uint16_t* Hs;        // [n][2 linear_rank_cols(r_max)] bf16: the packed s_a H (rank multiple of 8)
 };
 int32_t linear_rank_cols(int32_t r_max);
+
+// register-only matrix-core loop (measurement utility): workgroups x 4 waves,
+// each iters x 16 v_mfma_f32_32x32x16_bf16; out: workgroups x 256 floats
+hipError_t launch_calib_mfma(int32_t workgroups, int32_t iters, float* out, hipStream_t s);
 hipError_t launch_linear_mfma(const OpLaunch& o, const LinearLaunch& l, hipStream_t s);
 
 // vector-ALU kernels for any mix of f32 / bf16 storage

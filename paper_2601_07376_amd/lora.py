@@ -49,6 +49,7 @@ SIGNATURES = {
     "lora_apply_noalloc": (_i32, [_vp, _vp, _i32, _i64, _vp, _i32, _i64, _vp]),
     "lora_linear_workspace_bytes": (_sz, [_vp]),
     "lora_linear": (_i32, [_vp, _vp, _i32, _i64, _vp, _i32, _i64, _vp, _i32, _i64, _vp, _sz, _vp]),
+    "lora_calibrate_mfma": (_i32, [_i32, _i32, _vp, _vp]),
     "lora_grad_workspace_bytes": (_sz, [_vp]),
     "lora_grad": (_i32, [_vp, _vp, _i32, _i64, _vp, _i32, _i64, _vp, _i64, _vp, _vp, _i32,
                          _vp, _sz, _vp]),
