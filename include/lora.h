@@ -160,7 +160,8 @@ lora_status lora_plan_build_segments(const lora_table* t, int32_t n, int32_t num
  * Errors: VALUE (a field outside its range), and those of lora_plan_build. */
 typedef struct lora_policy {
   int32_t small_max;     /* groups of <= small_max rows take the small-group kernels, >= 0
-                            (-1: every group when n <= 1024, else groups of <= 16 rows) */
+                            (-1: every group when n <= 1024; groups of <= 16 rows when
+                            n < 64 x num_slots; none otherwise) */
   int32_t small_split;   /* small groups: 0 = one fused kernel, 1 = shrink per d-slice + expand
                             (-1: split when d_in >= 1024) */
   int32_t split_slices;  /* d-slices of the split small-group shrink, 1..8 (-1: min(4, d_in / 256)) */
@@ -169,6 +170,8 @@ typedef struct lora_policy {
                             second stream (-1: when n < 64 x num_slots) */
   int32_t grad_splits;   /* most d-slices of the gradient's first stage, 1..8
                             (-1: ceil(min(d_in, d_out) / 512)) */
+  int32_t block_rows;    /* rows per block of the large groups, 64 or 256 (-1: 64 when
+                            n < 12288, else 256); only that size's kernels are launched */
 } lora_policy;
 void        lora_policy_init(lora_policy* q);
 lora_status lora_plan_build_policy(const lora_table* t, int32_t n, const int32_t* idx,

@@ -32,6 +32,7 @@ struct lora_plan {
   int32_t r_max;        // largest live rank when the plan was built
   bool rank8;           // every live rank is a multiple of 8
   int32_t small_max;    // groups of <= small_max rows use the fused small-group kernel
+  bool fine;            // large groups in blocks of RB_FINE rows (else RB_ROWS)
   lora_policy pol;      // path selection of the ops on this plan (-1 fields: library choice)
 };
 
@@ -86,17 +87,19 @@ lora_status check_policy(const lora_policy& q) {
                   (q.split_slices == -1 || (q.split_slices >= 1 && q.split_slices <= lora::SPLIT_SLICES_MAX)) &&
                   (q.small_chunks == -1 || (q.small_chunks >= 1 && q.small_chunks <= 16)) &&
                   q.fork >= -1 && q.fork <= 1 &&
-                  (q.grad_splits == -1 || (q.grad_splits >= 1 && q.grad_splits <= lora::GRAD_SPLITS_MAX));
+                  (q.grad_splits == -1 || (q.grad_splits >= 1 && q.grad_splits <= lora::GRAD_SPLITS_MAX)) &&
+                  (q.block_rows == -1 || q.block_rows == lora::RB_FINE || q.block_rows == lora::RB_ROWS);
   if (!ok)
     return fail(LORA_ERR_VALUE, "policy field out of range (small_max %d, small_split %d, split_slices %d, "
-                "small_chunks %d, fork %d, grad_splits %d)", q.small_max, q.small_split, q.split_slices,
-                q.small_chunks, q.fork, q.grad_splits);
+                "small_chunks %d, fork %d, grad_splits %d, block_rows %d)", q.small_max, q.small_split,
+                q.split_slices, q.small_chunks, q.fork, q.grad_splits, q.block_rows);
   return LORA_OK;
 }
 
 lora_policy default_policy() {
   lora_policy q;
   q.small_max = q.small_split = q.split_slices = q.small_chunks = q.fork = q.grad_splits = -1;
+  q.block_rows = -1;
   return q;
 }
 
@@ -106,15 +109,14 @@ int32_t ub_large(const lora_plan* p) {
   const int32_t S = p->table->num_slots, n = p->n;
   return n / lora::RB_FINE + std::min(S, n / (p->small_max + 1)) + 1;   // either block size
 }
-// ... of a plan that chose RB_ROWS blocks, and of one that chose RB_FINE blocks
-// (it does so only below FINE_BELOW coarse blocks, and a group's fine blocks
-// are at most four times its coarse ones)
+// ... in the block size the plan uses, and 0 for the other one: the grouped
+// launches of that size are skipped
 int32_t ub_coarse(const lora_plan* p) {
-  if (p->small_max == INT32_MAX) return 0;
+  if (p->small_max == INT32_MAX || p->fine) return 0;
   const int32_t S = p->table->num_slots, n = p->n;
   return n / lora::RB_ROWS + std::min(S, n / (p->small_max + 1)) + 1;
 }
-int32_t ub_fine(const lora_plan* p) { return std::min(ub_large(p), 4 * lora::FINE_BELOW); }
+int32_t ub_fine(const lora_plan* p) { return p->fine ? ub_large(p) : 0; }
 int32_t ub_small(const lora_plan* p) {
   const int32_t S = p->table->num_slots, n = p->n;
   const int64_t all = n / lora::SMALL_ROWS + std::min(S, n) + 1;
@@ -216,7 +218,8 @@ lora_status make_plan(const lora_table* t, int32_t n, const int32_t* idx,
     p->rank8 = p->rank8 && (s.rank % 8 == 0);
   }
   p->pol = pol;
-  p->small_max = pol.small_max >= 0 ? pol.small_max : lora::small_max_policy(n);
+  p->small_max = pol.small_max >= 0 ? pol.small_max : lora::small_max_policy(n, t->num_slots);
+  p->fine = pol.block_rows >= 0 ? pol.block_rows == lora::RB_FINE : lora::fine_policy(n);
 
   lora::PlanLaunch a{};
   a.d = p->d;
@@ -229,6 +232,7 @@ lora_status make_plan(const lora_table* t, int32_t n, const int32_t* idx,
   a.n = n;
   a.num_slots = t->num_slots;
   a.small_max = p->small_max;
+  a.fine = p->fine ? 1 : 0;
   hipError_t e = lora::launch_plan(a, stream);
   if (e != hipSuccess) {
     delete p;
@@ -245,7 +249,19 @@ namespace lora {
 // Small-group policy.  Batches of up to 1024 rows (decode steps) send every
 // adapter group through the small-group kernels; larger batches send groups of
 // up to 16 rows there and larger groups through the grouped shrink + expand.
-int32_t small_max_policy(int32_t n) { return n <= 1024 ? INT32_MAX : SMALL_ROWS; }
+// Small-group path: every group of a batch of at most 1024 rows; groups of at
+// most SMALL_ROWS rows while the batch has fewer than 4 SMALL_ROWS rows per
+// slot (many small groups are then likely, and they run beside the large ones
+// on the second stream); none otherwise, where a few small groups cost less as
+// blocks of the grouped kernels than two more launches.
+int32_t small_max_policy(int32_t n, int32_t S) {
+  if (n <= 1024) return INT32_MAX;
+  return (int64_t)n < (int64_t)4 * SMALL_ROWS * S ? SMALL_ROWS : 0;
+}
+// Large-group blocks of RB_FINE rows below FINE_BELOW coarse blocks' worth of
+// rows (RB_ROWS blocks could not cover the chip), else RB_ROWS.  Chosen on the
+// host, so only the grouped kernels of that block size are launched.
+bool fine_policy(int32_t n) { return (int64_t)n < (int64_t)FINE_BELOW * RB_ROWS; }
 
 // Gradient workspace: fp32 partial planes (two per d-slice) and the summed bf16
 // hi / lo planes.
@@ -581,8 +597,8 @@ lora_status lora_shrink(const lora_plan* p, const void* X, lora_dtype x_dtype, i
   o.count_word = lora::HDR_NRB_TOTAL;
   o.first_word = -1;
   o.rb_ub = ub_large(p) + ub_small(p);
-  o.coarse_ub = ub_coarse(p) + ub_small(p);
-  o.fine_ub = ub_fine(p) + ub_small(p);
+  o.coarse_ub = p->fine ? 0 : ub_coarse(p) + ub_small(p);
+  o.fine_ub = p->fine ? ub_fine(p) + ub_small(p) : 0;
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e;
   if (x_dtype == LORA_BF16 && t->w_dtype == LORA_BF16)
@@ -605,8 +621,8 @@ lora_status lora_expand(const lora_plan* p, const float* H, int64_t ldh, void* Y
   o.count_word = lora::HDR_NRB_TOTAL;
   o.first_word = -1;
   o.rb_ub = ub_large(p) + ub_small(p);
-  o.coarse_ub = ub_coarse(p) + ub_small(p);
-  o.fine_ub = ub_fine(p) + ub_small(p);
+  o.coarse_ub = p->fine ? 0 : ub_coarse(p) + ub_small(p);
+  o.fine_ub = p->fine ? ub_fine(p) + ub_small(p) : 0;
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e;
   if (t->w_dtype == LORA_BF16)
@@ -685,7 +701,8 @@ lora_status apply_impl(const lora_plan* p, const void* X, lora_dtype x_dtype, in
     std::unique_lock<std::mutex> lk(g_aux_mutex, std::defer_lock);
     AuxStream* aux = nullptr;
     hipStream_t s_small = s;
-    if (allow_fork && ub_large(p) > 0 && fork_policy(p)) {
+    const bool has_small = p->small_max > 0;     // else the plan has no small group
+    if (allow_fork && has_small && ub_large(p) > 0 && fork_policy(p)) {
       lk.lock();
       aux = aux_stream(s);
       if (aux != nullptr) {
@@ -696,7 +713,7 @@ lora_status apply_impl(const lora_plan* p, const void* X, lora_dtype x_dtype, in
         lk.unlock();
       }
     }
-    {
+    if (has_small) {
       lora::OpLaunch os = o;
       os.count_word = lora::HDR_NSMALL;
       os.first_word = -1;
@@ -829,8 +846,8 @@ lora_status lora_linear(const lora_plan* p, const void* X, lora_dtype x_dtype, i
     os.count_word = lora::HDR_NRB_TOTAL;
     os.first_word = -1;
     os.rb_ub = ub_large(p) + ub_small(p);
-    os.coarse_ub = ub_coarse(p) + ub_small(p);
-    os.fine_ub = ub_fine(p) + ub_small(p);
+    os.coarse_ub = p->fine ? 0 : ub_coarse(p) + ub_small(p);
+    os.fine_ub = p->fine ? ub_fine(p) + ub_small(p) : 0;
     e = lora::launch_shrink_mfma(os, X, ldx, H, ldh, lora::SHRINK_KS_MAX, plane, s);
     if (e != hipSuccess) return hip_fail(e, "linear shrink launch");
   }

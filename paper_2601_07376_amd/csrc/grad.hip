@@ -181,6 +181,35 @@ __device__ __forceinline__ void rows_times_w2(f32x4 (&acc_h)[MT * NT], f32x4 (&a
   mfma_fence();
 }
 
+// Sum the four waves' accumulators in the fixed order ((w0 + w2) + (w1 + w3)),
+// leaving the total in wave 0: waves 1-3 park CH accumulators at a time in
+// s_red (3 x CH x 64 f32x4), one barrier per chunk.  The first barrier also
+// orders this tile's writes after the previous tile's reads of s_red.
+template <int N, int CH>
+__device__ __forceinline__ void reduce_waves3(f32x4 (&acc)[N], f32x4* s_red) {
+  const int lane = threadIdx.x & 63, w = wave_id();
+#pragma unroll
+  for (int c0 = 0; c0 < N; c0 += CH) {
+    __syncthreads();
+    if (w > 0) {
+#pragma unroll
+      for (int i = 0; i < CH; ++i)
+        if (c0 + i < N) s_red[((w - 1) * CH + i) * 64 + lane] = acc[c0 + i];
+    }
+    __syncthreads();
+    if (w == 0) {
+#pragma unroll
+      for (int i = 0; i < CH; ++i)
+        if (c0 + i < N) {
+          const f32x4 a1 = s_red[(0 * CH + i) * 64 + lane];
+          const f32x4 a2 = s_red[(1 * CH + i) * 64 + lane];
+          const f32x4 a3 = s_red[(2 * CH + i) * 64 + lane];
+          acc[c0 + i] = (acc[c0 + i] + a2) + (a1 + a3);
+        }
+    }
+  }
+}
+
 #ifndef HG_U
 #define HG_U 1
 #endif
@@ -191,7 +220,7 @@ __global__ __launch_bounds__(256) void hg_kernel(GradArgs g) {
   constexpr bool DB = NT <= 4;                           // double-buffered rounds
   constexpr int N = 2 * MT * NT, CH = N < 16 ? N : 16;
   constexpr int OS = MRB_ROWS + 1;                       // LDS row stride of the plane tile
-  constexpr int RED = 2 * CH * 64, OUT = (NT * 16 * OS + 3) / 4;
+  constexpr int RED = 3 * CH * 64, PL = NT * 16 * OS, OUT = (2 * PL + 3) / 4;
   __shared__ f32x4 s_red[RED > OUT ? RED : OUT];
   const int lane = threadIdx.x & 63, w = wave_id();
   const int n_blocks = g.hdr[HDR_NMRB];
@@ -237,15 +266,15 @@ __global__ __launch_bounds__(256) void hg_kernel(GradArgs g) {
       rows_times_w2<MT, NT, U, DB>(acc_h, acc_g, xrow, Aw, arow, kb, ke, yrow, Bw, brow, ob, oe, r);
     }
     vmem_drained();
-    reduce_waves<N, CH>(acc, s_red);
-    // wave 0 holds the totals; each plane's tile [j][64 columns] is staged in
-    // LDS and leaves as whole 256-byte row pieces
+    reduce_waves3<N, CH>(acc, s_red);
+    // wave 0 holds the totals; both planes' tiles [j][64 columns] are staged
+    // in LDS together and leave as whole 256-byte row pieces (one barrier, so
+    // no wave waits for the first plane's stores)
     float* s_o = reinterpret_cast<float*>(s_red);
     const int col0 = e * MRB_ROWS;
+    if (w == 0) {
 #pragma unroll
-    for (int which = 0; which < 2; ++which) {
-      __syncthreads();
-      if (w == 0) {
+      for (int which = 0; which < 2; ++which)
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -253,15 +282,17 @@ __global__ __launch_bounds__(256) void hg_kernel(GradArgs g) {
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
               const int i = mt * 16 + (lane >> 4) * 4 + v, j = nt * 16 + (lane & 15);
-              s_o[j * OS + i] = i < rows ? acc[which * MT * NT + mt * NT + nt][v] : 0.0f;
+              s_o[which * PL + j * OS + i] = i < rows ? acc[which * MT * NT + mt * NT + nt][v] : 0.0f;
             }
-      }
-      __syncthreads();
+    }
+    __syncthreads();
+#pragma unroll
+    for (int which = 0; which < 2; ++which) {
       if (which == 1 || g.H_saved == nullptr) {
         float* pl = plane(g, which, ks);
         for (int q = threadIdx.x; q < g.r_pad * (MRB_ROWS / 4); q += 256) {
           const int j = q / (MRB_ROWS / 4), c4 = (q - j * (MRB_ROWS / 4)) * 4;
-          const float* so = s_o + j * OS + c4;
+          const float* so = s_o + which * PL + j * OS + c4;
           stg_f4(pl + (int64_t)j * g.p_stride + col0 + c4, make_float4(so[0], so[1], so[2], so[3]));
         }
       }

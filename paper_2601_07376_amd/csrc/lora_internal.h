@@ -35,7 +35,7 @@ enum : int {
 };
 
 constexpr int RB_ROWS = 256;     // rows per large-group row block
-constexpr int RB_FINE = 64;      // ... when the batch has fewer than FINE_BELOW such blocks
+constexpr int RB_FINE = 64;      // ... when the batch has fewer than FINE_BELOW x RB_ROWS rows
 constexpr int FINE_BELOW = 48;
 constexpr int SHRINK_KS_MAX = 4; // most d-slices of the grouped shrink inside lora_apply
 constexpr int SMALL_ROWS = 16;   // rows per small-group entry (one matrix-core column tile)
@@ -99,8 +99,10 @@ struct PlanDev {
 // looked up once per device: the device of `stream` (NULL: the current one).
 hipError_t noalloc_scratch(hipStream_t stream, void** out);
 
-// Groups of at most this many rows take the fused small-group path.
-int32_t small_max_policy(int32_t n);
+// Groups of at most this many rows take the fused small-group path, and the
+// large-group block size (true: RB_FINE rows) of a batch of n rows over S slots.
+int32_t small_max_policy(int32_t n, int32_t S);
+bool fine_policy(int32_t n);
 PlanLayout plan_layout(int32_t n, int32_t num_slots);
 
 // ---- launchers (defined in the .hip files) --------------------------------
@@ -115,6 +117,7 @@ struct PlanLaunch {
   const SlotMeta* meta;
   int32_t n, num_slots;
   int32_t small_max;            // groups with <= small_max rows go to the fused small-group path
+  int32_t fine;                 // large-group blocks of RB_FINE rows (else RB_ROWS)
 };
 hipError_t launch_plan(const PlanLaunch& a, hipStream_t s);
 

@@ -319,8 +319,8 @@ __global__ __launch_bounds__(PLAN_THREADS) void plan_kernel(PlanLaunch a) {
   const int pf = block_excl_scan(nbf, s_wsum, tot_f);
   const int ps = block_excl_scan(nbs, s_wsum, tot_s);
   const int pm = block_excl_scan(nbm, s_wsum, tot_m);
-  // block size of the whole batch: fine blocks when coarse ones are too few
-  const bool fine = tot_c < FINE_BELOW;
+  // block size of the whole batch, chosen on the host (the launches follow it)
+  const bool fine = a.fine != 0;
   const int rbr = fine ? RB_FINE : RB_ROWS, nbl = fine ? nbf : nbc, pl = fine ? pf : pc;
   const int tot_l = fine ? tot_f : tot_c;
   for (int i = 0; i < nbl; ++i)
@@ -567,8 +567,8 @@ __global__ __launch_bounds__(T) void plan_small_kernel(PlanLaunch a) {
     tot[hi] = (int)((unsigned)ptot[i] >> 16);
   }
   const int off = v[0], moff = v[1], ps = v[3], pm = v[4];
-  // block size of the whole batch: fine blocks when coarse ones are too few
-  const bool fine = tot[2] < FINE_BELOW;
+  // block size of the whole batch, chosen on the host (the launches follow it)
+  const bool fine = a.fine != 0;
   const int rbr = fine ? RB_FINE : RB_ROWS, nbl = fine ? nbf : nbc, pl = fine ? v[7] : v[2];
   const int tot_l = fine ? tot[7] : tot[2];
   if (live) {
@@ -865,8 +865,8 @@ __global__ __launch_bounds__(PLAN_THREADS) void plan_scatter_kernel(PlanLaunch a
   int tot[8];
   block_scan_n<8>(v, tot, s_w);            // (barriers inside: s_misc is visible after it)
   const int off = v[0], moff = v[1], ps = v[3], pm = v[4];
-  // block size of the whole batch: fine blocks when coarse ones are too few
-  const bool fine = tot[2] < FINE_BELOW;
+  // block size of the whole batch, chosen on the host (the launches follow it)
+  const bool fine = a.fine != 0;
   const int rbr = fine ? RB_FINE : RB_ROWS, nbl = fine ? nbf : nbc, pl = fine ? v[7] : v[2];
   const int tot_l = fine ? tot[7] : tot[2];
   if (live) {

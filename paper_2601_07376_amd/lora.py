@@ -129,7 +129,8 @@ class Policy(ctypes.Structure):
     -1 keeps the library's choice."""
     _fields_ = [("small_max", ctypes.c_int32), ("small_split", ctypes.c_int32),
                 ("split_slices", ctypes.c_int32), ("small_chunks", ctypes.c_int32),
-                ("fork", ctypes.c_int32), ("grad_splits", ctypes.c_int32)]
+                ("fork", ctypes.c_int32), ("grad_splits", ctypes.c_int32),
+                ("block_rows", ctypes.c_int32)]
 
     def __init__(self, **kw):
         super().__init__()

@@ -108,6 +108,7 @@ def test_plan_build_validation():
 @pytest.mark.parametrize("field,value", [
     ("small_max", -2), ("small_split", 2), ("split_slices", 0), ("split_slices", 9),
     ("small_chunks", 17), ("fork", 3), ("grad_splits", 0), ("grad_splits", 9),
+    ("block_rows", 0), ("block_rows", 128),
 ])
 def test_plan_policy_validation(field, value):
     """A path policy outside its documented range is refused on the host

@@ -101,6 +101,23 @@ def test_apply_integer_exact(small):
     assert np.array_equal(workloads.decode(Yo, "f32"), ref)
 
 
+@pytest.mark.parametrize("small", [None, 16])
+@pytest.mark.parametrize("block_rows", [64, 256])
+def test_apply_block_rows(block_rows, small):
+    """Both large-group block sizes (the host picks one and launches only its
+    kernels) give the oracle's result bit for bit on integer-exact values, with
+    and without a small-group path beside them; ragged groups span several
+    blocks of either size."""
+    say(f"apply block_rows={block_rows} small={small}")
+    case = workloads.random_case(5, 3000, 256, 520, 40, rank_choices=(8, 16, 32, 64),
+                                 layout="segments", seg_len=(1, 700), y_dtype="f32",
+                                 int_values=True)
+    Yo, _ = run_apply(case, policy=dict(block_rows=block_rows, small_max=small))
+    X, A, B, Y, _ = f64_case(case)
+    ref = oracle.apply(effective(case), X, Y, A, B, case.scales)
+    assert np.array_equal(workloads.decode(Yo, "f32"), ref)
+
+
 def test_segments_plan_equals_index_plan():
     say("segments == indices")
     case = workloads.make_config(5)        # segment layout, 8 adapters
