@@ -52,6 +52,7 @@ BF16_PEAK_TFLOPS = 2500.0      # dense bf16 matrix cores
 FP32_PEAK_TFLOPS = 157.3       # vector fp32
 ROTATE_BYTES = 576 << 20       # >= 2 x 288 MB of rotating working set
 HEADLINE = 2
+IDS_MAX_ROWS = 1024            # lora_apply_ids row limit (LORA_APPLY_IDS_MAX_ROWS)
 
 
 def log(msg):
@@ -130,6 +131,10 @@ class Rig:
         import paper_2601_07376_amd as L
         from workloads.device import case_to_device
         self.case, self.L, self.torch = case, L, torch
+        # small bf16 forward batches run plan-free (lora_apply_ids: the kernels
+        # group the rows by adapter themselves, two launches per step)
+        self.plan_free = (case.mask is None and case.x_dtype == "bf16" and case.w_dtype == "bf16"
+                          and case.n <= IDS_MAX_ROWS and case.seg_offsets is None)
         base = case_to_device(case, "cuda")
         wdt = torch.bfloat16 if case.w_dtype == "bf16" else torch.float32
         self.sets = []
@@ -157,6 +162,8 @@ class Rig:
                 probe = L.Plan(table, idx=d["idx"], mask=d["mask"])
             if case.mask is None:
                 d["op_ws"] = L.apply_workspace(probe)
+                if self.plan_free:
+                    d["ids_ws"] = L.apply_ids_workspace(table, n)
             else:
                 d["op_ws"] = L.grad_workspace(probe)
                 d["dA"] = [torch.zeros(int(r_), case.d_in, dtype=torch.float32, device="cuda")
@@ -231,6 +238,23 @@ class Rig:
                                d["op_ws"].data_ptr(), d["op_ws"].numel(), stream)
         assert st == 0, lib.lora_last_error()
 
+    def run_ids(self, d):
+        """Enqueue lora_apply_ids (no plan) for one copy."""
+        lib = self.L.lib()
+        stream = ctypes.c_void_p(self.torch.cuda.current_stream().cuda_stream)
+        X, Y = d["X"], d["Y"]
+        st = lib.lora_apply_ids(d["table"].handle, self.case.n, d["idx"].data_ptr(), X.data_ptr(), 1,
+                                X.stride(0), Y.data_ptr(), 1 if self.case.y_dtype == "bf16" else 0,
+                                Y.stride(0), d["ids_ws"].data_ptr(), d["ids_ws"].numel(), stream)
+        assert st == 0, lib.lora_last_error()
+
+    def step_with_plan(self, i):
+        """Enqueue one step through a plan: plan build, then the op."""
+        d = self.sets[i % len(self.sets)]
+        h = self.build_plan(d)
+        self.run_op(d, h)
+        self.L.lib().lora_plan_destroy(h)   # host object only; enqueued work keeps its arguments
+
     def run_grad_x(self, d, h):
         """Enqueue the input gradient dX += s dY B A over the masked rows for one copy."""
         lib = self.L.lib()
@@ -260,11 +284,12 @@ class Rig:
         assert st == 0, lib.lora_last_error()
 
     def step(self, i):
-        """Enqueue one step on the current stream: plan build, then the op."""
-        d = self.sets[i % len(self.sets)]
-        h = self.build_plan(d)
-        self.run_op(d, h)
-        self.L.lib().lora_plan_destroy(h)   # host object only; enqueued work keeps its arguments
+        """Enqueue one step on the current stream: lora_apply_ids for a
+        plan-free batch, else plan build then the op."""
+        if self.plan_free:
+            self.run_ids(self.sets[i % len(self.sets)])
+        else:
+            self.step_with_plan(i)
 
 
 LOSS_VOCAB = 32768
@@ -417,7 +442,16 @@ def run_workload(cfg, steps, warmup, rate):
     handles = [rig.build_plan(d) for d in rig.sets]
     torch.cuda.synchronize()
     nc = len(rig.sets)
-    op_mean = timed(lambda i: rig.run_op(rig.sets[i % nc], handles[i % nc]), steps, "op_us") * 1e3
+    if rig.plan_free:
+        op_mean = timed(lambda i: rig.run_ids(rig.sets[i % nc]), steps, "op_us") * 1e3
+        # the same batch through a plan (plan build + lora_apply), for context
+        with_plan = dict(
+            step_us=timed(rig.step_with_plan, steps, "plan_path_step_us") * 1e3,
+            op_us=timed(lambda i: rig.run_op(rig.sets[i % nc], handles[i % nc]), steps,
+                        "plan_path_op_us") * 1e3)
+    else:
+        op_mean = timed(lambda i: rig.run_op(rig.sets[i % nc], handles[i % nc]), steps, "op_us") * 1e3
+        with_plan = None
     gx_us = adam_us = bw_us = None
     if case.mask is not None and case.x_dtype == "bf16":
         gx_us = timed(lambda i: rig.run_grad_x(rig.sets[i % nc], handles[i % nc]), steps, "grad_x_us") * 1e3
@@ -433,7 +467,8 @@ def run_workload(cfg, steps, warmup, rate):
     r = dict(workload=case.name, config=cfg, copies=copies, steps=steps,
              ms_per_step=ms_step, tokens_per_s=case.n / (ms_step * 1e-3),
              op_us_mean=op_mean, plan_us_mean=plan_us,
-             op=("lora_grad" if case.mask is not None else "lora_apply"),
+             op=("lora_grad" if case.mask is not None
+                 else "lora_apply_ids" if rig.plan_free else "lora_apply"),
              wall_ms_incl_gate=wall_ms, host_enqueue_ms_per_step=host_ms,
              **counts)
     r["op_GBps"] = counts["op_bytes"] / (op_mean * 1e-6) / 1e9
@@ -446,6 +481,11 @@ def run_workload(cfg, steps, warmup, rate):
                                  / 1e3 / peak_f)
     r["step_GBps"] = ws_bytes / (ms_step * 1e-3) / 1e9
     r["timing_spread_us"] = dict(dist)
+    if with_plan is not None:
+        with_plan["plan_us"] = plan_us
+        r["plan_path"] = with_plan
+        log(f"[bench]   through a plan: plan {plan_us:.2f} us + lora_apply {with_plan['op_us']:.2f} us; "
+            f"step {with_plan['step_us']:.2f} us")
     if lin_r is not None:
         r["linear"] = lin_r
         log(f"[bench]   lora_linear (X W^T + residual, {case.n} x {case.d_in} -> {case.d_out}): "
@@ -490,7 +530,7 @@ def run_workload(cfg, steps, warmup, rate):
                           hbm_frac=ab / (adam_us * 1e-6) / 1e9 / HBM_PEAK_GBS)
         log(f"[bench]   lora_adamw_step ({r['adamw']['tensors']} tensors, {el} elements): "
             f"{adam_us:.2f} us, {r['adamw']['GBps']:.0f} GB/s = {100 * r['adamw']['hbm_frac']:.1f}% HBM")
-    log(f"[bench]   plan {plan_us:.2f} us; {r['op']}: {op_mean:.2f} us, "
+    log(f"[bench]   {'(no plan)' if rig.plan_free else f'plan {plan_us:.2f} us;'} {r['op']}: {op_mean:.2f} us, "
         f"{r['op_GBps']:.0f} GB/s = {100 * r['op_hbm_frac']:.1f}% HBM, "
         f"{r['op_TFLOPs']:.1f} TFLOP/s; step {ms_step * 1e3:.2f} us, "
         f"{r['tokens_per_s']:.3e} tokens/s")
@@ -668,7 +708,9 @@ def main():
     h = results[HEADLINE]
     traffic = traffic_for(h)
     roof = dict(bound="hbm",
-                kernel="lora_apply on the decode batch (small_shrink_kernel + small_expand_kernel)",
+                kernel=("lora_apply_ids on the decode batch (ids_shrink_kernel + ids_expand_kernel)"
+                        if h["op"] == "lora_apply_ids" else
+                        "lora_apply on the decode batch (small_shrink_kernel + small_expand_kernel)"),
                 achieved=round(h["op_GBps"], 1), peak=HBM_PEAK_GBS, unit="GB/s",
                 frac=round(h["op_hbm_frac"], 4), traffic=traffic,
                 frac_of_copy=round(h["op_hbm_frac_of_copy"], 4), copy_GBps=round(calib["GBps"], 1),

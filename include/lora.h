@@ -248,6 +248,29 @@ lora_status lora_apply(const lora_plan* p, const void* X, lora_dtype x_dtype, in
 lora_status lora_apply_noalloc(const lora_plan* p, const void* X, lora_dtype x_dtype, int64_t ldx,
                                void* Y, lora_dtype y_dtype, int64_t ldy, void* stream);
 
+/* lora_apply_ids: lora_apply for a small batch without a plan (the decode
+ * step of Section 3.4: every row's adapter residual with its rows grouped by
+ * adapter, here inside the kernels).  Two launches and nothing before them:
+ * a shrink per (slot, d-slice) into the workspace's partial H planes and an
+ * expand per (slot, output-column chunk); each workgroup finds the rows
+ * T_a = {t : idx[t] = a} of its slot by scanning idx (ascending t).  Y[t] +=
+ * s_a (X[t] A_a^T) B_a^T for every row whose id names a slot with an adapter;
+ * rows with id -1, an id outside [-1, num_slots) or an id of an empty slot are
+ * left unchanged (as lora_apply treats them; lora_plan_build and
+ * lora_plan_export report such ids).  Arithmetic and result: those of
+ * lora_apply's split small-group path.  idx: device int32 [n], 4-byte aligned;
+ * 0 <= n <= LORA_APPLY_IDS_MAX_ROWS.  X bfloat16 [n, ldx], weights bfloat16
+ * (else LORA_ERR_DTYPE); Y float32 or bfloat16 [n, ldy], updated in place.
+ * ws: device, lora_apply_ids_workspace_bytes(t, n) bytes (0 when n = 0 or no
+ * slot holds an adapter), 16-byte aligned.  The table's metadata must have been
+ * uploaded.  Errors: NULL, SHAPE (n out of range), DTYPE, ALIGN, WORKSPACE,
+ * HIP; nothing is enqueued on an error. */
+#define LORA_APPLY_IDS_MAX_ROWS 1024
+size_t      lora_apply_ids_workspace_bytes(const lora_table* t, int32_t n);
+lora_status lora_apply_ids(const lora_table* t, int32_t n, const int32_t* idx, const void* X,
+                           lora_dtype x_dtype, int64_t ldx, void* Y, lora_dtype y_dtype,
+                           int64_t ldy, void* ws, size_t ws_bytes, void* stream);
+
 /* ---- the whole adapted layer (Section 3.4: LoRA layer equation, with the
  *      base projection shared by every row and the residual added per group) --
  *   Y[t, :] = X[t, :] W^T + s_a (X[t, :] A_a^T) B_a^T     for a row with adapter a,

@@ -766,6 +766,81 @@ lora_status lora_apply(const lora_plan* p, const void* X, lora_dtype x_dtype, in
   return apply_impl(p, X, x_dtype, ldx, Y, y_dtype, ldy, ws, ws_bytes, stream, true);
 }
 
+// ---- plan-free small batch -------------------------------------------------
+
+namespace {
+// live rank bound and d-slices of lora_apply_ids (from the table's host copy of
+// the slot metadata, as lora_plan_build takes them)
+struct IdsShape {
+  int32_t r_max;
+  bool rank8;
+  int32_t slices;
+  int64_t ldp;          // row stride of the partial planes: 16 x rank tiles
+};
+IdsShape ids_shape(const lora_table* t) {
+  IdsShape q{0, true, 1, 16};
+  for (const auto& s : t->host) {
+    if (s.rank <= 0) continue;
+    q.r_max = std::max(q.r_max, s.rank);
+    q.rank8 = q.rank8 && (s.rank % 8 == 0);
+  }
+  const int nt = (std::max(q.r_max, 1) + 15) / 16;
+  q.ldp = 16 * (nt <= 1 ? 1 : nt <= 2 ? 2 : nt <= 4 ? 4 : 8);
+  q.slices = std::max(1, std::min(lora::SPLIT_SLICES_MAX, std::min(4, t->d_in / 256)));
+  return q;
+}
+}  // namespace
+
+size_t lora_apply_ids_workspace_bytes(const lora_table* t, int32_t n) {
+  if (t == nullptr || n <= 0 || n > LORA_APPLY_IDS_MAX_ROWS) return 0;
+  const IdsShape q = ids_shape(t);
+  if (q.r_max == 0) return 0;
+  return al256((size_t)q.slices * (size_t)n * (size_t)q.ldp * 4);
+}
+
+lora_status lora_apply_ids(const lora_table* t, int32_t n, const int32_t* idx, const void* X,
+                           lora_dtype x_dtype, int64_t ldx, void* Y, lora_dtype y_dtype,
+                           int64_t ldy, void* ws, size_t ws_bytes, void* stream) {
+  if (t == nullptr) return fail(LORA_ERR_NULL, "table is NULL");
+  if (n < 0 || n > LORA_APPLY_IDS_MAX_ROWS)
+    return fail(LORA_ERR_SHAPE, "lora_apply_ids: n = %d outside [0, %d]", n, LORA_APPLY_IDS_MAX_ROWS);
+  lora_status st;
+  if ((st = check_matrix(X, x_dtype, ldx, t->d_in, "X", n)) != LORA_OK) return st;
+  if ((st = check_matrix(Y, y_dtype, ldy, t->d_out, "Y", n)) != LORA_OK) return st;
+  if (x_dtype != LORA_BF16 || t->w_dtype != LORA_BF16)
+    return fail(LORA_ERR_DTYPE, "lora_apply_ids needs bfloat16 X and adapter weights");
+  if (n > 0 && idx == nullptr) return fail(LORA_ERR_NULL, "idx is NULL");
+  if (idx != nullptr && !aligned(idx, 4)) return fail(LORA_ERR_ALIGN, "idx not 4-byte aligned");
+  const size_t need = lora_apply_ids_workspace_bytes(t, n);
+  if (need > 0) {
+    if (ws == nullptr) return fail(LORA_ERR_NULL, "apply_ids workspace is NULL");
+    if (!aligned(ws, 16)) return fail(LORA_ERR_ALIGN, "apply_ids workspace not 16-byte aligned");
+    if (ws_bytes < need) return fail(LORA_ERR_WORKSPACE, "apply_ids workspace %zu bytes < %zu", ws_bytes, need);
+  }
+  const IdsShape q = ids_shape(t);
+  if (n == 0 || q.r_max == 0) return ok();
+  lora::IdsLaunch l{};
+  l.meta = static_cast<const lora::SlotMeta*>(t->dev_meta);
+  l.num_slots = t->num_slots;
+  l.d_in = t->d_in;
+  l.d_out = t->d_out;
+  l.r_max = q.r_max;
+  l.rank8 = q.rank8;
+  l.y_bf16 = y_dtype == LORA_BF16;
+  l.ids = idx;
+  l.n = n;
+  l.X = X;
+  l.ldx = ldx;
+  l.Y = Y;
+  l.ldy = ldy;
+  l.H = static_cast<float*>(ws);
+  l.slices = q.slices;
+  l.n_chunks = std::max(1, std::min(16, (t->d_out + 1023) / 1024));
+  const hipError_t e = lora::launch_ids_mfma(l, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "apply_ids launch");
+  return ok();
+}
+
 lora_status lora_apply_noalloc(const lora_plan* p, const void* X, lora_dtype x_dtype, int64_t ldx,
                                void* Y, lora_dtype y_dtype, int64_t ldy, void* stream) {
   lora_status st = check_plan(p);

@@ -53,6 +53,9 @@ struct FwdArgs {
   int64_t hp_stride;        // elements between partial H planes
   int32_t cw;               // expand column chunk (0: chosen from the block count)
   int32_t force_fine;       // run the 64-row kernels whatever the plan chose (input gradient)
+  const int32_t* ids;       // plan-free small batch: per-row slot ids [n_ids]
+  int32_t n_ids;
+  int32_t num_slots;
 };
 
 __device__ __forceinline__ void entry_range(const FwdArgs& p, int& first, int& count) {
@@ -1384,6 +1387,241 @@ __global__ __launch_bounds__(FW * 64) void small_expand_kernel(FwdArgs p) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Plan-free small batches (decode).  Each workgroup finds the rows of its own
+// slot a, T_a = {t : ids[t] = a} (Section 3.4's grouping of rows by adapter),
+// by scanning the id array, so no plan is built and nothing else runs first.
+// Shrink unit = (slot, d-slice): the slot's rows in 16-row tiles times A's
+// slice, written to partial planes Hp[slice][t][0, LDH).  Expand unit = (slot,
+// column chunk): H = the planes summed in slice order, Y[t] += s H B^T.
+// Ids outside [0, S) and ids of empty slots match no workgroup: those rows are
+// left as they are, as with a plan.
+// ---------------------------------------------------------------------------
+// Rows t < n with ids[t] == a, ascending, into s_rows; the count (the same in
+// every thread).  ids_request issues the loads of the ids (n <= IDS_MAX_ROWS,
+// all at once), ids_rows_of compacts them.
+template <int NTHR>
+struct IdsRegs {
+  int v[IDS_MAX_ROWS / NTHR];
+};
+template <int NTHR>
+__device__ __forceinline__ void ids_request(const int32_t* ids, int n, IdsRegs<NTHR>& q) {
+#pragma unroll
+  for (int c = 0; c < IDS_MAX_ROWS / NTHR; ++c) {
+    const int i = c * NTHR + (int)threadIdx.x;
+    q.v[c] = i < n ? ldg(ids + i) : -1;
+  }
+}
+template <int NTHR>
+__device__ __forceinline__ int ids_rows_of(const IdsRegs<NTHR>& q, int n, int a, int* s_rows, int* s_wc) {
+  constexpr int NW = NTHR / 64, PER = IDS_MAX_ROWS / NTHR;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  int base = 0;
+#pragma unroll
+  for (int c = 0; c < PER; ++c) {
+    if (c * NTHR >= n) break;
+    const bool f = q.v[c] == a;
+    const uint64_t msk = __ballot(f);
+    const int pre = __popcll(msk & ((1ull << lane) - 1ull));
+    if (lane == 0) s_wc[w] = __popcll(msk);
+    __syncthreads();
+    int off = base, tot = 0;
+#pragma unroll
+    for (int qq = 0; qq < NW; ++qq) {
+      const int cq = s_wc[qq];
+      off += qq < w ? cq : 0;
+      tot += cq;
+    }
+    if (f) s_rows[off + pre] = c * NTHR + tid;
+    base += tot;
+    __syncthreads();
+  }
+  return base;
+}
+
+template <int NT, int U>
+__global__ __launch_bounds__(256) void ids_shrink_kernel(FwdArgs p) {
+  __shared__ f32x4 s_red[2 * NT * 64];
+  __shared__ int s_rows[IDS_MAX_ROWS];
+  __shared__ int s_wc[4];
+  const int lane = threadIdx.x & 63, w = wave_id();
+  const int mrow = lane & 15;
+  const int S = p.ks_max;
+  const int a = (int)blockIdx.x / S, sl = (int)blockIdx.x - a * S;
+  if (a >= p.num_slots) return;
+  // the slot record and the ids are requested together (neither waits for
+  // the other)
+  const Slot m = load_slot(p.meta, a);
+  IdsRegs<256> iq;
+  ids_request<256>(p.ids, p.n_ids, iq);
+  const int r = m.rank;
+  if (r <= 0) return;
+  const int cnt = ids_rows_of<256>(iq, p.n_ids, a, s_rows, s_wc);
+  if (cnt == 0) return;
+  const rsrc_t A = make_rsrc(m.A, (uint32_t)r * (uint32_t)p.d_in * 2u);
+  int kb, ke;
+  kslice(p.d_in, S, sl, kb, ke);
+  uint32_t arow[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int j = nt * 16 + mrow;
+    arow[nt] = (uint32_t)(j < r ? j : r - 1) * (uint32_t)p.d_in;
+  }
+  float* Hp = p.H + (int64_t)sl * p.hp_stride;
+  for (int t0 = 0; t0 < cnt; t0 += 16) {
+    const int i = t0 + mrow;
+    const uint16_t* xrow[1] = {p.X + (int64_t)s_rows[i < cnt ? i : cnt - 1] * p.ldx};
+    f32x4 acc[NT];
+#pragma unroll
+    for (int q = 0; q < NT; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+    shrink_steps<1, NT, U>(acc, xrow, A, arow, kb + w * 32, 128, ke);
+    reduce_waves<NT, NT>(acc, s_red);
+    if (w == 0) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int ii = t0 + (lane >> 4) * 4 + v;
+        if (ii >= cnt) continue;
+        float* hrow = Hp + (int64_t)s_rows[ii] * p.ldh;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) stg(hrow + nt * 16 + mrow, acc[nt][v]);
+      }
+    }
+  }
+}
+
+template <bool YBF16, int NT, bool RANK8>
+__global__ __launch_bounds__(FW * 64) void ids_expand_kernel(FwdArgs p) {
+  constexpr int KSM = (NT * 16 + 31) / 32;
+  constexpr int LDH = NT * 16;                // row stride of the partial planes
+  constexpr bool B_AHEAD = KSM <= 2;          // B of every slice requested up front
+  __shared__ int s_rows[IDS_MAX_ROWS];
+  __shared__ int s_wc[FW];
+  const int lane = threadIdx.x & 63, w = wave_id();
+  const int og = lane >> 4, mrow = lane & 15;
+  const int P = p.n_chunks, S = p.ks_max;
+  // siblings (same slot, different column chunk) share blockIdx % 8, i.e. one XCD
+  const int slot = (int)(blockIdx.x >> 3);
+  const int a = 8 * (slot / P) + (int)(blockIdx.x & 7);
+  const int pc = slot % P;
+  if (a >= p.num_slots) return;
+  // the slot record and the ids are requested together; B (which needs only
+  // the record) before the ids are compacted
+  const Slot m = load_slot(p.meta, a);
+  IdsRegs<FW * 64> iq;
+  ids_request<FW * 64>(p.ids, p.n_ids, iq);
+  const int r = m.rank;
+  if (r <= 0) return;
+  const float s = m.scale;
+  const rsrc_t Bw = make_rsrc(m.B, (uint32_t)p.d_out * (uint32_t)r * 2u);
+  const int c0 = pc * p.chunk;
+  const int c1 = min(p.d_out, c0 + p.chunk);
+  // B of this wave's column slices does not depend on the rows: requested
+  // before the id scan
+  bf16x8 bo_ahead[B_AHEAD ? FSL : 1][B_AHEAD ? KSM : 1][4];
+  if (B_AHEAD) {
+#pragma unroll
+    for (int sl = 0; sl < FSL; ++sl) {
+      const int o_w = c0 + 64 * (w + FW * sl);
+#pragma unroll
+      for (int ks = 0; ks < KSM; ++ks)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int o = out_col(o_w, q, mrow);
+          bo_ahead[B_AHEAD ? sl : 0][B_AHEAD ? ks : 0][q] =
+              wrow8<RANK8>(Bw, (uint32_t)(o < c1 ? o : c1 - 1) * r, ks * 32 + og * 8, r);
+        }
+    }
+  }
+  const int cnt = ids_rows_of<FW * 64>(iq, p.n_ids, a, s_rows, s_wc);
+  for (int t0 = 0; t0 < cnt; t0 += 16) {
+    const int i = t0 + mrow;
+    const bool rv = i < cnt;
+    const int trow = s_rows[rv ? i : cnt - 1];
+    YFrag<YBF16> yf[FSL];
+#pragma unroll
+    for (int sl = 0; sl < FSL; ++sl)
+      y_load<YBF16>(yf[sl], p.Y, p.ldy, trow, c0 + 64 * (w + FW * sl), og, c1);
+    // ---- H = sum of the planes in slice order, as hi / lo operands.  Up to
+    // rank 64 every plane of the lane's row is requested together; above, one
+    // plane at a time (register budget).
+    float h[KSM][8];
+#pragma unroll
+    for (int ks = 0; ks < KSM; ++ks)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) h[ks][e] = 0.0f;
+    if constexpr (KSM <= 2) {
+#pragma unroll
+      for (int ks = 0; ks < KSM; ++ks) {
+        const int j = ks * 32 + og * 8;
+        const int jj = j < LDH ? j : LDH - 8;
+        float4 q0[SPLIT_SMAX], q1[SPLIT_SMAX];
+#pragma unroll
+        for (int pl = 0; pl < SPLIT_SMAX; ++pl) {
+          const float* row = p.H + (int64_t)min(pl, S - 1) * p.hp_stride + (int64_t)trow * p.ldh + jj;
+          q0[pl] = ldg_f4(row);
+          q1[pl] = ldg_f4(row + 4);
+        }
+#pragma unroll
+        for (int pl = 0; pl < SPLIT_SMAX; ++pl) {
+          if (pl >= S) break;
+          h[ks][0] += q0[pl].x; h[ks][1] += q0[pl].y; h[ks][2] += q0[pl].z; h[ks][3] += q0[pl].w;
+          h[ks][4] += q1[pl].x; h[ks][5] += q1[pl].y; h[ks][6] += q1[pl].z; h[ks][7] += q1[pl].w;
+        }
+      }
+    } else {
+      for (int pl = 0; pl < S; ++pl) {
+        float4 q0[KSM], q1[KSM];
+#pragma unroll
+        for (int ks = 0; ks < KSM; ++ks) {
+          const int j = ks * 32 + og * 8;
+          const float* row = p.H + (int64_t)pl * p.hp_stride + (int64_t)trow * p.ldh + (j < LDH ? j : LDH - 8);
+          q0[ks] = ldg_f4(row);
+          q1[ks] = ldg_f4(row + 4);
+        }
+#pragma unroll
+        for (int ks = 0; ks < KSM; ++ks) {
+          h[ks][0] += q0[ks].x; h[ks][1] += q0[ks].y; h[ks][2] += q0[ks].z; h[ks][3] += q0[ks].w;
+          h[ks][4] += q1[ks].x; h[ks][5] += q1[ks].y; h[ks][6] += q1[ks].z; h[ks][7] += q1[ks].w;
+        }
+      }
+    }
+    bf16x8 hh[KSM], hl[KSM];
+#pragma unroll
+    for (int ks = 0; ks < KSM; ++ks) {
+      const int j = ks * 32 + og * 8;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) h[ks][e] = (rv && j < LDH && j + e < r) ? h[ks][e] : 0.0f;
+      split_hi_lo(h[ks], hh[ks], hl[ks]);
+    }
+    // ---- expand over this wave's column slices
+#pragma unroll
+    for (int sl = 0; sl < FSL; ++sl) {
+      const int o_w = c0 + 64 * (w + FW * sl);
+      f32x4 acc2[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) acc2[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KSM; ++ks) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          bf16x8 bo;
+          if (B_AHEAD) {
+            bo = bo_ahead[B_AHEAD ? sl : 0][B_AHEAD ? ks : 0][q];
+          } else {
+            const int o = out_col(o_w, q, mrow);
+            bo = wrow8<RANK8>(Bw, (uint32_t)(o < c1 ? o : c1 - 1) * r, ks * 32 + og * 8, r);
+          }
+          bo = sel(ks * 32 + og * 8 < r, bo);
+          acc2[q] = mfma_16x16x32(bo, hh[ks], acc2[q]);
+          acc2[q] = mfma_16x16x32(bo, hl[ks], acc2[q]);
+        }
+      }
+      mfma_fence();
+      if (rv && o_w < c1) y_store<YBF16>(yf[sl], p.Y, p.ldy, trow, o_w, og, c1, s, acc2);
+    }
+  }
+}
+
 template <typename K>
 hipError_t launch(K kernel, int grid, const FwdArgs& a, hipStream_t s, int threads = 256) {
   if (grid <= 0) return hipSuccess;
@@ -1457,10 +1695,12 @@ hipError_t launch_shrink_mfma(const OpLaunch& o, const void* X, int64_t ldx, flo
                    : nt <= 4 ? launch(shrink_fine_kernel<4, false>, gridf, a, s)
                              : launch(shrink_fine_kernel<8, false>, gridf, a, s);
   if (err != hipSuccess) return err;
-  // four k-steps per batch up to rank 64 (one at rank 128: register budget)
-  if (nt <= 1) return launch(shrink_kernel<1, 4>, grid, a, s);
-  if (nt <= 2) return launch(shrink_kernel<2, 4>, grid, a, s);
-  if (nt <= 4) return launch(shrink_kernel<4, 4>, grid, a, s);
+  // one 32-wide k-step per batch: the 4096 x 256-row prefill shrink measured
+  // 41 us at one step, 42 at two and 46 at four (fewer requests in flight per
+  // wave keep the HBM streams more orderly; the matrix cores are idle anyway)
+  if (nt <= 1) return launch(shrink_kernel<1, 1>, grid, a, s);
+  if (nt <= 2) return launch(shrink_kernel<2, 1>, grid, a, s);
+  if (nt <= 4) return launch(shrink_kernel<4, 1>, grid, a, s);
   return launch(shrink_kernel<8, 1>, grid, a, s);
 }
 
@@ -1567,6 +1807,51 @@ hipError_t launch_small_split_mfma(const OpLaunch& o, const void* X, int64_t ldx
   if (yb) return launch_small_expand_nt<true, false>(o, grid, a, s);
   if (o.rank8) return launch_small_expand_nt<false, true>(o, grid, a, s);
   return launch_small_expand_nt<false, false>(o, grid, a, s);
+}
+
+template <bool YB, bool R8>
+hipError_t launch_ids_expand_nt(int nt, int grid, const FwdArgs& a, hipStream_t s) {
+  constexpr int T = FW * 64;
+  if (nt <= 1) return launch(ids_expand_kernel<YB, 1, R8>, grid, a, s, T);
+  if (nt <= 2) return launch(ids_expand_kernel<YB, 2, R8>, grid, a, s, T);
+  if (nt <= 4) return launch(ids_expand_kernel<YB, 4, R8>, grid, a, s, T);
+  return launch(ids_expand_kernel<YB, 8, R8>, grid, a, s, T);
+}
+
+hipError_t launch_ids_mfma(const IdsLaunch& l, hipStream_t s) {
+  FwdArgs a{};
+  a.meta = l.meta;
+  a.d_in = l.d_in;
+  a.d_out = l.d_out;
+  a.num_slots = l.num_slots;
+  a.ids = l.ids;
+  a.n_ids = l.n;
+  a.X = reinterpret_cast<const uint16_t*>(l.X);
+  a.ldx = l.ldx;
+  a.Y = l.Y;
+  a.ldy = l.ldy;
+  const int nt = (l.r_max + 15) / 16;
+  const int tiles = nt <= 1 ? 1 : nt <= 2 ? 2 : nt <= 4 ? 4 : 8;
+  a.H = l.H;
+  a.ldh = tiles * 16;
+  a.ks_max = std::min(std::max(l.slices, 1), SPLIT_SMAX);
+  a.hp_stride = (int64_t)std::max(l.n, 1) * a.ldh;
+  const int g1 = l.num_slots * a.ks_max;
+  hipError_t e;
+  if (tiles == 1) e = launch(ids_shrink_kernel<1, 8>, g1, a, s);
+  else if (tiles == 2) e = launch(ids_shrink_kernel<2, 8>, g1, a, s);
+  else if (tiles == 4) e = launch(ids_shrink_kernel<4, 2>, g1, a, s);
+  else e = launch(ids_shrink_kernel<8, 1>, g1, a, s);
+  if (e != hipSuccess) return e;
+  constexpr int CW = 64 * FW * FSL;
+  const int P = std::max({1, l.n_chunks, (l.d_out + CW - 1) / CW});
+  a.n_chunks = P;
+  a.chunk = ((l.d_out + P - 1) / P + 63) / 64 * 64;
+  const int grid = 8 * P * ((l.num_slots + 7) / 8);
+  if (l.y_bf16 && l.rank8) return launch_ids_expand_nt<true, true>(nt, grid, a, s);
+  if (l.y_bf16) return launch_ids_expand_nt<true, false>(nt, grid, a, s);
+  if (l.rank8) return launch_ids_expand_nt<false, true>(nt, grid, a, s);
+  return launch_ids_expand_nt<false, false>(nt, grid, a, s);
 }
 
 hipError_t launch_bgmv_mfma(const OpLaunch& o, const void* X, int64_t ldx, void* Y,

@@ -39,6 +39,7 @@ constexpr int RB_FINE = 64;      // ... when the batch has fewer than FINE_BELOW
 constexpr int FINE_BELOW = 48;
 constexpr int SHRINK_KS_MAX = 4; // most d-slices of the grouped shrink inside lora_apply
 constexpr int SMALL_ROWS = 16;   // rows per small-group entry (one matrix-core column tile)
+constexpr int IDS_MAX_ROWS = 1024;  // most rows of a plan-free (lora_apply_ids) batch
 constexpr int MRB_ROWS = 64;     // trainable rows per gradient row block
 constexpr int PLAN_THREADS = 1024;
 constexpr int PLAN_WAVES = PLAN_THREADS / 64;
@@ -162,6 +163,24 @@ hipError_t launch_expand_mfma(const OpLaunch& o, const float* H, int64_t ldh, in
 hipError_t launch_grad_x_mfma(const OpLaunch& o, const void* dY, int64_t lddy, float* H, int64_t ldh,
                               int64_t hp_stride, void* dX, lora_dtype dx_dtype, int64_t lddx,
                               hipStream_t s);
+// plan-free small batch (lora_apply_ids): shrink per (slot, d-slice) into
+// partial planes H [slices][n][16 t] floats (t = 1, 2, 4 or 8 the rank tiles of
+// r_max), then expand per (slot, column chunk); every workgroup finds its
+// slot's rows in ids itself
+struct IdsLaunch {
+  const SlotMeta* meta;
+  int32_t num_slots, d_in, d_out, r_max;
+  bool rank8, y_bf16;
+  const int32_t* ids;
+  int32_t n;
+  const void* X;
+  int64_t ldx;
+  void* Y;
+  int64_t ldy;
+  float* H;
+  int32_t slices, n_chunks;
+};
+hipError_t launch_ids_mfma(const IdsLaunch& l, hipStream_t s);
 // fused small-group kernel: shrink into LDS + expand, entries [first, count)
 hipError_t launch_bgmv_mfma(const OpLaunch& o, const void* X, int64_t ldx, void* Y,
                             lora_dtype y_dtype, int64_t ldy, int32_t n_chunks, hipStream_t s);

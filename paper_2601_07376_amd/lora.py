@@ -47,6 +47,8 @@ SIGNATURES = {
     "lora_apply_workspace_bytes": (_sz, [_vp]),
     "lora_apply": (_i32, [_vp, _vp, _i32, _i64, _vp, _i32, _i64, _vp, _sz, _vp]),
     "lora_apply_noalloc": (_i32, [_vp, _vp, _i32, _i64, _vp, _i32, _i64, _vp]),
+    "lora_apply_ids_workspace_bytes": (_sz, [_vp, _i32]),
+    "lora_apply_ids": (_i32, [_vp, _i32, _vp, _vp, _i32, _i64, _vp, _i32, _i64, _vp, _sz, _vp]),
     "lora_linear_workspace_bytes": (_sz, [_vp]),
     "lora_linear": (_i32, [_vp, _vp, _i32, _i64, _vp, _i32, _i64, _vp, _i32, _i64, _vp, _sz, _vp]),
     "lora_calibrate_mfma": (_i32, [_i32, _i32, _vp, _vp]),
@@ -305,6 +307,24 @@ def apply_noalloc(plan, X, Y, stream=None):
     allocates nothing (for graph capture and loops that must not allocate)."""
     _check(lib().lora_apply_noalloc(plan.handle, _ptr(X), _dtype(X), _rowmajor(X, "X"), _ptr(Y),
                                     _dtype(Y), _rowmajor(Y, "Y"), _stream(stream)))
+    return Y
+
+
+def apply_ids_workspace(table, n):
+    return torch.empty(max(lib().lora_apply_ids_workspace_bytes(table.handle, n), 16),
+                       dtype=torch.uint8, device=table.device)
+
+
+def apply_ids(table, idx, X, Y, ws=None, stream=None):
+    """apply() for a small batch without a plan: Y[t] += s_a (X[t] A_a^T) B_a^T
+    for idx[t] = a, two launches (n <= 1024, bfloat16 X and weights)."""
+    n = int(idx.numel())
+    if ws is None:
+        ws = apply_ids_workspace(table, n)
+        _used_on(stream, ws)
+    _check(lib().lora_apply_ids(table.handle, n, _ptr(idx), _ptr(X), _dtype(X),
+                                _rowmajor(X, "X"), _ptr(Y), _dtype(Y), _rowmajor(Y, "Y"),
+                                _ptr(ws), ws.numel(), _stream(stream)))
     return Y
 
 

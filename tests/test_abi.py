@@ -237,3 +237,40 @@ def test_backward_rejects_null_plan():
                          lora.LORA_BF16, 64, None, 0, None, None, 0, ctypes.c_void_p(FAKE),
                          lora.LORA_F32, 64, ctypes.c_void_p(FAKE), 1 << 20, None)
     assert st == 1 and L.lora_last_error()
+
+
+def test_apply_ids_validation():
+    """lora_apply_ids refuses bad arguments on the host, before anything is
+    enqueued; its workspace is 0 bytes for n = 0 or a table without adapters,
+    and grows with n and the slices x rank tiles of the live ranks."""
+    L = lora.lib()
+    st, h = _create(S=4, d_in=1024, d_out=512)
+    assert st == 0
+    F = ctypes.c_void_p(FAKE)
+    assert L.lora_apply_ids_workspace_bytes(h, 100) == 0          # no adapter yet
+    assert L.lora_table_set(h, 0, 16, 2.0, F, F) == 0
+    need = L.lora_apply_ids_workspace_bytes(h, 100)
+    assert need == 4 * 100 * 16 * 4                                # 4 d-slices x n x 16 floats
+    assert L.lora_table_set(h, 2, 40, 1.0, F, F) == 0
+    assert L.lora_apply_ids_workspace_bytes(h, 100) == 4 * 100 * 64 * 4
+    assert L.lora_apply_ids_workspace_bytes(h, 0) == 0
+    assert L.lora_apply_ids_workspace_bytes(h, 1025) == 0
+    assert L.lora_apply_ids_workspace_bytes(None, 100) == 0
+    need = L.lora_apply_ids_workspace_bytes(h, 100)
+    args = lambda **kw: dict(dict(t=h, n=100, idx=F, X=F, xd=lora.LORA_BF16, ldx=1024, Y=F,
+                                  yd=lora.LORA_F32, ldy=512, ws=F, nb=need), **kw)
+    call = lambda a: L.lora_apply_ids(a["t"], a["n"], a["idx"], a["X"], a["xd"], a["ldx"], a["Y"],
+                                      a["yd"], a["ldy"], a["ws"], a["nb"], None)
+    assert call(args(t=None)) == 1
+    assert call(args(n=1025)) == 2
+    assert call(args(n=-1)) == 2
+    assert call(args(xd=lora.LORA_F32)) == 3
+    assert call(args(idx=None)) == 1
+    assert call(args(idx=ctypes.c_void_p(FAKE_ODD))) == 4
+    assert call(args(X=None)) == 1
+    assert call(args(ldx=1000)) in (2, 4)
+    assert call(args(ws=None)) == 1
+    assert call(args(ws=ctypes.c_void_p(FAKE_ODD))) == 4
+    assert call(args(nb=need - 1)) == 8
+    assert b"workspace" in L.lora_last_error()
+    L.lora_table_destroy(h)
