@@ -69,6 +69,12 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy", action="store_true",
                     help="(kept for old command lines: the calibrations always run)")
+    ap.add_argument("--pmc-summary", nargs="+", metavar="CSV",
+                    help="print the per-kernel table of rocprofv3 --pmc counter CSVs of bench "
+                         "runs (no GPU needed) and exit")
+    ap.add_argument("--stats-summary", metavar="CSV",
+                    help="print the markdown table of a rocprofv3 --kernel-trace --stats "
+                         "kernel_stats.csv (no GPU needed) and exit")
     return ap.parse_args()
 
 
@@ -652,7 +658,71 @@ def cpu_baseline(case, seconds):
                 single_thread=one)
 
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_bgmv.lora_apply.hbm_counters.txt")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "all_workloads.counters.txt")
+# kernels of one call of the headline op (lora_apply_ids on the decode batch)
+HEADLINE_KERNELS = ("ids_shrink_kernel", "ids_expand_kernel")
+# the calibration copy (torch's elementwise negation of 1 GiB float32 into a new
+# tensor): reads and writes exactly 1 GiB, which scales FETCH_SIZE / WRITE_SIZE
+CALIB_KERNEL = "neg_kernel"
+
+
+def _short_kernel(name):
+    n = name.replace("void ", "").replace("lora::(anonymous namespace)::", "")
+    n = n.split("(lora::")[0].split("(FwdArgs")[0]
+    if CALIB_KERNEL in n:
+        return "calibration copy (" + n[:60] + ")"
+    return n[:70]
+
+
+def pmc_summary(paths):
+    """Per-kernel means of rocprofv3 --pmc counter CSVs (one row per kernel, one
+    column per counter, dispatch durations under counters), the FETCH/WRITE
+    scale from the calibration copy, and the headline op's traffic per call."""
+    import csv
+    import collections
+    vals = collections.defaultdict(lambda: collections.defaultdict(list))
+    dur = collections.defaultdict(list)
+    for path in paths:
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                k = _short_kernel(r["Kernel_Name"])
+                vals[k][r["Counter_Name"]].append(float(r["Counter_Value"]))
+                dur[k].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3)
+    counters = sorted({c for d in vals.values() for c in d})
+    mean = {k: {c: (sum(v) / len(v)) for c, v in d.items()} for k, d in vals.items()}
+    calib = next((k for k in mean if k.startswith("calibration copy")), None)
+    fs = ws = None
+    if calib is not None:
+        if mean[calib].get("FETCH_SIZE"):
+            fs = (1 << 20) / mean[calib]["FETCH_SIZE"]
+        if mean[calib].get("WRITE_SIZE"):
+            ws = (1 << 20) / mean[calib]["WRITE_SIZE"]
+    out = []
+    if fs is not None:
+        out.append(f"fetch_scale: {fs:.4f}")
+    if ws is not None:
+        out.append(f"write_scale: {ws:.4f}")
+    head = [k for k in mean if k.startswith(HEADLINE_KERNELS)]
+    if fs is not None and ws is not None and head:
+        tb = sum(mean[k].get("FETCH_SIZE", 0) * fs + mean[k].get("WRITE_SIZE", 0) * ws for k in head)
+        out.append(f"traffic_bytes_per_launch: {int(round(tb * 1024))}")
+        out.append("headline_kernels: " + " + ".join(sorted(head)))
+    out.append("")
+    cols = ["kernel", "dispatches"] + counters + ["us/dispatch (under counters)"]
+    if fs is not None and ws is not None:
+        cols.insert(2 + len(counters), "HBM MB/dispatch (scaled)")
+    out.append("| " + " | ".join(cols) + " |")
+    out.append("|" + "---|" * len(cols))
+    order = sorted(mean, key=lambda k: -sum(dur[k]))
+    for k in order:
+        n = max(len(v) for v in vals[k].values())
+        row = [k, str(n)] + [f"{mean[k][c]:.1f}" if c in mean[k] else "" for c in counters]
+        if fs is not None and ws is not None:
+            row.append(f"{(mean[k].get('FETCH_SIZE', 0) * fs + mean[k].get('WRITE_SIZE', 0) * ws) * 1024 / 1e6:.2f}"
+                       if "FETCH_SIZE" in mean[k] or "WRITE_SIZE" in mean[k] else "")
+        row.append(f"{sum(dur[k]) / len(dur[k]):.2f}")
+        out.append("| " + " | ".join(row) + " |")
+    print("\n".join(out))
 
 
 def traffic_for(result):
@@ -667,7 +737,8 @@ def traffic_for(result):
             if ":" in ln and not ln.startswith((" ", "#", "|")):
                 k, v = ln.split(":", 1)
                 kv[k.strip()] = v.strip()
-    if kv.get("source_digest") != source_digest() or kv.get("workload") != result["workload"]:
+    if kv.get("source_digest") != source_digest() or kv.get("workload") != result["workload"] \
+            or kv.get("op") != result["op"]:
         return None
     try:
         return int(kv["traffic_bytes_per_launch"])
@@ -675,8 +746,26 @@ def traffic_for(result):
         return None
 
 
+def stats_summary(path):
+    """rocprofv3 --stats kernel table: calls, average / min / max us, share."""
+    import csv
+    rows = list(csv.DictReader(open(path)))
+    print("| kernel | calls | avg us | min us | max us | share |")
+    print("|---|---|---|---|---|---|")
+    for r in rows:
+        print(f"| {_short_kernel(r['Name'])} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+              f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | "
+              f"{float(r['Percentage']):.2f}% |")
+
+
 def main():
     args = parse()
+    if args.pmc_summary:
+        pmc_summary(args.pmc_summary)
+        return
+    if args.stats_summary:
+        stats_summary(args.stats_summary)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
