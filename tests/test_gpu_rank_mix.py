@@ -3,8 +3,8 @@ launch carries adapters of different ranks, each tile padded to its own rank).
 
 Every pairing of the rank classes 8, 16, 32, 64 and 128 (a class beside itself
 too) goes through each kernel family at ragged sizes: the grouped 64-row and
-256-row pairs, the small-group split and fused kernels, the adapter gradients
-and the input gradient.  Each kernel is instantiated for the batch's largest
+256-row pairs, the small-group split and fused kernels, the plan-free pair of
+lora_apply_ids, the adapter gradients and the input gradient.  Each kernel is instantiated for the batch's largest
 rank, so a pairing (a, b) runs the rank-a tiles inside the rank-b instance.
 A missing wait between a matrix-core result and its first reader shows up
 here as a wrong tile of the smaller rank.
@@ -20,7 +20,7 @@ import workloads
 from gpu_helpers import (DEV, MAX_ABS, REL_FRO, check_forward, check_grads, effective,
                          make_plan, make_table, run_apply, say)
 from helpers import f64_case
-from workloads.device import case_to_device
+from workloads.device import case_to_device, from_torch
 
 import paper_2601_07376_amd as L
 
@@ -67,9 +67,14 @@ def test_rank_pair_forward_and_backward(ra, rb):
         say(f"ranks ({ra}, {rb}) apply {name}")
         Yo, _ = run_apply(case, policy=pol)
         check_forward(case, Yo, eff)
-    say(f"ranks ({ra}, {rb}) grad and grad_x")
     dev = case_to_device(case, DEV)
     table = make_table(case, dev)
+    say(f"ranks ({ra}, {rb}) apply_ids")
+    Yi = dev["Y"].clone()
+    L.apply_ids(table, dev["idx"], dev["X"], Yi)
+    torch.cuda.synchronize()
+    check_forward(case, from_torch(Yi), eff)
+    say(f"ranks ({ra}, {rb}) grad and grad_x")
     plan = make_plan(case, dev, table, mask=True)
     dA, dB = L.grad(plan, dev["X"], dev["dY"])
     dX = torch.zeros(case.n, case.d_in, dtype=torch.float32, device=DEV)
