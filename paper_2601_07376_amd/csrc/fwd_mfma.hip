@@ -602,11 +602,21 @@ __global__ __launch_bounds__(256, (KSM == 1 || (YBF16 && KSM == 2 && U == 1)) ? 
       bj[h] = (pc - bcol[h] * (BS / 8)) * 8;
     }
 
+    // bf16 Y, one step per batch: Y comes in through the wave's output area
+    // as whole 128-byte lines of 8 rows (the 2-step group of the first step's
+    // batch), the way the results leave; else in the matrix-core layout
+    constexpr bool YL = YBF16 && U == 1;
+    int lrow[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) lrow[i] = srow[i] >= 0 ? srow[i] : trow[0];
     struct Buf {
       uint4 b[U][BPT];
-      Y8<YBF16> y[U][4];
+      Y8<YBF16> y[YL ? 1 : U][YL ? 1 : 4];
+      uint4 yl[YL ? 8 : 1];
     };
-    auto load = [&](Buf& q, int st0) {
+    // group: the batch starts a 128-byte group of columns (YL: it brings the
+    // group's Y lines)
+    auto load = [&](Buf& q, int st0, bool group) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int ob = c0 + 32 * min(st0 + u, nst - 1);
@@ -617,12 +627,22 @@ __global__ __launch_bounds__(256, (KSM == 1 || (YBF16 && KSM == 2 && U == 1)) ? 
           q.b[u][h] = __builtin_bit_cast(uint4, wrow8<RANK8>(Bw, (uint32_t)oc * r, bj[h], r));
         }
       }
+      if constexpr (YL) {
+        if (group) {
+          int o = c0 + 32 * min(st0, nst - 1) + (lane & 7) * 8;
+          o = o < p.d_out ? o : p.d_out - 8;
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int ob = c0 + 32 * min(st0 + u, nst - 1);
+          for (int i = 0; i < 8; ++i)
+            q.yl[i] = ldg16(reinterpret_cast<const uint16_t*>(p.Y) + (int64_t)lrow[i] * p.ldy + o);
+        }
+      } else {
 #pragma unroll
-        for (int tt = 0; tt < 4; ++tt)
-          y8_load<YBF16>(q.y[u][tt], p.Y, p.ldy, trow[tt], ob + 8 * og, p.d_out);
+        for (int u = 0; u < U; ++u) {
+          const int ob = c0 + 32 * min(st0 + u, nst - 1);
+#pragma unroll
+          for (int tt = 0; tt < 4; ++tt)
+            y8_load<YBF16>(q.y[u][tt], p.Y, p.ldy, trow[tt], ob + 8 * og, p.d_out);
+        }
       }
     };
     auto stage = [&](const Buf& q, int buf) {
@@ -633,7 +653,16 @@ __global__ __launch_bounds__(256, (KSM == 1 || (YBF16 && KSM == 2 && U == 1)) ? 
           *reinterpret_cast<uint4*>(&s_b[buf][u][bcol[h] * TS + bj[h]]) = q.b[u][h];
     };
     // product of step st (batch slot u), added to Y, into the wave's output area
-    auto run = [&](const Buf& q, int u, int st, int buf) {
+    auto run = [&](const Buf& q, int u, int st, int buf, bool group) {
+      if constexpr (YL) {
+        if (group) {                   // the group's Y lines into the area
+          asm volatile("" ::: "memory");
+#pragma unroll
+          for (int i = 0; i < 8; ++i)
+            *reinterpret_cast<uint4*>(so + (8 * i + (lane >> 3)) * OS + (lane & 7) * 16) = q.yl[i];
+          asm volatile("" ::: "memory");
+        }
+      }
       f32x4 acc[2][4];
 #pragma unroll
       for (int qq = 0; qq < 2; ++qq)
@@ -659,7 +688,10 @@ __global__ __launch_bounds__(256, (KSM == 1 || (YBF16 && KSM == 2 && U == 1)) ? 
 #pragma unroll
       for (int tt = 0; tt < 4; ++tt) {
         uint4 out[2];
-        y8_combine<YBF16>(q.y[u][tt], s, acc[0][tt], acc[1][tt], out);
+        Y8<YBF16> yv;
+        if constexpr (YL) yv.v[0] = *reinterpret_cast<const uint4*>(so + (16 * tt + mrow) * OS + cb);
+        else yv = q.y[YL ? 0 : u][YL ? 0 : tt];
+        y8_combine<YBF16>(yv, s, acc[0][tt], acc[1][tt], out);
         unsigned char* d = so + (16 * tt + mrow) * OS + cb;
         *reinterpret_cast<uint4*>(d) = out[0];
         if (!YBF16) *reinterpret_cast<uint4*>(d + 16) = out[1];
@@ -682,10 +714,10 @@ __global__ __launch_bounds__(256, (KSM == 1 || (YBF16 && KSM == 2 && U == 1)) ? 
       asm volatile("" ::: "memory");   // ... and the next writes come after the reads
     };
     // a batch of U steps from st0: products, and a flush after every SP-th step
-    auto batch = [&](const Buf& q, int st0, int buf) {
+    auto batch = [&](const Buf& q, int st0, int buf, bool group) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        run(q, u, st0 + u, buf);
+        run(q, u, st0 + u, buf, group && u == 0);
         if ((st0 + u) % SP == SP - 1) flush(st0 + u - (SP - 1));
       }
     };
@@ -694,7 +726,7 @@ __global__ __launch_bounds__(256, (KSM == 1 || (YBF16 && KSM == 2 && U == 1)) ? 
     // unconditional (past the last step they repeat it) and so are stores;
     // steps past the chunk store to the sink.  One exit, at the end of a pair.
     Buf b0, b1;
-    load(b0, 0);
+    load(b0, 0, true);
     // as many stores (to the sink) as a pair ends with after its last loads,
     // so that the loop is entered with the same sequence of memory operations
     // outstanding as it loops back with, and the compiler's wait counts stay
@@ -705,17 +737,18 @@ __global__ __launch_bounds__(256, (KSM == 1 || (YBF16 && KSM == 2 && U == 1)) ? 
     for (int i = 0; i < TAIL; ++i) stg16(sink + (i & 7), make_uint4(0u, 0u, 0u, (uint32_t)i));
     __builtin_amdgcn_sched_barrier(0);
     __syncthreads();                 // the previous unit's reads of s_b are done
+    // (U = 1 with SP = 2: b0 always holds an even step, which starts a group)
     for (int st = 0; st < nst; st += 2 * U) {
-      load(b1, st + U);
+      load(b1, st + U, U >= SP);
       __builtin_amdgcn_sched_barrier(0);
       stage(b0, 0);
       __syncthreads();
-      batch(b0, st, 0);
-      load(b0, st + 2 * U);
+      batch(b0, st, 0, true);
+      load(b0, st + 2 * U, true);
       __builtin_amdgcn_sched_barrier(0);
       stage(b1, 1);
       __syncthreads();
-      batch(b1, st + U, 1);
+      batch(b1, st + U, 1, U >= SP);
     }
   }
 }
