@@ -85,9 +85,12 @@ HEADLINE_SOURCES = ("fwd_mfma.hip", "api.cpp", "device_common.h", "lora_internal
 
 
 def source_digest(files=HEADLINE_SOURCES):
-    """Digest of the native sources the headline kernels come from."""
+    """Digest of the native sources the headline kernels come from (None: every
+    source file of the library)."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2601_07376_amd", "csrc")
+    if files is None:
+        files = [f for f in os.listdir(csrc) if f.endswith((".hip", ".cpp", ".h"))]
     for f in sorted(files):
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode() + b"\0" + fh.read())
@@ -661,6 +664,25 @@ def cpu_baseline(case, seconds):
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "all_workloads.counters.txt")
 # kernels of one call of the headline op (lora_apply_ids on the decode batch)
 HEADLINE_KERNELS = ("ids_shrink_kernel", "ids_expand_kernel")
+# kernels of one call of each measured op, per workload (each launched once per
+# call; names as the counter summary prints them)
+OP_KERNELS = {
+    ("tiny_sgmv_fp32", "lora_apply"): ("shrink_valu_kernel<false, false, 32>(ValuArgs)",
+                                        "expand_valu_kernel<false, false>(ValuArgs)"),
+    ("decode_bgmv", "lora_apply_ids"): ("ids_shrink_kernel<1, 8>", "ids_expand_kernel<true, 1, true>"),
+    ("prefill_sgmv", "lora_apply"): ("shrink_kernel<4, 1>", "expand_kernel<true, true, 2, 1>"),
+    ("prefill_sgmv", "lora_linear"): ("shrink_kernel<4, 1>", "linear_hpack_kernel(LinArgs)",
+                                      "linear_kernel<true, true, 64, 2, true, true>(LinArgs)"),
+    ("skewed_hetero", "lora_apply"): ("shrink_fine_kernel<4, false>",
+                                      "expand_fine_kernel<true, true, 2, 2, false>",
+                                      "small_shrink_kernel<4, 2>", "small_expand_kernel<true, 4, true>"),
+    ("masked_backward", "lora_grad"): ("hg_kernel<2>(GradArgs)", "hgsum_kernel(GradArgs)",
+                                       "dadb_kernel<2>(GradArgs)"),
+    ("masked_backward", "lora_grad_x"): ("shrink_fine_kernel<2, true>",
+                                         "expand_fine_kernel<false, true, 1, 1, true>"),
+    ("masked_backward", "lora_token_loss"): ("token_loss_kernel<true, true>(LossArgs)",),
+    ("masked_backward", "lora_adamw_step"): ("adamw_kernel(AdamArgs)",),
+}
 # the calibration copy (torch's elementwise negation of 1 GiB float32 into a new
 # tensor): reads and writes exactly 1 GiB, which scales FETCH_SIZE / WRITE_SIZE
 CALIB_KERNEL = "neg_kernel"
@@ -697,16 +719,21 @@ def pmc_summary(paths):
             fs = (1 << 20) / mean[calib]["FETCH_SIZE"]
         if mean[calib].get("WRITE_SIZE"):
             ws = (1 << 20) / mean[calib]["WRITE_SIZE"]
-    out = []
+    out = [f"source_digest: {source_digest()}", f"source_digest_all: {source_digest(None)}"]
     if fs is not None:
         out.append(f"fetch_scale: {fs:.4f}")
     if ws is not None:
         out.append(f"write_scale: {ws:.4f}")
     head = [k for k in mean if k.startswith(HEADLINE_KERNELS)]
+    hb = lambda k: (mean[k].get("FETCH_SIZE", 0) * fs + mean[k].get("WRITE_SIZE", 0) * ws) * 1024
     if fs is not None and ws is not None and head:
-        tb = sum(mean[k].get("FETCH_SIZE", 0) * fs + mean[k].get("WRITE_SIZE", 0) * ws for k in head)
-        out.append(f"traffic_bytes_per_launch: {int(round(tb * 1024))}")
+        out.append(f"traffic_bytes_per_launch: {int(round(sum(hb(k) for k in head)))}")
         out.append("headline_kernels: " + " + ".join(sorted(head)))
+    if fs is not None and ws is not None:
+        # every op whose kernels all appear: bytes per call
+        for (wl, op), ks in OP_KERNELS.items():
+            if all(k in mean for k in ks):
+                out.append(f"traffic {wl} {op}: {int(round(sum(hb(k) for k in ks)))}")
     out.append("")
     cols = ["kernel", "dispatches"] + counters + ["us/dispatch (under counters)"]
     if fs is not None and ws is not None:
@@ -725,23 +752,39 @@ def pmc_summary(paths):
     print("\n".join(out))
 
 
+def _traffic_kv():
+    kv = {}
+    if os.path.exists(TRAFFIC_FILE):
+        with open(TRAFFIC_FILE) as f:
+            for ln in f:
+                if ":" in ln and not ln.startswith((" ", "#", "|")):
+                    k, v = ln.split(":", 1)
+                    kv[k.strip()] = v.strip()
+    return kv
+
+
 def traffic_for(result):
     """HBM bytes per call of the headline op (the sum over its kernels) from the
     committed rocprofv3 counter summary, if its counters were taken on the
     current kernel sources; otherwise None."""
-    if not os.path.exists(TRAFFIC_FILE):
-        return None
-    kv = {}
-    with open(TRAFFIC_FILE) as f:
-        for ln in f:
-            if ":" in ln and not ln.startswith((" ", "#", "|")):
-                k, v = ln.split(":", 1)
-                kv[k.strip()] = v.strip()
+    kv = _traffic_kv()
     if kv.get("source_digest") != source_digest() or kv.get("workload") != result["workload"] \
             or kv.get("op") != result["op"]:
         return None
     try:
         return int(kv["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def op_traffic(workload, op):
+    """HBM bytes per call of any measured op from the same summary, gated on a
+    digest of every native source; None when the summary is stale or lacks it."""
+    kv = _traffic_kv()
+    if kv.get("source_digest_all") != source_digest(None):
+        return None
+    try:
+        return int(kv[f"traffic {workload} {op}"])
     except (KeyError, ValueError):
         return None
 
@@ -790,6 +833,14 @@ def main():
         if c == HEADLINE:
             head_case = case
     for r in results.values():
+        t = op_traffic(r["workload"], r["op"])
+        r["traffic"] = t
+        r["traffic_over_algorithmic"] = None if t is None else round(t / r["op_bytes"], 4)
+        for leg in ("linear", "grad_x", "token_loss", "adamw"):
+            if leg in r:
+                t = op_traffic(r["workload"], r[leg]["op"])
+                r[leg]["traffic"] = t
+                r[leg]["traffic_over_algorithmic"] = None if t is None else round(t / r[leg]["bytes"], 4)
         r["op_hbm_frac_of_copy"] = r["op_GBps"] / calib["GBps"]
         r["op_mfma_frac_of_calibrated"] = r["op_TFLOPs"] / calib_m["TFLOPs"]
         if "linear" in r:
