@@ -48,13 +48,20 @@ def test_side_stream_apply_and_backward(monkeypatch):
                                  y_dtype="f32")
     dev = case_to_device(case, DEV)
     table = make_table(case, dev)
+    # one pass on the current stream first: the first launch of a kernel loads
+    # its code, which can take longer on the host than the spin below on the GPU
+    warm = L.Plan(table, idx=dev["idx"], mask=dev["mask"])
+    L.apply(warm, dev["X"], dev["Y"].clone())
+    L.backward(warm, dev["X"], dev["dY"], torch.zeros_like(dev["X"], dtype=torch.float32))
+    torch.cuda.synchronize()
+    made.clear()
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
-    # a long queue on the side stream first, so the later kernels run after the
-    # current stream's allocations below
+    # a long queue on the side stream first (200 passes over 256 MB, about
+    # 20 ms), so the later kernels run after the current stream's allocations
     spin = torch.empty(64 << 20, dtype=torch.float32, device=DEV)
     with torch.cuda.stream(side):
-        for _ in range(20):
+        for _ in range(200):
             spin.mul_(1.0)
     Y = dev["Y"].clone()
     dX = torch.zeros(case.n, case.d_in, dtype=torch.float32, device=DEV)
@@ -70,6 +77,8 @@ def test_side_stream_apply_and_backward(monkeypatch):
     made.clear()
     assert len(ptrs) == 2
     fresh = [torch.empty(n, dtype=torch.uint8, device=DEV) for n in sizes]
+    # the check only means something while the side stream still has work queued
+    assert not side.query(), "side stream drained before the check: lengthen the spin"
     assert not set(ptrs) & {f.data_ptr() for f in fresh}, "workspace reused while in use"
     junk = _scribble(32 << 20)
     side.synchronize()
