@@ -66,7 +66,9 @@ typedef enum lora_status {
   LORA_ERR_DATA = 7,        /* the device flagged bad ids or segments (lora_plan_check) */
   LORA_ERR_WORKSPACE = 8,   /* workspace too small */
   LORA_ERR_HIP = 9,         /* a HIP runtime call failed */
-  LORA_ERR_VALUE = 10       /* a hyperparameter or step number is out of range */
+  LORA_ERR_VALUE = 10,      /* a hyperparameter or step number is out of range */
+  LORA_ERR_ALIAS = 11       /* debug build: an output overlaps an input or another output
+                               (the call enqueued nothing) */
 } lora_status;
 
 typedef enum lora_dtype { LORA_F32 = 0, LORA_BF16 = 1 } lora_dtype;
@@ -75,6 +77,9 @@ typedef enum lora_dtype { LORA_F32 = 0, LORA_BF16 = 1 } lora_dtype;
 #define LORA_DATA_BAD_ID       1u   /* an id outside [-1, num_slots) */
 #define LORA_DATA_EMPTY_SLOT   2u   /* an id naming a slot with no adapter */
 #define LORA_DATA_BAD_SEGMENTS 4u   /* seg_offsets not 0 = o_0 <= o_1 <= ... = n */
+#define LORA_DATA_BOUNDS       8u   /* debug build: a kernel read a plan value (row id,
+                                       adapter id) outside its bound; it used an in-range
+                                       value instead, so that call's results are void */
 
 typedef struct lora_table lora_table;
 typedef struct lora_plan lora_plan;
@@ -84,6 +89,37 @@ int32_t     lora_abi_version(void);
 const char* lora_status_string(lora_status s);
 /* Human-readable detail of the last error returned on this thread. */
 const char* lora_last_error(void);
+
+/* ---- debug build ---------------------------------------------------------
+ * The library is also built as liblora_mi355x_debug.so: the same entry points
+ * and results, plus checks that the release library leaves out.
+ *  - Before enqueuing anything, every op checks that its outputs overlap
+ *    neither its inputs (row-indexed matrices, the table's adapter weights,
+ *    the id array) nor each other nor the workspace, and returns
+ *    LORA_ERR_ALIAS if they do (X / Y, dY / dA / dB and H must be disjoint;
+ *    the release library leaves the result of an overlapping call undefined).
+ *  - Every kernel that reads the plan checks each row id and adapter id it
+ *    takes from it against [0, n) and [0, num_slots) before using it as an
+ *    index; a value out of range sets LORA_DATA_BOUNDS in the plan's data flag
+ *    (read by lora_plan_check) and is replaced by 0, so that no access leaves
+ *    the caller's buffers.
+ * lora_build_flags returns LORA_BUILD_DEBUG in the debug library, 0 in the
+ * release one. */
+#define LORA_BUILD_DEBUG 1
+int32_t     lora_build_flags(void);
+/* Test hook of the debug library: overwrite entry `index` of one plan array
+ * of row ids with `value`, after the work already on `stream` and before any
+ * later work (the call waits for the stream), so that a test can check that
+ * the kernels' bounds checks catch a bad plan.  Arrays: LORA_PLAN_PERM, the
+ * active rows in group order [n]; LORA_PLAN_M_PERM, the trainable rows [n];
+ * LORA_PLAN_SMALL_ROW, row index % 16 of small-group record index / 16.  The
+ * release library returns LORA_ERR_VALUE and writes nothing.  Errors: NULL,
+ * VALUE (unknown array, index past the array's capacity), HIP. */
+#define LORA_PLAN_PERM      0
+#define LORA_PLAN_M_PERM    1
+#define LORA_PLAN_SMALL_ROW 2
+lora_status lora_debug_plan_poke(lora_plan* p, int32_t array, int32_t index, int32_t value,
+                                 void* stream);
 
 /* ---- adapter table (Section 3.4, "Adapter table") -----------------------
  * One table per adapted layer.  A slot holds one pinned adapter version: its

@@ -161,6 +161,84 @@ lora_status check_plan(const lora_plan* p) {
   return LORA_OK;
 }
 
+// ---- debug build: outputs disjoint from inputs and from each other ------------
+#ifndef LORA_DEBUG
+#define LORA_DEBUG 0
+#endif
+constexpr bool kDebug = LORA_DEBUG != 0;
+
+// Bytes [lo, hi) of one buffer of an op (empty when lo == hi).
+struct Span {
+  uintptr_t lo, hi;
+  const char* what;
+  int32_t slot;        // adapter weights and gradients: their slot, else -1
+};
+
+// rows x cols elements of es bytes, rows ld elements apart
+Span rows_span(const void* ptr, int64_t rows, int64_t cols, int64_t ld, size_t es, const char* what,
+               int32_t slot = -1) {
+  if (ptr == nullptr || rows <= 0 || cols <= 0) return Span{0, 0, what, slot};
+  const uintptr_t lo = reinterpret_cast<uintptr_t>(ptr);
+  return Span{lo, lo + (uintptr_t)(((rows - 1) * ld + cols) * (int64_t)es), what, slot};
+}
+Span bytes_span(const void* ptr, size_t bytes, const char* what) {
+  const uintptr_t lo = reinterpret_cast<uintptr_t>(ptr);
+  return ptr == nullptr ? Span{0, 0, what, -1} : Span{lo, lo + bytes, what, -1};
+}
+
+// The buffers one call reads (inputs) and writes (outputs).  check() fails
+// with LORA_ERR_ALIAS when an output overlaps an input or another output.
+class Disjoint {
+ public:
+  explicit Disjoint(const char* op) : op_(op) {}
+  void in(const Span& s) {
+    if (s.lo < s.hi) ins_.push_back(s);
+  }
+  void out(const Span& s) {
+    if (s.lo < s.hi) outs_.push_back(s);
+  }
+  // the device copy of the slot table and every live slot's A and B
+  void weights(const lora_table* t) {
+    in(bytes_span(t->dev_meta, (size_t)t->num_slots * sizeof(lora::SlotMeta), "the slot table"));
+    const size_t es = dsize(t->w_dtype);
+    for (int32_t a = 0; a < t->num_slots; ++a) {
+      const lora::SlotMeta& m = t->host[a];
+      if (m.rank <= 0) continue;
+      in(rows_span(m.A, m.rank, t->d_in, t->d_in, es, "A", a));
+      in(rows_span(m.B, t->d_out, m.rank, m.rank, es, "B", a));
+    }
+  }
+  void plan(const lora_plan* p) { in(bytes_span(p->ws, p->L.total, "the plan workspace")); }
+  lora_status check() {
+    auto by_lo = [](const Span& a, const Span& b) { return a.lo < b.lo; };
+    std::sort(outs_.begin(), outs_.end(), by_lo);
+    for (size_t i = 0; i + 1 < outs_.size(); ++i)      // sorted: an overlap shows between neighbours
+      if (outs_[i + 1].lo < outs_[i].hi) return report(outs_[i], outs_[i + 1]);
+    std::sort(ins_.begin(), ins_.end(), by_lo);
+    std::vector<uintptr_t> hi_max(ins_.size());
+    for (size_t i = 0; i < ins_.size(); ++i) hi_max[i] = std::max(ins_[i].hi, i ? hi_max[i - 1] : 0);
+    for (const Span& o : outs_) {
+      // inputs starting before o ends; one of them reaches past o's start?
+      const size_t k = std::lower_bound(ins_.begin(), ins_.end(), Span{o.hi, o.hi, "", -1}, by_lo) -
+                       ins_.begin();
+      if (k == 0 || hi_max[k - 1] <= o.lo) continue;
+      for (size_t i = k; i-- > 0;)
+        if (ins_[i].hi > o.lo) return report(o, ins_[i]);
+    }
+    return LORA_OK;
+  }
+
+ private:
+  lora_status report(const Span& a, const Span& b) {
+    char sa[48] = "", sb[48] = "";
+    if (a.slot >= 0) snprintf(sa, sizeof(sa), " of slot %d", a.slot);
+    if (b.slot >= 0) snprintf(sb, sizeof(sb), " of slot %d", b.slot);
+    return fail(LORA_ERR_ALIAS, "%s: %s%s overlaps %s%s", op_, a.what, sa, b.what, sb);
+  }
+  const char* op_;
+  std::vector<Span> ins_, outs_;
+};
+
 lora_status make_plan(const lora_table* t, int32_t n, const int32_t* idx,
                       const int32_t* seg_offsets, const int32_t* seg_adapter, int32_t num_segs,
                       const uint8_t* mask, const lora_policy* policy, void* ws, size_t ws_bytes,
@@ -412,11 +490,40 @@ const char* lora_status_string(lora_status s) {
     case LORA_ERR_WORKSPACE: return "workspace too small";
     case LORA_ERR_HIP: return "HIP runtime error";
     case LORA_ERR_VALUE: return "hyperparameter or step number out of range";
+    case LORA_ERR_ALIAS: return "an output overlaps an input or another output";
   }
   return "unknown status";
 }
 
 const char* lora_last_error(void) { return g_err.c_str(); }
+
+int32_t lora_build_flags(void) { return kDebug ? LORA_BUILD_DEBUG : 0; }
+
+lora_status lora_debug_plan_poke(lora_plan* p, int32_t array, int32_t index, int32_t value,
+                                 void* stream) {
+  if (!kDebug) return fail(LORA_ERR_VALUE, "lora_debug_plan_poke: debug build only");
+  if (p == nullptr) return fail(LORA_ERR_NULL, "plan is NULL");
+  int32_t* base = nullptr;
+  int64_t len = 0, word = index;
+  switch (array) {
+    case LORA_PLAN_PERM: base = p->d.perm; len = p->n; break;
+    case LORA_PLAN_M_PERM: base = p->d.m_perm; len = p->n; break;
+    case LORA_PLAN_SMALL_ROW:          // row index % 16 of record index / 16
+      base = reinterpret_cast<int32_t*>(p->d.srec);
+      len = (int64_t)p->L.srec_max * lora::SMALL_ROWS;
+      word = (int64_t)(index / lora::SMALL_ROWS) * (sizeof(lora::SmallRec) / 4) +
+             offsetof(lora::SmallRec, row) / 4 + index % lora::SMALL_ROWS;
+      break;
+    default: return fail(LORA_ERR_VALUE, "lora_debug_plan_poke: unknown array %d", array);
+  }
+  if (index < 0 || index >= len)
+    return fail(LORA_ERR_VALUE, "lora_debug_plan_poke: index %d outside [0, %lld)", index, (long long)len);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = hipMemcpyAsync(base + word, &value, 4, hipMemcpyHostToDevice, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);     // `value` lives on this stack
+  if (e != hipSuccess) return hip_fail(e, "plan poke");
+  return ok();
+}
 
 // ---- table -----------------------------------------------------------------
 
@@ -595,6 +702,14 @@ lora_status lora_shrink(const lora_plan* p, const void* X, lora_dtype x_dtype, i
   const lora_table* t = p->table;
   if ((st = check_matrix(X, x_dtype, ldx, t->d_in, "X", p->n)) != LORA_OK) return st;
   if ((st = check_matrix(H, LORA_F32, ldh, std::max(p->r_max, 1), "H", p->n)) != LORA_OK) return st;
+  if (kDebug) {
+    Disjoint d("lora_shrink");
+    d.out(rows_span(H, p->n, std::max(p->r_max, 1), ldh, 4, "H"));
+    d.in(rows_span(X, p->n, t->d_in, ldx, dsize(x_dtype), "X"));
+    d.weights(t);
+    d.plan(p);
+    if ((st = d.check()) != LORA_OK) return st;
+  }
   if (p->n == 0) return ok();
   lora::OpLaunch o = op_base(p);
   o.count_word = lora::HDR_NRB_TOTAL;
@@ -619,6 +734,14 @@ lora_status lora_expand(const lora_plan* p, const float* H, int64_t ldh, void* Y
   const lora_table* t = p->table;
   if ((st = check_matrix(H, LORA_F32, ldh, std::max(p->r_max, 1), "H", p->n)) != LORA_OK) return st;
   if ((st = check_matrix(Y, y_dtype, ldy, t->d_out, "Y", p->n)) != LORA_OK) return st;
+  if (kDebug) {
+    Disjoint d("lora_expand");
+    d.out(rows_span(Y, p->n, t->d_out, ldy, dsize(y_dtype), "Y"));
+    d.in(rows_span(H, p->n, std::max(p->r_max, 1), ldh, 4, "H"));
+    d.weights(t);
+    d.plan(p);
+    if ((st = d.check()) != LORA_OK) return st;
+  }
   if (p->n == 0) return ok();
   lora::OpLaunch o = op_base(p);
   o.count_word = lora::HDR_NRB_TOTAL;
@@ -691,6 +814,15 @@ lora_status apply_impl(const lora_plan* p, const void* X, lora_dtype x_dtype, in
     if (ws == nullptr) return fail(LORA_ERR_NULL, "apply workspace is NULL");
     if (!aligned(ws, 16)) return fail(LORA_ERR_ALIGN, "apply workspace not 16-byte aligned");
     if (ws_bytes < need) return fail(LORA_ERR_WORKSPACE, "apply workspace %zu bytes < %zu", ws_bytes, need);
+  }
+  if (kDebug) {
+    Disjoint d(allow_fork ? "lora_apply" : "lora_apply_noalloc");
+    d.out(rows_span(Y, p->n, t->d_out, ldy, dsize(y_dtype), "Y"));
+    if (needs_ws) d.out(bytes_span(ws, need, "the workspace"));
+    d.in(rows_span(X, p->n, t->d_in, ldx, dsize(x_dtype), "X"));
+    d.weights(t);
+    d.plan(p);
+    if ((st = d.check()) != LORA_OK) return st;
   }
   if (p->n == 0) return ok();
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -820,6 +952,15 @@ lora_status lora_apply_ids(const lora_table* t, int32_t n, const int32_t* idx, c
     if (!aligned(ws, 16)) return fail(LORA_ERR_ALIGN, "apply_ids workspace not 16-byte aligned");
     if (ws_bytes < need) return fail(LORA_ERR_WORKSPACE, "apply_ids workspace %zu bytes < %zu", ws_bytes, need);
   }
+  if (kDebug) {
+    Disjoint d("lora_apply_ids");
+    d.out(rows_span(Y, n, t->d_out, ldy, dsize(y_dtype), "Y"));
+    if (need > 0) d.out(bytes_span(ws, need, "the workspace"));
+    d.in(rows_span(X, n, t->d_in, ldx, dsize(x_dtype), "X"));
+    d.in(bytes_span(idx, (size_t)n * 4, "idx"));
+    d.weights(t);
+    if ((st = d.check()) != LORA_OK) return st;
+  }
   const IdsShape q = ids_shape(t);
   if (n == 0 || q.r_max == 0) return ok();
   lora::IdsLaunch l{};
@@ -910,6 +1051,16 @@ lora_status lora_linear(const lora_plan* p, const void* X, lora_dtype x_dtype, i
   if (ws == nullptr) return fail(LORA_ERR_NULL, "linear workspace is NULL");
   if (!aligned(ws, 16)) return fail(LORA_ERR_ALIGN, "linear workspace not 16-byte aligned");
   if (ws_bytes < need) return fail(LORA_ERR_WORKSPACE, "linear workspace %zu bytes < %zu", ws_bytes, need);
+  if (kDebug) {
+    Disjoint d("lora_linear");
+    d.out(rows_span(Y, p->n, t->d_out, ldy, dsize(y_dtype), "Y"));
+    d.out(bytes_span(ws, need, "the workspace"));
+    d.in(rows_span(X, p->n, t->d_in, ldx, 2, "X"));
+    d.in(rows_span(W, t->d_out, t->d_in, ldw, 2, "W"));
+    d.weights(t);
+    d.plan(p);
+    if ((st = d.check()) != LORA_OK) return st;
+  }
   if (p->n == 0) return ok();
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int64_t ldh = (std::max(p->r_max, 1) + 7) / 8 * 8;
@@ -953,6 +1104,26 @@ lora_status lora_linear(const lora_plan* p, const void* X, lora_dtype x_dtype, i
 
 // ---- backward --------------------------------------------------------------
 
+namespace {
+// buffers of the adapter gradients (debug build): dA_a and dB_a written;
+// X, dY, H_saved, the weights and the plan read
+void grad_spans(Disjoint& d, const lora_plan* p, const void* X, lora_dtype x_dtype, int64_t ldx,
+                const void* dY, lora_dtype dy_dtype, int64_t lddy, const float* H_saved, int64_t ldh,
+                float* const* dA, float* const* dB) {
+  const lora_table* t = p->table;
+  for (int32_t a = 0; a < t->num_slots; ++a) {
+    const int32_t r = t->host[a].rank;
+    if (dA != nullptr) d.out(rows_span(dA[a], r, t->d_in, t->d_in, 4, "dA", a));
+    if (dB != nullptr) d.out(rows_span(dB[a], t->d_out, r, r, 4, "dB", a));
+  }
+  d.in(rows_span(X, p->n, t->d_in, ldx, dsize(x_dtype), "X"));
+  d.in(rows_span(dY, p->n, t->d_out, lddy, dsize(dy_dtype), "dY"));
+  d.in(rows_span(H_saved, p->n, std::max(p->r_max, 1), ldh, 4, "H_saved"));
+  d.weights(t);
+  d.plan(p);
+}
+}  // namespace
+
 size_t lora_grad_workspace_bytes(const lora_plan* p) {
   if (p == nullptr) return 0;
   return lora::grad_layout(ub_mrb(p), p->r_max).total;
@@ -983,6 +1154,12 @@ lora_status lora_grad(const lora_plan* p, const void* X, lora_dtype x_dtype, int
   if (ws == nullptr) return fail(LORA_ERR_NULL, "grad workspace is NULL");
   if (!aligned(ws, 16)) return fail(LORA_ERR_ALIGN, "grad workspace not 16-byte aligned");
   if (ws_bytes < need) return fail(LORA_ERR_WORKSPACE, "grad workspace %zu bytes < %zu", ws_bytes, need);
+  if (kDebug) {
+    Disjoint d("lora_grad");
+    grad_spans(d, p, X, x_dtype, ldx, dY, dy_dtype, lddy, H_saved, ldh, dA, dB);
+    d.out(bytes_span(ws, need, "the workspace"));
+    if ((st = d.check()) != LORA_OK) return st;
+  }
 
   const bool mfma = x_dtype == LORA_BF16 && t->w_dtype == LORA_BF16;
   lora::GradLaunch g{};
@@ -1041,6 +1218,15 @@ lora_status lora_grad_x(const lora_plan* p, const void* dY, lora_dtype dy_dtype,
   if (!aligned(ws, 16)) return fail(LORA_ERR_ALIGN, "input-gradient workspace not 16-byte aligned");
   if (ws_bytes < need)
     return fail(LORA_ERR_WORKSPACE, "input-gradient workspace %zu bytes < %zu", ws_bytes, need);
+  if (kDebug) {
+    Disjoint d("lora_grad_x");
+    d.out(rows_span(dX, p->n, t->d_in, lddx, dsize(dx_dtype), "dX"));
+    d.out(bytes_span(ws, need, "the workspace"));
+    d.in(rows_span(dY, p->n, t->d_out, lddy, dsize(dy_dtype), "dY"));
+    d.weights(t);
+    d.plan(p);
+    if ((st = d.check()) != LORA_OK) return st;
+  }
   if (p->n == 0) return ok();
   lora::OpLaunch o = op_base(p);
   o.d_in = t->d_out;                 // the shrink reads dY rows
@@ -1084,6 +1270,13 @@ lora_status lora_backward(const lora_plan* p, const void* X, lora_dtype x_dtype,
   if (ws == nullptr) return fail(LORA_ERR_NULL, "backward workspace is NULL");
   if (!aligned(ws, 16)) return fail(LORA_ERR_ALIGN, "backward workspace not 16-byte aligned");
   if (ws_bytes < need) return fail(LORA_ERR_WORKSPACE, "backward workspace %zu bytes < %zu", ws_bytes, need);
+  if (kDebug) {
+    Disjoint d("lora_backward");
+    grad_spans(d, p, X, x_dtype, ldx, dY, dy_dtype, lddy, H_saved, ldh, dA, dB);
+    d.out(rows_span(dX, p->n, t->d_in, lddx, dsize(dx_dtype), "dX"));
+    d.out(bytes_span(ws, need, "the workspace"));
+    if ((st = d.check()) != LORA_OK) return st;
+  }
   const size_t off = al256(lora_grad_workspace_bytes(p));
   char* wsb = static_cast<char*>(ws);
   hipStream_t s = static_cast<hipStream_t>(stream);

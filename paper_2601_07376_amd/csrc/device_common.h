@@ -190,6 +190,63 @@ __device__ __forceinline__ Slot load_slot(const Meta* meta, int a) {
   return s;
 }
 
+// ---- bounds checks of plan values (debug build) ------------------------------
+// Built with LORA_DEBUG=1, every kernel that reads the plan checks each row id
+// and adapter id it takes from a plan array before using it as an index: a
+// value outside [0, n) or [0, num_slots) sets LORA_DATA_BOUNDS in the plan's
+// data flag (header word 0, read by lora_plan_check) and is replaced by 0, so
+// that no access leaves the caller's buffers.  In the release build both
+// checks are the identity and compile to nothing.
+#ifndef LORA_DEBUG
+#define LORA_DEBUG 0
+#endif
+constexpr uint32_t DATA_BOUNDS_BIT = 8u;    // LORA_DATA_BOUNDS
+
+__device__ __forceinline__ void flag_bounds(const int32_t* hdr) {
+  atomicOr(reinterpret_cast<unsigned int*>(const_cast<int32_t*>(hdr)), DATA_BOUNDS_BIT);
+}
+// row id t of a batch of n rows
+__device__ __forceinline__ int ck_row(const int32_t* hdr, int t, int n) {
+#if LORA_DEBUG
+  if ((unsigned)t >= (unsigned)n) {
+    flag_bounds(hdr);
+    return 0;
+  }
+#else
+  (void)hdr;
+  (void)n;
+#endif
+  return t;
+}
+// adapter id a of a table of S slots
+__device__ __forceinline__ int ck_slot(const int32_t* hdr, int a, int S) {
+#if LORA_DEBUG
+  if ((unsigned)a >= (unsigned)S) {
+    flag_bounds(hdr);
+    return 0;
+  }
+#else
+  (void)hdr;
+  (void)S;
+#endif
+  return a;
+}
+
+// count of a run [off, off + cnt) of plan positions inside [0, n), or 0
+__device__ __forceinline__ int ck_count(const int32_t* hdr, int off, int cnt, int n) {
+#if LORA_DEBUG
+  if (off < 0 || cnt < 0 || off > n - cnt) {
+    flag_bounds(hdr);
+    return 0;
+  }
+#else
+  (void)hdr;
+  (void)off;
+  (void)n;
+#endif
+  return cnt;
+}
+
 // Lane shuffles through DPP (gfx9): a few cycles each, where ds_bpermute
 // (__shfl and friends) costs an LDS round trip.
 //   row_incl_scan   inclusive prefix sum inside each row of 16 lanes

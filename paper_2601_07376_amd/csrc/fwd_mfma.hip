@@ -56,6 +56,7 @@ struct FwdArgs {
   const int32_t* ids;       // plan-free small batch: per-row slot ids [n_ids]
   int32_t n_ids;
   int32_t num_slots;
+  int32_t n_rows;           // rows of the batch: the bound of every row id read from the plan
 };
 
 __device__ __forceinline__ void entry_range(const FwdArgs& p, int& first, int& count) {
@@ -276,7 +277,7 @@ __global__ __launch_bounds__(256) void shrink_kernel(FwdArgs p) {
   for (int unit = xr.first; unit < xr.end; unit += xr.step) {
     const int e = unit / nks, ks = unit - e * nks;
     const int4 en = load_entry(p.rb, first + e);
-    const int a = en.x, p0 = en.y, rows = en.z;
+    const int a = ck_slot(p.hdr, en.x, p.num_slots), p0 = en.y, rows = en.z;
     const Slot m = load_slot(p.meta, a);
     const int r = m.rank;
     const rsrc_t A = make_rsrc(m.A, (uint32_t)r * (uint32_t)p.d_in * 2u);
@@ -290,7 +291,7 @@ __global__ __launch_bounds__(256) void shrink_kernel(FwdArgs p) {
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt) {
       const int i = 64 * w + 16 * mt + mrow;
-      xrow[mt] = p.X + (int64_t)ldg(p.perm + p0 + (i < rows ? i : rows - 1)) * p.ldx;
+      xrow[mt] = p.X + (int64_t)ck_row(p.hdr, ldg(p.perm + p0 + (i < rows ? i : rows - 1)), p.n_rows) * p.ldx;
     }
     // row ids of the accumulator layout (rows 4 (l / 16) + v of each tile),
     // requested now so that the stores at the end do not wait on them
@@ -300,7 +301,7 @@ __global__ __launch_bounds__(256) void shrink_kernel(FwdArgs p) {
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         const int i = 64 * w + 16 * mt + (lane >> 4) * 4 + v;
-        orow[mt][v] = ldg(p.perm + p0 + (i < rows ? i : rows - 1));
+        orow[mt][v] = ck_row(p.hdr, ldg(p.perm + p0 + (i < rows ? i : rows - 1)), p.n_rows);
       }
     // this thread's A pieces: row j (clamped to the rank), columns 8 c .. 8 c + 7
     // of a step.  With fewer pieces than threads (rank <= 32) several threads
@@ -495,7 +496,7 @@ __global__ __launch_bounds__(256, (KSM == 1 || (YBF16 && KSM == 2 && U == 1)) ? 
     const int c0 = ch * CW, c1 = min(p.d_out, c0 + CW);
     const int nst = (c1 - c0 + 31) / 32;
     const int4 en = load_entry(p.rb, first + e);
-    const int a = en.x, p0 = en.y, rows = en.z;
+    const int a = ck_slot(p.hdr, en.x, p.num_slots), p0 = en.y, rows = en.z;
     const Slot m = load_slot(p.meta, a);
     const int r = m.rank;
     const float s = m.scale;
@@ -508,7 +509,7 @@ __global__ __launch_bounds__(256, (KSM == 1 || (YBF16 && KSM == 2 && U == 1)) ? 
     for (int tt = 0; tt < 4; ++tt) {
       const int i = 64 * w + 16 * tt + mrow;
       rv[tt] = i < rows;
-      trow[tt] = ldg(p.perm + p0 + (i < rows ? i : rows - 1));
+      trow[tt] = ck_row(p.hdr, ldg(p.perm + p0 + (i < rows ? i : rows - 1)), p.n_rows);
     }
     // rows of the store layout: instruction i, lane row lane / 8 (padding rows
     // store to the sink)
@@ -516,7 +517,7 @@ __global__ __launch_bounds__(256, (KSM == 1 || (YBF16 && KSM == 2 && U == 1)) ? 
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const int ri = 64 * w + 8 * i + (lane >> 3);
-      srow[i] = ri < rows ? ldg(p.perm + p0 + ri) : -1;
+      srow[i] = ri < rows ? ck_row(p.hdr, ldg(p.perm + p0 + ri), p.n_rows) : -1;
     }
 
     // H operands (hi / lo) of the wave's rows: the slices' partial sums added
@@ -779,7 +780,7 @@ __global__ __launch_bounds__(256) void shrink_fine_kernel(FwdArgs p) {
   for (int unit = xr.first; unit < xr.end; unit += xr.step) {
     const int e = unit / nks, ks = unit - e * nks;
     const int4 en = load_entry(p.rb, first + e);
-    const int a = en.x, p0 = en.y, rows = en.z;
+    const int a = ck_slot(p.hdr, en.x, p.num_slots), p0 = en.y, rows = en.z;
     const Slot m = load_slot(p.meta, a);
     const int r = m.rank;
     const rsrc_t A = make_rsrc(WT ? m.B : m.A, (uint32_t)r * (uint32_t)p.d_in * 2u);
@@ -794,11 +795,11 @@ __global__ __launch_bounds__(256) void shrink_fine_kernel(FwdArgs p) {
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt) {
       const int i = 16 * mt + mrow;
-      xrow[mt] = p.X + (int64_t)ldg(p.perm + p0 + (i < rows ? i : rows - 1)) * p.ldx;
+      xrow[mt] = p.X + (int64_t)ck_row(p.hdr, ldg(p.perm + p0 + (i < rows ? i : rows - 1)), p.n_rows) * p.ldx;
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         const int io = 16 * mt + (lane >> 4) * 4 + v;
-        orow[mt][v] = ldg(p.perm + p0 + (io < rows ? io : rows - 1));
+        orow[mt][v] = ck_row(p.hdr, ldg(p.perm + p0 + (io < rows ? io : rows - 1)), p.n_rows);
       }
     }
     uint32_t arow[NT];
@@ -918,7 +919,7 @@ __global__ __launch_bounds__(256, KSM == 1 ? 2 : 1) void expand_fine_kernel(FwdA
     const int e = unit / n_ch, ch = unit - e * n_ch;
     const int c0 = ch * CW, c1 = min(p.d_out, c0 + CW);
     const int4 en = load_entry(p.rb, first + e);
-    const int a = en.x, p0 = en.y, rows = en.z;
+    const int a = ck_slot(p.hdr, en.x, p.num_slots), p0 = en.y, rows = en.z;
     const Slot m = load_slot(p.meta, a);
     const int r = m.rank;
     const float s = m.scale;
@@ -931,13 +932,13 @@ __global__ __launch_bounds__(256, KSM == 1 ? 2 : 1) void expand_fine_kernel(FwdA
 #pragma unroll
     for (int tt = 0; tt < 4; ++tt) {
       const int i = 16 * tt + mrow;
-      trow[tt] = ldg(p.perm + p0 + (i < rows ? i : rows - 1));
+      trow[tt] = ck_row(p.hdr, ldg(p.perm + p0 + (i < rows ? i : rows - 1)), p.n_rows);
     }
     int srow[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const int ri = 8 * i + (lane >> 3);
-      srow[i] = ri < rows ? ldg(p.perm + p0 + ri) : -1;
+      srow[i] = ri < rows ? ck_row(p.hdr, ldg(p.perm + p0 + ri), p.n_rows) : -1;
     }
 
     // H of the block's rows: thread -> row tid / 4, float4 quarter tid % 4 of
@@ -945,7 +946,7 @@ __global__ __launch_bounds__(256, KSM == 1 ? 2 : 1) void expand_fine_kernel(FwdA
     // added in slice order (rows past the block and ranks past r are zero)
     {
       const int hr = tid >> 2, hq = tid & 3;
-      const int hrow = ldg(p.perm + p0 + (hr < rows ? hr : rows - 1));
+      const int hrow = ck_row(p.hdr, ldg(p.perm + p0 + (hr < rows ? hr : rows - 1)), p.n_rows);
       float4 q[SHRINK_KS_MAX][HQ];
 #pragma unroll
       for (int sl = 0; sl < SHRINK_KS_MAX; ++sl) {
@@ -1143,9 +1144,10 @@ __global__ __launch_bounds__(FW * 64) void fused_small_kernel(FwdArgs p) {
   const int er = min(e, p.n_rec - 1);
   const int4* rec = reinterpret_cast<const int4*>(p.srec + er);
   const int4 h0 = rec[0], h1 = rec[1];
-  const int trow = ldg(&p.srec[er].row[mrow]);
+  const int trow_rec = ldg(&p.srec[er].row[mrow]);
   const int count = p.hdr[p.count_word];
   if (e >= count) return;
+  const int trow = ck_row(p.hdr, trow_rec, p.n_rows);
   const void* Ap = uni_ptr(reinterpret_cast<const void*>(
       (uint64_t)(uint32_t)h0.x | ((uint64_t)(uint32_t)h0.y << 32)));
   const void* Bp = uni_ptr(reinterpret_cast<const void*>(
@@ -1273,9 +1275,10 @@ __global__ __launch_bounds__(256) void small_shrink_kernel(FwdArgs p) {
   const int er = min(e, p.n_rec - 1);
   const int4 h0 = *reinterpret_cast<const int4*>(p.srec + er);
   const int4 h1 = *(reinterpret_cast<const int4*>(p.srec + er) + 1);
-  const int trow = ldg(&p.srec[er].row[mrow]);
+  const int trow_rec = ldg(&p.srec[er].row[mrow]);
   const int count = p.hdr[p.count_word];
   if (e >= count) return;
+  const int trow = ck_row(p.hdr, trow_rec, p.n_rows);
   const void* Ap = uni_ptr(reinterpret_cast<const void*>(
       (uint64_t)(uint32_t)h0.x | ((uint64_t)(uint32_t)h0.y << 32)));
   const int r = uni(h1.y);
@@ -1320,7 +1323,7 @@ __global__ __launch_bounds__(FW * 64) void small_expand_kernel(FwdArgs p) {
   const int er = min(e, p.n_rec - 1);
   const int4 h0 = *reinterpret_cast<const int4*>(p.srec + er);
   const int4 h1 = *(reinterpret_cast<const int4*>(p.srec + er) + 1);
-  const int trow = ldg(&p.srec[er].row[mrow]);
+  const int trow_rec = ldg(&p.srec[er].row[mrow]);
   const int count = p.hdr[p.count_word];
   // the record's partial planes depend on e alone: requested in the same
   // round trip as the record (clamped, unconditional; stored to LDS below)
@@ -1335,6 +1338,7 @@ __global__ __launch_bounds__(FW * 64) void small_expand_kernel(FwdArgs p) {
     pv[u] = ldg_f4(p.H + (int64_t)pl * p.hp_stride + (int64_t)er * 16 * LDH + 4 * q);
   }
   if (e >= count) return;
+  const int trow = ck_row(p.hdr, trow_rec, p.n_rows);
   const void* Bp = uni_ptr(reinterpret_cast<const void*>(
       (uint64_t)(uint32_t)h0.z | ((uint64_t)(uint32_t)h0.w << 32)));
   const int rows = uni(h1.x), r = uni(h1.y);
@@ -1674,6 +1678,8 @@ FwdArgs base_args(const OpLaunch& o) {
   a.d_out = o.d_out;
   a.count_word = o.count_word;
   a.first_word = o.first_word;
+  a.num_slots = o.num_slots;
+  a.n_rows = o.n;
   return a;
 }
 

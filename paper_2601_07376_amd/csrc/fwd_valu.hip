@@ -30,6 +30,8 @@ struct ValuArgs {
   int64_t ldh;
   void* Y;
   int64_t ldy;
+  int32_t num_slots;
+  int32_t n_rows;           // rows of the batch: the bound of every row id read from the plan
 };
 
 // Work unit: an entry's rows in groups of VG; each group's operands are staged
@@ -55,7 +57,7 @@ __global__ __launch_bounds__(256) void shrink_valu_kernel(ValuArgs p) {
   for (int tile = blockIdx.x; tile < count * VGROUPS; tile += gridDim.x) {
     const int e = tile / VGROUPS, g = tile - e * VGROUPS;
     const int4 en = load_entry(p.rb, first + e);
-    const int a = en.x, rows = min(VG, en.z - g * VG), p0 = en.y + g * VG;
+    const int a = ck_slot(p.hdr, en.x, p.num_slots), rows = min(VG, en.z - g * VG), p0 = en.y + g * VG;
     if (rows <= 0) continue;
     const Slot m = load_slot(p.meta, a);
     const int r = m.rank;
@@ -63,7 +65,7 @@ __global__ __launch_bounds__(256) void shrink_valu_kernel(ValuArgs p) {
 #pragma unroll
     for (int u = 0; u < XL; ++u) {
       const int i = (tid + 256 * u) / VK;
-      xt[u] = p.perm[p0 + (i < rows ? i : rows - 1)];
+      xt[u] = ck_row(p.hdr, p.perm[p0 + (i < rows ? i : rows - 1)], p.n_rows);
     }
     float xv[XL], av[AL];
     auto fetch = [&](int k0) {
@@ -113,7 +115,7 @@ __global__ __launch_bounds__(256) void shrink_valu_kernel(ValuArgs p) {
     for (int mm = 0; mm < PM; ++mm) {
       const int q = tid + 256 * mm, i = q / max(r, 1), j = q - i * max(r, 1);
       if (r == 0 || i >= rows) continue;
-      p.H[(int64_t)p.perm[p0 + i] * p.ldh + j] = acc[mm];
+      p.H[(int64_t)ck_row(p.hdr, p.perm[p0 + i], p.n_rows) * p.ldh + j] = acc[mm];
     }
   }
 }
@@ -133,7 +135,7 @@ __global__ __launch_bounds__(256) void expand_valu_kernel(ValuArgs p) {
     const int g = tile % VGROUPS, eo = tile / VGROUPS;
     const int e = eo / n_ot, o = (eo - e * n_ot) * 256 + tid;
     const int4 en = load_entry(p.rb, first + e);
-    const int a = en.x, rows = min(VG, en.z - g * VG), p0 = en.y + g * VG;
+    const int a = ck_slot(p.hdr, en.x, p.num_slots), rows = min(VG, en.z - g * VG), p0 = en.y + g * VG;
     if (rows <= 0) continue;
     const Slot m = load_slot(p.meta, a);
     const int r = m.rank;
@@ -146,7 +148,7 @@ __global__ __launch_bounds__(256) void expand_valu_kernel(ValuArgs p) {
     float yv[VG];
 #pragma unroll
     for (int i = 0; i < VG; ++i) {
-      yt[i] = p.perm[p0 + (i < rows ? i : rows - 1)];
+      yt[i] = ck_row(p.hdr, p.perm[p0 + (i < rows ? i : rows - 1)], p.n_rows);
       const int64_t yo = (int64_t)yt[i] * p.ldy + oc;
       yv[i] = YB ? bf16_to_f32(reinterpret_cast<const uint16_t*>(p.Y)[yo])
                  : reinterpret_cast<const float*>(p.Y)[yo];
@@ -162,7 +164,7 @@ __global__ __launch_bounds__(256) void expand_valu_kernel(ValuArgs p) {
 #pragma unroll
     for (int u = 0; u < HL; ++u) {
       const int q = tid + 256 * u, i = q / LORA_MAX_RANK, j = q % LORA_MAX_RANK;
-      s_h[i][j] = (i < rows && j < r) ? p.H[(int64_t)p.perm[p0 + i] * p.ldh + j] : 0.0f;
+      s_h[i][j] = (i < rows && j < r) ? p.H[(int64_t)ck_row(p.hdr, p.perm[p0 + i], p.n_rows) * p.ldh + j] : 0.0f;
     }
     __syncthreads();
     float acc[VG];
@@ -200,6 +202,8 @@ ValuArgs base_args(const OpLaunch& o) {
   a.d_out = o.d_out;
   a.count_word = o.count_word;
   a.first_word = o.first_word;
+  a.num_slots = o.num_slots;
+  a.n_rows = o.n;
   return a;
 }
 

@@ -35,6 +35,7 @@ struct GradArgs {
   const int32_t* m_blk;
   const SlotMeta* meta;
   int32_t d_in, d_out, num_slots;
+  int32_t n_rows;                         // rows of the batch: the bound of every row id read from the plan
   const void* X;
   int64_t ldx;
   const void* dY;
@@ -231,7 +232,7 @@ __global__ __launch_bounds__(256) void hg_kernel(GradArgs g) {
   for (int tile = xr.first; tile < xr.end; tile += xr.step) {
     const int e = tile / nks, ks = tile - e * nks;
     const int4 en = load_entry(g.mrb, e);
-    const int a = en.x, p0 = en.y, rows = en.z;
+    const int a = ck_slot(g.hdr, en.x, g.num_slots), p0 = en.y, rows = en.z;
     const Slot m = load_slot(g.meta, a);
     const int r = m.rank;
     const rsrc_t Aw = make_rsrc(m.A, (uint32_t)r * (uint32_t)g.d_in * 2u);
@@ -241,7 +242,7 @@ __global__ __launch_bounds__(256) void hg_kernel(GradArgs g) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       const int i = mt * 16 + (lane & 15);
-      const int t = g.m_perm[p0 + (i < rows ? i : rows - 1)];
+      const int t = ck_row(g.hdr, g.m_perm[p0 + (i < rows ? i : rows - 1)], g.n_rows);
       xrow[mt] = X + (int64_t)t * g.ldx;
       yrow[mt] = dY + (int64_t)t * g.lddy;
     }
@@ -302,7 +303,7 @@ __global__ __launch_bounds__(256) void hg_kernel(GradArgs g) {
       for (int q = lane; q < MRB_ROWS * g.r_pad; q += 64) {
         const int i = q / g.r_pad, j = q - i * g.r_pad;
         float h = 0.0f;
-        if (ks == 0 && i < rows && j < r) h = g.H_saved[(int64_t)g.m_perm[p0 + i] * g.ldh + j];
+        if (ks == 0 && i < rows && j < r) h = g.H_saved[(int64_t)ck_row(g.hdr, g.m_perm[p0 + i], g.n_rows) * g.ldh + j];
         ph[(int64_t)j * g.p_stride + col0 + i] = h;
       }
     }
@@ -391,7 +392,8 @@ __device__ __forceinline__ void dadb_tile(const GradArgs& g, int sl, int c0, uin
   const int r = m.rank;
   float* out = IS_B ? g.dB[sl] : g.dA[sl];
   const int dcol = IS_B ? g.d_out : g.d_in;
-  const int mc = uni(g.m_counts[a]), moff = uni(g.m_offsets[a]), blk0 = uni(g.m_blk[a]);
+  const int moff = uni(g.m_offsets[a]), blk0 = uni(g.m_blk[a]);
+  const int mc = ck_count(g.hdr, moff, uni(g.m_counts[a]), g.n_rows);
   const float s = m.scale;
   const uint16_t* src = reinterpret_cast<const uint16_t*>(IS_B ? g.dY : g.X);
   const int64_t ld = IS_B ? g.lddy : g.ldx;
@@ -412,7 +414,7 @@ __device__ __forceinline__ void dadb_tile(const GradArgs& g, int sl, int c0, uin
     __syncthreads();
     for (int i = tid; i < DT_WIN; i += 256) {
       const int p = w0 * DT_ROWS + i;
-      s_rows[i] = g.m_perm[moff + (p < mc ? p : mc - 1)];
+      s_rows[i] = ck_row(g.hdr, g.m_perm[moff + (p < mc ? p : mc - 1)], g.n_rows);
     }
     __syncthreads();
 
@@ -575,7 +577,7 @@ __global__ __launch_bounds__(256) void hg_valu_kernel(GradArgs g) {
   const int n_blocks = g.hdr[HDR_NMRB];
   for (int e = blockIdx.x; e < n_blocks; e += gridDim.x) {
     const int4 en = load_entry(g.mrb, e);
-    const int a = en.x, p0 = en.y, rows = en.z;
+    const int a = ck_slot(g.hdr, en.x, g.num_slots), p0 = en.y, rows = en.z;
     const Slot m = load_slot(g.meta, a);
     const int r = m.rank;
     float* ph = plane(g, 0, 0);
@@ -584,7 +586,7 @@ __global__ __launch_bounds__(256) void hg_valu_kernel(GradArgs g) {
       const int i = q / g.r_pad, j = q - i * g.r_pad;
       float h = 0.0f, gg = 0.0f;
       if (i < rows && j < r) {
-        const int t = g.m_perm[p0 + i];
+        const int t = ck_row(g.hdr, g.m_perm[p0 + i], g.n_rows);
         if (g.H_saved != nullptr) {
           h = g.H_saved[(int64_t)t * g.ldh + j];
         } else {
@@ -626,12 +628,13 @@ __global__ __launch_bounds__(256) void dadb_valu_kernel(GradArgs g) {
     if (j >= r) continue;
     float* out = isB ? g.dB[sl] : g.dA[sl];
     if (out == nullptr) continue;
-    const int mc = g.m_counts[a], moff = g.m_offsets[a], blk0 = g.m_blk[a];
+    const int moff = g.m_offsets[a], blk0 = g.m_blk[a];
+    const int mc = ck_count(g.hdr, moff, g.m_counts[a], g.n_rows);
     if (mc == 0 && g.accumulate) continue;
     const float* pl = plane(g, isB ? 0 : 1, 0) + (int64_t)j * g.p_stride;
     float acc = 0.0f;
     for (int p = 0; p < mc; ++p) {
-      const int t = g.m_perm[moff + p];
+      const int t = ck_row(g.hdr, g.m_perm[moff + p], g.n_rows);
       const float hv = pl[blk0 * MRB_ROWS + p];
       const float xv = isB ? ldv<XB>(g.dY, (int64_t)t * g.lddy + col) : ldv<XB>(g.X, (int64_t)t * g.ldx + col);
       acc = fmaf(xv, hv, acc);
@@ -654,6 +657,7 @@ GradArgs make_args(const GradLaunch& l) {
   g.d_in = l.o.d_in;
   g.d_out = l.o.d_out;
   g.num_slots = l.o.num_slots;
+  g.n_rows = l.o.n;
   g.X = l.X;
   g.ldx = l.ldx;
   g.dY = l.dY;

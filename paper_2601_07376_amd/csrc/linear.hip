@@ -58,6 +58,7 @@ struct LinArgs {
   void* Y;
   int64_t ldy;
   int32_t n, d_in, d_out;
+  int32_t num_slots;
   int32_t m_tiles, n_tiles;
   const int32_t* hdr;
   const int32_t* run_start;
@@ -268,12 +269,12 @@ __global__ __launch_bounds__(256) void linear_hpack_kernel(LinArgs p) {
   const int g8 = p.rp / 8;
   for (int e = blockIdx.x; e < count; e += gridDim.x) {
     const int4 en = load_entry(p.rb, e);
-    const int a = en.x, p0 = en.y, rows = en.z;
+    const int a = ck_slot(p.hdr, en.x, p.num_slots), p0 = en.y, rows = en.z;
     const Slot sm = load_slot(p.meta, a);
     const int r = sm.rank;
     for (int q = threadIdx.x; q < rows * g8; q += 256) {
       const int i = q / g8, j = (q - i * g8) * 8;
-      const int t = p.perm[p0 + i];
+      const int t = ck_row(p.hdr, p.perm[p0 + i], p.n);
       float h[8];
 #pragma unroll
       for (int k = 0; k < 8; ++k) h[k] = 0.0f;
@@ -389,7 +390,7 @@ __global__ __launch_bounds__(256, 1) void linear_kernel(LinArgs p) {
         cur_run = kr;
         rs = uni(p.run_start[k_first + kr]);
         re = uni(p.run_end[k_first + kr]);
-        const Slot sm = load_slot(p.meta, uni(p.run_adapter[k_first + kr]));
+        const Slot sm = load_slot(p.meta, ck_slot(p.hdr, uni(p.run_adapter[k_first + kr]), p.num_slots));
         Ba = static_cast<const uint16_t*>(sm.B);
         rr = sm.rank;
       }
@@ -483,7 +484,7 @@ __global__ __launch_bounds__(256, 1) void linear_kernel(LinArgs p) {
     const int rs = uni(p.run_start[k]);
     if (rs >= r0 + LT_M) break;
     const int re = uni(p.run_end[k]);
-    const Slot sm = load_slot(p.meta, uni(p.run_adapter[k]));
+    const Slot sm = load_slot(p.meta, ck_slot(p.hdr, uni(p.run_adapter[k]), p.num_slots));
     const int r = sm.rank;
     const rsrc_t Bw = make_rsrc(sm.B, (uint32_t)p.d_out * (uint32_t)r * 2u);
     for (int j0 = 0; j0 < r; j0 += 16) {
@@ -599,6 +600,7 @@ hipError_t launch_linear_mfma(const OpLaunch& o, const LinearLaunch& l, hipStrea
   a.Y = l.Y;
   a.ldy = l.ldy;
   a.n = o.n;
+  a.num_slots = o.num_slots;
   a.d_in = o.d_in;
   a.d_out = o.d_out;
   a.m_tiles = (o.n + LT_M - 1) / LT_M;

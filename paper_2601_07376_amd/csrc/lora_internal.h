@@ -33,6 +33,8 @@ enum : int {
   HDR_RB_ROWS = 8,    // rows per large-group block of this plan: RB_ROWS or RB_FINE
   HDR_WORDS = 64
 };
+static_assert(HDR_FLAGS == 0, "the debug build's bounds checks set bits of header word 0");
+static_assert(LORA_DATA_BOUNDS == 8u, "device_common.h's DATA_BOUNDS_BIT");
 
 constexpr int RB_ROWS = 256;     // rows per large-group row block
 constexpr int RB_FINE = 64;      // ... when the batch has fewer than FINE_BELOW x RB_ROWS rows

@@ -4,6 +4,11 @@ Argument marshalling only: torch provides device memory and the current HIP
 stream; every step of the computation runs in the library's HIP kernels.  The
 library must be built (``paper_2601_07376_amd.build.build()``); importing this
 module without it raises immediately, there is no fallback.
+
+``Table(..., debug=True)`` binds a table, the plans built on it and every op
+called with them to the debug build liblora_mi355x_debug.so (overlap checks of
+each op's buffers, bounds checks of plan values in the kernels); tables and
+plans of the two libraries do not mix.
 """
 import ctypes
 import os
@@ -13,12 +18,16 @@ import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "liblora_mi355x.so")
+DEBUG_LIB_PATH = os.path.join(_HERE, "liblora_mi355x_debug.so")
 
 LORA_F32, LORA_BF16 = 0, 1
-LORA_DATA_BAD_ID, LORA_DATA_EMPTY_SLOT, LORA_DATA_BAD_SEGMENTS = 1, 2, 4
+LORA_DATA_BAD_ID, LORA_DATA_EMPTY_SLOT, LORA_DATA_BAD_SEGMENTS, LORA_DATA_BOUNDS = 1, 2, 4, 8
+LORA_BUILD_DEBUG = 1
+LORA_PLAN_PERM, LORA_PLAN_M_PERM, LORA_PLAN_SMALL_ROW = 0, 1, 2
 STATUS = {0: "LORA_OK", 1: "LORA_ERR_NULL", 2: "LORA_ERR_SHAPE", 3: "LORA_ERR_DTYPE",
           4: "LORA_ERR_ALIGN", 5: "LORA_ERR_RANK", 6: "LORA_ERR_SLOT", 7: "LORA_ERR_DATA",
-          8: "LORA_ERR_WORKSPACE", 9: "LORA_ERR_HIP"}
+          8: "LORA_ERR_WORKSPACE", 9: "LORA_ERR_HIP", 10: "LORA_ERR_VALUE",
+          11: "LORA_ERR_ALIAS"}
 
 _vp, _i32, _i64, _sz, _f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_float
 _pp = ctypes.POINTER(ctypes.c_void_p)
@@ -28,6 +37,8 @@ SIGNATURES = {
     "lora_abi_version": (_i32, []),
     "lora_status_string": (ctypes.c_char_p, [_i32]),
     "lora_last_error": (ctypes.c_char_p, []),
+    "lora_build_flags": (_i32, []),
+    "lora_debug_plan_poke": (_i32, [_vp, _i32, _i32, _i32, _vp]),
     "lora_table_device_bytes": (_sz, [_i32]),
     "lora_table_create": (_i32, [_i32, _i32, _i32, _i32, _vp, _sz, _pp]),
     "lora_table_set": (_i32, [_vp, _i32, _i32, _f32, _vp, _vp]),
@@ -65,23 +76,24 @@ SIGNATURES = {
                                ctypes.c_float, ctypes.c_float, _vp, _vp, _vp, _i32, _i64, _vp]),
 }
 
-_lib = None
+_libs = {}
 
 
-def lib():
-    """Load the shared library (raises if it has not been built)."""
-    global _lib
-    if _lib is None:
-        if not os.path.exists(LIB_PATH):
-            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+def lib(debug=False):
+    """Load the shared library, or its debug build (raises if it has not been
+    built)."""
+    path = DEBUG_LIB_PATH if debug else LIB_PATH
+    if path not in _libs:
+        if not os.path.exists(path):
+            raise RuntimeError(f"{path} is missing: build it with "
                                "paper_2601_07376_amd.build.build() (hipcc, gfx950)")
-        L = ctypes.CDLL(LIB_PATH)
+        L = ctypes.CDLL(path)
         for name, (res, args) in SIGNATURES.items():
             f = getattr(L, name)
             f.restype = res
             f.argtypes = args
-        _lib = L
-    return _lib
+        _libs[path] = L
+    return _libs[path]
 
 
 class LoraError(RuntimeError):
@@ -90,9 +102,10 @@ class LoraError(RuntimeError):
         self.status = status
 
 
-def _check(status):
+def _check(status, L=None):
+    """Raise for a nonzero status, with the detail of the library that returned it."""
     if status != 0:
-        raise LoraError(status, lib().lora_last_error().decode())
+        raise LoraError(status, (L or lib()).lora_last_error().decode())
 
 
 def _dtype(t):
@@ -155,8 +168,8 @@ def _rowmajor(t, name):
 class Table:
     """Adapter table of one adapted layer (slot -> rank, scale, A, B)."""
 
-    def __init__(self, num_slots, d_in, d_out, w_dtype=torch.bfloat16, device="cuda"):
-        L = lib()
+    def __init__(self, num_slots, d_in, d_out, w_dtype=torch.bfloat16, device="cuda", debug=False):
+        L = self.lib = lib(debug)
         self.num_slots, self.d_in, self.d_out = num_slots, d_in, d_out
         self.w_dtype = w_dtype
         self.device = torch.device(device)
@@ -165,7 +178,7 @@ class Table:
         h = ctypes.c_void_p()
         _check(L.lora_table_create(num_slots, d_in, d_out,
                                    LORA_BF16 if w_dtype == torch.bfloat16 else LORA_F32,
-                                   _ptr(self.meta), nbytes, ctypes.byref(h)))
+                                   _ptr(self.meta), nbytes, ctypes.byref(h)), L)
         self.handle = h
         self.ranks = [0] * num_slots
         self.scales = [0.0] * num_slots
@@ -181,22 +194,23 @@ class Table:
         if A.shape != (r, self.d_in) or B.shape != (self.d_out, r):
             raise ValueError(f"shapes {tuple(A.shape)}, {tuple(B.shape)} do not match "
                              f"[r, {self.d_in}], [{self.d_out}, r]")
-        _check(lib().lora_table_set(self.handle, slot, r, float(scale), _ptr(A), _ptr(B)))
+        _check(self.lib.lora_table_set(self.handle, slot, r, float(scale), _ptr(A), _ptr(B)),
+               self.lib)
         self.ranks[slot], self.scales[slot] = r, float(scale)
         self._weights[slot] = (A, B)
 
     def clear(self, slot):
-        _check(lib().lora_table_clear(self.handle, slot))
+        _check(self.lib.lora_table_clear(self.handle, slot), self.lib)
         self.ranks[slot], self.scales[slot] = 0, 0.0
         self._weights[slot] = None
 
     def upload(self, stream=None):
-        _check(lib().lora_table_upload(self.handle, _stream(stream)))
+        _check(self.lib.lora_table_upload(self.handle, _stream(stream)), self.lib)
 
     def __del__(self):
-        h = getattr(self, "handle", None)
-        if h is not None and _lib is not None:
-            _lib.lora_table_destroy(h)
+        h, L = getattr(self, "handle", None), getattr(self, "lib", None)
+        if h is not None and L is not None:
+            L.lora_table_destroy(h)
             self.handle = None
 
 
@@ -205,7 +219,7 @@ class Plan:
 
     def __init__(self, table, idx=None, mask=None, seg_offsets=None, seg_adapter=None, n=None,
                  stream=None, policy=None):
-        L = lib()
+        L = self.lib = table.lib
         self.table = table
         if idx is not None:
             n = idx.numel()
@@ -223,15 +237,15 @@ class Plan:
             pol = policy if isinstance(policy, Policy) else Policy(**policy)
             _check(L.lora_plan_build_policy(table.handle, self.n, _ptr(idx), _ptr(mask),
                                             ctypes.byref(pol), _ptr(self.ws), self.ws.numel(),
-                                            _stream(stream), ctypes.byref(h)))
+                                            _stream(stream), ctypes.byref(h)), L)
         elif idx is not None:
             _check(L.lora_plan_build(table.handle, self.n, _ptr(idx), _ptr(mask), _ptr(self.ws),
-                                     self.ws.numel(), _stream(stream), ctypes.byref(h)))
+                                     self.ws.numel(), _stream(stream), ctypes.byref(h)), L)
         else:
             _check(L.lora_plan_build_segments(table.handle, self.n, seg_adapter.numel(),
                                               _ptr(seg_offsets), _ptr(seg_adapter), _ptr(mask),
                                               _ptr(self.ws), self.ws.numel(), _stream(stream),
-                                              ctypes.byref(h)))
+                                              ctypes.byref(h)), L)
         self.handle = h
 
     def export(self, stream=None):
@@ -243,10 +257,11 @@ class Plan:
         n_runs = ctypes.c_int32()
         flags = ctypes.c_uint32()
         p = lambda k: arrs[k].ctypes.data_as(ctypes.c_void_p)
-        _check(lib().lora_plan_export(self.handle, p("counts"), p("offsets"), p("perm"),
-                                      ctypes.byref(n_runs), p("run_start"), p("run_len"),
-                                      p("run_adapter"), p("m_counts"), p("m_offsets"),
-                                      p("m_perm"), ctypes.byref(flags), _stream(stream)))
+        _check(self.lib.lora_plan_export(self.handle, p("counts"), p("offsets"), p("perm"),
+                                         ctypes.byref(n_runs), p("run_start"), p("run_len"),
+                                         p("run_adapter"), p("m_counts"), p("m_offsets"),
+                                         p("m_perm"), ctypes.byref(flags), _stream(stream)),
+               self.lib)
         n_act, m_n_act, nr = int(arrs["offsets"][-1]), int(arrs["m_offsets"][-1]), n_runs.value
         return dict(counts=arrs["counts"], offsets=arrs["offsets"], perm=arrs["perm"][:n_act],
                     n_runs=nr, run_start=arrs["run_start"][:nr], run_len=arrs["run_len"][:nr],
@@ -257,15 +272,21 @@ class Plan:
     def check(self, stream=None):
         """Data-error flags (LORA_DATA_* bits); 0 when clean."""
         flags = ctypes.c_uint32()
-        st = lib().lora_plan_check(self.handle, ctypes.byref(flags), _stream(stream))
+        st = self.lib.lora_plan_check(self.handle, ctypes.byref(flags), _stream(stream))
         if st not in (0, 7):
-            _check(st)
+            _check(st, self.lib)
         return flags.value
 
+    def debug_poke(self, array, index, value, stream=None):
+        """Debug library only: overwrite one row id of the plan (a test hook
+        for the kernels' bounds checks; array LORA_PLAN_*)."""
+        _check(self.lib.lora_debug_plan_poke(self.handle, int(array), int(index), int(value),
+                                             _stream(stream)), self.lib)
+
     def __del__(self):
-        h = getattr(self, "handle", None)
-        if h is not None and _lib is not None:
-            _lib.lora_plan_destroy(h)
+        h, L = getattr(self, "handle", None), getattr(self, "lib", None)
+        if h is not None and L is not None:
+            L.lora_plan_destroy(h)
             self.handle = None
 
 
@@ -275,20 +296,20 @@ def shrink(plan, X, H=None, stream=None):
         r = max(max(plan.table.ranks), 1)
         H = torch.zeros(plan.n, (r + 7) // 8 * 8, dtype=torch.float32, device=X.device)
         _used_on(stream, H)
-    _check(lib().lora_shrink(plan.handle, _ptr(X), _dtype(X), _rowmajor(X, "X"), _ptr(H),
-                             _rowmajor(H, "H"), _stream(stream)))
+    _check(plan.lib.lora_shrink(plan.handle, _ptr(X), _dtype(X), _rowmajor(X, "X"), _ptr(H),
+                                _rowmajor(H, "H"), _stream(stream)), plan.lib)
     return H
 
 
 def expand(plan, H, Y, stream=None):
     """Y[t] += s_a H[t, :r_a] B_a^T in place."""
-    _check(lib().lora_expand(plan.handle, _ptr(H), _rowmajor(H, "H"), _ptr(Y), _dtype(Y),
-                             _rowmajor(Y, "Y"), _stream(stream)))
+    _check(plan.lib.lora_expand(plan.handle, _ptr(H), _rowmajor(H, "H"), _ptr(Y), _dtype(Y),
+                                _rowmajor(Y, "Y"), _stream(stream)), plan.lib)
     return Y
 
 
 def apply_workspace(plan):
-    return torch.empty(max(lib().lora_apply_workspace_bytes(plan.handle), 16), dtype=torch.uint8,
+    return torch.empty(max(plan.lib.lora_apply_workspace_bytes(plan.handle), 16), dtype=torch.uint8,
                        device=plan.table.device)
 
 
@@ -297,21 +318,21 @@ def apply(plan, X, Y, ws=None, stream=None):
     if ws is None:
         ws = apply_workspace(plan)
         _used_on(stream, ws)
-    _check(lib().lora_apply(plan.handle, _ptr(X), _dtype(X), _rowmajor(X, "X"), _ptr(Y),
-                            _dtype(Y), _rowmajor(Y, "Y"), _ptr(ws), ws.numel(), _stream(stream)))
+    _check(plan.lib.lora_apply(plan.handle, _ptr(X), _dtype(X), _rowmajor(X, "X"), _ptr(Y),
+                               _dtype(Y), _rowmajor(Y, "Y"), _ptr(ws), ws.numel(), _stream(stream)), plan.lib)
     return Y
 
 
 def apply_noalloc(plan, X, Y, stream=None):
     """apply() with the library's fixed per-GPU scratch instead of a workspace:
     allocates nothing (for graph capture and loops that must not allocate)."""
-    _check(lib().lora_apply_noalloc(plan.handle, _ptr(X), _dtype(X), _rowmajor(X, "X"), _ptr(Y),
-                                    _dtype(Y), _rowmajor(Y, "Y"), _stream(stream)))
+    _check(plan.lib.lora_apply_noalloc(plan.handle, _ptr(X), _dtype(X), _rowmajor(X, "X"), _ptr(Y),
+                                       _dtype(Y), _rowmajor(Y, "Y"), _stream(stream)), plan.lib)
     return Y
 
 
 def apply_ids_workspace(table, n):
-    return torch.empty(max(lib().lora_apply_ids_workspace_bytes(table.handle, n), 16),
+    return torch.empty(max(table.lib.lora_apply_ids_workspace_bytes(table.handle, n), 16),
                        dtype=torch.uint8, device=table.device)
 
 
@@ -322,14 +343,14 @@ def apply_ids(table, idx, X, Y, ws=None, stream=None):
     if ws is None:
         ws = apply_ids_workspace(table, n)
         _used_on(stream, ws)
-    _check(lib().lora_apply_ids(table.handle, n, _ptr(idx), _ptr(X), _dtype(X),
-                                _rowmajor(X, "X"), _ptr(Y), _dtype(Y), _rowmajor(Y, "Y"),
-                                _ptr(ws), ws.numel(), _stream(stream)))
+    _check(table.lib.lora_apply_ids(table.handle, n, _ptr(idx), _ptr(X), _dtype(X),
+                                    _rowmajor(X, "X"), _ptr(Y), _dtype(Y), _rowmajor(Y, "Y"),
+                                    _ptr(ws), ws.numel(), _stream(stream)), table.lib)
     return Y
 
 
 def linear_workspace(plan):
-    return torch.empty(max(lib().lora_linear_workspace_bytes(plan.handle), 16), dtype=torch.uint8,
+    return torch.empty(max(plan.lib.lora_linear_workspace_bytes(plan.handle), 16), dtype=torch.uint8,
                        device=plan.table.device)
 
 
@@ -338,14 +359,14 @@ def linear(plan, X, W, Y, ws=None, stream=None):
     if ws is None:
         ws = linear_workspace(plan)
         _used_on(stream, ws)
-    _check(lib().lora_linear(plan.handle, _ptr(X), _dtype(X), _rowmajor(X, "X"), _ptr(W),
-                             _dtype(W), _rowmajor(W, "W"), _ptr(Y), _dtype(Y), _rowmajor(Y, "Y"),
-                             _ptr(ws), ws.numel(), _stream(stream)))
+    _check(plan.lib.lora_linear(plan.handle, _ptr(X), _dtype(X), _rowmajor(X, "X"), _ptr(W),
+                                _dtype(W), _rowmajor(W, "W"), _ptr(Y), _dtype(Y), _rowmajor(Y, "Y"),
+                                _ptr(ws), ws.numel(), _stream(stream)), plan.lib)
     return Y
 
 
 def grad_workspace(plan):
-    return torch.empty(max(lib().lora_grad_workspace_bytes(plan.handle), 16), dtype=torch.uint8,
+    return torch.empty(max(plan.lib.lora_grad_workspace_bytes(plan.handle), 16), dtype=torch.uint8,
                        device=plan.table.device)
 
 
@@ -367,14 +388,14 @@ def grad(plan, X, dY, dA=None, dB=None, H_saved=None, accumulate=False, ws=None,
     pa = (ctypes.c_void_p * t.num_slots)(*[g.data_ptr() if g is not None else None for g in dA])
     pb = (ctypes.c_void_p * t.num_slots)(*[g.data_ptr() if g is not None else None for g in dB])
     ldh = _rowmajor(H_saved, "H_saved") if H_saved is not None else 0
-    _check(lib().lora_grad(plan.handle, _ptr(X), _dtype(X), _rowmajor(X, "X"), _ptr(dY),
-                           _dtype(dY), _rowmajor(dY, "dY"), _ptr(H_saved), ldh, pa, pb,
-                           1 if accumulate else 0, _ptr(ws), ws.numel(), _stream(stream)))
+    _check(plan.lib.lora_grad(plan.handle, _ptr(X), _dtype(X), _rowmajor(X, "X"), _ptr(dY),
+                              _dtype(dY), _rowmajor(dY, "dY"), _ptr(H_saved), ldh, pa, pb,
+                              1 if accumulate else 0, _ptr(ws), ws.numel(), _stream(stream)), plan.lib)
     return dA, dB
 
 
 def grad_x_workspace(plan):
-    return torch.empty(max(lib().lora_grad_x_workspace_bytes(plan.handle), 16), dtype=torch.uint8,
+    return torch.empty(max(plan.lib.lora_grad_x_workspace_bytes(plan.handle), 16), dtype=torch.uint8,
                        device=plan.table.device)
 
 
@@ -383,13 +404,13 @@ def grad_x(plan, dY, dX, ws=None, stream=None):
     if ws is None:
         ws = grad_x_workspace(plan)
         _used_on(stream, ws)
-    _check(lib().lora_grad_x(plan.handle, _ptr(dY), _dtype(dY), _rowmajor(dY, "dY"), _ptr(dX),
-                             _dtype(dX), _rowmajor(dX, "dX"), _ptr(ws), ws.numel(), _stream(stream)))
+    _check(plan.lib.lora_grad_x(plan.handle, _ptr(dY), _dtype(dY), _rowmajor(dY, "dY"), _ptr(dX),
+                                _dtype(dX), _rowmajor(dX, "dX"), _ptr(ws), ws.numel(), _stream(stream)), plan.lib)
     return dX
 
 
 def backward_workspace(plan):
-    return torch.empty(max(lib().lora_backward_workspace_bytes(plan.handle), 16), dtype=torch.uint8,
+    return torch.empty(max(plan.lib.lora_backward_workspace_bytes(plan.handle), 16), dtype=torch.uint8,
                        device=plan.table.device)
 
 
@@ -412,10 +433,10 @@ def backward(plan, X, dY, dX, dA=None, dB=None, H_saved=None, accumulate=False, 
     pa = (ctypes.c_void_p * t.num_slots)(*[g.data_ptr() if g is not None else None for g in dA])
     pb = (ctypes.c_void_p * t.num_slots)(*[g.data_ptr() if g is not None else None for g in dB])
     ldh = _rowmajor(H_saved, "H_saved") if H_saved is not None else 0
-    _check(lib().lora_backward(plan.handle, _ptr(X), _dtype(X), _rowmajor(X, "X"), _ptr(dY),
-                               _dtype(dY), _rowmajor(dY, "dY"), _ptr(H_saved), ldh, pa, pb,
-                               1 if accumulate else 0, _ptr(dX), _dtype(dX), _rowmajor(dX, "dX"),
-                               _ptr(ws), ws.numel(), _stream(stream)))
+    _check(plan.lib.lora_backward(plan.handle, _ptr(X), _dtype(X), _rowmajor(X, "X"), _ptr(dY),
+                                  _dtype(dY), _rowmajor(dY, "dY"), _ptr(H_saved), ldh, pa, pb,
+                                  1 if accumulate else 0, _ptr(dX), _dtype(dX), _rowmajor(dX, "dX"),
+                                  _ptr(ws), ws.numel(), _stream(stream)), plan.lib)
     return dA, dB, dX
 
 

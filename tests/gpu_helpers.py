@@ -28,8 +28,10 @@ def torch_wdtype(case):
     return torch.bfloat16 if case.w_dtype == "bf16" else torch.float32
 
 
-def make_table(case, dev):
-    t = L.Table(case.num_slots, case.d_in, case.d_out, w_dtype=torch_wdtype(case), device=DEV)
+def make_table(case, dev, debug=False):
+    """debug: bind the table (and its plans and ops) to the debug library."""
+    t = L.Table(case.num_slots, case.d_in, case.d_out, w_dtype=torch_wdtype(case), device=DEV,
+                debug=debug)
     for a in range(case.num_slots):
         if case.ranks[a] > 0:
             t.set(a, dev["A"][a], dev["B"][a], float(case.scales[a]))

@@ -37,8 +37,8 @@ def test_every_declared_symbol_is_exported_and_bound():
 def test_version_and_strings():
     L = lora.lib()
     assert L.lora_abi_version() == 1
-    for s in range(11):
-        assert L.lora_status_string(s)
+    for s in range(12):
+        assert L.lora_status_string(s) != b"unknown status"
     assert L.lora_status_string(99) == b"unknown status"
 
 
@@ -143,8 +143,9 @@ def test_library_reads_no_environment():
     for f in os.listdir(csrc):
         text = open(os.path.join(csrc, f)).read()
         assert "getenv" not in text, f"{f} reads the environment"
-    data = open(lora.LIB_PATH, "rb").read()
-    assert b"getenv" not in data
+    for path in (lora.LIB_PATH, lora.DEBUG_LIB_PATH):
+        if os.path.exists(path):
+            assert b"getenv" not in open(path, "rb").read(), path
 
 
 def test_ops_reject_null_plan():
@@ -161,10 +162,13 @@ def test_ops_reject_null_plan():
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
-    monkeypatch.setattr(lora, "_lib", None)
+    monkeypatch.setattr(lora, "_libs", {})
     monkeypatch.setattr(lora, "LIB_PATH", str(tmp_path / "missing.so"))
+    monkeypatch.setattr(lora, "DEBUG_LIB_PATH", str(tmp_path / "missing_debug.so"))
     with pytest.raises(RuntimeError, match="missing"):
         lora.lib()
+    with pytest.raises(RuntimeError, match="missing"):
+        lora.lib(debug=True)
 
 
 def _adam(**kw):
