@@ -50,3 +50,63 @@ def test_apply_graph_replays_match_eager():
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(Y.view(torch.int32), eager.view(torch.int32)), f"replay {rep}"
+
+
+def _decode_ids(rng, n, S):
+    ids = rng.integers(0, S, size=n).astype(np.int32)
+    ids[rng.random(n) < 0.1] = -1
+    return torch.from_numpy(ids).to(DEV)
+
+
+def test_decode_step_graph_new_ids_each_replay():
+    """A decode step captured once and replayed with other ids, as a serving
+    loop does: the ids live in one device buffer that the caller rewrites
+    before each replay.  Two graphs on the decode workload (256 rows, 64
+    slots of rank 16, 4096 -> 4096): plan build + lora_apply, and
+    lora_apply_ids.  Every replay must give the bytes of eager calls on that
+    replay's ids (a plan built from them, and lora_apply_ids)."""
+    say("graph capture of a decode step, new ids each replay")
+    case = workloads.make_config(2, y_dtype="bf16")
+    dev = case_to_device(case, DEV)
+    table = L.Table(case.num_slots, case.d_in, case.d_out, w_dtype=torch.bfloat16, device=DEV)
+    for a in range(case.num_slots):
+        table.set(a, dev["A"][a], dev["B"][a], float(case.scales[a]))
+    table.upload()
+    n, S = case.n, case.num_slots
+    ids = dev["idx"].clone()
+    Y0 = dev["Y"].clone()
+    Yp, Yi = Y0.clone(), Y0.clone()
+    ws_ids = L.apply_ids_workspace(table, n)
+    # eager calls first (they also create anything the library makes once)
+    warm = L.Plan(table, idx=ids)
+    ws_apply = L.apply_workspace(warm)
+    L.apply(warm, dev["X"], Yp.clone(), ws=ws_apply)
+    L.apply_ids(table, ids, dev["X"], Yi.clone(), ws=ws_ids)
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    g_plan, g_ids = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g_plan, stream=s):
+            plan = L.Plan(table, idx=ids)                # workspace from the graph's pool
+            L.apply(plan, dev["X"], Yp, ws=ws_apply)
+        with torch.cuda.graph(g_ids, stream=s):
+            L.apply_ids(table, ids, dev["X"], Yi, ws=ws_ids)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(5)
+    for rep in range(3):
+        ids.copy_(_decode_ids(rng, n, S))              # the next step's ids, eager
+        Yp.copy_(Y0)
+        Yi.copy_(Y0)
+        torch.cuda.synchronize()
+        g_plan.replay()
+        g_ids.replay()
+        torch.cuda.synchronize()
+        ep, ei = Y0.clone(), Y0.clone()
+        L.apply(L.Plan(table, idx=ids), dev["X"], ep)
+        L.apply_ids(table, ids, dev["X"], ei)
+        torch.cuda.synchronize()
+        assert torch.equal(Yp.view(torch.int16), ep.view(torch.int16)), f"plan + apply, replay {rep}"
+        assert torch.equal(Yi.view(torch.int16), ei.view(torch.int16)), f"apply_ids, replay {rep}"
+        assert not torch.equal(Yp.view(torch.int16), Y0.view(torch.int16))
+    del plan
