@@ -196,7 +196,7 @@ lora_status lora_plan_build_segments(const lora_table* t, int32_t n, int32_t num
  * Errors: VALUE (a field outside its range), and those of lora_plan_build. */
 typedef struct lora_policy {
   int32_t small_max;     /* groups of <= small_max rows take the small-group kernels, >= 0
-                            (-1: every group when n <= 1024; groups of <= 16 rows when
+                            (-1: every group when n <= 1024; groups of <= 32 rows when
                             n < 64 x num_slots; none otherwise) */
   int32_t small_split;   /* small groups: 0 = one fused kernel, 1 = shrink per d-slice + expand
                             (-1: split when d_in >= 1024) */
