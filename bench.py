@@ -419,15 +419,24 @@ def run_workload(cfg, steps, warmup, rate):
 
     dist = {}
 
-    def timed(enqueue, k, key=None, blocks=8):
+    def timed(enqueue, k, key=None, blocks=8, warm=0):
         """Average GPU time (ms) per call of enqueue(i) over k back-to-back calls:
         the calls are queued behind a GPU-side start gate, so the GPU never waits
         on the host, and events on the compute stream bracket them; an event
         after each of `blocks` blocks gives the spread of block averages
-        (median, p10, p90 in us, stored under `key`)."""
+        (median, p10, p90 in us, stored under `key`).  warm > 0: that many
+        untimed calls first, whose host cost also sizes the gate."""
+        leg_ms = host_ms
+        if warm > 0:
+            torch.cuda.synchronize()
+            c1 = time.perf_counter()
+            for i in range(warm):
+                enqueue(i)
+            leg_ms = max(host_ms, (time.perf_counter() - c1) * 1e3 / warm)
+            torch.cuda.synchronize()
         nb = max(1, min(blocks, k // 8))
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(nb + 1)]
-        gate_ms = min(500.0, 2.0 + 2.0 * host_ms * k)
+        gate_ms = min(500.0, 2.0 + 2.0 * leg_ms * k)
         torch.cuda.synchronize()
         torch.cuda._sleep(int(gate_ms * rate))
         ev[0].record()
@@ -463,10 +472,15 @@ def run_workload(cfg, steps, warmup, rate):
         with_plan = None
     gx_us = adam_us = bw_us = None
     if case.mask is not None and case.x_dtype == "bf16":
-        gx_us = timed(lambda i: rig.run_grad_x(rig.sets[i % nc], handles[i % nc]), steps, "grad_x_us") * 1e3
-        bw_us = timed(lambda i: rig.run_backward(rig.sets[i % nc], handles[i % nc]), steps, "backward_us") * 1e3
+        # the other legs: a few untimed calls each first, and at least 50 timed
+        kl = max(steps, 50)
+        gx_us = timed(lambda i: rig.run_grad_x(rig.sets[i % nc], handles[i % nc]), kl, "grad_x_us",
+                      warm=4) * 1e3
+        bw_us = timed(lambda i: rig.run_backward(rig.sets[i % nc], handles[i % nc]), kl, "backward_us",
+                      warm=4) * 1e3
     if case.mask is not None:
-        adam_us = timed(lambda i: rig.run_adamw(rig.sets[i % nc]), steps, "adamw_us") * 1e3
+        adam_us = timed(lambda i: rig.run_adamw(rig.sets[i % nc]), max(steps, 50), "adamw_us",
+                        warm=4) * 1e3
     loss_r = token_loss_leg(case, timed, steps) if case.mask is not None else None
     lin_r = linear_leg(case, rig, handles[0], timed, steps) if cfg == 3 else None
     for h in handles:
