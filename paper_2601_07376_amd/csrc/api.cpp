@@ -325,15 +325,14 @@ lora_status make_plan(const lora_table* t, int32_t n, const int32_t* idx,
 namespace lora {
 
 // Small-group policy.  Batches of up to 1024 rows (decode steps) send every
-// adapter group through the small-group kernels; larger batches send groups of
-// up to 16 rows there and larger groups through the grouped shrink + expand.
-// Small-group path: every group of a batch of at most 1024 rows; groups of at
-// most SMALL_ROWS rows while the batch has fewer than 4 SMALL_ROWS rows per
-// slot (many small groups are then likely, and they run beside the large ones
-// on the second stream); none otherwise, where a few small groups cost less as
-// blocks of the grouped kernels than two more launches.
-// (groups of up to 32 rows, two records each at most: the skewed mixed batch
-// measured 92.4 against 95.8 us per apply with 16)
+// adapter group through the small-group kernels.  Larger batches with fewer
+// than 4 SMALL_ROWS rows per slot send groups of up to 2 SMALL_ROWS rows there
+// (two records each at most; many small groups are then likely, and they run
+// beside the large ones on the second stream: the skewed mixed batch measured
+// 92.4 against 95.8 us per apply with a limit of SMALL_ROWS), and the larger
+// groups through the grouped shrink + expand.  Other batches send none: a few
+// small groups cost less as blocks of the grouped kernels than two more
+// launches.
 int32_t small_max_policy(int32_t n, int32_t S) {
   if (n <= 1024) return INT32_MAX;
   return (int64_t)n < (int64_t)4 * SMALL_ROWS * S ? 2 * SMALL_ROWS : 0;
